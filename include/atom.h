@@ -1,0 +1,213 @@
+/*
+ * atom.h - C ABI of libatom: one swapped GPT training step on one MI355X.
+ *
+ * The model of Atom (arXiv 2403.10504): a complete GPT-3-style model lives in
+ * host memory (Section I; Section III-A, "Design Overview"); it is cut at
+ * decoder-block boundaries into contiguous sub-models ("groups") that a
+ * static analysis fits into a GPU memory budget (Section III-D, Algorithm 1);
+ * the runtime swaps groups into the GPU on one stream while another runs the
+ * current group (Section IV), and gradient accumulation over C micro-batches
+ * lengthens compute per swap (Section III-C).
+ *
+ * Layer chain ("nodes", topologically sorted as in Section III-D):
+ *   node 0        embedding: wte [V][d], wpe [T][d]
+ *   nodes 1..L    decoder blocks (pre-LayerNorm GPT block)
+ *   node L+1      final LayerNorm + LM head ("Logits" layer): lnf_g, lnf_b,
+ *                 w_head [Vp][d] with Vp = V rounded up to 128 (zero rows)
+ * Linear weights are [out][in]: y = x W^T + b.  A block holds, in order:
+ *   ln1_g [d], ln1_b [d], w_qkv [3d][d], b_qkv [3d], w_o [d][d], b_o [d],
+ *   ln2_g [d], ln2_b [d], w_fc [f][d], b_fc [f], w_pr [d][f], b_pr [d].
+ * Each node's tensors are one contiguous host range (tensor offsets aligned
+ * to 256 bytes, see atom_node_layout) and consecutive nodes are adjacent, so
+ * a group swaps with one copy.
+ *
+ * Ownership.  The caller owns the device arena (one allocation of exactly
+ * atom_plan.arena_bytes, e.g. a torch uint8 tensor) and the three streams;
+ * both must outlive the context.  The library never allocates device memory.
+ * The library owns the pinned host model (weights in the working dtype), the
+ * host gradient buffers and the fp32 gradient accumulators.
+ *
+ * Errors.  Every call returns an atom_status; nothing throws across the ABI.
+ * atom_last_error(ctx) describes the last failure on a context.  Calls that
+ * enqueue GPU work report launch errors at once; execution errors surface at
+ * the next synchronising call (atom_step, atom_sync, atom_ctx_destroy).
+ * Threading: one context per host thread.
+ */
+#ifndef ATOM_H
+#define ATOM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ATOM_MAX_NODES 256
+
+typedef enum atom_status {
+  ATOM_OK = 0,
+  ATOM_EINVAL = -1,       /* bad argument or unsupported shape */
+  ATOM_ENOPLAN = -2,      /* no partition fits the device budget */
+  ATOM_EBUDGET = -3,      /* arena smaller than the plan needs */
+  ATOM_EHIP = -4,         /* a HIP runtime call failed */
+  ATOM_ESTATE = -5,       /* call-order violation (e.g. compute on a group not swapped in) */
+  ATOM_ENOMEM_HOST = -6   /* pinned host allocation failed */
+} atom_status;
+
+typedef enum atom_dtype { ATOM_F32 = 0, ATOM_BF16 = 1 } atom_dtype;
+typedef enum atom_ckpt_policy { ATOM_CKPT_DEVICE = 0, ATOM_CKPT_HOST = 1 } atom_ckpt_policy;
+
+/* Model and step shape (Table II gives the GPT-3 shapes).  d_model must be
+ * a multiple of 64 (at most 8192), d_model / n_head must be 64 or 128, and
+ * accum is the gradient-accumulation degree C (micro-batches per step). */
+typedef struct atom_config {
+  int32_t n_layer, d_model, n_head, d_mlp, vocab, seq_len, batch, accum;
+  int32_t dtype; /* atom_dtype: working precision of weights and activations */
+  int32_t ckpt;  /* atom_ckpt_policy: where block-input checkpoints live */
+} atom_config;
+
+/* Cost of one node of the augmented graph (Section III-D: the node's
+ * loading time t^u, forward time t^f, backward time t^b; memory is its
+ * weight bytes, which sets the slot it needs).  Times in seconds; t_fwd and
+ * t_bwd are per micro-batch, t_bwd includes the forward recompute; t_store
+ * is the time to copy the node's gradients back to the host. */
+typedef struct atom_node_cost {
+  uint64_t weight_bytes;
+  double t_fwd, t_bwd, t_load, t_store;
+} atom_node_cost;
+
+/* A partition of the chain into contiguous groups and its static layout.
+ * Group g holds nodes first[g]..last[g] and uses weight slot g % n_slots;
+ * the last n_slots groups stay resident from the forward into the backward.
+ * arena_bytes = reserve_bytes + n_slots * slot_bytes + gradient slots. */
+typedef struct atom_plan {
+  int32_t n_nodes, n_groups, n_slots, overlap_ok, exhaustive, accum;
+  int32_t first[ATOM_MAX_NODES], last[ATOM_MAX_NODES];
+  uint64_t budget_bytes, reserve_bytes, slot_bytes, arena_bytes;
+  uint64_t h2d_bytes, d2h_bytes, forced_h2d_bytes;
+  double pred_fwd_s, pred_step_s;
+  int64_t n_evaluated;
+} atom_plan;
+
+/* One tensor of a node's host range. */
+typedef struct atom_tensor_desc {
+  char name[16];
+  int32_t rows, cols;     /* cols == 1 for vectors */
+  uint64_t offset, bytes; /* within the node's range, working dtype */
+} atom_tensor_desc;
+
+typedef struct atom_ctx atom_ctx;
+
+/* Library version string. */
+const char* atom_version(void);
+/* Short text for a status code. */
+const char* atom_status_string(int status);
+
+/* Tensor layout of node `node` under cfg.  Writes up to `max` descriptors,
+ * the count to *n_out and the node's total bytes to *node_bytes.
+ * ATOM_EINVAL for a bad node index or config. */
+int atom_node_layout(const atom_config* cfg, int32_t node, atom_tensor_desc* out, int32_t max, int32_t* n_out,
+                     uint64_t* node_bytes);
+
+/* Analytic node costs for cfg (n = n_layer + 2 entries): FLOP counts at an
+ * assumed MFMA rate and bytes at an assumed host-link rate (the values are
+ * stated in the design notes); callers may substitute measured costs. */
+int atom_node_costs(const atom_config* cfg, atom_node_cost* out, int32_t n);
+
+/* Device bytes the step needs besides weight and gradient slots
+ * (checkpoints, activations, workspace, tokens). */
+int atom_reserve_bytes(const atom_config* cfg, uint64_t* out);
+
+/* Planner core (Algorithm 1 with the constraints and selection rule of
+ * Section III-D as read in the design notes): searches contiguous
+ * partitions of `n` nodes with the given costs, a device budget and
+ * `reserve` bytes of non-slot memory.  Exhaustive for n <= 20 nodes; for
+ * longer chains it searches the structured family that identical decoder
+ * blocks allow.  Returns ATOM_ENOPLAN when no partition fits. */
+int atom_plan_search(const atom_config* cfg, uint64_t budget_bytes, uint64_t reserve_bytes,
+                     const atom_node_cost* costs, int32_t n, atom_plan* out);
+
+/* atom_plan_partition: the static analysis of Section III-D for cfg under
+ * a device budget.  costs == NULL uses atom_node_costs; the reserve comes
+ * from atom_reserve_bytes.  Errors: ATOM_EINVAL, ATOM_ENOPLAN. */
+int atom_plan_partition(const atom_config* cfg, uint64_t device_budget_bytes, const atom_node_cost* costs,
+                        int32_t n_costs, atom_plan* out);
+
+/* A plan for a given partition: group g ends at node last[g] (strictly
+ * increasing, last[n_groups-1] = n_layer + 1), with n_slots weight slots
+ * (1 <= n_slots <= n_groups, at least min(n_groups, 2)).  Fills the slot
+ * size, arena size and transfer bytes from the layout; predicted times use
+ * the analytic costs.  ATOM_EINVAL for a malformed partition. */
+int atom_plan_fixed(const atom_config* cfg, int32_t n_groups, const int32_t* last, int32_t n_slots, atom_plan* out);
+
+/* Create a context: validates cfg against plan, carves the arena, allocates
+ * the pinned host model (zero weights; fill them through atom_host_tensor)
+ * and the host gradient buffers.  Streams are hipStream_t handles (e.g.
+ * torch.cuda.Stream().cuda_stream); they must be distinct.  Errors:
+ * ATOM_EINVAL, ATOM_EBUDGET (arena_bytes < plan->arena_bytes),
+ * ATOM_ENOMEM_HOST, ATOM_EHIP. */
+int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_arena, uint64_t arena_bytes,
+                    void* compute_stream, void* h2d_stream, void* d2h_stream, atom_ctx** out);
+/* Waits for all work, frees host memory and events.  NULL is ignored. */
+void atom_ctx_destroy(atom_ctx* ctx);
+
+/* Host buffers of a node: which = 0 weights (working dtype, writable),
+ * 1 fp32 gradient accumulators (sum over committed steps), 2 gradients of
+ * the last step in the working dtype. */
+int atom_host_tensor(atom_ctx* ctx, int32_t node, int32_t which, void** ptr, uint64_t* bytes);
+
+/* Zero the fp32 gradient accumulators. */
+int atom_zero_grads(atom_ctx* ctx);
+
+/* Upload tokens for the next step: host int32 [accum][batch][seq_len + 1];
+ * inputs are [..., :T], next-token targets [..., 1:]; every id must be in
+ * [0, vocab) (ATOM_EINVAL otherwise).  Synchronous. */
+int atom_set_tokens(atom_ctx* ctx, const int32_t* tokens);
+
+/* --- the per-group calls atom_step composes (all asynchronous) --- */
+
+/* Swap group `group`'s weights into its slot on the H2D stream, after the
+ * slot's previous occupant has finished its last compute.  ATOM_ESTATE if
+ * the group is already resident. */
+int atom_swap_in(atom_ctx* ctx, int32_t group);
+/* Forward of one node for micro-batch `micro` on the compute stream.  Node 0
+ * embeds the tokens; a block node writes its output checkpoint; node L+1
+ * runs the final LayerNorm, the LM head, the cross-entropy and the head's
+ * backward (it starts the gradient of the residual stream).  ATOM_ESTATE if
+ * the node's group is not swapped in, or its input is not ready. */
+int atom_block_fwd(atom_ctx* ctx, int32_t node, int32_t micro);
+/* Backward of one node for micro-batch `micro`: a block restores its input
+ * checkpoint, recomputes its forward and writes its gradients into the
+ * group's gradient slot; node 0 runs the embedding backward.  Node L+1 has no
+ * separate backward (ATOM_EINVAL). */
+int atom_block_bwd(atom_ctx* ctx, int32_t node, int32_t micro);
+/* Copy group `group`'s gradients to the host on the D2H stream, then (on a
+ * host thread) add them to the fp32 accumulators.  Releases the group's
+ * weight slot. */
+int atom_swap_out(atom_ctx* ctx, int32_t group);
+/* Wait for every stream and host accumulation; *loss_out (may be NULL)
+ * receives the mean loss of the step. */
+int atom_sync(atom_ctx* ctx, float* loss_out);
+
+/* One whole training step: uploads tokens, runs the plan's schedule (swap-in
+ * with prefetch, forward of every group for every micro-batch, head, backward
+ * with reloads, gradient swap-out and host accumulation) and waits.  The mean
+ * loss goes to *loss_out.  Synchronous. */
+int atom_step(atom_ctx* ctx, const int32_t* tokens, float* loss_out);
+
+/* Per-step counters of the last atom_step. */
+typedef struct atom_stats {
+  uint64_t h2d_bytes, d2h_bytes;
+  double step_s, host_accum_s;
+  int32_t swap_ins, swap_outs;
+} atom_stats;
+int atom_get_stats(atom_ctx* ctx, atom_stats* out);
+
+/* Text of the last error on ctx (never NULL). */
+const char* atom_last_error(const atom_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ATOM_H */

@@ -250,6 +250,20 @@ def embed_backward(dx, tok, vocab, seq_len):
     return {"wte": dwte, "wpe": dwpe}
 
 
+def cross_entropy_rows(z, y, scale):
+    """Per-row next-token cross-entropy and its gradient.
+
+    loss[r] = logsumexp(z[r]) - z[r, y[r]];  dz = (softmax(z) - onehot(y)) * scale.
+    """
+    m = z.max(axis=1, keepdims=True)
+    lse = (m + np.log(np.exp(z - m).sum(axis=1, keepdims=True)))[:, 0]
+    rows = np.arange(z.shape[0])
+    loss = lse - z[rows, y]
+    dz = np.exp(z - lse[:, None])
+    dz[rows, y] -= 1.0
+    return loss, dz * scale
+
+
 def head_forward_backward(x, p, targets, n_total, chunk=4096):
     """Final LN, logits z = LN(x) W_head^T, cross-entropy against `targets`.
 
@@ -270,13 +284,8 @@ def head_forward_backward(x, p, targets, n_total, chunk=4096):
     for lo in range(0, xf.shape[0], chunk):
         hi = min(xf.shape[0], lo + chunk)
         z = yhat[lo:hi] @ W.T
-        m = z.max(axis=1, keepdims=True)
-        lse = (m + np.log(np.exp(z - m).sum(axis=1, keepdims=True)))[:, 0]
-        rows = np.arange(hi - lo)
-        loss_sum += float((lse - z[rows, yf[lo:hi]]).sum())
-        dz = np.exp(z - lse[:, None])
-        dz[rows, yf[lo:hi]] -= 1.0
-        dz /= n_total
+        loss_rows, dz = cross_entropy_rows(z, yf[lo:hi], 1.0 / n_total)
+        loss_sum += float(loss_rows.sum())
         dyhat[lo:hi] = dz @ W
         dW += dz.T @ yhat[lo:hi]
     dx, dg, db = layer_norm_backward(dyhat, xhat, rstd, p["lnf_g"])

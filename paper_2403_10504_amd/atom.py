@@ -1,0 +1,316 @@
+"""ctypes binding of libatom (include/atom.h, include/atom_kernels.h).
+
+Argument marshalling only: every function here forwards to the C ABI function
+of the same name; no step of the method runs in Python.  PyTorch is used by
+`Session` for the device arena (one uint8 tensor) and the three streams.
+
+The library must have been built (`python -m paper_2403_10504_amd.build`);
+loading fails loudly otherwise.  There is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libatom.so")
+
+ATOM_MAX_NODES = 256
+ATOM_OK, ATOM_EINVAL, ATOM_ENOPLAN, ATOM_EBUDGET, ATOM_EHIP, ATOM_ESTATE, ATOM_ENOMEM_HOST = 0, -1, -2, -3, -4, -5, -6
+ATOM_F32, ATOM_BF16 = 0, 1
+ATOM_CKPT_DEVICE, ATOM_CKPT_HOST = 0, 1
+(ATOM_EPI_STORE, ATOM_EPI_STORE_F32, ATOM_EPI_ACC_F32, ATOM_EPI_BIAS, ATOM_EPI_BIAS_GELU, ATOM_EPI_BIAS_RESID,
+ ATOM_EPI_GELU_BWD) = range(7)
+WEIGHTS, GRAD_ACC, GRAD_LAST = 0, 1, 2
+
+
+class atom_config(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("n_layer", "d_model", "n_head", "d_mlp", "vocab", "seq_len", "batch", "accum", "dtype", "ckpt")]
+
+
+class atom_node_cost(ctypes.Structure):
+    _fields_ = [("weight_bytes", ctypes.c_uint64), ("t_fwd", ctypes.c_double), ("t_bwd", ctypes.c_double),
+                ("t_load", ctypes.c_double), ("t_store", ctypes.c_double)]
+
+
+class atom_plan(ctypes.Structure):
+    _fields_ = [("n_nodes", ctypes.c_int32), ("n_groups", ctypes.c_int32), ("n_slots", ctypes.c_int32),
+                ("overlap_ok", ctypes.c_int32), ("exhaustive", ctypes.c_int32), ("accum", ctypes.c_int32),
+                ("first", ctypes.c_int32 * ATOM_MAX_NODES), ("last", ctypes.c_int32 * ATOM_MAX_NODES),
+                ("budget_bytes", ctypes.c_uint64), ("reserve_bytes", ctypes.c_uint64),
+                ("slot_bytes", ctypes.c_uint64), ("arena_bytes", ctypes.c_uint64),
+                ("h2d_bytes", ctypes.c_uint64), ("d2h_bytes", ctypes.c_uint64),
+                ("forced_h2d_bytes", ctypes.c_uint64), ("pred_fwd_s", ctypes.c_double),
+                ("pred_step_s", ctypes.c_double), ("n_evaluated", ctypes.c_int64)]
+
+    def groups(self):
+        return [(self.first[g], self.last[g]) for g in range(self.n_groups)]
+
+
+class atom_tensor_desc(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 16), ("rows", ctypes.c_int32), ("cols", ctypes.c_int32),
+                ("offset", ctypes.c_uint64), ("bytes", ctypes.c_uint64)]
+
+
+class atom_stats(ctypes.Structure):
+    _fields_ = [("h2d_bytes", ctypes.c_uint64), ("d2h_bytes", ctypes.c_uint64), ("step_s", ctypes.c_double),
+                ("host_accum_s", ctypes.c_double), ("swap_ins", ctypes.c_int32), ("swap_outs", ctypes.c_int32)]
+
+
+class AtomError(RuntimeError):
+    def __init__(self, status, msg=""):
+        self.status = status
+        super().__init__(f"{status_string(status)} ({status}){': ' + msg if msg else ''}")
+
+
+_lib = None
+P = ctypes.c_void_p
+I32, I64, U64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64
+_SIGS = {
+    "atom_version": (ctypes.c_char_p, []),
+    "atom_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "atom_node_layout": (ctypes.c_int, [P, I32, P, I32, P, P]),
+    "atom_node_costs": (ctypes.c_int, [P, P, I32]),
+    "atom_reserve_bytes": (ctypes.c_int, [P, P]),
+    "atom_plan_search": (ctypes.c_int, [P, U64, U64, P, I32, P]),
+    "atom_plan_partition": (ctypes.c_int, [P, U64, P, I32, P]),
+    "atom_plan_fixed": (ctypes.c_int, [P, I32, P, I32, P]),
+    "atom_ctx_create": (ctypes.c_int, [P, P, P, U64, P, P, P, P]),
+    "atom_ctx_destroy": (None, [P]),
+    "atom_host_tensor": (ctypes.c_int, [P, I32, I32, P, P]),
+    "atom_zero_grads": (ctypes.c_int, [P]),
+    "atom_set_tokens": (ctypes.c_int, [P, P]),
+    "atom_swap_in": (ctypes.c_int, [P, I32]),
+    "atom_block_fwd": (ctypes.c_int, [P, I32, I32]),
+    "atom_block_bwd": (ctypes.c_int, [P, I32, I32]),
+    "atom_swap_out": (ctypes.c_int, [P, I32]),
+    "atom_sync": (ctypes.c_int, [P, P]),
+    "atom_step": (ctypes.c_int, [P, P, P]),
+    "atom_get_stats": (ctypes.c_int, [P, P]),
+    "atom_last_error": (ctypes.c_char_p, [P]),
+    "atom_k_gemm": (ctypes.c_int, [ctypes.c_int] * 7 + [P, I64, P, I64, P, I64, P, P, P, I64, P]),
+    "atom_k_layernorm_fwd": (ctypes.c_int, [ctypes.c_int, P, P, P, P, P, P, I64, ctypes.c_int, P]),
+    "atom_k_layernorm_bwd_part_floats": (I64, [I64, ctypes.c_int]),
+    "atom_k_layernorm_bwd": (ctypes.c_int, [ctypes.c_int, P, P, P, P, P, P, P, ctypes.c_int, P, P, P, I64,
+                                            ctypes.c_int, P]),
+    "atom_k_attn_fwd": (ctypes.c_int, [ctypes.c_int, P, P, P] + [ctypes.c_int] * 4 + [P]),
+    "atom_k_attn_bwd": (ctypes.c_int, [ctypes.c_int, P, P, P, P, P, P] + [ctypes.c_int] * 4 + [P]),
+    "atom_k_colsum_part_floats": (I64, [I64, ctypes.c_int]),
+    "atom_k_colsum": (ctypes.c_int, [ctypes.c_int, P, I64, ctypes.c_int, P, P, P]),
+    "atom_k_xent": (ctypes.c_int, [ctypes.c_int, P, I64, P, P, I64, P, I64, ctypes.c_int, ctypes.c_float, P]),
+    "atom_k_embed_fwd": (ctypes.c_int, [ctypes.c_int, P, P, P, P, I64, ctypes.c_int, ctypes.c_int, P]),
+}
+EXPORTED = tuple(_SIGS)
+
+
+def lib():
+    """The loaded libatom (raises if it was not built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2403_10504_amd.build`")
+        h = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(h, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = h
+    return _lib
+
+
+def status_string(status):
+    return lib().atom_status_string(status).decode()
+
+
+def _check(status, ctx=None):
+    if status != ATOM_OK:
+        msg = lib().atom_last_error(ctx).decode() if ctx else ""
+        raise AtomError(status, msg)
+
+
+def _ref(x):
+    return ctypes.byref(x)
+
+
+def make_config(cfg) -> atom_config:
+    """atom_config from a synthetic.Config (or any object with the same fields)."""
+    return atom_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_mlp, cfg.vocab, cfg.seq_len, cfg.batch,
+                       cfg.accum, ATOM_BF16 if cfg.dtype == "bf16" else ATOM_F32,
+                       ATOM_CKPT_HOST if getattr(cfg, "ckpt_host", False) else ATOM_CKPT_DEVICE)
+
+
+# ------------------------------------------------------------------ planner
+def atom_version():
+    return lib().atom_version().decode()
+
+
+def atom_node_layout(c: atom_config, node: int):
+    descs = (atom_tensor_desc * 16)()
+    n = I32()
+    nb = U64()
+    _check(lib().atom_node_layout(_ref(c), node, descs, 16, _ref(n), _ref(nb)))
+    return [(d.name.decode(), d.rows, d.cols, d.offset, d.bytes) for d in descs[: n.value]], nb.value
+
+
+def atom_node_costs(c: atom_config):
+    n = c.n_layer + 2
+    out = (atom_node_cost * n)()
+    _check(lib().atom_node_costs(_ref(c), out, n))
+    return out
+
+
+def atom_reserve_bytes(c: atom_config) -> int:
+    v = U64()
+    _check(lib().atom_reserve_bytes(_ref(c), _ref(v)))
+    return v.value
+
+
+def costs_array(costs):
+    """atom_node_cost array from a list of dicts (weight_bytes, t_fwd, t_bwd, t_load, t_store)."""
+    arr = (atom_node_cost * len(costs))()
+    for i, x in enumerate(costs):
+        arr[i] = atom_node_cost(int(x["weight_bytes"]), x["t_fwd"], x["t_bwd"], x["t_load"], x["t_store"])
+    return arr
+
+
+def atom_plan_search(c: atom_config, budget: int, reserve: int, costs) -> atom_plan:
+    p = atom_plan()
+    arr = costs if isinstance(costs, ctypes.Array) else costs_array(costs)
+    _check(lib().atom_plan_search(_ref(c), budget, reserve, arr, len(arr), _ref(p)))
+    return p
+
+
+def atom_plan_partition(c: atom_config, budget: int, costs=None) -> atom_plan:
+    p = atom_plan()
+    if costs is None:
+        _check(lib().atom_plan_partition(_ref(c), budget, None, 0, _ref(p)))
+    else:
+        arr = costs if isinstance(costs, ctypes.Array) else costs_array(costs)
+        _check(lib().atom_plan_partition(_ref(c), budget, arr, len(arr), _ref(p)))
+    return p
+
+
+def atom_plan_fixed(c: atom_config, last_nodes, n_slots: int) -> atom_plan:
+    p = atom_plan()
+    arr = (I32 * len(last_nodes))(*last_nodes)
+    _check(lib().atom_plan_fixed(_ref(c), len(last_nodes), arr, n_slots, _ref(p)))
+    return p
+
+
+# ------------------------------------------------------------------ context
+def atom_ctx_create(c: atom_config, plan: atom_plan, arena_ptr: int, arena_bytes: int, cs: int, hs: int, ds: int):
+    ctx = P()
+    _check(lib().atom_ctx_create(_ref(c), _ref(plan), arena_ptr, arena_bytes, cs, hs, ds, _ref(ctx)))
+    return ctx
+
+
+def atom_ctx_destroy(ctx):
+    lib().atom_ctx_destroy(ctx)
+
+
+def atom_host_tensor(ctx, node: int, which: int):
+    ptr = P()
+    nb = U64()
+    _check(lib().atom_host_tensor(ctx, node, which, _ref(ptr), _ref(nb)), ctx)
+    return ptr.value, nb.value
+
+
+def atom_zero_grads(ctx):
+    _check(lib().atom_zero_grads(ctx), ctx)
+
+
+def _tokens_ptr(tokens):
+    t = np.ascontiguousarray(tokens, dtype=np.int32)
+    return t, t.ctypes.data_as(P)
+
+
+def atom_set_tokens(ctx, tokens):
+    t, p = _tokens_ptr(tokens)
+    _check(lib().atom_set_tokens(ctx, p), ctx)
+
+
+def atom_swap_in(ctx, group: int):
+    _check(lib().atom_swap_in(ctx, group), ctx)
+
+
+def atom_block_fwd(ctx, node: int, micro: int):
+    _check(lib().atom_block_fwd(ctx, node, micro), ctx)
+
+
+def atom_block_bwd(ctx, node: int, micro: int):
+    _check(lib().atom_block_bwd(ctx, node, micro), ctx)
+
+
+def atom_swap_out(ctx, group: int):
+    _check(lib().atom_swap_out(ctx, group), ctx)
+
+
+def atom_sync(ctx) -> float:
+    v = ctypes.c_float()
+    _check(lib().atom_sync(ctx, _ref(v)), ctx)
+    return v.value
+
+
+def atom_step(ctx, tokens) -> float:
+    t, p = _tokens_ptr(tokens)
+    v = ctypes.c_float()
+    _check(lib().atom_step(ctx, p, _ref(v)), ctx)
+    return v.value
+
+
+def atom_get_stats(ctx) -> atom_stats:
+    s = atom_stats()
+    _check(lib().atom_get_stats(ctx, _ref(s)), ctx)
+    return s
+
+
+# ------------------------------------------------------------------ kernels
+def _kcall(name, *args):
+    _check(getattr(lib(), name)(*args))
+
+
+def atom_k_gemm(dtype, a_kcontig, b_kcontig, epi, M, N, K, A, lda, B, ldb, C, ldc, bias=None, resid=None, aux=None,
+                ldaux=0, stream=None):
+    _kcall("atom_k_gemm", dtype, int(a_kcontig), int(b_kcontig), epi, M, N, K, A, lda, B, ldb, C, ldc, bias, resid,
+           aux, ldaux, stream)
+
+
+def atom_k_layernorm_fwd(dtype, x, gamma, beta, y, mean, rstd, rows, d, stream=None):
+    _kcall("atom_k_layernorm_fwd", dtype, x, gamma, beta, y, mean, rstd, rows, d, stream)
+
+
+def atom_k_layernorm_bwd_part_floats(rows, d):
+    return lib().atom_k_layernorm_bwd_part_floats(rows, d)
+
+
+def atom_k_layernorm_bwd(dtype, dy, x, mean, rstd, gamma, dres, dres_lp, accumulate, dgamma, dbeta, part, rows, d,
+                         stream=None):
+    _kcall("atom_k_layernorm_bwd", dtype, dy, x, mean, rstd, gamma, dres, dres_lp, int(accumulate), dgamma, dbeta,
+           part, rows, d, stream)
+
+
+def atom_k_attn_fwd(dtype, qkv, o, lse, B, T, H, dh, stream=None):
+    _kcall("atom_k_attn_fwd", dtype, qkv, o, lse, B, T, H, dh, stream)
+
+
+def atom_k_attn_bwd(dtype, qkv, o, dout, lse, delta, dqkv, B, T, H, dh, stream=None):
+    _kcall("atom_k_attn_bwd", dtype, qkv, o, dout, lse, delta, dqkv, B, T, H, dh, stream)
+
+
+def atom_k_colsum_part_floats(rows, cols):
+    return lib().atom_k_colsum_part_floats(rows, cols)
+
+
+def atom_k_colsum(dtype, x, rows, cols, out, part, stream=None):
+    _kcall("atom_k_colsum", dtype, x, rows, cols, out, part, stream)
+
+
+def atom_k_xent(dtype, logits, ldz, tgt, dz, lddz, loss_rows, rows, V, scale, stream=None):
+    _kcall("atom_k_xent", dtype, logits, ldz, tgt, dz, lddz, loss_rows, rows, V, ctypes.c_float(scale), stream)
+
+
+def atom_k_embed_fwd(dtype, tok, wte, wpe, x, n_tok, T, d, stream=None):
+    _kcall("atom_k_embed_fwd", dtype, tok, wte, wpe, x, n_tok, T, d, stream)

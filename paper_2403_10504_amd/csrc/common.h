@@ -1,0 +1,123 @@
+// Device-side helpers shared by the CDNA4 (gfx950) kernels of libatom.
+//
+// Element types: activations and weights are either fp32 (validation mode) or
+// bfloat16 stored as raw uint16 bit patterns.  Accumulation is always fp32.
+//
+// MFMA convention used by every kernel.  A 16x16 output tile is produced by
+// __builtin_amdgcn_mfma_f32_16x16x32_bf16 (bf16) or by eight
+// __builtin_amdgcn_mfma_f32_16x16x4f32 (fp32) over a 32-wide slice of the
+// contraction index k.  Lane l supplies operand row (or column) l % 16 and the
+// eight k values 8*(l/16) .. 8*(l/16)+7 of the slice, as one "fragment".  The
+// same (lane group, element) -> k map is used for both operands, so any
+// permutation of k inside a slice leaves the contraction unchanged.  That
+// freedom lets a kernel feed the fp32 accumulators of one MFMA straight into
+// the next one (attention's P tile) by choosing which k each element holds.
+// Output: lane l holds D[4*(l/16) + r][l % 16] in accumulator r (r = 0..3).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef uint16_t bf16_t;
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+#define ATOM_DEV __device__ __forceinline__
+
+ATOM_DEV float bf2f(bf16_t h) { return __uint_as_float(static_cast<uint32_t>(h) << 16); }
+
+// fp32 -> bf16, round to nearest even; NaN stays NaN.
+ATOM_DEV bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<bf16_t>(u >> 16);
+}
+
+template <typename T> ATOM_DEV float to_f(T v);
+template <> ATOM_DEV float to_f<float>(float v) { return v; }
+template <> ATOM_DEV float to_f<bf16_t>(bf16_t v) { return bf2f(v); }
+
+template <typename T> ATOM_DEV T from_f(float v);
+template <> ATOM_DEV float from_f<float>(float v) { return v; }
+template <> ATOM_DEV bf16_t from_f<bf16_t>(float v) { return f2bf(v); }
+
+// A fragment: eight consecutive-k elements of one operand row for one lane.
+template <typename T> struct Frag;
+template <> struct Frag<bf16_t> { uint4 v; };
+template <> struct Frag<float> { float4 lo, hi; };
+
+// Load a fragment from 8 contiguous elements (16-byte aligned for bf16,
+// 32-byte aligned for fp32), from LDS or global memory.
+ATOM_DEV void frag_load(Frag<bf16_t>& f, const bf16_t* p) { f.v = *reinterpret_cast<const uint4*>(p); }
+ATOM_DEV void frag_load(Frag<float>& f, const float* p) {
+  f.lo = *reinterpret_cast<const float4*>(p);
+  f.hi = *reinterpret_cast<const float4*>(p + 4);
+}
+// Load a fragment from two runs of four contiguous elements (elements 0..3
+// from p0, 4..7 from p1).
+ATOM_DEV void frag_load2(Frag<bf16_t>& f, const bf16_t* p0, const bf16_t* p1) {
+  uint2 a = *reinterpret_cast<const uint2*>(p0);
+  uint2 b = *reinterpret_cast<const uint2*>(p1);
+  f.v = make_uint4(a.x, a.y, b.x, b.y);
+}
+ATOM_DEV void frag_load2(Frag<float>& f, const float* p0, const float* p1) {
+  f.lo = *reinterpret_cast<const float4*>(p0);
+  f.hi = *reinterpret_cast<const float4*>(p1);
+}
+ATOM_DEV void frag_zero(Frag<bf16_t>& f) { f.v = make_uint4(0, 0, 0, 0); }
+ATOM_DEV void frag_zero(Frag<float>& f) {
+  f.lo = make_float4(0.f, 0.f, 0.f, 0.f);
+  f.hi = f.lo;
+}
+// Build a fragment from eight fp32 values (rounded to the element type).
+ATOM_DEV void frag_from_f32(Frag<bf16_t>& f, const float* x) {
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    w[i] = static_cast<uint32_t>(f2bf(x[2 * i])) | (static_cast<uint32_t>(f2bf(x[2 * i + 1])) << 16);
+  f.v = make_uint4(w[0], w[1], w[2], w[3]);
+}
+ATOM_DEV void frag_from_f32(Frag<float>& f, const float* x) {
+  f.lo = make_float4(x[0], x[1], x[2], x[3]);
+  f.hi = make_float4(x[4], x[5], x[6], x[7]);
+}
+
+// acc += A_frag x B_frag over one 32-wide k slice (16x16 output tile).
+ATOM_DEV void mfma16(f32x4_t& acc, const Frag<bf16_t>& a, const Frag<bf16_t>& b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a.v),
+                                                 __builtin_bit_cast(bf16x8_t, b.v), acc, 0, 0, 0);
+}
+ATOM_DEV void mfma16(f32x4_t& acc, const Frag<float>& a, const Frag<float>& b) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.x, b.lo.x, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.y, b.lo.y, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.z, b.lo.z, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.w, b.lo.w, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.x, b.hi.x, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.y, b.hi.y, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.z, b.hi.z, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.w, b.hi.w, acc, 0, 0, 0);
+}
+
+// Wavefront (64 lanes) reductions.
+ATOM_DEV float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+ATOM_DEV float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// GELU, tanh form, and its derivative.
+ATOM_DEV float gelu_f(float u) {
+  const float c = 0.7978845608028654f, a = 0.044715f;
+  return 0.5f * u * (1.f + tanhf(c * (u + a * u * u * u)));
+}
+ATOM_DEV float gelu_grad_f(float u) {
+  const float c = 0.7978845608028654f, a = 0.044715f;
+  float t = tanhf(c * (u + a * u * u * u));
+  return 0.5f * (1.f + t) + 0.5f * u * (1.f - t * t) * c * (1.f + 3.f * a * u * u);
+}

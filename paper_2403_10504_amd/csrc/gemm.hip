@@ -1,0 +1,332 @@
+// Dense GEMM on CDNA4 matrix cores with fused epilogues.
+//
+//   C[m][n] (op)= sum_k A(m,k) * B(k,n),   fp32 accumulation.
+//
+// Operand layouts (both row-major in memory):
+//   A_KC: A(m,k) = A[m*lda + k]   (k contiguous)   else A(m,k) = A[k*lda + m]
+//   B_KC: B(k,n) = B[n*ldb + k]   (k contiguous)   else B(k,n) = B[k*ldb + n]
+// The three products of a linear layer y = x W^T + b with W stored [out][in]:
+//   forward   y  = x  W^T : A = x  (KC),          B = W  (KC)
+//   data grad dx = dy W   : A = dy (KC),          B = W  (not KC)
+//   weight grad dW = dy^T x: A = dy (not KC),      B = x  (not KC)
+//
+// Tiling: 128x128 output tile per 256-thread workgroup (2x2 waves of 64x64),
+// 128-byte k tile (64 bf16 or 32 fp32), double-buffered in LDS.  Every
+// operand is staged in LDS with k contiguous (rows padded to 144 bytes to
+// spread ds_read_b128 over the banks); operands that are not k-contiguous in
+// memory are transposed while being written to LDS.  Each lane reads
+// 16x16x32 MFMA fragments (see common.h) and accumulates 16 tiles.
+// Workgroup ids are remapped so that neighbouring output tiles, which share
+// A rows or B columns, run on the same XCD (each XCD has its own L2).
+#include "common.h"
+#include "launch.h"
+
+namespace atom {
+namespace {
+
+constexpr int BM = 128, BN = 128, NT = 256;
+constexpr int ROW_BYTES = 128, PITCH_BYTES = 144;
+
+template <typename T>
+struct Tile {
+  static constexpr int BK = ROW_BYTES / sizeof(T);    // k per tile
+  static constexpr int PITCH = PITCH_BYTES / sizeof(T);
+  static constexpr int KV = 16 / sizeof(T);           // elements per 16 bytes
+  static constexpr int PAIR = 4 / sizeof(T);          // elements per dword
+  static constexpr int NSLICE = BK / 32;
+};
+
+// Stages a 128-row x BK tile of one operand (rows = m for A, n for B).
+// Registers hold the next tile while the current one is being consumed.
+template <typename T, bool KC>
+struct Loader {
+  uint32_t r[16];
+
+  // KC: rows are contiguous along k.  128 rows x 8 chunks of 16 bytes.
+  // !KC: memory is [k][row]; each thread loads KV k-rows x PAIR rows.
+  __device__ void load(const T* __restrict__ X, int64_t ld, int R, int K, int r0, int k0, int tid) {
+    using TL = Tile<T>;
+    if constexpr (KC) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        int c = tid + NT * i;
+        int row = c >> 3, kc = c & 7;
+        int gr = r0 + row, gk = k0 + kc * TL::KV;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (gr < R && gk < K) v = *reinterpret_cast<const uint4*>(X + static_cast<int64_t>(gr) * ld + gk);
+        r[4 * i + 0] = v.x; r[4 * i + 1] = v.y; r[4 * i + 2] = v.z; r[4 * i + 3] = v.w;
+      }
+    } else {
+      constexpr int UNITS_PER_KB = 128 / TL::PAIR;            // 64 (bf16) or 128 (fp32)
+      constexpr int UNITS_PER_THREAD = (8 * UNITS_PER_KB) / NT; // 2 or 4
+#pragma unroll
+      for (int i = 0; i < UNITS_PER_THREAD; ++i) {
+        int u = tid + NT * i;
+        int kb = u / UNITS_PER_KB, rc = u % UNITS_PER_KB;
+        int gr = r0 + rc * TL::PAIR;
+#pragma unroll
+        for (int j = 0; j < TL::KV; ++j) {
+          int gk = k0 + kb * TL::KV + j;
+          uint32_t v = 0;
+          if (gr < R && gk < K) v = *reinterpret_cast<const uint32_t*>(X + static_cast<int64_t>(gk) * ld + gr);
+          r[i * TL::KV + j] = v;
+        }
+      }
+    }
+  }
+
+  __device__ void store(T* __restrict__ S, int tid) {
+    using TL = Tile<T>;
+    if constexpr (KC) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        int c = tid + NT * i;
+        int row = c >> 3, kc = c & 7;
+        *reinterpret_cast<uint4*>(S + row * TL::PITCH + kc * TL::KV) =
+            make_uint4(r[4 * i], r[4 * i + 1], r[4 * i + 2], r[4 * i + 3]);
+      }
+    } else {
+      constexpr int UNITS_PER_KB = 128 / TL::PAIR;
+      constexpr int UNITS_PER_THREAD = (8 * UNITS_PER_KB) / NT;
+#pragma unroll
+      for (int i = 0; i < UNITS_PER_THREAD; ++i) {
+        int u = tid + NT * i;
+        int kb = u / UNITS_PER_KB, rc = u % UNITS_PER_KB;
+        const uint32_t* d = r + i * TL::KV;
+        if constexpr (sizeof(T) == 2) {
+          // d[j] packs (row 2rc, row 2rc+1) at k = 8kb + j; transpose to two
+          // 16-byte rows of 8 consecutive k.
+          uint4 lo, hi;
+          lo.x = (d[0] & 0xffffu) | (d[1] << 16); hi.x = (d[0] >> 16) | (d[1] & 0xffff0000u);
+          lo.y = (d[2] & 0xffffu) | (d[3] << 16); hi.y = (d[2] >> 16) | (d[3] & 0xffff0000u);
+          lo.z = (d[4] & 0xffffu) | (d[5] << 16); hi.z = (d[4] >> 16) | (d[5] & 0xffff0000u);
+          lo.w = (d[6] & 0xffffu) | (d[7] << 16); hi.w = (d[6] >> 16) | (d[7] & 0xffff0000u);
+          *reinterpret_cast<uint4*>(S + (2 * rc) * TL::PITCH + kb * 8) = lo;
+          *reinterpret_cast<uint4*>(S + (2 * rc + 1) * TL::PITCH + kb * 8) = hi;
+        } else {
+          *reinterpret_cast<uint4*>(S + rc * TL::PITCH + kb * 4) = make_uint4(d[0], d[1], d[2], d[3]);
+        }
+      }
+    }
+  }
+};
+
+template <typename T>
+__device__ __forceinline__ void store4(T* p, const float* v, bool vec, int nvalid) {
+  if (vec) {
+    if constexpr (sizeof(T) == 2) {
+      uint2 w;
+      w.x = static_cast<uint32_t>(f2bf(v[0])) | (static_cast<uint32_t>(f2bf(v[1])) << 16);
+      w.y = static_cast<uint32_t>(f2bf(v[2])) | (static_cast<uint32_t>(f2bf(v[3])) << 16);
+      *reinterpret_cast<uint2*>(p) = w;
+    } else {
+      *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+  } else {
+    for (int r = 0; r < nvalid; ++r) p[r] = from_f<T>(v[r]);
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void load4(const T* p, float* v, bool vec, int nvalid) {
+  if (vec) {
+    if constexpr (sizeof(T) == 2) {
+      uint2 w = *reinterpret_cast<const uint2*>(p);
+      v[0] = bf2f(w.x & 0xffff); v[1] = bf2f(w.x >> 16); v[2] = bf2f(w.y & 0xffff); v[3] = bf2f(w.y >> 16);
+    } else {
+      float4 w = *reinterpret_cast<const float4*>(p);
+      v[0] = w.x; v[1] = w.y; v[2] = w.z; v[3] = w.w;
+    }
+  } else {
+    for (int r = 0; r < 4; ++r) v[r] = r < nvalid ? to_f<T>(p[r]) : 0.f;
+  }
+}
+
+template <typename T, bool AKC, bool BKC, int EPI>
+__global__ void __launch_bounds__(NT, 2) gemm_kernel(GemmArgs g) {
+  using TL = Tile<T>;
+  __shared__ __attribute__((aligned(16))) T As[2][BM * TL::PITCH];
+  __shared__ __attribute__((aligned(16))) T Bs[2][BN * TL::PITCH];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, w = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int wm = w >> 1, wn = w & 1;
+
+  // Tile order: XCD-aware remap, then groups of 8 row-tiles sweeping columns.
+  const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
+  const int total = tiles_m * tiles_n;
+  int pid = blockIdx.x;
+  if ((total & 7) == 0) pid = (pid & 7) * (total >> 3) + (pid >> 3);
+  constexpr int GROUP = 8;
+  const int per_group = GROUP * tiles_n;
+  const int first_m = (pid / per_group) * GROUP;
+  const int gsize = min(tiles_m - first_m, GROUP);
+  const int pid_m = first_m + (pid % per_group) % gsize;
+  const int pid_n = (pid % per_group) / gsize;
+  const int m0 = pid_m * BM, n0 = pid_n * BN;
+
+  const T* __restrict__ A = static_cast<const T*>(g.A);
+  const T* __restrict__ B = static_cast<const T*>(g.B);
+
+  Loader<T, AKC> la;
+  Loader<T, BKC> lb;
+  f32x4_t acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int nk = (g.K + TL::BK - 1) / TL::BK;
+  la.load(A, g.lda, g.M, g.K, m0, 0, tid);
+  lb.load(B, g.ldb, g.N, g.K, n0, 0, tid);
+  la.store(As[0], tid);
+  lb.store(Bs[0], tid);
+  __syncthreads();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    const bool more = kt + 1 < nk;
+    if (more) {
+      la.load(A, g.lda, g.M, g.K, m0, (kt + 1) * TL::BK, tid);
+      lb.load(B, g.ldb, g.N, g.K, n0, (kt + 1) * TL::BK, tid);
+    }
+    const T* as = As[cur];
+    const T* bs = Bs[cur];
+#pragma unroll
+    for (int s = 0; s < TL::NSLICE; ++s) {
+      Frag<T> fa[4], fb[4];
+      const int kk = s * 32 + lg * 8;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) frag_load(fa[i], as + (wm * 64 + i * 16 + lr) * TL::PITCH + kk);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) frag_load(fb[j], bs + (wn * 64 + j * 16 + lr) * TL::PITCH + kk);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) mfma16(acc[i][j], fb[j], fa[i]);
+    }
+    if (more) {
+      la.store(As[cur ^ 1], tid);
+      lb.store(Bs[cur ^ 1], tid);
+    }
+    __syncthreads();
+  }
+
+  // Epilogue: acc[i][j][r] = C[m][nb + r].
+  const bool ld_vec = (g.ldc & 3) == 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + wm * 64 + i * 16 + lr;
+    if (m >= g.M) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int nb = n0 + wn * 64 + j * 16 + lg * 4;
+      if (nb >= g.N) continue;
+      const int nvalid = min(4, g.N - nb);
+      const bool vec = ld_vec && nvalid == 4;
+      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      const int64_t off = static_cast<int64_t>(m) * g.ldc + nb;
+      if constexpr (EPI == EPI_STORE) {
+        store4<T>(static_cast<T*>(g.C) + off, v, vec, nvalid);
+      } else if constexpr (EPI == EPI_STORE_F32) {
+        store4<float>(static_cast<float*>(g.C) + off, v, vec, nvalid);
+      } else if constexpr (EPI == EPI_ACC_F32) {
+        float o[4];
+        load4<float>(static_cast<const float*>(g.C) + off, o, vec, nvalid);
+        for (int r = 0; r < 4; ++r) v[r] += o[r];
+        store4<float>(static_cast<float*>(g.C) + off, v, vec, nvalid);
+      } else if constexpr (EPI == EPI_BIAS) {
+        float b[4];
+        load4<T>(static_cast<const T*>(g.bias) + nb, b, (nvalid == 4) && ((nb & 3) == 0), nvalid);
+        for (int r = 0; r < 4; ++r) v[r] += b[r];
+        store4<T>(static_cast<T*>(g.C) + off, v, vec, nvalid);
+      } else if constexpr (EPI == EPI_BIAS_GELU) {
+        float b[4];
+        load4<T>(static_cast<const T*>(g.bias) + nb, b, (nvalid == 4) && ((nb & 3) == 0), nvalid);
+        float gv[4];
+        for (int r = 0; r < 4; ++r) {
+          // g = GELU(u) of the stored (rounded) u, so the backward sees the same u.
+          float u = to_f<T>(from_f<T>(v[r] + b[r]));
+          v[r] = u;
+          gv[r] = gelu_f(u);
+        }
+        const int64_t aoff = static_cast<int64_t>(m) * g.ldaux + nb;
+        store4<T>(static_cast<T*>(g.aux) + aoff, v, vec && (g.ldaux & 3) == 0, nvalid);
+        store4<T>(static_cast<T*>(g.C) + off, gv, vec, nvalid);
+      } else if constexpr (EPI == EPI_BIAS_RESID) {
+        float b[4], x[4];
+        load4<T>(static_cast<const T*>(g.bias) + nb, b, (nvalid == 4) && ((nb & 3) == 0), nvalid);
+        load4<float>(g.resid + off, x, vec, nvalid);
+        for (int r = 0; r < 4; ++r) v[r] = x[r] + (v[r] + b[r]);
+        store4<float>(static_cast<float*>(g.C) + off, v, vec, nvalid);
+      } else if constexpr (EPI == EPI_GELU_BWD) {
+        float u[4];
+        const int64_t aoff = static_cast<int64_t>(m) * g.ldaux + nb;
+        load4<T>(static_cast<const T*>(g.aux) + aoff, u, vec && (g.ldaux & 3) == 0, nvalid);
+        for (int r = 0; r < 4; ++r) v[r] *= gelu_grad_f(u[r]);
+        store4<T>(static_cast<T*>(g.C) + off, v, vec, nvalid);
+      }
+    }
+  }
+}
+
+template <typename T, bool AKC, bool BKC>
+hipError_t launch_t(const GemmArgs& g, int epi, hipStream_t s) {
+  const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+  dim3 grid(tiles), block(NT);
+  switch (epi) {
+#define ATOM_CASE(E) \
+  case E: hipLaunchKernelGGL((gemm_kernel<T, AKC, BKC, E>), grid, block, 0, s, g); break;
+    ATOM_CASE(EPI_STORE)
+    ATOM_CASE(EPI_STORE_F32)
+    ATOM_CASE(EPI_ACC_F32)
+    ATOM_CASE(EPI_BIAS)
+    ATOM_CASE(EPI_BIAS_GELU)
+    ATOM_CASE(EPI_BIAS_RESID)
+    ATOM_CASE(EPI_GELU_BWD)
+#undef ATOM_CASE
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+// Shape and alignment rules checked before launch (bounds inside the kernel
+// rely on them): K a multiple of 8 (bf16) or 4 (fp32), so a 16-byte k chunk
+// is either wholly inside or wholly outside; a k-contiguous operand needs a
+// leading dimension that keeps 16-byte chunks aligned; a bf16 operand that is
+// not k-contiguous is read as dwords of two rows, so it needs an even row
+// count and an even leading dimension; all pointers 16-byte aligned.
+hipError_t gemm_check(const GemmArgs& g, int dtype, bool akc, bool bkc) {
+  const int kv = dtype == DT_BF16 ? 8 : 4;
+  if (g.M < 0 || g.N < 0 || g.K < 0) return hipErrorInvalidValue;
+  if (g.K % kv) return hipErrorInvalidValue;
+  if (akc ? g.lda % kv : (dtype == DT_BF16 && ((g.lda | g.M) & 1))) return hipErrorInvalidValue;
+  if (bkc ? g.ldb % kv : (dtype == DT_BF16 && ((g.ldb | g.N) & 1))) return hipErrorInvalidValue;
+  if ((reinterpret_cast<uintptr_t>(g.A) | reinterpret_cast<uintptr_t>(g.B) | reinterpret_cast<uintptr_t>(g.C)) & 15)
+    return hipErrorInvalidValue;
+  if (akc ? g.lda < g.K : g.lda < g.M) return hipErrorInvalidValue;
+  if (bkc ? g.ldb < g.K : g.ldb < g.N) return hipErrorInvalidValue;
+  if (g.ldc < g.N) return hipErrorInvalidValue;
+  return hipSuccess;
+}
+
+hipError_t gemm(const GemmArgs& g, int dtype, bool akc, bool bkc, int epi, hipStream_t s) {
+  hipError_t e = gemm_check(g, dtype, akc, bkc);
+  if (e != hipSuccess) return e;
+  if (g.M == 0 || g.N == 0) return hipSuccess;
+  if (dtype == DT_BF16) {
+    if (akc && bkc) return launch_t<bf16_t, true, true>(g, epi, s);
+    if (akc && !bkc) return launch_t<bf16_t, true, false>(g, epi, s);
+    if (!akc && !bkc) return launch_t<bf16_t, false, false>(g, epi, s);
+    return launch_t<bf16_t, false, true>(g, epi, s);
+  }
+  if (akc && bkc) return launch_t<float, true, true>(g, epi, s);
+  if (akc && !bkc) return launch_t<float, true, false>(g, epi, s);
+  if (!akc && !bkc) return launch_t<float, false, false>(g, epi, s);
+  return launch_t<float, false, true>(g, epi, s);
+}
+
+}  // namespace atom

@@ -1,0 +1,56 @@
+// Host-side layout rules shared by the planner and the runtime: the tensor
+// layout of each node's host range and the static carving of the device
+// arena.  Pure C++; no HIP dependency.
+#pragma once
+
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/atom.h"
+
+namespace atom {
+
+constexpr uint64_t ALIGN = 256;
+inline uint64_t align_up(uint64_t x, uint64_t a = ALIGN) { return (x + a - 1) / a * a; }
+inline int64_t vocab_padded(int64_t V) { return (V + 127) / 128 * 128; }
+inline int elem_bytes(const atom_config& c) { return c.dtype == ATOM_BF16 ? 2 : 4; }
+// Rows of the logits chunk of the LM head (the [N][V] fp32 logits are never
+// held whole).
+constexpr int64_t HEAD_CHUNK = 2048;
+
+struct TensorDesc {
+  std::string name;
+  int64_t rows, cols;
+  uint64_t offset, bytes;
+};
+
+// Tensors of node `node` with 256-byte aligned offsets; returns node bytes.
+uint64_t node_tensors(const atom_config& c, int node, std::vector<TensorDesc>* out);
+
+// Validation of a configuration; returns an empty string when usable.
+std::string check_config(const atom_config& c);
+
+// Offsets (bytes from the arena base) of every region of the device arena.
+struct ArenaLayout {
+  // reserve regions
+  uint64_t tok_in, tok_tgt, emb_perm, emb_seg, emb_uniq;
+  uint64_t ckpt, ckpt_bytes_each;  // (L+1) x accum x [N][d] fp32 block inputs
+  uint64_t dres, dres_lp;          // accum x [N][d] fp32 / working dtype
+  uint64_t loss_rows, loss_out;
+  uint64_t ws;                     // start of the union workspace
+  // block workspace (offsets inside ws)
+  uint64_t a, qkv, o, x1, c, u, g, mu1, rs1, mu2, rs2, lse, delta, du, dbuf, dout, dqkv, part;
+  // head workspace (offsets inside ws)
+  uint64_t yhat, fmu, frs, logits, dz, dyhat, hpart;
+  uint64_t ws_bytes, part_floats;
+  uint64_t reserve_bytes;
+  // slots (valid once a plan is known)
+  uint64_t wslots, gslots, accslot;
+  uint64_t arena_bytes;
+};
+
+ArenaLayout arena_layout(const atom_config& c, uint64_t slot_bytes, int n_slots);
+
+}  // namespace atom

@@ -1,0 +1,446 @@
+// Row- and column-wise kernels of the GPT step: LayerNorm forward and
+// backward, deterministic column sums (bias and LayerNorm-parameter grads),
+// token/position embedding forward and backward, softmax cross-entropy, and
+// small helpers.  All are HBM-bound: each reads its inputs once with
+// coalesced accesses and reduces inside a wavefront or a workgroup in a fixed
+// order, so every result is bitwise reproducible.
+#include "common.h"
+#include "launch.h"
+
+namespace atom {
+namespace {
+
+constexpr float LN_EPS = 1e-5f;
+
+// ---------------------------------------------------------------- LayerNorm
+// One 256-thread workgroup per row; thread t owns columns t, t+256, ...
+// (at most MAXE of them).  Reductions: wavefront shuffles, then the four
+// wave sums in order, so results do not depend on scheduling.
+__device__ __forceinline__ float block_sum4(float v, float* sh) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  v = wave_sum(v);
+  if (lane == 0) sh[w] = v;
+  __syncthreads();
+  const float r = (sh[0] + sh[1]) + (sh[2] + sh[3]);
+  __syncthreads();
+  return r;
+}
+
+template <typename T, int MAXE>
+__global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ x, const T* __restrict__ gamma,
+                                                     const T* __restrict__ beta, T* __restrict__ y,
+                                                     float* __restrict__ mean, float* __restrict__ rstd, int d) {
+  __shared__ float sh[4];
+  const int tid = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const float* xr = x + row * d;
+  float v[MAXE];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXE; ++i) {
+    const int c = tid + 256 * i;
+    v[i] = c < d ? xr[c] : 0.f;
+    s += v[i];
+  }
+  const float mu = block_sum4(s, sh) / static_cast<float>(d);
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXE; ++i)
+    if (tid + 256 * i < d) {
+      const float t = v[i] - mu;
+      q += t * t;
+    }
+  const float var = block_sum4(q, sh) / static_cast<float>(d);
+  const float r = 1.f / sqrtf(var + LN_EPS);
+  T* yr = y + row * d;
+#pragma unroll
+  for (int i = 0; i < MAXE; ++i) {
+    const int c = tid + 256 * i;
+    if (c < d) yr[c] = from_f<T>((v[i] - mu) * r * to_f<T>(gamma[c]) + to_f<T>(beta[c]));
+  }
+  if (tid == 0) {
+    mean[row] = mu;
+    rstd[row] = r;
+  }
+}
+
+// Backward: LNB_ROWS consecutive rows per workgroup; per-thread partial
+// column sums of dy*xhat and dy go to part[block][2][d].
+constexpr int LNB_ROWS = 16;
+
+template <typename T, int MAXE>
+__global__ void __launch_bounds__(256) ln_bwd_kernel(const T* __restrict__ dy, const float* __restrict__ x,
+                                                     const float* __restrict__ mean, const float* __restrict__ rstd,
+                                                     const T* __restrict__ gamma, float* __restrict__ dres,
+                                                     T* __restrict__ dres_lp, int accumulate,
+                                                     float* __restrict__ part, int64_t rows, int d) {
+  // colacc[0][c] / colacc[1][c]: this workgroup's running sums of dy*xhat and
+  // dy for column c (each column is owned by one thread).
+  extern __shared__ float colacc[];
+  __shared__ float sh[4];
+  const int tid = threadIdx.x;
+  for (int c = tid; c < 2 * d; c += 256) colacc[c] = 0.f;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * LNB_ROWS;
+#pragma unroll 1
+  for (int rr = 0; rr < LNB_ROWS; ++rr) {
+    const int64_t row = r0 + rr;
+    if (row >= rows) break;
+    const float mu = mean[row], r = rstd[row];
+    const T* dyr = dy + row * d;
+    const float* xr = x + row * d;
+    float* dr = dres + row * d;
+    float dyv[MAXE], xh[MAXE];
+    float sa = 0.f, sb = 0.f;
+#pragma unroll
+    for (int i = 0; i < MAXE; ++i) {
+      const int c = tid + 256 * i;
+      dyv[i] = 0.f;
+      xh[i] = 0.f;
+      if (c < d) {
+        dyv[i] = to_f<T>(dyr[c]);
+        xh[i] = (xr[c] - mu) * r;
+        const float gp = dyv[i] * to_f<T>(gamma[c]);
+        sa += gp;
+        sb += gp * xh[i];
+        colacc[c] += dyv[i] * xh[i];
+        colacc[d + c] += dyv[i];
+      }
+    }
+    const float a = block_sum4(sa, sh) / static_cast<float>(d);
+    const float b = block_sum4(sb, sh) / static_cast<float>(d);
+#pragma unroll
+    for (int i = 0; i < MAXE; ++i) {
+      const int c = tid + 256 * i;
+      if (c < d) {
+        const float dx = r * (dyv[i] * to_f<T>(gamma[c]) - a - xh[i] * b);
+        const float o = accumulate ? dr[c] + dx : dx;
+        dr[c] = o;
+        if (dres_lp) dres_lp[row * d + c] = from_f<T>(o);
+      }
+    }
+  }
+  float* p = part + static_cast<int64_t>(blockIdx.x) * 2 * d;
+  for (int c = tid; c < 2 * d; c += 256) p[c] = colacc[c];
+}
+
+// ------------------------------------------------------------- column sums
+constexpr int CS_ROWS = 64;
+
+template <typename T>
+__global__ void __launch_bounds__(256) colsum_partial_kernel(const T* __restrict__ x, int64_t rows, int cols,
+                                                             int64_t ld, float* __restrict__ part) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= cols) return;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * CS_ROWS;
+  const int64_t r1 = min(rows, r0 + CS_ROWS);
+  float s = 0.f;
+  for (int64_t r = r0; r < r1; ++r) s += to_f<T>(x[r * ld + c]);
+  part[static_cast<int64_t>(blockIdx.y) * cols + c] = s;
+}
+
+template <typename TO>
+__global__ void __launch_bounds__(256) sum_parts_kernel(const float* __restrict__ part, int64_t nparts, int cols,
+                                                        int64_t stride, TO* __restrict__ out, int accumulate) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= cols) return;
+  float s = 0.f;
+  for (int64_t p = 0; p < nparts; ++p) s += part[p * stride + c];
+  if (accumulate) s += to_f<TO>(out[c]);
+  out[c] = from_f<TO>(s);
+}
+
+// --------------------------------------------------------------- embedding
+template <typename T>
+__global__ void __launch_bounds__(256) embed_fwd_kernel(const int32_t* __restrict__ tok, const T* __restrict__ wte,
+                                                        const T* __restrict__ wpe, float* __restrict__ x, int T_,
+                                                        int d) {
+  const int64_t n = blockIdx.x;
+  const int64_t v = tok[n];
+  const int64_t t = n % T_;
+  for (int c = threadIdx.x; c < d; c += 256)
+    x[n * d + c] = to_f<T>(wte[v * d + c]) + to_f<T>(wpe[t * d + c]);
+}
+
+template <typename TO>
+__global__ void __launch_bounds__(256) embed_bwd_wte_kernel(const float* __restrict__ dx,
+                                                            const int32_t* __restrict__ perm,
+                                                            const int32_t* __restrict__ seg,
+                                                            const int32_t* __restrict__ uniq, TO* __restrict__ dwte,
+                                                            int d, int accumulate) {
+  const int u = blockIdx.x;
+  const int p0 = seg[u], p1 = seg[u + 1];
+  const int64_t v = uniq[u];
+  for (int c = threadIdx.x; c < d; c += 256) {
+    float s = 0.f;
+    for (int p = p0; p < p1; ++p) s += dx[static_cast<int64_t>(perm[p]) * d + c];
+    if (accumulate) s += to_f<TO>(dwte[v * d + c]);
+    dwte[v * d + c] = from_f<TO>(s);
+  }
+}
+
+template <typename TO>
+__global__ void __launch_bounds__(256) embed_bwd_wpe_kernel(const float* __restrict__ dx, TO* __restrict__ dwpe,
+                                                            int T_, int B, int d, int accumulate) {
+  const int64_t t = blockIdx.x;
+  for (int c = threadIdx.x; c < d; c += 256) {
+    float s = 0.f;
+    for (int b = 0; b < B; ++b) s += dx[(static_cast<int64_t>(b) * T_ + t) * d + c];
+    if (accumulate) s += to_f<TO>(dwpe[t * d + c]);
+    dwpe[t * d + c] = from_f<TO>(s);
+  }
+}
+
+// ------------------------------------------------------------ cross-entropy
+__device__ __forceinline__ void merge_ms(float& m, float& s, float m2, float s2) {
+  const float mm = fmaxf(m, m2);
+  s = s * __expf(m - mm) + s2 * __expf(m2 - mm);
+  m = mm;
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) xent_kernel(const float* __restrict__ z, int64_t ldz,
+                                                   const int32_t* __restrict__ tgt, T* __restrict__ dz, int64_t lddz,
+                                                   float* __restrict__ loss_rows, int V, float scale) {
+  __shared__ float sm[8], ss[8];
+  const int64_t row = blockIdx.x;
+  const float* zr = z + row * ldz;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  float m = -INFINITY, s = 0.f;
+  for (int v = tid; v < V; v += 256) {
+    const float x = zr[v];
+    if (x > m) {
+      s = s * __expf(m - x) + 1.f;
+      m = x;
+    } else {
+      s += __expf(x - m);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float m2 = __shfl_xor(m, o, 64), s2 = __shfl_xor(s, o, 64);
+    merge_ms(m, s, m2, s2);
+  }
+  if (lane == 0) {
+    sm[w] = m;
+    ss[w] = s;
+  }
+  __syncthreads();
+  m = sm[0];
+  s = ss[0];
+  for (int i = 1; i < 4; ++i) merge_ms(m, s, sm[i], ss[i]);
+  const float lse = m + logf(s);
+  const int y = tgt[row];
+  T* dr = dz + row * lddz;
+  for (int v = tid; v < lddz; v += 256) {
+    float g = 0.f;
+    if (v < V) g = (__expf(zr[v] - lse) - (v == y ? 1.f : 0.f)) * scale;
+    dr[v] = from_f<T>(g);
+  }
+  if (tid == 0) loss_rows[row] = lse - zr[y];
+}
+
+// ---------------------------------------------------------------- helpers
+__global__ void __launch_bounds__(256) sum_fixed_kernel(const float* __restrict__ x, int64_t n,
+                                                        float* __restrict__ out) {
+  __shared__ double sh[256];
+  double s = 0.0;
+  for (int64_t i = threadIdx.x; i < n; i += 256) s += static_cast<double>(x[i]);
+  sh[threadIdx.x] = s;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) sh[threadIdx.x] += sh[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[0] = static_cast<float>(sh[0]);
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) convert_kernel(const float* __restrict__ x, T* __restrict__ y, int64_t n) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * 256)
+    y[i] = from_f<T>(x[i]);
+}
+
+__global__ void __launch_bounds__(256) fill_zero_kernel(uint4* __restrict__ p, int64_t n16, uint8_t* tail,
+                                                        int ntail) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n16;
+       i += static_cast<int64_t>(gridDim.x) * 256)
+    p[i] = make_uint4(0, 0, 0, 0);
+  if (blockIdx.x == 0 && static_cast<int>(threadIdx.x) < ntail) tail[threadIdx.x] = 0;
+}
+
+inline unsigned grid_for(int64_t n) {
+  int64_t g = (n + 255) / 256;
+  return static_cast<unsigned>(g < 1 ? 1 : (g > 65536 ? 65536 : g));
+}
+
+template <typename T>
+hipError_t ln_fwd_t(const float* x, const void* gamma, const void* beta, void* y, float* mean, float* rstd,
+                    int64_t rows, int d, hipStream_t s) {
+  const int ne = (d + 255) / 256;
+  dim3 grid(static_cast<unsigned>(rows)), block(256);
+  auto g = static_cast<const T*>(gamma);
+  auto b = static_cast<const T*>(beta);
+  auto yy = static_cast<T*>(y);
+#define ATOM_LNF(E) hipLaunchKernelGGL((ln_fwd_kernel<T, E>), grid, block, 0, s, x, g, b, yy, mean, rstd, d)
+  if (ne <= 1) ATOM_LNF(1);
+  else if (ne <= 2) ATOM_LNF(2);
+  else if (ne <= 4) ATOM_LNF(4);
+  else if (ne <= 8) ATOM_LNF(8);
+  else if (ne <= 16) ATOM_LNF(16);
+  else ATOM_LNF(32);
+#undef ATOM_LNF
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t ln_bwd_t(const void* dy, const float* x, const float* mean, const float* rstd, const void* gamma,
+                    float* dres, void* dres_lp, bool acc, float* part, int64_t rows, int d, hipStream_t s) {
+  const int ne = (d + 255) / 256;
+  dim3 grid(static_cast<unsigned>((rows + LNB_ROWS - 1) / LNB_ROWS)), block(256);
+  auto a0 = static_cast<const T*>(dy);
+  auto g = static_cast<const T*>(gamma);
+  auto lp = static_cast<T*>(dres_lp);
+  const int ac = acc ? 1 : 0;
+#define ATOM_LNB(E) \
+  hipLaunchKernelGGL((ln_bwd_kernel<T, E>), grid, block, 2 * d * sizeof(float), s, a0, x, mean, rstd, g, dres, lp, \
+                     ac, part, rows, d)
+  if (ne <= 1) ATOM_LNB(1);
+  else if (ne <= 2) ATOM_LNB(2);
+  else if (ne <= 4) ATOM_LNB(4);
+  else if (ne <= 8) ATOM_LNB(8);
+  else if (ne <= 16) ATOM_LNB(16);
+  else ATOM_LNB(32);
+#undef ATOM_LNB
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t layernorm_fwd(int dtype, const float* x, const void* gamma, const void* beta, void* y, float* mean,
+                         float* rstd, int64_t rows, int d, hipStream_t s) {
+  if (d <= 0 || d % 64 || d > 8192 || rows < 0) return hipErrorInvalidValue;
+  if (rows == 0) return hipSuccess;
+  return dtype == DT_BF16 ? ln_fwd_t<bf16_t>(x, gamma, beta, y, mean, rstd, rows, d, s)
+                          : ln_fwd_t<float>(x, gamma, beta, y, mean, rstd, rows, d, s);
+}
+
+int64_t layernorm_bwd_blocks(int64_t rows) { return (rows + LNB_ROWS - 1) / LNB_ROWS; }
+
+hipError_t layernorm_bwd(int dtype, const void* dy, const float* x, const float* mean, const float* rstd,
+                         const void* gamma, float* dres, void* dres_lp, bool accumulate, float* part, int64_t rows,
+                         int d, hipStream_t s) {
+  if (d <= 0 || d % 64 || d > 8192 || rows < 0) return hipErrorInvalidValue;
+  if (rows == 0) return hipSuccess;
+  return dtype == DT_BF16 ? ln_bwd_t<bf16_t>(dy, x, mean, rstd, gamma, dres, dres_lp, accumulate, part, rows, d, s)
+                          : ln_bwd_t<float>(dy, x, mean, rstd, gamma, dres, dres_lp, accumulate, part, rows, d, s);
+}
+
+int64_t colsum_blocks(int64_t rows) { return (rows + CS_ROWS - 1) / CS_ROWS; }
+
+hipError_t colsum_partial(int in_dtype, const void* x, int64_t rows, int cols, int64_t ld, float* part,
+                          hipStream_t s) {
+  if (rows <= 0 || cols <= 0) return hipErrorInvalidValue;
+  dim3 grid(static_cast<unsigned>((cols + 255) / 256), static_cast<unsigned>(colsum_blocks(rows))), block(256);
+  if (in_dtype == DT_BF16)
+    hipLaunchKernelGGL(colsum_partial_kernel<bf16_t>, grid, block, 0, s, static_cast<const bf16_t*>(x), rows, cols,
+                       ld, part);
+  else
+    hipLaunchKernelGGL(colsum_partial_kernel<float>, grid, block, 0, s, static_cast<const float*>(x), rows, cols,
+                       ld, part);
+  return hipGetLastError();
+}
+
+hipError_t sum_parts(const float* part, int64_t nparts, int cols, int64_t part_stride, int out_dtype, void* out,
+                     bool accumulate, hipStream_t s) {
+  if (cols <= 0) return hipErrorInvalidValue;
+  dim3 grid(static_cast<unsigned>((cols + 255) / 256)), block(256);
+  if (out_dtype == DT_BF16)
+    hipLaunchKernelGGL(sum_parts_kernel<bf16_t>, grid, block, 0, s, part, nparts, cols, part_stride,
+                       static_cast<bf16_t*>(out), accumulate ? 1 : 0);
+  else
+    hipLaunchKernelGGL(sum_parts_kernel<float>, grid, block, 0, s, part, nparts, cols, part_stride,
+                       static_cast<float*>(out), accumulate ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t embed_fwd(int dtype, const int32_t* tok, const void* wte, const void* wpe, float* x, int64_t n_tok,
+                     int T, int d, hipStream_t s) {
+  if (n_tok <= 0) return hipSuccess;
+  dim3 grid(static_cast<unsigned>(n_tok)), block(256);
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL(embed_fwd_kernel<bf16_t>, grid, block, 0, s, tok, static_cast<const bf16_t*>(wte),
+                       static_cast<const bf16_t*>(wpe), x, T, d);
+  else
+    hipLaunchKernelGGL(embed_fwd_kernel<float>, grid, block, 0, s, tok, static_cast<const float*>(wte),
+                       static_cast<const float*>(wpe), x, T, d);
+  return hipGetLastError();
+}
+
+hipError_t embed_bwd(int out_dtype, const float* dx, const int32_t* perm, const int32_t* seg, const int32_t* uniq,
+                     int n_uniq, void* dwte, void* dwpe, int V, int T, int B, int d, bool accumulate,
+                     hipStream_t s) {
+  const size_t esz = out_dtype == DT_BF16 ? 2 : 4;
+  hipError_t e;
+  if (!accumulate) {
+    e = fill_zero(dwte, static_cast<int64_t>(V) * d * esz, s);
+    if (e != hipSuccess) return e;
+  }
+  const int ac = accumulate ? 1 : 0;
+  if (n_uniq > 0) {
+    if (out_dtype == DT_BF16)
+      hipLaunchKernelGGL(embed_bwd_wte_kernel<bf16_t>, dim3(n_uniq), dim3(256), 0, s, dx, perm, seg, uniq,
+                         static_cast<bf16_t*>(dwte), d, ac);
+    else
+      hipLaunchKernelGGL(embed_bwd_wte_kernel<float>, dim3(n_uniq), dim3(256), 0, s, dx, perm, seg, uniq,
+                         static_cast<float*>(dwte), d, ac);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  if (out_dtype == DT_BF16)
+    hipLaunchKernelGGL(embed_bwd_wpe_kernel<bf16_t>, dim3(T), dim3(256), 0, s, dx, static_cast<bf16_t*>(dwpe), T, B,
+                       d, ac);
+  else
+    hipLaunchKernelGGL(embed_bwd_wpe_kernel<float>, dim3(T), dim3(256), 0, s, dx, static_cast<float*>(dwpe), T, B, d,
+                       ac);
+  return hipGetLastError();
+}
+
+hipError_t xent_fwd_bwd(int dtype, const float* logits, int64_t ldz, const int32_t* tgt, void* dz, int64_t lddz,
+                        float* loss_rows, int64_t rows, int V, float scale, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (V <= 0 || lddz < V || ldz < V) return hipErrorInvalidValue;
+  dim3 grid(static_cast<unsigned>(rows)), block(256);
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL(xent_kernel<bf16_t>, grid, block, 0, s, logits, ldz, tgt, static_cast<bf16_t*>(dz), lddz,
+                       loss_rows, V, scale);
+  else
+    hipLaunchKernelGGL(xent_kernel<float>, grid, block, 0, s, logits, ldz, tgt, static_cast<float*>(dz), lddz,
+                       loss_rows, V, scale);
+  return hipGetLastError();
+}
+
+hipError_t sum_fixed(const float* x, int64_t n, float* out, hipStream_t s) {
+  hipLaunchKernelGGL(sum_fixed_kernel, dim3(1), dim3(256), 0, s, x, n, out);
+  return hipGetLastError();
+}
+
+hipError_t convert_f32(int dtype, const float* x, void* y, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL(convert_kernel<bf16_t>, dim3(grid_for(n)), dim3(256), 0, s, x, static_cast<bf16_t*>(y), n);
+  else
+    hipLaunchKernelGGL(convert_kernel<float>, dim3(grid_for(n)), dim3(256), 0, s, x, static_cast<float*>(y), n);
+  return hipGetLastError();
+}
+
+hipError_t fill_zero(void* p, int64_t bytes, hipStream_t s) {
+  if (bytes <= 0) return hipSuccess;
+  if (reinterpret_cast<uintptr_t>(p) & 15) return hipErrorInvalidValue;
+  const int64_t n16 = bytes / 16;
+  const int ntail = static_cast<int>(bytes - n16 * 16);
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(grid_for(n16)), dim3(256), 0, s, static_cast<uint4*>(p), n16,
+                     static_cast<uint8_t*>(p) + n16 * 16, ntail);
+  return hipGetLastError();
+}
+
+}  // namespace atom

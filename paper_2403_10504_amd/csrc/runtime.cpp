@@ -1,0 +1,929 @@
+// Runtime of the swapped GPT step: the context, the pinned host model, the
+// swap engine (weights in on the H2D stream, gradients out on the D2H stream,
+// events between them and the compute stream), the composition of each
+// node's forward and backward from the kernels, host-side gradient
+// accumulation, and the schedule of a whole step.
+//
+// Schedule (Section IV: one stream runs the current sub-model, another
+// prefetches the next; completed sub-models are swapped out; the last forward
+// sub-model is not swapped out before the backward).  With K weight slots,
+// group j lives in slot j % K:
+//   forward : load groups 0..K-1; after group j's forward is enqueued, load
+//             group j+K (its slot frees when group j's compute ends);
+//   backward: the last K groups are still resident; after group j's backward
+//             its gradients are copied out and group j-K is reloaded into
+//             the slot group j just freed.
+// Gradients of a group go to one of two gradient slots (by backward order),
+// are copied to pinned host memory, and a host thread adds them to the fp32
+// accumulators.  Every kernel reduces in a fixed order, so a step gives
+// bitwise the same result for any plan (swapping or not).
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <algorithm>
+#include <atomic>
+#include <chrono>
+#include <condition_variable>
+#include <deque>
+#include <functional>
+#include <mutex>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "launch.h"
+#include "layout.h"
+
+namespace atom {
+
+// ------------------------------------------------------------ host pool
+// Fixed pool of threads for the host gradient accumulation.
+class HostPool {
+ public:
+  explicit HostPool(int n) : n_(std::max(1, n)) {
+    for (int i = 1; i < n_; ++i) th_.emplace_back([this, i] { loop(i); });
+  }
+  ~HostPool() {
+    {
+      std::lock_guard<std::mutex> l(m_);
+      stop_ = true;
+      ++gen_;
+    }
+    cv_.notify_all();
+    for (auto& t : th_) t.join();
+  }
+  int size() const { return n_; }
+  // Runs fn(i) for i in [0, n) on all threads; returns when all are done.
+  void run(const std::function<void(int)>& fn) {
+    {
+      std::lock_guard<std::mutex> l(m_);
+      fn_ = &fn;
+      pending_ = n_ - 1;
+      ++gen_;
+    }
+    cv_.notify_all();
+    fn(0);
+    std::unique_lock<std::mutex> l(m_);
+    done_cv_.wait(l, [this] { return pending_ == 0; });
+    fn_ = nullptr;
+  }
+
+ private:
+  void loop(int i) {
+    uint64_t seen = 0;
+    for (;;) {
+      const std::function<void(int)>* f;
+      {
+        std::unique_lock<std::mutex> l(m_);
+        cv_.wait(l, [&] { return gen_ != seen; });
+        seen = gen_;
+        if (stop_) return;
+        f = fn_;
+      }
+      (*f)(i);
+      {
+        std::lock_guard<std::mutex> l(m_);
+        if (--pending_ == 0) done_cv_.notify_one();
+      }
+    }
+  }
+  int n_;
+  std::vector<std::thread> th_;
+  std::mutex m_;
+  std::condition_variable cv_, done_cv_;
+  const std::function<void(int)>* fn_ = nullptr;
+  int pending_ = 0;
+  uint64_t gen_ = 0;
+  bool stop_ = false;
+};
+
+}  // namespace atom
+
+using namespace atom;
+
+struct Range {
+  uint64_t off, n;  // element offset and count within the host model
+};
+
+struct atom_ctx {
+  atom_config cfg{};
+  atom_plan plan{};
+  ArenaLayout lay{};
+  uint8_t* arena = nullptr;
+  hipStream_t cs = nullptr, hs = nullptr, ds = nullptr;
+  int L = 0, G = 0, K = 0, C = 0, H = 0, dh = 0, dt = 0, e = 0, d = 0, f = 0, V = 0, B = 0, T = 0;
+  int64_t N = 0, Vp = 0;
+
+  // host model (pinned), per-node ranges
+  uint8_t* h_w = nullptr;   // weights, working dtype
+  uint8_t* h_g = nullptr;   // gradients of the last step, working dtype
+  float* h_acc = nullptr;   // fp32 accumulators (element-indexed like h_w)
+  uint64_t model_bytes = 0;
+  std::vector<uint64_t> node_off, node_bytes;
+  std::vector<std::vector<TensorDesc>> tens;
+  std::vector<int> node_group;
+  std::vector<uint64_t> group_off, group_bytes;
+  std::vector<std::vector<Range>> group_ranges;  // tensors of each group (for accumulation)
+
+  // residency and events
+  std::vector<int> slot_owner;            // group whose weights occupy the slot
+  std::vector<char> resident, need_wait, gclaimed;
+  std::vector<hipEvent_t> ev_loaded, ev_lastuse, ev_gready, ev_stored;
+  std::vector<char> lastuse_recorded, stored_recorded;
+  int gslot_last[2] = {-1, -1};
+
+  // per-step validation state
+  bool tokens_ok = false;
+  std::vector<char> fwd_done, bwd_done;   // [node][micro]
+  std::vector<int> n_uniq;                // per micro
+
+  // host accumulation
+  HostPool* pool = nullptr;
+  std::thread acc_thread;
+  std::mutex acc_m;
+  std::condition_variable acc_cv, acc_done_cv;
+  std::deque<int> acc_q;
+  int acc_busy = 0;
+  bool acc_stop = false;
+  int acc_error = 0;
+  std::string acc_errmsg;
+  double acc_seconds = 0;
+
+  std::vector<int32_t> h_tok;  // staging for token uploads
+  atom_stats stats{};
+  std::string err;
+};
+
+namespace {
+
+int fail(atom_ctx* c, int code, const std::string& msg) {
+  if (c) c->err = msg;
+  return code;
+}
+
+#define HIPCHK(ctx, expr)                                                                 \
+  do {                                                                                    \
+    hipError_t _e = (expr);                                                               \
+    if (_e != hipSuccess)                                                                 \
+      return fail(ctx, ATOM_EHIP, std::string(#expr) + ": " + hipGetErrorString(_e));     \
+  } while (0)
+
+inline uint8_t* A(atom_ctx* c, uint64_t off) { return c->arena + off; }
+inline uint8_t* WS(atom_ctx* c, uint64_t off) { return c->arena + c->lay.ws + off; }
+
+float* ckpt_ptr(atom_ctx* c, int idx, int micro) {
+  return reinterpret_cast<float*>(A(c, c->lay.ckpt) +
+                                  (static_cast<uint64_t>(idx) * c->C + micro) * c->lay.ckpt_bytes_each);
+}
+
+// Device pointer of a weight tensor of `node` in its group's slot.
+const void* wptr(atom_ctx* c, int node, int t) {
+  const int g = c->node_group[node];
+  const uint64_t in_group = c->node_off[node] - c->group_off[g];
+  return A(c, c->lay.wslots + static_cast<uint64_t>(g % c->K) * c->plan.slot_bytes + in_group +
+                  c->tens[node][t].offset);
+}
+
+// Gradient target of a tensor: fp32 accumulation slot (bf16 with C > 1) or
+// the group's gradient slot in the working dtype.
+struct GradTarget {
+  void* p;
+  int dtype;      // DT_F32 or DT_BF16
+  bool accumulate;
+};
+
+bool use_accslot(atom_ctx* c) { return c->dt == DT_BF16 && c->C > 1; }
+
+GradTarget gptr(atom_ctx* c, int node, int t, int micro) {
+  const int g = c->node_group[node];
+  const uint64_t in_group = c->node_off[node] - c->group_off[g] + c->tens[node][t].offset;
+  if (use_accslot(c)) return {A(c, c->lay.accslot + 2 * in_group), DT_F32, micro > 0};
+  const int gs = (c->G - 1 - g) & 1;
+  return {A(c, c->lay.gslots + static_cast<uint64_t>(gs) * c->plan.slot_bytes + in_group),
+          c->dt == DT_BF16 ? DT_BF16 : DT_F32, micro > 0};
+}
+
+int wgrad_epi(const GradTarget& t) {
+  if (t.dtype == DT_F32) return t.accumulate ? EPI_ACC_F32 : EPI_STORE_F32;
+  return EPI_STORE;
+}
+
+// Waits (on the compute stream) for the weights of the node's group and for
+// the gradient slot the group will write.
+int prepare_group(atom_ctx* c, int node, bool grads) {
+  const int g = c->node_group[node];
+  if (!c->resident[g]) return fail(c, ATOM_ESTATE, "group " + std::to_string(g) + " is not swapped in");
+  if (c->need_wait[g]) {
+    HIPCHK(c, hipStreamWaitEvent(c->cs, c->ev_loaded[g], 0));
+    c->need_wait[g] = 0;
+  }
+  if (grads && !c->gclaimed[g]) {
+    const int gs = (c->G - 1 - g) & 1;
+    const int prev = c->gslot_last[gs];
+    if (prev >= 0 && prev != g && c->stored_recorded[prev]) HIPCHK(c, hipStreamWaitEvent(c->cs, c->ev_stored[prev], 0));
+    c->gslot_last[gs] = g;
+    c->gclaimed[g] = 1;
+  }
+  return ATOM_OK;
+}
+
+int finish_group_use(atom_ctx* c, int node) {
+  const int g = c->node_group[node];
+  HIPCHK(c, hipEventRecord(c->ev_lastuse[g], c->cs));
+  c->lastuse_recorded[g] = 1;
+  return ATOM_OK;
+}
+
+#define KCHK(ctx, expr)                                                                       \
+  do {                                                                                        \
+    hipError_t _e = (expr);                                                                   \
+    if (_e != hipSuccess)                                                                     \
+      return fail(ctx, ATOM_EHIP, std::string("kernel launch ") + #expr + ": " + hipGetErrorString(_e)); \
+  } while (0)
+
+GemmArgs gargs(const void* A_, int64_t lda, const void* B_, int64_t ldb, void* C_, int64_t ldc, int M, int N,
+               int K) {
+  GemmArgs g{};
+  g.A = A_;
+  g.B = B_;
+  g.C = C_;
+  g.lda = lda;
+  g.ldb = ldb;
+  g.ldc = ldc;
+  g.ldaux = ldc;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  return g;
+}
+
+// Tensor indices inside a block node.
+enum { T_LN1G, T_LN1B, T_WQKV, T_BQKV, T_WO, T_BO, T_LN2G, T_LN2B, T_WFC, T_BFC, T_WPR, T_BPR };
+enum { T_WTE, T_WPE };
+enum { T_LNFG, T_LNFB, T_WHEAD };
+
+// Forward of block `node` on micro-batch `micro`; recompute == true stops
+// before the last projection (the backward does not need the block output).
+int block_forward(atom_ctx* c, int node, int micro, bool recompute) {
+  const int dt = c->dt, d = c->d, f = c->f;
+  const int64_t N = c->N;
+  hipStream_t s = c->cs;
+  const float* x = ckpt_ptr(c, node - 1, micro);
+  const auto& L = c->lay;
+  void* a = WS(c, L.a);
+  void* qkv = WS(c, L.qkv);
+  void* o = WS(c, L.o);
+  float* x1 = reinterpret_cast<float*>(WS(c, L.x1));
+  void* cc = WS(c, L.c);
+  void* u = WS(c, L.u);
+  void* g = WS(c, L.g);
+  float* mu1 = reinterpret_cast<float*>(WS(c, L.mu1));
+  float* rs1 = reinterpret_cast<float*>(WS(c, L.rs1));
+  float* mu2 = reinterpret_cast<float*>(WS(c, L.mu2));
+  float* rs2 = reinterpret_cast<float*>(WS(c, L.rs2));
+  float* lse = reinterpret_cast<float*>(WS(c, L.lse));
+
+  KCHK(c, layernorm_fwd(dt, x, wptr(c, node, T_LN1G), wptr(c, node, T_LN1B), a, mu1, rs1, N, d, s));
+  GemmArgs q = gargs(a, d, wptr(c, node, T_WQKV), d, qkv, 3 * d, static_cast<int>(N), 3 * d, d);
+  q.bias = wptr(c, node, T_BQKV);
+  KCHK(c, gemm(q, dt, true, true, EPI_BIAS, s));
+  KCHK(c, attn_fwd(dt, qkv, o, lse, c->B, c->T, c->H, c->dh, s));
+  GemmArgs po = gargs(o, d, wptr(c, node, T_WO), d, x1, d, static_cast<int>(N), d, d);
+  po.bias = wptr(c, node, T_BO);
+  po.resid = x;
+  KCHK(c, gemm(po, dt, true, true, EPI_BIAS_RESID, s));
+  KCHK(c, layernorm_fwd(dt, x1, wptr(c, node, T_LN2G), wptr(c, node, T_LN2B), cc, mu2, rs2, N, d, s));
+  GemmArgs fc = gargs(cc, d, wptr(c, node, T_WFC), d, g, f, static_cast<int>(N), f, d);
+  fc.bias = wptr(c, node, T_BFC);
+  fc.aux = u;
+  fc.ldaux = f;
+  KCHK(c, gemm(fc, dt, true, true, EPI_BIAS_GELU, s));
+  if (!recompute) {
+    GemmArgs pr = gargs(g, f, wptr(c, node, T_WPR), f, ckpt_ptr(c, node, micro), d, static_cast<int>(N), d, f);
+    pr.bias = wptr(c, node, T_BPR);
+    pr.resid = x1;
+    KCHK(c, gemm(pr, dt, true, true, EPI_BIAS_RESID, s));
+  }
+  return ATOM_OK;
+}
+
+// Bias gradient: column sums of x [N][cols] (dtype in_dt) into target.
+int bias_grad(atom_ctx* c, int in_dt, const void* x, int cols, float* part, const GradTarget& t) {
+  KCHK(c, colsum_partial(in_dt, x, c->N, cols, cols, part, c->cs));
+  KCHK(c, sum_parts(part, colsum_blocks(c->N), cols, cols, t.dtype, t.p, t.accumulate, c->cs));
+  return ATOM_OK;
+}
+
+// LayerNorm backward into dres (accumulate) plus gamma/beta gradients.
+int ln_grad(atom_ctx* c, const void* dy, const float* x, const float* mu, const float* rs, const void* gamma,
+            float* dres, void* dres_lp, bool acc, float* part, const GradTarget& tg, const GradTarget& tb) {
+  const int d = c->d;
+  KCHK(c, layernorm_bwd(c->dt, dy, x, mu, rs, gamma, dres, dres_lp, acc, part, c->N, d, c->cs));
+  const int64_t np = layernorm_bwd_blocks(c->N);
+  KCHK(c, sum_parts(part, np, d, 2 * static_cast<int64_t>(d), tg.dtype, tg.p, tg.accumulate, c->cs));
+  KCHK(c, sum_parts(part + d, np, d, 2 * static_cast<int64_t>(d), tb.dtype, tb.p, tb.accumulate, c->cs));
+  return ATOM_OK;
+}
+
+int block_backward(atom_ctx* c, int node, int micro) {
+  int st = block_forward(c, node, micro, true);
+  if (st != ATOM_OK) return st;
+  const int dt = c->dt, d = c->d, f = c->f;
+  const int Nn = static_cast<int>(c->N);
+  hipStream_t s = c->cs;
+  const auto& L = c->lay;
+  const float* x = ckpt_ptr(c, node - 1, micro);
+  float* dres = reinterpret_cast<float*>(A(c, L.dres)) + static_cast<int64_t>(micro) * c->N * d;
+  void* dlp = dt == DT_BF16 ? static_cast<void*>(A(c, L.dres_lp) + static_cast<uint64_t>(micro) * c->N * d * 2)
+                            : static_cast<void*>(dres);
+  void* dres_lp_out = dt == DT_BF16 ? dlp : nullptr;
+  void* a = WS(c, L.a);
+  void* qkv = WS(c, L.qkv);
+  void* o = WS(c, L.o);
+  float* x1 = reinterpret_cast<float*>(WS(c, L.x1));
+  void* cc = WS(c, L.c);
+  void* u = WS(c, L.u);
+  void* g = WS(c, L.g);
+  float* mu1 = reinterpret_cast<float*>(WS(c, L.mu1));
+  float* rs1 = reinterpret_cast<float*>(WS(c, L.rs1));
+  float* mu2 = reinterpret_cast<float*>(WS(c, L.mu2));
+  float* rs2 = reinterpret_cast<float*>(WS(c, L.rs2));
+  float* lse = reinterpret_cast<float*>(WS(c, L.lse));
+  float* delta = reinterpret_cast<float*>(WS(c, L.delta));
+  void* du = WS(c, L.du);
+  void* dbuf = WS(c, L.dbuf);
+  void* dout = WS(c, L.dout);
+  void* dqkv = WS(c, L.dqkv);
+  float* part = reinterpret_cast<float*>(WS(c, L.part));
+
+  // MLP output projection: x2 = x1 + g W_pr^T + b_pr
+  GradTarget t = gptr(c, node, T_BPR, micro);
+  if ((st = bias_grad(c, DT_F32, dres, d, part, t)) != ATOM_OK) return st;
+  t = gptr(c, node, T_WPR, micro);
+  KCHK(c, gemm(gargs(dlp, d, g, f, t.p, f, d, f, Nn), dt, false, false, wgrad_epi(t), s));
+  GemmArgs gd = gargs(dlp, d, wptr(c, node, T_WPR), f, du, f, Nn, f, d);
+  gd.aux = u;
+  gd.ldaux = f;
+  KCHK(c, gemm(gd, dt, true, false, EPI_GELU_BWD, s));
+  // MLP input projection: u = c W_fc^T + b_fc
+  t = gptr(c, node, T_BFC, micro);
+  if ((st = bias_grad(c, dt, du, f, part, t)) != ATOM_OK) return st;
+  t = gptr(c, node, T_WFC, micro);
+  KCHK(c, gemm(gargs(du, f, cc, d, t.p, d, f, d, Nn), dt, false, false, wgrad_epi(t), s));
+  KCHK(c, gemm(gargs(du, f, wptr(c, node, T_WFC), d, dbuf, d, Nn, d, f), dt, true, false, EPI_STORE, s));
+  // LN2
+  st = ln_grad(c, dbuf, x1, mu2, rs2, wptr(c, node, T_LN2G), dres, dres_lp_out, true, part,
+               gptr(c, node, T_LN2G, micro), gptr(c, node, T_LN2B, micro));
+  if (st != ATOM_OK) return st;
+  // attention output projection: x1 = x + o W_o^T + b_o
+  t = gptr(c, node, T_BO, micro);
+  if ((st = bias_grad(c, DT_F32, dres, d, part, t)) != ATOM_OK) return st;
+  t = gptr(c, node, T_WO, micro);
+  KCHK(c, gemm(gargs(dlp, d, o, d, t.p, d, d, d, Nn), dt, false, false, wgrad_epi(t), s));
+  KCHK(c, gemm(gargs(dlp, d, wptr(c, node, T_WO), d, dout, d, Nn, d, d), dt, true, false, EPI_STORE, s));
+  // attention
+  KCHK(c, attn_bwd(dt, qkv, o, dout, lse, delta, dqkv, c->B, c->T, c->H, c->dh, s));
+  // QKV projection: qkv = a W_qkv^T + b_qkv
+  t = gptr(c, node, T_BQKV, micro);
+  if ((st = bias_grad(c, dt, dqkv, 3 * d, part, t)) != ATOM_OK) return st;
+  t = gptr(c, node, T_WQKV, micro);
+  KCHK(c, gemm(gargs(dqkv, 3 * d, a, d, t.p, d, 3 * d, d, Nn), dt, false, false, wgrad_epi(t), s));
+  KCHK(c, gemm(gargs(dqkv, 3 * d, wptr(c, node, T_WQKV), d, dbuf, d, Nn, d, 3 * d), dt, true, false, EPI_STORE, s));
+  // LN1
+  return ln_grad(c, dbuf, x, mu1, rs1, wptr(c, node, T_LN1G), dres, dres_lp_out, true, part,
+                 gptr(c, node, T_LN1G, micro), gptr(c, node, T_LN1B, micro));
+}
+
+// Head: final LN, logits in token chunks, cross-entropy, and the head's
+// backward, which initialises dres for the micro-batch.
+int head_forward_backward(atom_ctx* c, int node, int micro) {
+  const int dt = c->dt, d = c->d;
+  const int64_t N = c->N, Vp = c->Vp;
+  hipStream_t s = c->cs;
+  const auto& L = c->lay;
+  const float* x = ckpt_ptr(c, c->L, micro);
+  void* yhat = WS(c, L.yhat);
+  float* fmu = reinterpret_cast<float*>(WS(c, L.fmu));
+  float* frs = reinterpret_cast<float*>(WS(c, L.frs));
+  float* logits = reinterpret_cast<float*>(WS(c, L.logits));
+  uint8_t* dz = WS(c, L.dz);
+  void* dyhat = WS(c, L.dyhat);
+  float* part = reinterpret_cast<float*>(WS(c, L.hpart));
+  float* dres = reinterpret_cast<float*>(A(c, L.dres)) + static_cast<int64_t>(micro) * N * d;
+  void* dres_lp_out = dt == DT_BF16 ? static_cast<void*>(A(c, L.dres_lp) + static_cast<uint64_t>(micro) * N * d * 2)
+                                    : nullptr;
+  const int32_t* tgt = reinterpret_cast<const int32_t*>(A(c, L.tok_tgt)) + static_cast<int64_t>(micro) * N;
+  float* loss_rows = reinterpret_cast<float*>(A(c, L.loss_rows)) + static_cast<int64_t>(micro) * N;
+  const float scale = 1.0f / static_cast<float>(static_cast<double>(c->C) * static_cast<double>(N));
+
+  KCHK(c, layernorm_fwd(dt, x, wptr(c, node, T_LNFG), wptr(c, node, T_LNFB), yhat, fmu, frs, N, d, s));
+  const void* W = wptr(c, node, T_WHEAD);
+  for (int64_t r0 = 0; r0 < N; r0 += HEAD_CHUNK) {
+    const int rows = static_cast<int>(std::min<int64_t>(HEAD_CHUNK, N - r0));
+    KCHK(c, gemm(gargs(static_cast<uint8_t*>(yhat) + r0 * d * c->e, d, W, d, logits, Vp, rows,
+                       static_cast<int>(Vp), d),
+                 dt, true, true, EPI_STORE_F32, s));
+    KCHK(c, xent_fwd_bwd(dt, logits, Vp, tgt + r0, dz + r0 * Vp * c->e, Vp, loss_rows + r0, rows, c->V, scale, s));
+  }
+  KCHK(c, gemm(gargs(dz, Vp, W, d, dyhat, d, static_cast<int>(N), d, static_cast<int>(Vp)), dt, true, false,
+               EPI_STORE, s));
+  GradTarget t = gptr(c, node, T_WHEAD, micro);
+  KCHK(c, gemm(gargs(dz, Vp, yhat, d, t.p, d, static_cast<int>(Vp), d, static_cast<int>(N)), dt, false, false,
+               wgrad_epi(t), s));
+  return ln_grad(c, dyhat, x, fmu, frs, wptr(c, node, T_LNFG), dres, dres_lp_out, false, part,
+                 gptr(c, node, T_LNFG, micro), gptr(c, node, T_LNFB, micro));
+}
+
+int embed_forward(atom_ctx* c, int micro) {
+  const int32_t* tok = reinterpret_cast<const int32_t*>(A(c, c->lay.tok_in)) + static_cast<int64_t>(micro) * c->N;
+  KCHK(c, embed_fwd(c->dt, tok, wptr(c, 0, T_WTE), wptr(c, 0, T_WPE), ckpt_ptr(c, 0, micro), c->N, c->T, c->d,
+                    c->cs));
+  return ATOM_OK;
+}
+
+int embed_backward(atom_ctx* c, int micro) {
+  const auto& L = c->lay;
+  const int64_t N = c->N;
+  const float* dres = reinterpret_cast<const float*>(A(c, L.dres)) + static_cast<int64_t>(micro) * N * c->d;
+  const int32_t* perm = reinterpret_cast<const int32_t*>(A(c, L.emb_perm)) + static_cast<int64_t>(micro) * N;
+  const int32_t* seg = reinterpret_cast<const int32_t*>(A(c, L.emb_seg)) + static_cast<int64_t>(micro) * (N + 1);
+  const int32_t* uniq = reinterpret_cast<const int32_t*>(A(c, L.emb_uniq)) + static_cast<int64_t>(micro) * N;
+  GradTarget te = gptr(c, 0, T_WTE, micro), tp = gptr(c, 0, T_WPE, micro);
+  KCHK(c, embed_bwd(te.dtype, dres, perm, seg, uniq, c->n_uniq[micro], te.p, tp.p, c->V, c->T, c->B, c->d,
+                    te.accumulate, c->cs));
+  return ATOM_OK;
+}
+
+// ------------------------------------------------------ host accumulation
+template <typename T>
+void accum_range(float* acc, const T* g, uint64_t n);
+template <>
+void accum_range<float>(float* acc, const float* g, uint64_t n) {
+  for (uint64_t i = 0; i < n; ++i) acc[i] += g[i];
+}
+template <>
+void accum_range<uint16_t>(float* acc, const uint16_t* g, uint64_t n) {
+  for (uint64_t i = 0; i < n; ++i) {
+    uint32_t u = static_cast<uint32_t>(g[i]) << 16;
+    float v;
+    memcpy(&v, &u, 4);
+    acc[i] += v;
+  }
+}
+
+void accumulate_group(atom_ctx* c, int g) {
+  const auto& rs = c->group_ranges[g];
+  uint64_t total = 0;
+  for (auto& r : rs) total += r.n;
+  const int nt = c->pool->size();
+  c->pool->run([&](int ti) {
+    // split the concatenated ranges into nt equal pieces
+    const uint64_t lo = total * ti / nt, hi = total * (ti + 1) / nt;
+    uint64_t pos = 0;
+    for (auto& r : rs) {
+      const uint64_t a = std::max(lo, pos), b = std::min(hi, pos + r.n);
+      if (a < b) {
+        const uint64_t off = r.off + (a - pos);
+        if (c->dt == DT_BF16)
+          accum_range<uint16_t>(c->h_acc + off, reinterpret_cast<const uint16_t*>(c->h_g) + off, b - a);
+        else
+          accum_range<float>(c->h_acc + off, reinterpret_cast<const float*>(c->h_g) + off, b - a);
+      }
+      pos += r.n;
+    }
+  });
+}
+
+void acc_loop(atom_ctx* c) {
+  for (;;) {
+    int g;
+    {
+      std::unique_lock<std::mutex> l(c->acc_m);
+      c->acc_cv.wait(l, [c] { return c->acc_stop || !c->acc_q.empty(); });
+      if (c->acc_q.empty()) return;
+      g = c->acc_q.front();
+      c->acc_q.pop_front();
+    }
+    hipError_t e = hipEventSynchronize(c->ev_stored[g]);
+    if (e == hipSuccess) {
+      auto t0 = std::chrono::steady_clock::now();
+      accumulate_group(c, g);
+      c->acc_seconds += std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+    }
+    {
+      std::lock_guard<std::mutex> l(c->acc_m);
+      if (e != hipSuccess && !c->acc_error) {
+        c->acc_error = ATOM_EHIP;
+        c->acc_errmsg = std::string("gradient copy failed: ") + hipGetErrorString(e);
+      }
+      --c->acc_busy;
+    }
+    c->acc_done_cv.notify_all();
+  }
+}
+
+int wait_accum(atom_ctx* c) {
+  std::unique_lock<std::mutex> l(c->acc_m);
+  c->acc_done_cv.wait(l, [c] { return c->acc_busy == 0; });
+  if (c->acc_error) {
+    const int e = c->acc_error;
+    c->acc_error = 0;
+    return fail(c, e, c->acc_errmsg);
+  }
+  return ATOM_OK;
+}
+
+bool group_bwd_complete(atom_ctx* c, int g) {
+  for (int n = c->plan.first[g]; n <= c->plan.last[g]; ++n)
+    for (int m = 0; m < c->C; ++m) {
+      const size_t k = static_cast<size_t>(n) * c->C + m;
+      if (n == c->L + 1 ? !c->fwd_done[k] : !c->bwd_done[k]) return false;
+    }
+  return true;
+}
+
+void reset_step_state(atom_ctx* c) {
+  std::fill(c->fwd_done.begin(), c->fwd_done.end(), 0);
+  std::fill(c->bwd_done.begin(), c->bwd_done.end(), 0);
+  std::fill(c->gclaimed.begin(), c->gclaimed.end(), 0);
+  std::fill(c->resident.begin(), c->resident.end(), 0);
+  std::fill(c->need_wait.begin(), c->need_wait.end(), 0);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- C ABI
+extern "C" {
+
+int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_arena, uint64_t arena_bytes,
+                    void* compute_stream, void* h2d_stream, void* d2h_stream, atom_ctx** out) {
+  if (!out) return ATOM_EINVAL;
+  *out = nullptr;
+  if (!cfg || !plan || !dev_arena || !compute_stream || !h2d_stream || !d2h_stream) return ATOM_EINVAL;
+  if (!check_config(*cfg).empty()) return ATOM_EINVAL;
+  if (compute_stream == h2d_stream || compute_stream == d2h_stream || h2d_stream == d2h_stream) return ATOM_EINVAL;
+  if (cfg->ckpt != ATOM_CKPT_DEVICE) return ATOM_EINVAL;  // host checkpoints: not supported by this build
+  const int n = cfg->n_layer + 2;
+  if (plan->n_nodes != n || plan->n_groups < 1 || plan->n_groups > n || plan->n_slots < 1 ||
+      plan->n_slots > plan->n_groups || plan->accum != cfg->accum)
+    return ATOM_EINVAL;
+  if (plan->first[0] != 0 || plan->last[plan->n_groups - 1] != n - 1) return ATOM_EINVAL;
+  for (int g = 0; g < plan->n_groups; ++g) {
+    if (plan->first[g] > plan->last[g]) return ATOM_EINVAL;
+    if (g > 0 && plan->first[g] != plan->last[g - 1] + 1) return ATOM_EINVAL;
+  }
+  if (plan->n_slots < std::min(plan->n_groups, 2)) return ATOM_EINVAL;
+  if (reinterpret_cast<uintptr_t>(dev_arena) & (ALIGN - 1)) return ATOM_EINVAL;
+
+  atom_ctx* c = new atom_ctx();
+  c->cfg = *cfg;
+  c->plan = *plan;
+  c->L = cfg->n_layer;
+  c->G = plan->n_groups;
+  c->K = plan->n_slots;
+  c->C = cfg->accum;
+  c->H = cfg->n_head;
+  c->d = cfg->d_model;
+  c->dh = c->d / c->H;
+  c->f = cfg->d_mlp;
+  c->V = cfg->vocab;
+  c->Vp = vocab_padded(cfg->vocab);
+  c->B = cfg->batch;
+  c->T = cfg->seq_len;
+  c->N = static_cast<int64_t>(c->B) * c->T;
+  c->dt = cfg->dtype == ATOM_BF16 ? DT_BF16 : DT_F32;
+  c->e = elem_bytes(*cfg);
+
+  // host ranges per node and group
+  c->tens.resize(n);
+  c->node_off.resize(n);
+  c->node_bytes.resize(n);
+  c->node_group.resize(n);
+  uint64_t off = 0;
+  for (int i = 0; i < n; ++i) {
+    c->node_off[i] = off;
+    c->node_bytes[i] = node_tensors(*cfg, i, &c->tens[i]);
+    off += c->node_bytes[i];
+  }
+  c->model_bytes = off;
+  uint64_t smax = 0;
+  c->group_off.resize(c->G);
+  c->group_bytes.resize(c->G);
+  c->group_ranges.resize(c->G);
+  for (int g = 0; g < c->G; ++g) {
+    c->group_off[g] = c->node_off[plan->first[g]];
+    uint64_t b = 0;
+    for (int i = plan->first[g]; i <= plan->last[g]; ++i) {
+      c->node_group[i] = g;
+      b += c->node_bytes[i];
+      for (auto& t : c->tens[i])
+        c->group_ranges[g].push_back({(c->node_off[i] + t.offset) / c->e, t.bytes / c->e});
+    }
+    c->group_bytes[g] = b;
+    smax = std::max(smax, b);
+  }
+  if (smax > plan->slot_bytes) {
+    delete c;
+    return ATOM_EINVAL;
+  }
+  c->lay = arena_layout(*cfg, plan->slot_bytes, plan->n_slots);
+  if (arena_bytes < c->lay.arena_bytes) {
+    delete c;
+    return ATOM_EBUDGET;
+  }
+  c->arena = static_cast<uint8_t*>(dev_arena);
+  c->cs = static_cast<hipStream_t>(compute_stream);
+  c->hs = static_cast<hipStream_t>(h2d_stream);
+  c->ds = static_cast<hipStream_t>(d2h_stream);
+
+  // pinned host model
+  if (hipHostMalloc(reinterpret_cast<void**>(&c->h_w), c->model_bytes, hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc(reinterpret_cast<void**>(&c->h_g), c->model_bytes, hipHostMallocDefault) != hipSuccess) {
+    atom_ctx_destroy(c);
+    return ATOM_ENOMEM_HOST;
+  }
+  const uint64_t n_elem = c->model_bytes / c->e;
+  if (posix_memalign(reinterpret_cast<void**>(&c->h_acc), 4096, n_elem * 4) != 0) {
+    c->h_acc = nullptr;
+    atom_ctx_destroy(c);
+    return ATOM_ENOMEM_HOST;
+  }
+  unsigned hw = std::thread::hardware_concurrency();
+  int nthreads = static_cast<int>(std::min(16u, std::max(1u, hw)));
+  c->pool = new HostPool(nthreads);
+  {
+    // zero host buffers in parallel
+    const uint64_t nb = c->model_bytes;
+    c->pool->run([&](int ti) {
+      const int nt = c->pool->size();
+      const uint64_t lo = nb * ti / nt, hi = nb * (ti + 1) / nt;
+      memset(c->h_w + lo, 0, hi - lo);
+      memset(c->h_g + lo, 0, hi - lo);
+      const uint64_t elo = n_elem * ti / nt, ehi = n_elem * (ti + 1) / nt;
+      memset(c->h_acc + elo, 0, (ehi - elo) * 4);
+    });
+  }
+  c->slot_owner.assign(c->K, -1);
+  c->resident.assign(c->G, 0);
+  c->need_wait.assign(c->G, 0);
+  c->gclaimed.assign(c->G, 0);
+  c->lastuse_recorded.assign(c->G, 0);
+  c->stored_recorded.assign(c->G, 0);
+  c->fwd_done.assign(static_cast<size_t>(n) * c->C, 0);
+  c->bwd_done.assign(static_cast<size_t>(n) * c->C, 0);
+  c->n_uniq.assign(c->C, 0);
+  auto mk = [&](std::vector<hipEvent_t>& v) {
+    v.assign(c->G, nullptr);
+    for (auto& e : v)
+      if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return false;
+    return true;
+  };
+  if (!mk(c->ev_loaded) || !mk(c->ev_lastuse) || !mk(c->ev_gready) || !mk(c->ev_stored)) {
+    atom_ctx_destroy(c);
+    return ATOM_EHIP;
+  }
+  c->acc_thread = std::thread(acc_loop, c);
+  *out = c;
+  return ATOM_OK;
+}
+
+void atom_ctx_destroy(atom_ctx* c) {
+  if (!c) return;
+  if (c->cs) hipStreamSynchronize(c->cs);
+  if (c->hs) hipStreamSynchronize(c->hs);
+  if (c->ds) hipStreamSynchronize(c->ds);
+  if (c->acc_thread.joinable()) {
+    {
+      std::lock_guard<std::mutex> l(c->acc_m);
+      c->acc_stop = true;
+    }
+    c->acc_cv.notify_all();
+    c->acc_thread.join();
+  }
+  for (auto* v : {&c->ev_loaded, &c->ev_lastuse, &c->ev_gready, &c->ev_stored})
+    for (auto e : *v)
+      if (e) hipEventDestroy(e);
+  delete c->pool;
+  if (c->h_w) hipHostFree(c->h_w);
+  if (c->h_g) hipHostFree(c->h_g);
+  free(c->h_acc);
+  delete c;
+}
+
+int atom_host_tensor(atom_ctx* c, int32_t node, int32_t which, void** ptr, uint64_t* bytes) {
+  if (!c || !ptr || node < 0 || node > c->L + 1 || which < 0 || which > 2) return fail(c, ATOM_EINVAL, "bad argument");
+  const uint64_t off = c->node_off[node];
+  if (which == 0) *ptr = c->h_w + off;
+  else if (which == 1) *ptr = c->h_acc + off / c->e;
+  else *ptr = c->h_g + off;
+  if (bytes) *bytes = which == 1 ? c->node_bytes[node] / c->e * 4 : c->node_bytes[node];
+  return ATOM_OK;
+}
+
+int atom_zero_grads(atom_ctx* c) {
+  if (!c) return ATOM_EINVAL;
+  int s = wait_accum(c);
+  if (s != ATOM_OK) return s;
+  memset(c->h_acc, 0, c->model_bytes / c->e * 4);
+  return ATOM_OK;
+}
+
+int atom_set_tokens(atom_ctx* c, const int32_t* tokens) {
+  if (!c || !tokens) return fail(c, ATOM_EINVAL, "null tokens");
+  const int64_t N = c->N, T = c->T, C = c->C;
+  for (int64_t i = 0; i < C * c->B * (T + 1); ++i)
+    if (tokens[i] < 0 || tokens[i] >= c->V) return fail(c, ATOM_EINVAL, "token id out of range");
+  // [inp C*N][tgt C*N][perm C*N][seg C*(N+1)][uniq C*N]
+  std::vector<int32_t> inp(C * N), tgt(C * N), perm(C * N), seg(C * (N + 1)), uniq(C * N);
+  std::vector<int32_t> count(c->V);
+  for (int64_t m = 0; m < C; ++m) {
+    for (int64_t b = 0; b < c->B; ++b)
+      for (int64_t t = 0; t < T; ++t) {
+        inp[m * N + b * T + t] = tokens[(m * c->B + b) * (T + 1) + t];
+        tgt[m * N + b * T + t] = tokens[(m * c->B + b) * (T + 1) + t + 1];
+      }
+    // stable counting sort of token positions by token id
+    std::fill(count.begin(), count.end(), 0);
+    for (int64_t n = 0; n < N; ++n) ++count[inp[m * N + n]];
+    int nu = 0, pos = 0;
+    std::vector<int32_t> start(c->V);
+    for (int v = 0; v < c->V; ++v) {
+      start[v] = pos;
+      if (count[v]) {
+        uniq[m * N + nu] = v;
+        seg[m * (N + 1) + nu] = pos;
+        ++nu;
+      }
+      pos += count[v];
+    }
+    seg[m * (N + 1) + nu] = pos;
+    for (int64_t n = 0; n < N; ++n) perm[m * N + start[inp[m * N + n]]++] = static_cast<int32_t>(n);
+    c->n_uniq[m] = nu;
+  }
+  const auto& L = c->lay;
+  HIPCHK(c, hipMemcpyAsync(A(c, L.tok_in), inp.data(), C * N * 4, hipMemcpyHostToDevice, c->cs));
+  HIPCHK(c, hipMemcpyAsync(A(c, L.tok_tgt), tgt.data(), C * N * 4, hipMemcpyHostToDevice, c->cs));
+  HIPCHK(c, hipMemcpyAsync(A(c, L.emb_perm), perm.data(), C * N * 4, hipMemcpyHostToDevice, c->cs));
+  HIPCHK(c, hipMemcpyAsync(A(c, L.emb_seg), seg.data(), C * (N + 1) * 4, hipMemcpyHostToDevice, c->cs));
+  HIPCHK(c, hipMemcpyAsync(A(c, L.emb_uniq), uniq.data(), C * N * 4, hipMemcpyHostToDevice, c->cs));
+  HIPCHK(c, hipStreamSynchronize(c->cs));
+  c->tokens_ok = true;
+  reset_step_state(c);
+  return ATOM_OK;
+}
+
+int atom_swap_in(atom_ctx* c, int32_t g) {
+  if (!c || g < 0 || g >= c->G) return fail(c, ATOM_EINVAL, "bad group");
+  if (c->resident[g]) return fail(c, ATOM_ESTATE, "group " + std::to_string(g) + " is already resident");
+  const int s = g % c->K;
+  const int prev = c->slot_owner[s];
+  if (prev >= 0 && prev != g) {
+    if (c->resident[prev]) {
+      // the previous occupant must have been used since it was loaded
+      if (!c->lastuse_recorded[prev] && c->need_wait[prev])
+        return fail(c, ATOM_ESTATE, "slot holds group " + std::to_string(prev) + " that was never used");
+      c->resident[prev] = 0;
+    }
+    if (c->lastuse_recorded[prev]) HIPCHK(c, hipStreamWaitEvent(c->hs, c->ev_lastuse[prev], 0));
+  } else if (prev == g && c->lastuse_recorded[g]) {
+    HIPCHK(c, hipStreamWaitEvent(c->hs, c->ev_lastuse[g], 0));
+  }
+  uint8_t* dst = A(c, c->lay.wslots + static_cast<uint64_t>(s) * c->plan.slot_bytes);
+  HIPCHK(c, hipMemcpyAsync(dst, c->h_w + c->group_off[g], c->group_bytes[g], hipMemcpyHostToDevice, c->hs));
+  HIPCHK(c, hipEventRecord(c->ev_loaded[g], c->hs));
+  c->slot_owner[s] = g;
+  c->resident[g] = 1;
+  c->need_wait[g] = 1;
+  c->lastuse_recorded[g] = 0;
+  c->stats.h2d_bytes += c->group_bytes[g];
+  c->stats.swap_ins += 1;
+  return ATOM_OK;
+}
+
+int atom_block_fwd(atom_ctx* c, int32_t node, int32_t micro) {
+  if (!c || node < 0 || node > c->L + 1 || micro < 0 || micro >= c->C) return fail(c, ATOM_EINVAL, "bad node/micro");
+  if (!c->tokens_ok) return fail(c, ATOM_ESTATE, "tokens not set");
+  if (node > 0 && !c->fwd_done[static_cast<size_t>(node - 1) * c->C + micro])
+    return fail(c, ATOM_ESTATE, "input of node " + std::to_string(node) + " not computed");
+  int st = prepare_group(c, node, node == c->L + 1);
+  if (st != ATOM_OK) return st;
+  if (node == 0) st = embed_forward(c, micro);
+  else if (node <= c->L) st = block_forward(c, node, micro, false);
+  else st = head_forward_backward(c, node, micro);
+  if (st != ATOM_OK) return st;
+  c->fwd_done[static_cast<size_t>(node) * c->C + micro] = 1;
+  return finish_group_use(c, node);
+}
+
+int atom_block_bwd(atom_ctx* c, int32_t node, int32_t micro) {
+  if (!c || node < 0 || node > c->L || micro < 0 || micro >= c->C) return fail(c, ATOM_EINVAL, "bad node/micro");
+  const size_t k = static_cast<size_t>(node) * c->C + micro;
+  const size_t up = static_cast<size_t>(node + 1) * c->C + micro;
+  const bool up_done = node + 1 == c->L + 1 ? c->fwd_done[up] : c->bwd_done[up];
+  if (!up_done) return fail(c, ATOM_ESTATE, "gradient of node " + std::to_string(node) + " output not computed");
+  if (c->bwd_done[k]) return fail(c, ATOM_ESTATE, "backward already done");
+  int st = prepare_group(c, node, true);
+  if (st != ATOM_OK) return st;
+  st = node == 0 ? embed_backward(c, micro) : block_backward(c, node, micro);
+  if (st != ATOM_OK) return st;
+  c->bwd_done[k] = 1;
+  return finish_group_use(c, node);
+}
+
+int atom_swap_out(atom_ctx* c, int32_t g) {
+  if (!c || g < 0 || g >= c->G) return fail(c, ATOM_EINVAL, "bad group");
+  if (!group_bwd_complete(c, g)) return fail(c, ATOM_ESTATE, "group " + std::to_string(g) + " backward incomplete");
+  const int gs = (c->G - 1 - g) & 1;
+  uint8_t* gsl = A(c, c->lay.gslots + static_cast<uint64_t>(gs) * c->plan.slot_bytes);
+  if (use_accslot(c)) {
+    // fp32 accumulation slot -> working dtype in the gradient slot, per tensor
+    for (int n = c->plan.first[g]; n <= c->plan.last[g]; ++n)
+      for (auto& t : c->tens[n]) {
+        const uint64_t in_group = c->node_off[n] - c->group_off[g] + t.offset;
+        KCHK(c, convert_f32(c->dt, reinterpret_cast<const float*>(A(c, c->lay.accslot + 2 * in_group)), gsl + in_group,
+                            static_cast<int64_t>(t.bytes / c->e), c->cs));
+      }
+  }
+  HIPCHK(c, hipEventRecord(c->ev_gready[g], c->cs));
+  HIPCHK(c, hipStreamWaitEvent(c->ds, c->ev_gready[g], 0));
+  HIPCHK(c, hipMemcpyAsync(c->h_g + c->group_off[g], gsl, c->group_bytes[g], hipMemcpyDeviceToHost, c->ds));
+  HIPCHK(c, hipEventRecord(c->ev_stored[g], c->ds));
+  c->stored_recorded[g] = 1;
+  c->stats.d2h_bytes += c->group_bytes[g];
+  c->stats.swap_outs += 1;
+  {
+    std::lock_guard<std::mutex> l(c->acc_m);
+    c->acc_q.push_back(g);
+    ++c->acc_busy;
+  }
+  c->acc_cv.notify_one();
+  return ATOM_OK;
+}
+
+int atom_sync(atom_ctx* c, float* loss_out) {
+  if (!c) return ATOM_EINVAL;
+  if (loss_out) {
+    float* lr = reinterpret_cast<float*>(A(c, c->lay.loss_rows));
+    float* lo = reinterpret_cast<float*>(A(c, c->lay.loss_out));
+    KCHK(c, sum_fixed(lr, static_cast<int64_t>(c->C) * c->N, lo, c->cs));
+    float v = 0.f;
+    HIPCHK(c, hipMemcpyAsync(&v, lo, 4, hipMemcpyDeviceToHost, c->cs));
+    HIPCHK(c, hipStreamSynchronize(c->cs));
+    *loss_out = v / static_cast<float>(static_cast<double>(c->C) * static_cast<double>(c->N));
+  }
+  HIPCHK(c, hipStreamSynchronize(c->cs));
+  HIPCHK(c, hipStreamSynchronize(c->hs));
+  HIPCHK(c, hipStreamSynchronize(c->ds));
+  return wait_accum(c);
+}
+
+int atom_step(atom_ctx* c, const int32_t* tokens, float* loss_out) {
+  if (!c) return ATOM_EINVAL;
+  auto t0 = std::chrono::steady_clock::now();
+  c->stats = atom_stats{};
+  c->acc_seconds = 0;
+  int st = atom_set_tokens(c, tokens);
+  if (st != ATOM_OK) return st;
+  const int G = c->G, K = c->K, C = c->C;
+  const atom_plan& p = c->plan;
+#define STEP(expr)                 \
+  do {                             \
+    if ((st = (expr)) != ATOM_OK) { \
+      atom_sync(c, nullptr);       \
+      return st;                   \
+    }                              \
+  } while (0)
+  // forward
+  for (int j = 0; j < std::min(G, K); ++j) STEP(atom_swap_in(c, j));
+  for (int j = 0; j < G; ++j) {
+    for (int n = p.first[j]; n <= p.last[j]; ++n)
+      for (int m = 0; m < C; ++m) STEP(atom_block_fwd(c, n, m));
+    if (j + K < G) STEP(atom_swap_in(c, j + K));
+  }
+  // backward
+  for (int j = G - 1; j >= 0; --j) {
+    for (int n = std::min(p.last[j], c->L); n >= p.first[j]; --n)
+      for (int m = 0; m < C; ++m) STEP(atom_block_bwd(c, n, m));
+    STEP(atom_swap_out(c, j));
+    if (j - K >= 0) STEP(atom_swap_in(c, j - K));
+  }
+#undef STEP
+  st = atom_sync(c, loss_out);
+  c->stats.step_s = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+  c->stats.host_accum_s = c->acc_seconds;
+  return st;
+}
+
+int atom_get_stats(atom_ctx* c, atom_stats* out) {
+  if (!c || !out) return ATOM_EINVAL;
+  *out = c->stats;
+  return ATOM_OK;
+}
+
+const char* atom_last_error(const atom_ctx* c) {
+  if (!c) return "null context";
+  return c->err.c_str();
+}
+
+}  // extern "C"

@@ -1,0 +1,220 @@
+"""Kernel-level parity: each HIP kernel through the C ABI vs the fp64 oracle.
+
+Inputs are seeded, rounded to the working precision before both sides see
+them.  Sizes span several tiles and end in ragged tails.  Tolerances
+(normwise max-norm relative error, see gpu_util.rel_err):
+  * bf16 outputs: one rounding to bf16 (2^-9 relative) on top of an fp32
+    accumulation -> 8e-3;
+  * fp32 outputs from bf16 inputs: products are exact in fp32, the sums round
+    at 2^-24 per add -> 1e-4 for K up to a few thousand;
+  * fp32 mode: 1e-5.
+"""
+import numpy as np
+import pytest
+
+from oracle import gpt
+from paper_2403_10504_amd import atom as A
+from tests import gpu_util as U
+
+pytestmark = pytest.mark.gpu
+
+TOL_OUT = {"bf16": 8e-3, "f32": 1e-5}
+
+
+def stream():
+    return U.torch().cuda.current_stream().cuda_stream
+
+
+# ---------------------------------------------------------------------- GEMM
+def gemm_case(dtype, akc, bkc, M, N, K, epi, seed):
+    r = U.rng(seed)
+    a_shape = (M, K) if akc else (K, M)
+    b_shape = (N, K) if bkc else (K, N)
+    Am = U.rep(r.standard_normal(a_shape), dtype)
+    Bm = U.rep(r.standard_normal(b_shape), dtype)
+    Aop = Am if akc else Am.T
+    Bop = Bm.T if bkc else Bm  # [K][N]
+    acc = Aop.astype(np.float64) @ Bop.astype(np.float64)
+    bias = U.rep(r.standard_normal(N), dtype)
+    resid = r.standard_normal((M, N)).astype(np.float32)
+    aux = U.rep(r.standard_normal((M, N)), dtype)
+    cinit = r.standard_normal((M, N)).astype(np.float32)
+    dA, dB = U.dev(Am, dtype), U.dev(Bm, dtype)
+    out_f32 = epi in (A.ATOM_EPI_STORE_F32, A.ATOM_EPI_ACC_F32, A.ATOM_EPI_BIAS_RESID)
+    dC = U.dev_f32(cinit) if epi == A.ATOM_EPI_ACC_F32 else U.empty((M, N), "f32" if out_f32 else dtype)
+    dbias, dres, daux = U.dev(bias, dtype), U.dev_f32(resid), U.dev(aux, dtype)
+    if epi == A.ATOM_EPI_BIAS_GELU:
+        daux = U.empty((M, N), dtype)
+    A.atom_k_gemm(U.dt_code(dtype), akc, bkc, epi, M, N, K, U.ptr(dA), a_shape[1], U.ptr(dB), b_shape[1], U.ptr(dC), N,
+                  U.ptr(dbias), U.ptr(dres), U.ptr(daux), N, stream())
+    U.sync()
+    got = U.host(dC)
+    if epi == A.ATOM_EPI_STORE or epi == A.ATOM_EPI_STORE_F32:
+        ref = acc
+    elif epi == A.ATOM_EPI_ACC_F32:
+        ref = cinit + acc
+    elif epi == A.ATOM_EPI_BIAS:
+        ref = acc + bias
+    elif epi == A.ATOM_EPI_BIAS_RESID:
+        ref = resid + acc + bias
+    elif epi == A.ATOM_EPI_BIAS_GELU:
+        u = acc + bias
+        assert U.rel_err(U.host(daux), u) < TOL_OUT[dtype]
+        ref = gpt.gelu(U.rep(u, dtype).astype(np.float64))
+    elif epi == A.ATOM_EPI_GELU_BWD:
+        ref = acc * gpt.gelu_grad(aux.astype(np.float64))
+    tol = 1e-4 if (out_f32 and dtype == "bf16") else TOL_OUT[dtype]
+    return U.rel_err(got, ref), tol
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("akc,bkc", [(1, 1), (1, 0), (0, 0), (0, 1)])
+@pytest.mark.parametrize("M,N,K", [(200, 136, 72), (256, 384, 512), (130, 66, 520), (2, 2, 8)])
+def test_gemm_layouts(dtype, akc, bkc, M, N, K):
+    err, tol = gemm_case(dtype, akc, bkc, M, N, K, A.ATOM_EPI_STORE, seed=M * 7 + N + K)
+    assert err < tol, err
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("epi", [A.ATOM_EPI_STORE_F32, A.ATOM_EPI_ACC_F32, A.ATOM_EPI_BIAS, A.ATOM_EPI_BIAS_GELU,
+                                 A.ATOM_EPI_BIAS_RESID, A.ATOM_EPI_GELU_BWD])
+def test_gemm_epilogues(dtype, epi):
+    for akc, bkc in ((1, 1), (1, 0), (0, 0)):
+        err, tol = gemm_case(dtype, akc, bkc, 260, 196, 136, epi, seed=epi * 3 + akc + 2 * bkc)
+        assert err < tol, (akc, bkc, err)
+
+
+def test_gemm_rejects_unsupported_shapes():
+    t = U.empty((64, 64), "bf16")
+    with pytest.raises(A.AtomError):  # K not a multiple of 8
+        A.atom_k_gemm(A.ATOM_BF16, 1, 1, 0, 64, 64, 60, U.ptr(t), 64, U.ptr(t), 64, U.ptr(t), 64)
+    with pytest.raises(A.AtomError):  # odd rows for a non-k-contiguous bf16 operand
+        A.atom_k_gemm(A.ATOM_BF16, 0, 1, 0, 63, 64, 64, U.ptr(t), 64, U.ptr(t), 64, U.ptr(t), 64)
+
+
+# ----------------------------------------------------------------- LayerNorm
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("rows,d", [(37, 256), (130, 768), (17, 320), (5, 4096), (3, 5120)])
+def test_layernorm_fwd_bwd(dtype, rows, d):
+    r = U.rng(rows + d)
+    x = (r.standard_normal((rows, d)) * 2 + 0.5).astype(np.float32)
+    g = U.rep(1 + 0.2 * r.standard_normal(d), dtype)
+    b = U.rep(0.1 * r.standard_normal(d), dtype)
+    dy = U.rep(r.standard_normal((rows, d)), dtype)
+    dres0 = r.standard_normal((rows, d)).astype(np.float32)
+    y_ref, (xhat, rstd) = gpt.layer_norm(x.astype(np.float64), g, b)
+    dx_ref, dg_ref, db_ref = gpt.layer_norm_backward(dy.astype(np.float64), xhat, rstd, g)
+    dx, dg_, db_ = U.dev_f32(x), U.dev(g, dtype), U.dev(b, dtype)
+    y = U.empty((rows, d), dtype)
+    mean, rs = U.empty(rows, "f32"), U.empty(rows, "f32")
+    A.atom_k_layernorm_fwd(U.dt_code(dtype), U.ptr(dx), U.ptr(dg_), U.ptr(db_), U.ptr(y), U.ptr(mean), U.ptr(rs),
+                           rows, d, stream())
+    U.sync()
+    assert U.rel_err(U.host(y), y_ref) < TOL_OUT[dtype]
+    assert U.rel_err(U.host(rs), rstd[:, 0]) < 1e-5
+    assert U.rel_err(U.host(mean), x.astype(np.float64).mean(axis=1)) < 1e-5
+    for acc in (0, 1):
+        ddy = U.dev(dy, dtype)
+        dres = U.dev_f32(dres0)
+        lp = U.empty((rows, d), dtype)
+        dgam, dbet = U.empty(d, "f32"), U.empty(d, "f32")
+        part = U.empty(A.atom_k_layernorm_bwd_part_floats(rows, d), "f32")
+        A.atom_k_layernorm_bwd(U.dt_code(dtype), U.ptr(ddy), U.ptr(dx), U.ptr(mean), U.ptr(rs), U.ptr(dg_),
+                               U.ptr(dres), U.ptr(lp), acc, U.ptr(dgam), U.ptr(dbet), U.ptr(part), rows, d, stream())
+        U.sync()
+        ref = dx_ref + (dres0 if acc else 0)
+        assert U.rel_err(U.host(dres), ref) < 1e-4
+        assert U.rel_err(U.host(lp), ref) < TOL_OUT[dtype]
+        assert U.rel_err(U.host(dgam), dg_ref) < 1e-4
+        assert U.rel_err(U.host(dbet), db_ref) < 1e-4
+
+
+# ----------------------------------------------------------------- attention
+ATTN_CASES = [(2, 100, 2, 64), (1, 128, 3, 128), (1, 1, 1, 64), (2, 200, 1, 128), (1, 64, 2, 64), (1, 257, 1, 64)]
+
+
+def attn_inputs(B, T, H, dh, dtype, seed):
+    r = U.rng(seed)
+    d = H * dh
+    qkv = U.rep(r.standard_normal((B * T, 3 * d)), dtype)
+    do = U.rep(r.standard_normal((B * T, d)), dtype)
+    return qkv, do
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("B,T,H,dh", ATTN_CASES)
+def test_attention_fwd_bwd(dtype, B, T, H, dh):
+    d = H * dh
+    qkv, do = attn_inputs(B, T, H, dh, dtype, seed=B * 1000 + T + H + dh)
+    o_ref, lse_ref = gpt.causal_attention(qkv.reshape(B, T, 3 * d).astype(np.float64), H)
+    dqkv_ref = gpt.causal_attention_backward(do.reshape(B, T, d).astype(np.float64),
+                                             qkv.reshape(B, T, 3 * d).astype(np.float64), H)
+    dq = U.dev(qkv, dtype)
+    o = U.empty((B * T, d), dtype)
+    lse = U.empty((B, H, T), "f32")
+    A.atom_k_attn_fwd(U.dt_code(dtype), U.ptr(dq), U.ptr(o), U.ptr(lse), B, T, H, dh, stream())
+    U.sync()
+    # bf16: P is rounded to bf16 before the P V product, then o is stored in bf16
+    tol = 1.5e-2 if dtype == "bf16" else 1e-5
+    assert U.rel_err(U.host(o), o_ref.reshape(B * T, d)) < tol
+    assert np.max(np.abs(U.host(lse) - lse_ref)) < 1e-4 * max(1.0, np.max(np.abs(lse_ref)))
+    ddo = U.dev(do, dtype)
+    delta = U.empty((B, H, T), "f32")
+    dqkv = U.empty((B * T, 3 * d), dtype)
+    A.atom_k_attn_bwd(U.dt_code(dtype), U.ptr(dq), U.ptr(o), U.ptr(ddo), U.ptr(lse), U.ptr(delta), U.ptr(dqkv), B, T,
+                      H, dh, stream())
+    U.sync()
+    got = U.host(dqkv).reshape(B, T, 3 * d)
+    tol = 2e-2 if dtype == "bf16" else 1e-4
+    for part in range(3):
+        sl = slice(part * d, (part + 1) * d)
+        assert U.rel_err(got[:, :, sl], dqkv_ref[:, :, sl]) < tol, part
+
+
+# ------------------------------------------------------- cross-entropy etc.
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("rows,V,ld", [(33, 1000, 1024), (5, 50257, 50304), (1, 7, 128)])
+def test_cross_entropy_rows(dtype, rows, V, ld):
+    r = U.rng(rows + V)
+    z = np.zeros((rows, ld), np.float32)
+    z[:, :V] = (r.standard_normal((rows, V)) * 3).astype(np.float32)
+    y = r.integers(0, V, rows).astype(np.int32)
+    scale = 1.0 / (rows * 4)
+    loss_ref, dz_ref = gpt.cross_entropy_rows(z[:, :V].astype(np.float64), y, scale)
+    dzt = U.dev_f32(z)
+    dz = U.dev(np.full((rows, ld), 7.0, np.float32), dtype)
+    loss = U.empty(rows, "f32")
+    A.atom_k_xent(U.dt_code(dtype), U.ptr(dzt), ld, U.ptr(U.dev_i32(y)), U.ptr(dz), ld, U.ptr(loss), rows, V, scale,
+                  stream())
+    U.sync()
+    assert U.rel_err(U.host(loss), loss_ref) < 1e-5
+    g = U.host(dz)
+    assert U.rel_err(g[:, :V], dz_ref) < TOL_OUT[dtype] + 1e-5
+    assert np.all(g[:, V:] == 0)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_colsum(dtype):
+    r = U.rng(3)
+    for rows, cols in ((1000, 300), (64, 2304), (7, 5)):
+        x = U.rep(r.standard_normal((rows, cols)), dtype)
+        out = U.empty(cols, "f32")
+        part = U.empty(A.atom_k_colsum_part_floats(rows, cols), "f32")
+        A.atom_k_colsum(U.dt_code(dtype), U.ptr(U.dev(x, dtype)), rows, cols, U.ptr(out), U.ptr(part), stream())
+        U.sync()
+        assert U.rel_err(U.host(out), x.astype(np.float64).sum(axis=0)) < 1e-5
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_embedding_forward(dtype):
+    r = U.rng(4)
+    V, T, d, B = 300, 50, 128, 3
+    wte = U.rep(r.standard_normal((V, d)), dtype)
+    wpe = U.rep(r.standard_normal((T, d)), dtype)
+    tok = r.integers(0, V, (B, T)).astype(np.int32)
+    ref = gpt.embed_forward(tok, {"wte": wte, "wpe": wpe}).reshape(B * T, d)
+    x = U.empty((B * T, d), "f32")
+    A.atom_k_embed_fwd(U.dt_code(dtype), U.ptr(U.dev_i32(tok)), U.ptr(U.dev(wte, dtype)), U.ptr(U.dev(wpe, dtype)),
+                       U.ptr(x), B * T, T, d, stream())
+    U.sync()
+    assert U.rel_err(U.host(x), ref) < 1e-7
