@@ -78,15 +78,17 @@ int64_t atom_k_colsum_part_floats(int64_t rows, int cols);
 int atom_k_colsum(int dtype, const void* x, int64_t rows, int cols, float* out, float* part, void* stream);
 
 /* Softmax cross-entropy rows: logits fp32 [rows][ldz] with V valid columns,
- * target ids tgt[rows] in [0, V); dz = (softmax - onehot) * scale (dtype,
- * row pitch lddz, columns V..lddz-1 zeroed); loss_rows = logsumexp - z[y]. */
+ * target ids tgt[rows]; dz = (softmax - onehot) * scale (dtype, row pitch
+ * lddz, columns V..lddz-1 zeroed); loss_rows = logsumexp - z[y] (NaN for a
+ * target outside [0, V), which is never read). */
 int atom_k_xent(int dtype, const float* logits, int64_t ldz, const int32_t* tgt, void* dz, int64_t lddz,
                 float* loss_rows, int64_t rows, int V, float scale, void* stream);
 
-/* x[n][c] = wte[tok[n]][c] + wpe[n % T][c]; x fp32 [n_tok][d]; every
- * tok in [0, V) (not checked on the device). */
+/* Token and position embedding (node 0 of the layer chain):
+ * x[n][c] = wte[tok[n]][c] + wpe[n % T][c]; x fp32 [n_tok][d].  A token id
+ * outside [0, V) yields a NaN row (no out-of-range read). */
 int atom_k_embed_fwd(int dtype, const int32_t* tok, const void* wte, const void* wpe, float* x, int64_t n_tok,
-                     int T, int d, void* stream);
+                     int T, int V, int d, void* stream);
 
 #ifdef __cplusplus
 }

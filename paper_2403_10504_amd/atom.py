@@ -101,7 +101,7 @@ _SIGS = {
     "atom_k_colsum_part_floats": (I64, [I64, ctypes.c_int]),
     "atom_k_colsum": (ctypes.c_int, [ctypes.c_int, P, I64, ctypes.c_int, P, P, P]),
     "atom_k_xent": (ctypes.c_int, [ctypes.c_int, P, I64, P, P, I64, P, I64, ctypes.c_int, ctypes.c_float, P]),
-    "atom_k_embed_fwd": (ctypes.c_int, [ctypes.c_int, P, P, P, P, I64, ctypes.c_int, ctypes.c_int, P]),
+    "atom_k_embed_fwd": (ctypes.c_int, [ctypes.c_int, P, P, P, P, I64, ctypes.c_int, ctypes.c_int, ctypes.c_int, P]),
 }
 EXPORTED = tuple(_SIGS)
 
@@ -312,5 +312,5 @@ def atom_k_xent(dtype, logits, ldz, tgt, dz, lddz, loss_rows, rows, V, scale, st
     _kcall("atom_k_xent", dtype, logits, ldz, tgt, dz, lddz, loss_rows, rows, V, ctypes.c_float(scale), stream)
 
 
-def atom_k_embed_fwd(dtype, tok, wte, wpe, x, n_tok, T, d, stream=None):
-    _kcall("atom_k_embed_fwd", dtype, tok, wte, wpe, x, n_tok, T, d, stream)
+def atom_k_embed_fwd(dtype, tok, wte, wpe, x, n_tok, T, V, d, stream=None):
+    _kcall("atom_k_embed_fwd", dtype, tok, wte, wpe, x, n_tok, T, V, d, stream)

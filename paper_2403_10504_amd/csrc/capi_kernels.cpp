@@ -90,9 +90,9 @@ int atom_k_xent(int dtype, const float* logits, int64_t ldz, const int32_t* tgt,
 }
 
 int atom_k_embed_fwd(int dtype, const int32_t* tok, const void* wte, const void* wpe, float* x, int64_t n_tok, int T,
-                     int d, void* stream) {
-  if (!dt_ok(dtype) || !tok || !wte || !wpe || !x || T <= 0 || d <= 0) return ATOM_EINVAL;
-  return st(embed_fwd(dtype, tok, wte, wpe, x, n_tok, T, d, S(stream)));
+                     int V, int d, void* stream) {
+  if (!dt_ok(dtype) || !tok || !wte || !wpe || !x || T <= 0 || V <= 0 || d <= 0) return ATOM_EINVAL;
+  return st(embed_fwd(dtype, tok, wte, wpe, x, n_tok, T, V, d, S(stream)));
 }
 
 }  // extern "C"

@@ -54,9 +54,10 @@ hipError_t colsum_partial(int in_dtype, const void* x, int64_t rows, int cols, i
 hipError_t sum_parts(const float* part, int64_t nparts, int cols, int64_t part_stride, int out_dtype, void* out,
                      bool accumulate, hipStream_t s);
 
-// Embedding: x[n] = wte[tok[n]] + wpe[n % T] (x fp32).
+// Embedding: x[n] = wte[tok[n]] + wpe[n % T] (x fp32); ids outside [0, V)
+// give NaN rows.
 hipError_t embed_fwd(int dtype, const int32_t* tok, const void* wte, const void* wpe, float* x, int64_t n_tok,
-                     int T, int d, hipStream_t s);
+                     int T, int V, int d, hipStream_t s);
 // dwte rows of the listed unique tokens = sum of dx rows in `perm` order;
 // all other rows zero (unless accumulate); dwpe[t] (op)= sum_b dx[b*T + t].
 hipError_t embed_bwd(int out_dtype, const float* dx, const int32_t* perm, const int32_t* seg,

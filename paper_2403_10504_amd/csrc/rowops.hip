@@ -150,15 +150,17 @@ __global__ void __launch_bounds__(256) sum_parts_kernel(const float* __restrict_
 }
 
 // --------------------------------------------------------------- embedding
+// A token id outside [0, V) gives a NaN row instead of an out-of-range read.
 template <typename T>
 __global__ void __launch_bounds__(256) embed_fwd_kernel(const int32_t* __restrict__ tok, const T* __restrict__ wte,
                                                         const T* __restrict__ wpe, float* __restrict__ x, int T_,
-                                                        int d) {
+                                                        int V, int d) {
   const int64_t n = blockIdx.x;
   const int64_t v = tok[n];
   const int64_t t = n % T_;
+  const bool ok = v >= 0 && v < V;
   for (int c = threadIdx.x; c < d; c += 256)
-    x[n * d + c] = to_f<T>(wte[v * d + c]) + to_f<T>(wpe[t * d + c]);
+    x[n * d + c] = ok ? to_f<T>(wte[v * d + c]) + to_f<T>(wpe[t * d + c]) : __builtin_nanf("");
 }
 
 template <typename TO>
@@ -166,10 +168,11 @@ __global__ void __launch_bounds__(256) embed_bwd_wte_kernel(const float* __restr
                                                             const int32_t* __restrict__ perm,
                                                             const int32_t* __restrict__ seg,
                                                             const int32_t* __restrict__ uniq, TO* __restrict__ dwte,
-                                                            int d, int accumulate) {
+                                                            int V, int d, int accumulate) {
   const int u = blockIdx.x;
   const int p0 = seg[u], p1 = seg[u + 1];
   const int64_t v = uniq[u];
+  if (v < 0 || v >= V) return;
   for (int c = threadIdx.x; c < d; c += 256) {
     float s = 0.f;
     for (int p = p0; p < p1; ++p) s += dx[static_cast<int64_t>(perm[p]) * d + c];
@@ -191,7 +194,14 @@ __global__ void __launch_bounds__(256) embed_bwd_wpe_kernel(const float* __restr
 }
 
 // ------------------------------------------------------------ cross-entropy
+// Merge two (max, sum of exp(x - max)) pairs; an empty pair is (-inf, 0).
 __device__ __forceinline__ void merge_ms(float& m, float& s, float m2, float s2) {
+  if (m2 == -INFINITY) return;
+  if (m == -INFINITY) {
+    m = m2;
+    s = s2;
+    return;
+  }
   const float mm = fmaxf(m, m2);
   s = s * __expf(m - mm) + s2 * __expf(m2 - mm);
   m = mm;
@@ -236,7 +246,8 @@ __global__ void __launch_bounds__(256) xent_kernel(const float* __restrict__ z, 
     if (v < V) g = (__expf(zr[v] - lse) - (v == y ? 1.f : 0.f)) * scale;
     dr[v] = from_f<T>(g);
   }
-  if (tid == 0) loss_rows[row] = lse - zr[y];
+  // a target outside [0, V) gives a NaN loss instead of an out-of-range read
+  if (tid == 0) loss_rows[row] = (y >= 0 && y < V) ? lse - zr[y] : __builtin_nanf("");
 }
 
 // ---------------------------------------------------------------- helpers
@@ -365,15 +376,16 @@ hipError_t sum_parts(const float* part, int64_t nparts, int cols, int64_t part_s
 }
 
 hipError_t embed_fwd(int dtype, const int32_t* tok, const void* wte, const void* wpe, float* x, int64_t n_tok,
-                     int T, int d, hipStream_t s) {
+                     int T, int V, int d, hipStream_t s) {
   if (n_tok <= 0) return hipSuccess;
+  if (T <= 0 || V <= 0 || d <= 0) return hipErrorInvalidValue;
   dim3 grid(static_cast<unsigned>(n_tok)), block(256);
   if (dtype == DT_BF16)
     hipLaunchKernelGGL(embed_fwd_kernel<bf16_t>, grid, block, 0, s, tok, static_cast<const bf16_t*>(wte),
-                       static_cast<const bf16_t*>(wpe), x, T, d);
+                       static_cast<const bf16_t*>(wpe), x, T, V, d);
   else
     hipLaunchKernelGGL(embed_fwd_kernel<float>, grid, block, 0, s, tok, static_cast<const float*>(wte),
-                       static_cast<const float*>(wpe), x, T, d);
+                       static_cast<const float*>(wpe), x, T, V, d);
   return hipGetLastError();
 }
 
@@ -390,10 +402,10 @@ hipError_t embed_bwd(int out_dtype, const float* dx, const int32_t* perm, const 
   if (n_uniq > 0) {
     if (out_dtype == DT_BF16)
       hipLaunchKernelGGL(embed_bwd_wte_kernel<bf16_t>, dim3(n_uniq), dim3(256), 0, s, dx, perm, seg, uniq,
-                         static_cast<bf16_t*>(dwte), d, ac);
+                           static_cast<bf16_t*>(dwte), V, d, ac);
     else
       hipLaunchKernelGGL(embed_bwd_wte_kernel<float>, dim3(n_uniq), dim3(256), 0, s, dx, perm, seg, uniq,
-                         static_cast<float*>(dwte), d, ac);
+                         static_cast<float*>(dwte), V, d, ac);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   if (out_dtype == DT_BF16)

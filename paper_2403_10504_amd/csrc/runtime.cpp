@@ -437,7 +437,7 @@ int head_forward_backward(atom_ctx* c, int node, int micro) {
 
 int embed_forward(atom_ctx* c, int micro) {
   const int32_t* tok = reinterpret_cast<const int32_t*>(A(c, c->lay.tok_in)) + static_cast<int64_t>(micro) * c->N;
-  KCHK(c, embed_fwd(c->dt, tok, wptr(c, 0, T_WTE), wptr(c, 0, T_WPE), ckpt_ptr(c, 0, micro), c->N, c->T, c->d,
+  KCHK(c, embed_fwd(c->dt, tok, wptr(c, 0, T_WTE), wptr(c, 0, T_WPE), ckpt_ptr(c, 0, micro), c->N, c->T, c->V, c->d,
                     c->cs));
   return ATOM_OK;
 }

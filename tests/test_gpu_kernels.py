@@ -182,10 +182,10 @@ def test_cross_entropy_rows(dtype, rows, V, ld):
     scale = 1.0 / (rows * 4)
     loss_ref, dz_ref = gpt.cross_entropy_rows(z[:, :V].astype(np.float64), y, scale)
     dzt = U.dev_f32(z)
+    dy = U.dev_i32(y)
     dz = U.dev(np.full((rows, ld), 7.0, np.float32), dtype)
     loss = U.empty(rows, "f32")
-    A.atom_k_xent(U.dt_code(dtype), U.ptr(dzt), ld, U.ptr(U.dev_i32(y)), U.ptr(dz), ld, U.ptr(loss), rows, V, scale,
-                  stream())
+    A.atom_k_xent(U.dt_code(dtype), U.ptr(dzt), ld, U.ptr(dy), U.ptr(dz), ld, U.ptr(loss), rows, V, scale, stream())
     U.sync()
     assert U.rel_err(U.host(loss), loss_ref) < 1e-5
     g = U.host(dz)
@@ -198,9 +198,10 @@ def test_colsum(dtype):
     r = U.rng(3)
     for rows, cols in ((1000, 300), (64, 2304), (7, 5)):
         x = U.rep(r.standard_normal((rows, cols)), dtype)
+        dx = U.dev(x, dtype)
         out = U.empty(cols, "f32")
         part = U.empty(A.atom_k_colsum_part_floats(rows, cols), "f32")
-        A.atom_k_colsum(U.dt_code(dtype), U.ptr(U.dev(x, dtype)), rows, cols, U.ptr(out), U.ptr(part), stream())
+        A.atom_k_colsum(U.dt_code(dtype), U.ptr(dx), rows, cols, U.ptr(out), U.ptr(part), stream())
         U.sync()
         assert U.rel_err(U.host(out), x.astype(np.float64).sum(axis=0)) < 1e-5
 
@@ -213,8 +214,19 @@ def test_embedding_forward(dtype):
     wpe = U.rep(r.standard_normal((T, d)), dtype)
     tok = r.integers(0, V, (B, T)).astype(np.int32)
     ref = gpt.embed_forward(tok, {"wte": wte, "wpe": wpe}).reshape(B * T, d)
+    # every device buffer stays referenced until the kernel has finished
+    dtok, dwte, dwpe = U.dev_i32(tok), U.dev(wte, dtype), U.dev(wpe, dtype)
     x = U.empty((B * T, d), "f32")
-    A.atom_k_embed_fwd(U.dt_code(dtype), U.ptr(U.dev_i32(tok)), U.ptr(U.dev(wte, dtype)), U.ptr(U.dev(wpe, dtype)),
-                       U.ptr(x), B * T, T, d, stream())
+    A.atom_k_embed_fwd(U.dt_code(dtype), U.ptr(dtok), U.ptr(dwte), U.ptr(dwpe), U.ptr(x), B * T, T, V, d, stream())
     U.sync()
     assert U.rel_err(U.host(x), ref) < 1e-7
+    # an id outside [0, V) yields a NaN row, never an out-of-range read
+    bad = tok.copy()
+    bad[1, 3] = V
+    bad[2, 0] = -5
+    dbad = U.dev_i32(bad)
+    A.atom_k_embed_fwd(U.dt_code(dtype), U.ptr(dbad), U.ptr(dwte), U.ptr(dwpe), U.ptr(x), B * T, T, V, d, stream())
+    U.sync()
+    got = U.host(x).reshape(B, T, d)
+    assert np.all(np.isnan(got[1, 3])) and np.all(np.isnan(got[2, 0]))
+    assert np.array_equal(np.isnan(got).any(axis=2), (bad < 0) | (bad >= V))
