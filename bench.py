@@ -1,0 +1,252 @@
+#!/usr/bin/env python3
+"""Throughput of the swapped GPT training step on one MI355X.
+
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 6.7b] [--accum C]
+
+One step = the whole hot path over one batch: swap-in of every group,
+forward, LM head and cross-entropy, backward with recompute, gradient
+swap-out and host fp32 accumulation (atom_step).  Inputs are synthetic and
+seeded (weights N(0, 0.02), uniform tokens) with the shapes of the named
+GPT-3 configuration; the host model is already in pinned memory when timing
+starts, and each timed step starts with no weights on the device.
+
+Prints one JSON line.  `value` is training tokens/s.  `roofline` is the
+dominant kernel (the weight-gradient GEMM) against the bf16 MFMA peak, its
+average launch time measured with HIP events on the compute stream inside
+the timed steps.  `step_roofline` is the step against max(FLOP time at MFMA
+peak, forced host-to-device bytes at the link rate measured in the same run).
+`cpu_baseline` is the fp64 oracle on a bounded sample on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+HBM_PEAK_GBS = 8000.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def step_flops(cfg):
+    """Algorithmic FLOPs of one training step (forward + backward, no recompute):
+    6 per parameter per token for the linear layers (blocks and LM head) plus
+    6 T d per token per layer for causal attention (half of the T x T scores)."""
+    N = cfg.accum * cfg.batch * cfg.seq_len
+    L, d, V, T = cfg.n_layer, cfg.d_model, cfg.vocab, cfg.seq_len
+    per_block = 4 * d * d + 2 * d * cfg.d_mlp
+    return N * (6.0 * (L * per_block + V * d) + 6.0 * L * T * d)
+
+
+def cpu_baseline(cfg):
+    """The fp64 oracle on a bounded sample of the workload, extrapolated to one step.
+
+    Sample: one decoder block forward + backward on one sequence of T' =
+    min(T, 512) tokens, with its causal attention (forward + backward) also
+    timed alone; the LM head + cross-entropy forward + backward on 512 tokens.
+    Weights are converted to fp64 before the clock starts.
+    Extrapolation: the block's non-attention time scales with tokens, its
+    attention time with T^2 per sequence; the head scales with tokens.
+    """
+    import numpy as np
+    from threadpoolctl import threadpool_info, threadpool_limits
+
+    import synthetic
+    from oracle import gpt
+
+    cores = len(os.sched_getaffinity(0))
+    T, d, H, V = cfg.seq_len, cfg.d_model, cfg.n_head, cfg.vocab
+    Ts = min(T, 512)
+    n_head_tok = min(512, cfg.batch * T)
+    with threadpool_limits(limits=cores):
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        rng = np.random.default_rng(0)
+        # weights handed over in fp64 so the timed region holds only the step's arithmetic
+        p = {name: synthetic.gen_param(cfg, 1, name).astype(np.float64) for name, _, _ in synthetic.param_specs(cfg, 1)}
+        x = rng.standard_normal((1, Ts, d))
+        dout = rng.standard_normal((1, Ts, d)) * 1e-3
+        t0 = time.perf_counter()
+        _, cache = gpt.block_forward(x, p, H)
+        gpt.block_backward(dout, cache, p, H)
+        t_block = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        gpt.causal_attention(cache["qkv"], H)
+        gpt.causal_attention_backward(cache["o"], cache["qkv"], H)
+        t_attn = time.perf_counter() - t0
+        del cache, p
+        ph = {name: synthetic.gen_param(cfg, cfg.n_layer + 1, name).astype(np.float64)
+              for name in ("lnf_g", "lnf_b", "w_head")}
+        xh = rng.standard_normal((1, n_head_tok, d))
+        tgt = rng.integers(0, V, (1, n_head_tok))
+        t0 = time.perf_counter()
+        gpt.head_forward_backward(xh, ph, tgt, n_head_tok)
+        t_head = time.perf_counter() - t0
+    r = T / Ts
+    t_block_seq = (t_block - t_attn) * r + t_attn * r * r
+    n_tok = cfg.accum * cfg.batch * T
+    t_step = cfg.accum * cfg.batch * cfg.n_layer * t_block_seq + t_head * n_tok / n_head_tok
+    return {
+        "value": n_tok / t_step,
+        "unit": "tokens/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"fp64 NumPy oracle: one decoder block forward+backward on a {Ts}-token sequence "
+                   f"({t_block:.2f} s, of which causal attention {t_attn:.2f} s) and the LM head + "
+                   f"cross-entropy forward+backward on {n_head_tok} tokens ({t_head:.2f} s); extrapolated to "
+                   f"{cfg.accum}x{cfg.batch} sequences of {T} tokens x {cfg.n_layer} blocks (attention x "
+                   f"(T/{Ts})^2, the rest x tokens)"),
+        "extrapolated_step_s": t_step,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="6.7b")
+    ap.add_argument("--accum", type=int, default=None, help="gradient-accumulation degree C")
+    ap.add_argument("--budget-gb", type=float, default=None, help="device budget (default: the config's)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "
+              f"(the data-parallel path across GPUs is a design, not an implementation).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synthetic
+    from paper_2403_10504_amd import Session
+    from paper_2403_10504_amd import atom as A
+
+    cfg = synthetic.CONFIGS[args.config]
+    if args.accum:
+        cfg = cfg.with_(accum=args.accum)
+    budget = int(args.budget_gb * 1e9) if args.budget_gb else (cfg.budget_bytes or (1 << 50))
+    torch.cuda.set_device(0)
+
+    t0 = time.time()
+    sess = Session(cfg, budget=budget)
+    plan = sess.plan
+    log(f"plan: {plan.n_groups} groups, {plan.n_slots} slots of {plan.slot_bytes / 1e6:.1f} MB, "
+        f"arena {plan.arena_bytes / 1e9:.2f} GB, H2D/step {plan.h2d_bytes / 1e9:.2f} GB ({time.time() - t0:.1f} s)")
+    t0 = time.time()
+    sess.load_weights()
+    log(f"host model filled ({time.time() - t0:.1f} s)")
+    tokens = synthetic.gen_tokens(cfg)
+
+    link_bytes = min(1 << 30, plan.n_slots * plan.slot_bytes // 2)
+    h2d_gbs, d2h_gbs, bidir_gbs = A.atom_link_bench(sess.ctx, link_bytes, 4)
+    log(f"host link: H2D {h2d_gbs:.1f} GB/s, D2H {d2h_gbs:.1f} GB/s, both {bidir_gbs:.1f} GB/s")
+
+    for i in range(args.warmup):
+        loss = sess.step(tokens)
+        log(f"warmup step {i}: loss {loss:.5f} ({sess.stats().step_s * 1e3:.1f} ms)")
+
+    # dominant kernel: weight-gradient GEMM (A and B not k-contiguous)
+    # (bf16 at C = 1 writes bf16 gradients; otherwise micro-batch 0 stores fp32)
+    wgrad_epi = A.ATOM_EPI_STORE if (cfg.accum == 1 and cfg.dtype == "bf16") else A.ATOM_EPI_STORE_F32
+    A.atom_probe_gemm(sess.ctx, 0, 0, wgrad_epi)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    step_times, losses = [], []
+    for i in range(args.steps):
+        losses.append(sess.step(tokens))
+        step_times.append(sess.stats().step_s)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    launches, probe_s, probe_flops = A.atom_probe_read(sess.ctx)
+    A.atom_probe_gemm(sess.ctx, 0, 0, -1)
+    st = sess.stats()
+    log(f"timed {args.steps} steps: {elapsed / args.steps * 1e3:.1f} ms/step, loss {losses[-1]:.5f}, "
+        f"host accumulate {st.host_accum_s * 1e3:.1f} ms")
+    if not all(math.isfinite(l) for l in losses):
+        raise RuntimeError(f"non-finite loss: {losses}")
+
+    ms_per_step = elapsed / args.steps * 1e3
+    n_tok = cfg.accum * cfg.batch * cfg.seq_len
+    tokens_per_s = n_tok / (ms_per_step / 1e3)
+    peak = MFMA_PEAK_TFLOPS[cfg.dtype]
+    achieved = probe_flops / probe_s / 1e12 if probe_s > 0 else 0.0
+    fl = step_flops(cfg)
+    t_mfma = fl / (peak * 1e12)
+    t_h2d_r0 = plan.forced_h2d_bytes / (h2d_gbs * 1e9)
+    t_h2d_r1 = plan.h2d_bytes / (h2d_gbs * 1e9)
+    r0 = max(t_mfma, t_h2d_r0)
+
+    result = {
+        "metric": "training tokens/sec on 1 MI355X (swapped); % of max(MFMA, H2D) roofline",
+        "value": round(tokens_per_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded N(0,0.02) weights, uniform tokens)",
+        "config": {
+            "workload": (f"GPT-3 {args.config} swapped training step: {cfg.n_layer} layers, d_model {cfg.d_model}, "
+                         f"{cfg.n_head} heads, MLP {cfg.d_mlp}, vocab {cfg.vocab}; batch {cfg.batch} x seq "
+                         f"{cfg.seq_len}, accum {cfg.accum}; "
+                         + (f"device budget {budget / 1e9:.0f} GB" if budget < (1 << 49) else "whole model resident")),
+            "global_batch": cfg.accum * cfg.batch,
+            "seq_len": cfg.seq_len,
+            "accum": cfg.accum,
+            "device_budget_gb": round(budget / 1e9, 2) if budget < (1 << 49) else None,
+            "parallelism": "single GPU",
+        },
+        "roofline": {
+            "bound": "mfma",
+            "kernel": f"gemm_kernel<{cfg.dtype}, A not k-contiguous, B not k-contiguous, epilogue {wgrad_epi}> "
+                      "(weight gradients)",
+            "achieved": round(achieved, 2),
+            "peak": peak,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4),
+            "traffic": None,
+            "launches": launches,
+            "avg_launch_us": round(probe_s / max(launches, 1) * 1e6, 2),
+        },
+        "step_roofline": {
+            "flops_per_step": fl,
+            "t_mfma_s": t_mfma,
+            "forced_h2d_bytes": plan.forced_h2d_bytes,
+            "plan_h2d_bytes": plan.h2d_bytes,
+            "d2h_bytes": plan.d2h_bytes,
+            "h2d_gbs": round(h2d_gbs, 2),
+            "d2h_gbs": round(d2h_gbs, 2),
+            "bidir_gbs": round(bidir_gbs, 2),
+            "t_h2d_s": t_h2d_r0,
+            "bound": "mfma" if t_mfma >= t_h2d_r0 else "h2d",
+            "frac_r0": round(r0 / (ms_per_step / 1e3), 4),
+            "frac_r1": round(max(t_mfma, t_h2d_r1) / (ms_per_step / 1e3), 4),
+            "host_accum_ms": round(st.host_accum_s * 1e3, 2),
+        },
+        "plan": {"groups": plan.n_groups, "slots": plan.n_slots, "slot_mb": round(plan.slot_bytes / 1e6, 1),
+                 "arena_gb": round(plan.arena_bytes / 1e9, 3), "pred_step_ms": round(plan.pred_step_s * 1e3, 1)},
+        "loss": losses[-1],
+    }
+    sess.close()
+    if not args.no_cpu_baseline:
+        log("timing the oracle on the host (cpu_baseline)")
+        result["cpu_baseline"] = cpu_baseline(cfg)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -203,6 +203,23 @@ typedef struct atom_stats {
 } atom_stats;
 int atom_get_stats(atom_ctx* ctx, atom_stats* out);
 
+/* Kernel probe for measurement.  While enabled, every launch of the GEMM
+ * instantiation (a_kcontig, b_kcontig, epilogue as in atom_kernels.h) that
+ * the step makes is bracketed by timing events on the compute stream;
+ * atom_probe_read returns the number of launches, their summed duration and
+ * their summed algorithmic FLOPs (2*M*N*K) since the probe was enabled.
+ * epi < 0 disables the probe.  At most 4096 launches are recorded per step. */
+int atom_probe_gemm(atom_ctx* ctx, int32_t a_kcontig, int32_t b_kcontig, int32_t epi);
+int atom_probe_read(atom_ctx* ctx, int64_t* launches, double* seconds, double* flops);
+
+/* Host-link microbenchmark on the context's own pinned buffers and arena
+ * (weight-slot region; call between steps): `bytes` per copy (clamped to the
+ * slot region), `iters` repetitions.  Rates in GB/s (1e9 bytes/s): pinned
+ * host to device alone, device to pinned host alone, and both directions at
+ * once on the H2D and D2H streams (sum of both directions). */
+int atom_link_bench(atom_ctx* ctx, uint64_t bytes, int32_t iters, double* h2d_gbs, double* d2h_gbs,
+                    double* bidir_gbs);
+
 /* Text of the last error on ctx (never NULL). */
 const char* atom_last_error(const atom_ctx* ctx);
 

@@ -90,6 +90,9 @@ _SIGS = {
     "atom_sync": (ctypes.c_int, [P, P]),
     "atom_step": (ctypes.c_int, [P, P, P]),
     "atom_get_stats": (ctypes.c_int, [P, P]),
+    "atom_probe_gemm": (ctypes.c_int, [P, I32, I32, I32]),
+    "atom_probe_read": (ctypes.c_int, [P, P, P, P]),
+    "atom_link_bench": (ctypes.c_int, [P, U64, I32, P, P, P]),
     "atom_last_error": (ctypes.c_char_p, [P]),
     "atom_k_gemm": (ctypes.c_int, [ctypes.c_int] * 7 + [P, I64, P, I64, P, I64, P, P, P, I64, P]),
     "atom_k_layernorm_fwd": (ctypes.c_int, [ctypes.c_int, P, P, P, P, P, P, I64, ctypes.c_int, P]),
@@ -265,6 +268,24 @@ def atom_get_stats(ctx) -> atom_stats:
     s = atom_stats()
     _check(lib().atom_get_stats(ctx, _ref(s)), ctx)
     return s
+
+
+def atom_probe_gemm(ctx, a_kcontig: int, b_kcontig: int, epi: int):
+    _check(lib().atom_probe_gemm(ctx, a_kcontig, b_kcontig, epi), ctx)
+
+
+def atom_probe_read(ctx):
+    n = I64()
+    sec = ctypes.c_double()
+    fl = ctypes.c_double()
+    _check(lib().atom_probe_read(ctx, _ref(n), _ref(sec), _ref(fl)), ctx)
+    return n.value, sec.value, fl.value
+
+
+def atom_link_bench(ctx, nbytes: int, iters: int):
+    h, d, b = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    _check(lib().atom_link_bench(ctx, nbytes, iters, _ref(h), _ref(d), _ref(b)), ctx)
+    return h.value, d.value, b.value
 
 
 # ------------------------------------------------------------------ kernels

@@ -150,7 +150,14 @@ struct atom_ctx {
   std::string acc_errmsg;
   double acc_seconds = 0;
 
-  std::vector<int32_t> h_tok;  // staging for token uploads
+  // GEMM probe (measurement): events around launches of one instantiation
+  int probe_akc = -1, probe_bkc = -1, probe_epi = -1;
+  std::vector<hipEvent_t> probe_ev;  // 2 per launch
+  std::vector<double> probe_flop;    // per pending launch
+  int probe_pending = 0;
+  int64_t probe_launches = 0;
+  double probe_seconds = 0, probe_flops = 0;
+
   atom_stats stats{};
   std::string err;
 };
@@ -258,6 +265,38 @@ GemmArgs gargs(const void* A_, int64_t lda, const void* B_, int64_t ldb, void* C
   return g;
 }
 
+constexpr int PROBE_MAX = 4096;
+
+// Drain recorded probe events (after the compute stream has finished them).
+int probe_collect(atom_ctx* c) {
+  for (int i = 0; i < c->probe_pending; ++i) {
+    float ms = 0.f;
+    HIPCHK(c, hipEventElapsedTime(&ms, c->probe_ev[2 * i], c->probe_ev[2 * i + 1]));
+    c->probe_seconds += ms * 1e-3;
+    c->probe_flops += c->probe_flop[i];
+    c->probe_launches += 1;
+  }
+  c->probe_pending = 0;
+  return ATOM_OK;
+}
+
+// Every GEMM of the step goes through here so the probe can time it.
+hipError_t run_gemm(atom_ctx* c, const GemmArgs& g, bool akc, bool bkc, int epi) {
+  const bool probe = c->probe_epi == epi && c->probe_akc == static_cast<int>(akc) &&
+                     c->probe_bkc == static_cast<int>(bkc) && c->probe_pending < PROBE_MAX;
+  if (probe) {
+    hipError_t e = hipEventRecord(c->probe_ev[2 * c->probe_pending], c->cs);
+    if (e != hipSuccess) return e;
+  }
+  hipError_t e = gemm(g, c->dt, akc, bkc, epi, c->cs);
+  if (e != hipSuccess || !probe) return e;
+  e = hipEventRecord(c->probe_ev[2 * c->probe_pending + 1], c->cs);
+  if (e != hipSuccess) return e;
+  c->probe_flop[c->probe_pending] = 2.0 * g.M * g.N * static_cast<double>(g.K);
+  c->probe_pending += 1;
+  return hipSuccess;
+}
+
 // Tensor indices inside a block node.
 enum { T_LN1G, T_LN1B, T_WQKV, T_BQKV, T_WO, T_BO, T_LN2G, T_LN2B, T_WFC, T_BFC, T_WPR, T_BPR };
 enum { T_WTE, T_WPE };
@@ -287,23 +326,23 @@ int block_forward(atom_ctx* c, int node, int micro, bool recompute) {
   KCHK(c, layernorm_fwd(dt, x, wptr(c, node, T_LN1G), wptr(c, node, T_LN1B), a, mu1, rs1, N, d, s));
   GemmArgs q = gargs(a, d, wptr(c, node, T_WQKV), d, qkv, 3 * d, static_cast<int>(N), 3 * d, d);
   q.bias = wptr(c, node, T_BQKV);
-  KCHK(c, gemm(q, dt, true, true, EPI_BIAS, s));
+  KCHK(c, run_gemm(c, q, true, true, EPI_BIAS));
   KCHK(c, attn_fwd(dt, qkv, o, lse, c->B, c->T, c->H, c->dh, s));
   GemmArgs po = gargs(o, d, wptr(c, node, T_WO), d, x1, d, static_cast<int>(N), d, d);
   po.bias = wptr(c, node, T_BO);
   po.resid = x;
-  KCHK(c, gemm(po, dt, true, true, EPI_BIAS_RESID, s));
+  KCHK(c, run_gemm(c, po, true, true, EPI_BIAS_RESID));
   KCHK(c, layernorm_fwd(dt, x1, wptr(c, node, T_LN2G), wptr(c, node, T_LN2B), cc, mu2, rs2, N, d, s));
   GemmArgs fc = gargs(cc, d, wptr(c, node, T_WFC), d, g, f, static_cast<int>(N), f, d);
   fc.bias = wptr(c, node, T_BFC);
   fc.aux = u;
   fc.ldaux = f;
-  KCHK(c, gemm(fc, dt, true, true, EPI_BIAS_GELU, s));
+  KCHK(c, run_gemm(c, fc, true, true, EPI_BIAS_GELU));
   if (!recompute) {
     GemmArgs pr = gargs(g, f, wptr(c, node, T_WPR), f, ckpt_ptr(c, node, micro), d, static_cast<int>(N), d, f);
     pr.bias = wptr(c, node, T_BPR);
     pr.resid = x1;
-    KCHK(c, gemm(pr, dt, true, true, EPI_BIAS_RESID, s));
+    KCHK(c, run_gemm(c, pr, true, true, EPI_BIAS_RESID));
   }
   return ATOM_OK;
 }
@@ -361,17 +400,17 @@ int block_backward(atom_ctx* c, int node, int micro) {
   GradTarget t = gptr(c, node, T_BPR, micro);
   if ((st = bias_grad(c, DT_F32, dres, d, part, t)) != ATOM_OK) return st;
   t = gptr(c, node, T_WPR, micro);
-  KCHK(c, gemm(gargs(dlp, d, g, f, t.p, f, d, f, Nn), dt, false, false, wgrad_epi(t), s));
+  KCHK(c, run_gemm(c, gargs(dlp, d, g, f, t.p, f, d, f, Nn), false, false, wgrad_epi(t)));
   GemmArgs gd = gargs(dlp, d, wptr(c, node, T_WPR), f, du, f, Nn, f, d);
   gd.aux = u;
   gd.ldaux = f;
-  KCHK(c, gemm(gd, dt, true, false, EPI_GELU_BWD, s));
+  KCHK(c, run_gemm(c, gd, true, false, EPI_GELU_BWD));
   // MLP input projection: u = c W_fc^T + b_fc
   t = gptr(c, node, T_BFC, micro);
   if ((st = bias_grad(c, dt, du, f, part, t)) != ATOM_OK) return st;
   t = gptr(c, node, T_WFC, micro);
-  KCHK(c, gemm(gargs(du, f, cc, d, t.p, d, f, d, Nn), dt, false, false, wgrad_epi(t), s));
-  KCHK(c, gemm(gargs(du, f, wptr(c, node, T_WFC), d, dbuf, d, Nn, d, f), dt, true, false, EPI_STORE, s));
+  KCHK(c, run_gemm(c, gargs(du, f, cc, d, t.p, d, f, d, Nn), false, false, wgrad_epi(t)));
+  KCHK(c, run_gemm(c, gargs(du, f, wptr(c, node, T_WFC), d, dbuf, d, Nn, d, f), true, false, EPI_STORE));
   // LN2
   st = ln_grad(c, dbuf, x1, mu2, rs2, wptr(c, node, T_LN2G), dres, dres_lp_out, true, part,
                gptr(c, node, T_LN2G, micro), gptr(c, node, T_LN2B, micro));
@@ -380,16 +419,16 @@ int block_backward(atom_ctx* c, int node, int micro) {
   t = gptr(c, node, T_BO, micro);
   if ((st = bias_grad(c, DT_F32, dres, d, part, t)) != ATOM_OK) return st;
   t = gptr(c, node, T_WO, micro);
-  KCHK(c, gemm(gargs(dlp, d, o, d, t.p, d, d, d, Nn), dt, false, false, wgrad_epi(t), s));
-  KCHK(c, gemm(gargs(dlp, d, wptr(c, node, T_WO), d, dout, d, Nn, d, d), dt, true, false, EPI_STORE, s));
+  KCHK(c, run_gemm(c, gargs(dlp, d, o, d, t.p, d, d, d, Nn), false, false, wgrad_epi(t)));
+  KCHK(c, run_gemm(c, gargs(dlp, d, wptr(c, node, T_WO), d, dout, d, Nn, d, d), true, false, EPI_STORE));
   // attention
   KCHK(c, attn_bwd(dt, qkv, o, dout, lse, delta, dqkv, c->B, c->T, c->H, c->dh, s));
   // QKV projection: qkv = a W_qkv^T + b_qkv
   t = gptr(c, node, T_BQKV, micro);
   if ((st = bias_grad(c, dt, dqkv, 3 * d, part, t)) != ATOM_OK) return st;
   t = gptr(c, node, T_WQKV, micro);
-  KCHK(c, gemm(gargs(dqkv, 3 * d, a, d, t.p, d, 3 * d, d, Nn), dt, false, false, wgrad_epi(t), s));
-  KCHK(c, gemm(gargs(dqkv, 3 * d, wptr(c, node, T_WQKV), d, dbuf, d, Nn, d, 3 * d), dt, true, false, EPI_STORE, s));
+  KCHK(c, run_gemm(c, gargs(dqkv, 3 * d, a, d, t.p, d, 3 * d, d, Nn), false, false, wgrad_epi(t)));
+  KCHK(c, run_gemm(c, gargs(dqkv, 3 * d, wptr(c, node, T_WQKV), d, dbuf, d, Nn, d, 3 * d), true, false, EPI_STORE));
   // LN1
   return ln_grad(c, dbuf, x, mu1, rs1, wptr(c, node, T_LN1G), dres, dres_lp_out, true, part,
                  gptr(c, node, T_LN1G, micro), gptr(c, node, T_LN1B, micro));
@@ -421,16 +460,16 @@ int head_forward_backward(atom_ctx* c, int node, int micro) {
   const void* W = wptr(c, node, T_WHEAD);
   for (int64_t r0 = 0; r0 < N; r0 += HEAD_CHUNK) {
     const int rows = static_cast<int>(std::min<int64_t>(HEAD_CHUNK, N - r0));
-    KCHK(c, gemm(gargs(static_cast<uint8_t*>(yhat) + r0 * d * c->e, d, W, d, logits, Vp, rows,
-                       static_cast<int>(Vp), d),
-                 dt, true, true, EPI_STORE_F32, s));
+    KCHK(c, run_gemm(c, gargs(static_cast<uint8_t*>(yhat) + r0 * d * c->e, d, W, d, logits, Vp, rows,
+                              static_cast<int>(Vp), d),
+                     true, true, EPI_STORE_F32));
     KCHK(c, xent_fwd_bwd(dt, logits, Vp, tgt + r0, dz + r0 * Vp * c->e, Vp, loss_rows + r0, rows, c->V, scale, s));
   }
-  KCHK(c, gemm(gargs(dz, Vp, W, d, dyhat, d, static_cast<int>(N), d, static_cast<int>(Vp)), dt, true, false,
-               EPI_STORE, s));
+  KCHK(c, run_gemm(c, gargs(dz, Vp, W, d, dyhat, d, static_cast<int>(N), d, static_cast<int>(Vp)), true, false,
+                   EPI_STORE));
   GradTarget t = gptr(c, node, T_WHEAD, micro);
-  KCHK(c, gemm(gargs(dz, Vp, yhat, d, t.p, d, static_cast<int>(Vp), d, static_cast<int>(N)), dt, false, false,
-               wgrad_epi(t), s));
+  KCHK(c, run_gemm(c, gargs(dz, Vp, yhat, d, t.p, d, static_cast<int>(Vp), d, static_cast<int>(N)), false, false,
+                   wgrad_epi(t)));
   return ln_grad(c, dyhat, x, fmu, frs, wptr(c, node, T_LNFG), dres, dres_lp_out, false, part,
                  gptr(c, node, T_LNFG, micro), gptr(c, node, T_LNFB, micro));
 }
@@ -683,6 +722,13 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
     atom_ctx_destroy(c);
     return ATOM_EHIP;
   }
+  c->probe_ev.assign(2 * PROBE_MAX, nullptr);
+  c->probe_flop.assign(PROBE_MAX, 0.0);
+  for (auto& e : c->probe_ev)
+    if (hipEventCreate(&e) != hipSuccess) {
+      atom_ctx_destroy(c);
+      return ATOM_EHIP;
+    }
   c->acc_thread = std::thread(acc_loop, c);
   *out = c;
   return ATOM_OK;
@@ -701,7 +747,7 @@ void atom_ctx_destroy(atom_ctx* c) {
     c->acc_cv.notify_all();
     c->acc_thread.join();
   }
-  for (auto* v : {&c->ev_loaded, &c->ev_lastuse, &c->ev_gready, &c->ev_stored})
+  for (auto* v : {&c->ev_loaded, &c->ev_lastuse, &c->ev_gready, &c->ev_stored, &c->probe_ev})
     for (auto e : *v)
       if (e) hipEventDestroy(e);
   delete c->pool;
@@ -875,6 +921,8 @@ int atom_sync(atom_ctx* c, float* loss_out) {
   HIPCHK(c, hipStreamSynchronize(c->cs));
   HIPCHK(c, hipStreamSynchronize(c->hs));
   HIPCHK(c, hipStreamSynchronize(c->ds));
+  int st = probe_collect(c);
+  if (st != ATOM_OK) return st;
   return wait_accum(c);
 }
 
@@ -913,6 +961,65 @@ int atom_step(atom_ctx* c, const int32_t* tokens, float* loss_out) {
   c->stats.step_s = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
   c->stats.host_accum_s = c->acc_seconds;
   return st;
+}
+
+int atom_probe_gemm(atom_ctx* c, int32_t akc, int32_t bkc, int32_t epi) {
+  if (!c) return ATOM_EINVAL;
+  HIPCHK(c, hipStreamSynchronize(c->cs));
+  int st = probe_collect(c);
+  if (st != ATOM_OK) return st;
+  c->probe_akc = akc ? 1 : 0;
+  c->probe_bkc = bkc ? 1 : 0;
+  c->probe_epi = epi;
+  c->probe_launches = 0;
+  c->probe_seconds = 0;
+  c->probe_flops = 0;
+  return ATOM_OK;
+}
+
+int atom_probe_read(atom_ctx* c, int64_t* launches, double* seconds, double* flops) {
+  if (!c) return ATOM_EINVAL;
+  HIPCHK(c, hipStreamSynchronize(c->cs));
+  int st = probe_collect(c);
+  if (st != ATOM_OK) return st;
+  if (launches) *launches = c->probe_launches;
+  if (seconds) *seconds = c->probe_seconds;
+  if (flops) *flops = c->probe_flops;
+  return ATOM_OK;
+}
+
+int atom_link_bench(atom_ctx* c, uint64_t bytes, int32_t iters, double* h2d, double* d2h, double* bidir) {
+  if (!c || iters < 1) return ATOM_EINVAL;
+  HIPCHK(c, hipStreamSynchronize(c->cs));
+  HIPCHK(c, hipStreamSynchronize(c->hs));
+  HIPCHK(c, hipStreamSynchronize(c->ds));
+  const uint64_t region = static_cast<uint64_t>(c->K) * c->plan.slot_bytes;
+  // two device halves so both directions can run at once on distinct memory
+  const uint64_t n = std::min<uint64_t>(std::min<uint64_t>(bytes, region / 2), c->model_bytes);
+  if (n == 0) return fail(c, ATOM_EINVAL, "no room for the link benchmark");
+  uint8_t* dev0 = A(c, c->lay.wslots);
+  uint8_t* dev1 = dev0 + n;
+  auto timed = [&](bool up, bool down) -> double {
+    auto t0 = std::chrono::steady_clock::now();
+    for (int i = 0; i < iters; ++i) {
+      if (up) (void)hipMemcpyAsync(dev0, c->h_w, n, hipMemcpyHostToDevice, c->hs);
+      if (down) (void)hipMemcpyAsync(c->h_g, dev1, n, hipMemcpyDeviceToHost, c->ds);
+    }
+    (void)hipStreamSynchronize(c->hs);
+    (void)hipStreamSynchronize(c->ds);
+    return std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+  };
+  timed(true, true);  // warm-up
+  const double tu = timed(true, false), td = timed(false, true), tb = timed(true, true);
+  HIPCHK(c, hipGetLastError());
+  // slots no longer hold any group's weights
+  std::fill(c->slot_owner.begin(), c->slot_owner.end(), -1);
+  std::fill(c->resident.begin(), c->resident.end(), 0);
+  const double gb = static_cast<double>(n) * iters / 1e9;
+  if (h2d) *h2d = gb / tu;
+  if (d2h) *d2h = gb / td;
+  if (bidir) *bidir = 2.0 * gb / tb;
+  return ATOM_OK;
 }
 
 int atom_get_stats(atom_ctx* c, atom_stats* out) {
