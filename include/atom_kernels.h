@@ -38,10 +38,13 @@ enum {
  * and ldaux.  Requirements: K % 8 == 0 (bf16) or K % 4 == 0 (fp32); the
  * leading dimension of a k-contiguous operand a multiple of 8 (bf16) or 4
  * (fp32); for bf16 an operand that is not k-contiguous needs an even row
- * count and an even leading dimension; A, B, C 16-byte aligned. */
+ * count and an even leading dimension; A, B, C 16-byte aligned.
+ * ws (fp32, ws_bytes, 16-byte aligned, may be NULL) lets a problem with few
+ * output tiles and a long k split k over workgroups for the store epilogues
+ * (STORE, STORE_F32, ACC_F32); the partials are summed in a fixed order. */
 int atom_k_gemm(int dtype, int a_kcontig, int b_kcontig, int epi, int M, int N, int K, const void* A, int64_t lda,
                 const void* B, int64_t ldb, void* C, int64_t ldc, const void* bias, const float* resid, void* aux,
-                int64_t ldaux, void* stream);
+                int64_t ldaux, float* ws, uint64_t ws_bytes, void* stream);
 
 /* LayerNorm forward over rows of d (d % 64 == 0, d <= 8192), eps 1e-5,
  * biased variance: y = (x - mean) * rstd * gamma + beta.  x fp32 [rows][d];

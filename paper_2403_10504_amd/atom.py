@@ -94,7 +94,7 @@ _SIGS = {
     "atom_probe_read": (ctypes.c_int, [P, P, P, P]),
     "atom_link_bench": (ctypes.c_int, [P, U64, I32, P, P, P]),
     "atom_last_error": (ctypes.c_char_p, [P]),
-    "atom_k_gemm": (ctypes.c_int, [ctypes.c_int] * 7 + [P, I64, P, I64, P, I64, P, P, P, I64, P]),
+    "atom_k_gemm": (ctypes.c_int, [ctypes.c_int] * 7 + [P, I64, P, I64, P, I64, P, P, P, I64, P, U64, P]),
     "atom_k_layernorm_fwd": (ctypes.c_int, [ctypes.c_int, P, P, P, P, P, P, I64, ctypes.c_int, P]),
     "atom_k_layernorm_bwd_part_floats": (I64, [I64, ctypes.c_int]),
     "atom_k_layernorm_bwd": (ctypes.c_int, [ctypes.c_int, P, P, P, P, P, P, P, ctypes.c_int, P, P, P, I64,
@@ -294,9 +294,9 @@ def _kcall(name, *args):
 
 
 def atom_k_gemm(dtype, a_kcontig, b_kcontig, epi, M, N, K, A, lda, B, ldb, C, ldc, bias=None, resid=None, aux=None,
-                ldaux=0, stream=None):
+                ldaux=0, stream=None, ws=None, ws_bytes=0):
     _kcall("atom_k_gemm", dtype, int(a_kcontig), int(b_kcontig), epi, M, N, K, A, lda, B, ldb, C, ldc, bias, resid,
-           aux, ldaux, stream)
+           aux, ldaux, ws, ws_bytes, stream)
 
 
 def atom_k_layernorm_fwd(dtype, x, gamma, beta, y, mean, rstd, rows, d, stream=None):

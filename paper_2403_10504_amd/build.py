@@ -50,6 +50,8 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
     hipcc = _hipcc()
     os.makedirs(BUILD, exist_ok=True)
     common = ["-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function", "-I", CSRC]
+    # extra compiler flags, e.g. a -D override of a tile configuration
+    common += os.environ.get("ATOM_HIPCC_FLAGS", "").split()
     cmds, objs = [], []
     for src in HIP_SOURCES:
         obj = os.path.join(BUILD, src + ".o")

@@ -21,7 +21,7 @@ extern "C" {
 
 int atom_k_gemm(int dtype, int a_kcontig, int b_kcontig, int epi, int M, int N, int K, const void* A, int64_t lda,
                 const void* B, int64_t ldb, void* C, int64_t ldc, const void* bias, const float* resid, void* aux,
-                int64_t ldaux, void* stream) {
+                int64_t ldaux, float* ws, uint64_t ws_bytes, void* stream) {
   if (!dt_ok(dtype) || !A || !B || !C || epi < ATOM_EPI_STORE || epi > ATOM_EPI_GELU_BWD) return ATOM_EINVAL;
   if ((epi == ATOM_EPI_BIAS || epi == ATOM_EPI_BIAS_GELU || epi == ATOM_EPI_BIAS_RESID) && !bias) return ATOM_EINVAL;
   if ((epi == ATOM_EPI_BIAS_GELU || epi == ATOM_EPI_GELU_BWD) && (!aux || ldaux < N)) return ATOM_EINVAL;
@@ -40,6 +40,8 @@ int atom_k_gemm(int dtype, int a_kcontig, int b_kcontig, int epi, int M, int N, 
   g.M = M;
   g.N = N;
   g.K = K;
+  g.ws = ws;
+  g.ws_bytes = ws ? ws_bytes : 0;
   return st(gemm(g, dtype, a_kcontig != 0, b_kcontig != 0, epi, S(stream)));
 }
 

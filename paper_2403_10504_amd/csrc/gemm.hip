@@ -10,22 +10,41 @@
 //   data grad dx = dy W   : A = dy (KC),          B = W  (not KC)
 //   weight grad dW = dy^T x: A = dy (not KC),      B = x  (not KC)
 //
-// Tiling: 128x128 output tile per 256-thread workgroup (2x2 waves of 64x64),
-// 128-byte k tile (64 bf16 or 32 fp32), double-buffered in LDS.  Every
-// operand is staged in LDS with k contiguous (rows padded to 144 bytes to
-// spread ds_read_b128 over the banks); operands that are not k-contiguous in
-// memory are transposed while being written to LDS.  Each lane reads
-// 16x16x32 MFMA fragments (see common.h) and accumulates 16 tiles.
-// Workgroup ids are remapped so that neighbouring output tiles, which share
-// A rows or B columns, run on the same XCD (each XCD has its own L2).
+// Tiling: a BM x BN output tile per workgroup of WM x WN waves (a large tile
+// for big problems, 128x128 otherwise), 128-byte k tile (64 bf16 or 32 fp32)
+// double-buffered in LDS.  Every operand is staged in LDS with k contiguous
+// (rows padded to 144 bytes to spread ds_read_b128 over the banks); operands
+// that are not k-contiguous in memory are transposed while being written to
+// LDS.  Each lane reads 16x16x32 MFMA fragments (see common.h).  Larger
+// per-wave tiles raise the MFMA work per byte read from LDS.  Workgroup ids
+// are remapped so that neighbouring output tiles, which share A rows or B
+// columns, run on the same XCD (each XCD has its own L2).  Problems with few
+// output tiles and a long k (weight gradients of narrow layers) split k over
+// workgroups; the fp32 partials are summed in split order by a second kernel,
+// so the result does not depend on scheduling.
+#include <algorithm>
+
 #include "common.h"
 #include "launch.h"
 
 namespace atom {
 namespace {
 
-constexpr int BM = 128, BN = 128, NT = 256;
 constexpr int ROW_BYTES = 128, PITCH_BYTES = 144;
+
+// Workgroup tile BM x BN computed by WM x WN waves, each owning a
+// (BM/WM) x (BN/WN) block of 16x16 MFMA tiles.
+#ifndef ATOM_GEMM_CFG
+#define ATOM_GEMM_CFG 256, 256, 4, 2
+#endif
+template <int BM_, int BN_, int WM_, int WN_>
+struct Cfg {
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
+  static constexpr int NT = 64 * WM_ * WN_;
+  static constexpr int TM = BM_ / (16 * WM_), TN = BN_ / (16 * WN_);
+};
+using Big = Cfg<ATOM_GEMM_CFG>;   // large problems
+using Small = Cfg<128, 128, 2, 2>; // few output tiles
 
 template <typename T>
 struct Tile {
@@ -36,39 +55,43 @@ struct Tile {
   static constexpr int NSLICE = BK / 32;
 };
 
-// Stages a 128-row x BK tile of one operand (rows = m for A, n for B).
-// Registers hold the next tile while the current one is being consumed.
-template <typename T, bool KC>
+// Stages an R-row x BK tile of one operand (rows = m for A, n for B) with NT
+// threads.  Registers hold the next tile while the current one is consumed.
+template <typename T, bool KC, int R, int NT>
 struct Loader {
-  uint32_t r[16];
+  using TL = Tile<T>;
+  static constexpr int DW = R * ROW_BYTES / 4 / NT;   // dwords per thread
+  static constexpr int UPK = R / TL::PAIR;            // !KC: dword units per k row
+  static constexpr int UPT = 8 * UPK / NT;            // !KC: units per thread
+  uint32_t r[DW];
 
-  // KC: rows are contiguous along k.  128 rows x 8 chunks of 16 bytes.
-  // !KC: memory is [k][row]; each thread loads KV k-rows x PAIR rows.
-  __device__ void load(const T* __restrict__ X, int64_t ld, int R, int K, int r0, int k0, int tid) {
-    using TL = Tile<T>;
+  // KC: rows are contiguous along k, R rows x 8 chunks of 16 bytes.
+  // !KC: memory is [k][row]; a unit is KV consecutive k rows x PAIR rows.
+  __device__ void load(const T* __restrict__ X, int64_t ld, int Rlim, int K, int r0, int k0, int tid) {
     if constexpr (KC) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        int c = tid + NT * i;
-        int row = c >> 3, kc = c & 7;
-        int gr = r0 + row, gk = k0 + kc * TL::KV;
+      for (int i = 0; i < DW / 4; ++i) {
+        const int c = tid + NT * i;
+        const int row = c >> 3, kc = c & 7;
+        const int gr = r0 + row, gk = k0 + kc * TL::KV;
         uint4 v = make_uint4(0, 0, 0, 0);
-        if (gr < R && gk < K) v = *reinterpret_cast<const uint4*>(X + static_cast<int64_t>(gr) * ld + gk);
-        r[4 * i + 0] = v.x; r[4 * i + 1] = v.y; r[4 * i + 2] = v.z; r[4 * i + 3] = v.w;
+        if (gr < Rlim && gk < K) v = *reinterpret_cast<const uint4*>(X + static_cast<int64_t>(gr) * ld + gk);
+        r[4 * i + 0] = v.x;
+        r[4 * i + 1] = v.y;
+        r[4 * i + 2] = v.z;
+        r[4 * i + 3] = v.w;
       }
     } else {
-      constexpr int UNITS_PER_KB = 128 / TL::PAIR;            // 64 (bf16) or 128 (fp32)
-      constexpr int UNITS_PER_THREAD = (8 * UNITS_PER_KB) / NT; // 2 or 4
 #pragma unroll
-      for (int i = 0; i < UNITS_PER_THREAD; ++i) {
-        int u = tid + NT * i;
-        int kb = u / UNITS_PER_KB, rc = u % UNITS_PER_KB;
-        int gr = r0 + rc * TL::PAIR;
+      for (int i = 0; i < UPT; ++i) {
+        const int u = tid + NT * i;
+        const int kb = u / UPK, rc = u % UPK;
+        const int gr = r0 + rc * TL::PAIR;
 #pragma unroll
         for (int j = 0; j < TL::KV; ++j) {
-          int gk = k0 + kb * TL::KV + j;
+          const int gk = k0 + kb * TL::KV + j;
           uint32_t v = 0;
-          if (gr < R && gk < K) v = *reinterpret_cast<const uint32_t*>(X + static_cast<int64_t>(gk) * ld + gr);
+          if (gr < Rlim && gk < K) v = *reinterpret_cast<const uint32_t*>(X + static_cast<int64_t>(gk) * ld + gr);
           r[i * TL::KV + j] = v;
         }
       }
@@ -76,22 +99,19 @@ struct Loader {
   }
 
   __device__ void store(T* __restrict__ S, int tid) {
-    using TL = Tile<T>;
     if constexpr (KC) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        int c = tid + NT * i;
-        int row = c >> 3, kc = c & 7;
+      for (int i = 0; i < DW / 4; ++i) {
+        const int c = tid + NT * i;
+        const int row = c >> 3, kc = c & 7;
         *reinterpret_cast<uint4*>(S + row * TL::PITCH + kc * TL::KV) =
             make_uint4(r[4 * i], r[4 * i + 1], r[4 * i + 2], r[4 * i + 3]);
       }
     } else {
-      constexpr int UNITS_PER_KB = 128 / TL::PAIR;
-      constexpr int UNITS_PER_THREAD = (8 * UNITS_PER_KB) / NT;
 #pragma unroll
-      for (int i = 0; i < UNITS_PER_THREAD; ++i) {
-        int u = tid + NT * i;
-        int kb = u / UNITS_PER_KB, rc = u % UNITS_PER_KB;
+      for (int i = 0; i < UPT; ++i) {
+        const int u = tid + NT * i;
+        const int kb = u / UPK, rc = u % UPK;
         const uint32_t* d = r + i * TL::KV;
         if constexpr (sizeof(T) == 2) {
           // d[j] packs (row 2rc, row 2rc+1) at k = 8kb + j; transpose to two
@@ -142,18 +162,71 @@ __device__ __forceinline__ void load4(const T* p, float* v, bool vec, int nvalid
   }
 }
 
-template <typename T, bool AKC, bool BKC, int EPI>
-__global__ void __launch_bounds__(NT, 2) gemm_kernel(GemmArgs g) {
+// Epilogue of one 4-wide output fragment: v[r] = C[m][nb + r] before the op.
+template <typename T, int EPI>
+__device__ __forceinline__ void epilogue4(const GemmArgs& g, int m, int nb, float* v, bool ld_vec) {
+  const int nvalid = min(4, g.N - nb);
+  const bool vec = ld_vec && nvalid == 4;
+  const int64_t off = static_cast<int64_t>(m) * g.ldc + nb;
+  if constexpr (EPI == EPI_STORE) {
+    store4<T>(static_cast<T*>(g.C) + off, v, vec, nvalid);
+  } else if constexpr (EPI == EPI_STORE_F32) {
+    store4<float>(static_cast<float*>(g.C) + off, v, vec, nvalid);
+  } else if constexpr (EPI == EPI_ACC_F32) {
+    float o[4];
+    load4<float>(static_cast<const float*>(g.C) + off, o, vec, nvalid);
+    for (int r = 0; r < 4; ++r) v[r] += o[r];
+    store4<float>(static_cast<float*>(g.C) + off, v, vec, nvalid);
+  } else if constexpr (EPI == EPI_BIAS) {
+    float b[4];
+    load4<T>(static_cast<const T*>(g.bias) + nb, b, nvalid == 4, nvalid);
+    for (int r = 0; r < 4; ++r) v[r] += b[r];
+    store4<T>(static_cast<T*>(g.C) + off, v, vec, nvalid);
+  } else if constexpr (EPI == EPI_BIAS_GELU) {
+    float b[4], gv[4];
+    load4<T>(static_cast<const T*>(g.bias) + nb, b, nvalid == 4, nvalid);
+    for (int r = 0; r < 4; ++r) {
+      // g = GELU(u) of the stored (rounded) u, so the backward sees the same u.
+      const float u = to_f<T>(from_f<T>(v[r] + b[r]));
+      v[r] = u;
+      gv[r] = gelu_f(u);
+    }
+    const int64_t aoff = static_cast<int64_t>(m) * g.ldaux + nb;
+    store4<T>(static_cast<T*>(g.aux) + aoff, v, vec && (g.ldaux & 3) == 0, nvalid);
+    store4<T>(static_cast<T*>(g.C) + off, gv, vec, nvalid);
+  } else if constexpr (EPI == EPI_BIAS_RESID) {
+    float b[4], x[4];
+    load4<T>(static_cast<const T*>(g.bias) + nb, b, nvalid == 4, nvalid);
+    load4<float>(g.resid + off, x, vec, nvalid);
+    for (int r = 0; r < 4; ++r) v[r] = x[r] + (v[r] + b[r]);
+    store4<float>(static_cast<float*>(g.C) + off, v, vec, nvalid);
+  } else if constexpr (EPI == EPI_GELU_BWD) {
+    float u[4];
+    const int64_t aoff = static_cast<int64_t>(m) * g.ldaux + nb;
+    load4<T>(static_cast<const T*>(g.aux) + aoff, u, vec && (g.ldaux & 3) == 0, nvalid);
+    for (int r = 0; r < 4; ++r) v[r] *= gelu_grad_f(u[r]);
+    store4<T>(static_cast<T*>(g.C) + off, v, vec, nvalid);
+  }
+}
+
+// One output tile per workgroup (blockIdx.x), one k range per split
+// (blockIdx.y).  With splits > 1 the raw fp32 sums go to the workspace
+// ws[split][M][N] and splitk_reduce applies the epilogue.
+template <typename T, bool AKC, bool BKC, int EPI, class CF>
+__global__ void __launch_bounds__(CF::NT) gemm_kernel(GemmArgs g) {
   using TL = Tile<T>;
+  constexpr int BM = CF::BM, BN = CF::BN, NT = CF::NT, TM = CF::TM, TN = CF::TN;
   __shared__ __attribute__((aligned(16))) T As[2][BM * TL::PITCH];
   __shared__ __attribute__((aligned(16))) T Bs[2][BN * TL::PITCH];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
-  const int wm = w >> 1, wn = w & 1;
+  const int wm = w / CF::WN, wn = w % CF::WN;
 
-  // Tile order: XCD-aware remap, then groups of 8 row-tiles sweeping columns.
+  // Tile order: XCD-aware remap (consecutive ids go round-robin over the 8
+  // XCDs, so give each XCD a contiguous range), then groups of 8 row-tiles
+  // sweeping the columns.
   const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
   const int total = tiles_m * tiles_n;
   int pid = blockIdx.x;
@@ -169,42 +242,47 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(GemmArgs g) {
   const T* __restrict__ A = static_cast<const T*>(g.A);
   const T* __restrict__ B = static_cast<const T*>(g.B);
 
-  Loader<T, AKC> la;
-  Loader<T, BKC> lb;
-  f32x4_t acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const int nk_all = (g.K + TL::BK - 1) / TL::BK;
+  const int per_split = (nk_all + gridDim.y - 1) / gridDim.y;
+  const int kt0 = blockIdx.y * per_split;
+  const int kt1 = min(nk_all, kt0 + per_split);
 
-  const int nk = (g.K + TL::BK - 1) / TL::BK;
-  la.load(A, g.lda, g.M, g.K, m0, 0, tid);
-  lb.load(B, g.ldb, g.N, g.K, n0, 0, tid);
-  la.store(As[0], tid);
-  lb.store(Bs[0], tid);
+  Loader<T, AKC, BM, NT> la;
+  Loader<T, BKC, BN, NT> lb;
+  f32x4_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  if (kt0 < kt1) {
+    la.load(A, g.lda, g.M, g.K, m0, kt0 * TL::BK, tid);
+    lb.load(B, g.ldb, g.N, g.K, n0, kt0 * TL::BK, tid);
+    la.store(As[0], tid);
+    lb.store(Bs[0], tid);
+  }
   __syncthreads();
 
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < nk;
+  for (int kt = kt0; kt < kt1; ++kt) {
+    const int cur = (kt - kt0) & 1;
+    const bool more = kt + 1 < kt1;
     if (more) {
       la.load(A, g.lda, g.M, g.K, m0, (kt + 1) * TL::BK, tid);
       lb.load(B, g.ldb, g.N, g.K, n0, (kt + 1) * TL::BK, tid);
     }
-    const T* as = As[cur];
-    const T* bs = Bs[cur];
+    const T* as = As[cur] + (wm * TM * 16 + lr) * TL::PITCH + lg * 8;
+    const T* bs = Bs[cur] + (wn * TN * 16 + lr) * TL::PITCH + lg * 8;
 #pragma unroll
     for (int s = 0; s < TL::NSLICE; ++s) {
-      Frag<T> fa[4], fb[4];
-      const int kk = s * 32 + lg * 8;
+      Frag<T> fa[TM], fb[TN];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) frag_load(fa[i], as + (wm * 64 + i * 16 + lr) * TL::PITCH + kk);
+      for (int i = 0; i < TM; ++i) frag_load(fa[i], as + i * 16 * TL::PITCH + s * 32);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) frag_load(fb[j], bs + (wn * 64 + j * 16 + lr) * TL::PITCH + kk);
+      for (int j = 0; j < TN; ++j) frag_load(fb[j], bs + j * 16 * TL::PITCH + s * 32);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) mfma16(acc[i][j], fb[j], fa[i]);
+        for (int j = 0; j < TN; ++j) mfma16(acc[i][j], fb[j], fa[i]);
     }
     if (more) {
       la.store(As[cur ^ 1], tid);
@@ -213,71 +291,75 @@ __global__ void __launch_bounds__(NT, 2) gemm_kernel(GemmArgs g) {
     __syncthreads();
   }
 
-  // Epilogue: acc[i][j][r] = C[m][nb + r].
+  // acc[i][j][r] = C[m][nb + r]
+  if (gridDim.y > 1) {
+    float* ws = g.ws + static_cast<int64_t>(blockIdx.y) * g.M * g.N;
+    const bool vec_ws = (g.N & 3) == 0;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int m = m0 + (wm * TM + i) * 16 + lr;
+      if (m >= g.M) continue;
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int nb = n0 + (wn * TN + j) * 16 + lg * 4;
+        if (nb >= g.N) continue;
+        const int nvalid = min(4, g.N - nb);
+        float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+        store4<float>(ws + static_cast<int64_t>(m) * g.N + nb, v, vec_ws && nvalid == 4, nvalid);
+      }
+    }
+    return;
+  }
   const bool ld_vec = (g.ldc & 3) == 0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int m = m0 + wm * 64 + i * 16 + lr;
+  for (int i = 0; i < TM; ++i) {
+    const int m = m0 + (wm * TM + i) * 16 + lr;
     if (m >= g.M) continue;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int nb = n0 + wn * 64 + j * 16 + lg * 4;
+    for (int j = 0; j < TN; ++j) {
+      const int nb = n0 + (wn * TN + j) * 16 + lg * 4;
       if (nb >= g.N) continue;
-      const int nvalid = min(4, g.N - nb);
-      const bool vec = ld_vec && nvalid == 4;
       float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-      const int64_t off = static_cast<int64_t>(m) * g.ldc + nb;
-      if constexpr (EPI == EPI_STORE) {
-        store4<T>(static_cast<T*>(g.C) + off, v, vec, nvalid);
-      } else if constexpr (EPI == EPI_STORE_F32) {
-        store4<float>(static_cast<float*>(g.C) + off, v, vec, nvalid);
-      } else if constexpr (EPI == EPI_ACC_F32) {
-        float o[4];
-        load4<float>(static_cast<const float*>(g.C) + off, o, vec, nvalid);
-        for (int r = 0; r < 4; ++r) v[r] += o[r];
-        store4<float>(static_cast<float*>(g.C) + off, v, vec, nvalid);
-      } else if constexpr (EPI == EPI_BIAS) {
-        float b[4];
-        load4<T>(static_cast<const T*>(g.bias) + nb, b, (nvalid == 4) && ((nb & 3) == 0), nvalid);
-        for (int r = 0; r < 4; ++r) v[r] += b[r];
-        store4<T>(static_cast<T*>(g.C) + off, v, vec, nvalid);
-      } else if constexpr (EPI == EPI_BIAS_GELU) {
-        float b[4];
-        load4<T>(static_cast<const T*>(g.bias) + nb, b, (nvalid == 4) && ((nb & 3) == 0), nvalid);
-        float gv[4];
-        for (int r = 0; r < 4; ++r) {
-          // g = GELU(u) of the stored (rounded) u, so the backward sees the same u.
-          float u = to_f<T>(from_f<T>(v[r] + b[r]));
-          v[r] = u;
-          gv[r] = gelu_f(u);
-        }
-        const int64_t aoff = static_cast<int64_t>(m) * g.ldaux + nb;
-        store4<T>(static_cast<T*>(g.aux) + aoff, v, vec && (g.ldaux & 3) == 0, nvalid);
-        store4<T>(static_cast<T*>(g.C) + off, gv, vec, nvalid);
-      } else if constexpr (EPI == EPI_BIAS_RESID) {
-        float b[4], x[4];
-        load4<T>(static_cast<const T*>(g.bias) + nb, b, (nvalid == 4) && ((nb & 3) == 0), nvalid);
-        load4<float>(g.resid + off, x, vec, nvalid);
-        for (int r = 0; r < 4; ++r) v[r] = x[r] + (v[r] + b[r]);
-        store4<float>(static_cast<float*>(g.C) + off, v, vec, nvalid);
-      } else if constexpr (EPI == EPI_GELU_BWD) {
-        float u[4];
-        const int64_t aoff = static_cast<int64_t>(m) * g.ldaux + nb;
-        load4<T>(static_cast<const T*>(g.aux) + aoff, u, vec && (g.ldaux & 3) == 0, nvalid);
-        for (int r = 0; r < 4; ++r) v[r] *= gelu_grad_f(u[r]);
-        store4<T>(static_cast<T*>(g.C) + off, v, vec, nvalid);
-      }
+      epilogue4<T, EPI>(g, m, nb, v, ld_vec);
     }
   }
 }
 
-template <typename T, bool AKC, bool BKC>
-hipError_t launch_t(const GemmArgs& g, int epi, hipStream_t s) {
-  const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-  dim3 grid(tiles), block(NT);
+// Sum of the split partials in split order, then the epilogue (store in the
+// element type, store fp32, or add to fp32).
+template <typename T, int EPI>
+__global__ void __launch_bounds__(256) splitk_reduce(GemmArgs g, int splits) {
+  const int64_t MN = static_cast<int64_t>(g.M) * g.N;
+  const int64_t q = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
+  if (q >= MN) return;
+  const int m = static_cast<int>(q / g.N);
+  const int nb = static_cast<int>(q % g.N);
+  if ((g.N & 3) == 0) {
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < splits; ++s) {
+      const float4 p = *reinterpret_cast<const float4*>(g.ws + s * MN + q);
+      v[0] += p.x; v[1] += p.y; v[2] += p.z; v[3] += p.w;
+    }
+    epilogue4<T, EPI>(g, m, nb, v, (g.ldc & 3) == 0);
+  } else {
+    for (int e = 0; e < 4 && q + e < MN; ++e) {
+      const int mm = static_cast<int>((q + e) / g.N), nn = static_cast<int>((q + e) % g.N);
+      float v[4] = {0.f, 0.f, 0.f, 0.f};
+      for (int s = 0; s < splits; ++s) v[0] += g.ws[s * MN + q + e];
+      GemmArgs g1 = g;
+      g1.N = nn + 1;  // one valid column at nn
+      epilogue4<T, EPI>(g1, mm, nn, v, false);
+    }
+  }
+}
+
+template <typename T, bool AKC, bool BKC, class CF>
+hipError_t launch_cfg(const GemmArgs& g, int epi, int splits, hipStream_t s) {
+  const int tiles = ((g.M + CF::BM - 1) / CF::BM) * ((g.N + CF::BN - 1) / CF::BN);
+  dim3 grid(tiles, splits), block(CF::NT);
   switch (epi) {
 #define ATOM_CASE(E) \
-  case E: hipLaunchKernelGGL((gemm_kernel<T, AKC, BKC, E>), grid, block, 0, s, g); break;
+  case E: hipLaunchKernelGGL((gemm_kernel<T, AKC, BKC, E, CF>), grid, block, 0, s, g); break;
     ATOM_CASE(EPI_STORE)
     ATOM_CASE(EPI_STORE_F32)
     ATOM_CASE(EPI_ACC_F32)
@@ -288,7 +370,39 @@ hipError_t launch_t(const GemmArgs& g, int epi, hipStream_t s) {
 #undef ATOM_CASE
     default: return hipErrorInvalidValue;
   }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || splits == 1) return e;
+  const int64_t MN = static_cast<int64_t>(g.M) * g.N;
+  dim3 rgrid(static_cast<unsigned>((MN / 4 + 255) / 256 + 1)), rblock(256);
+  switch (epi) {
+    case EPI_STORE: hipLaunchKernelGGL((splitk_reduce<T, EPI_STORE>), rgrid, rblock, 0, s, g, splits); break;
+    case EPI_STORE_F32: hipLaunchKernelGGL((splitk_reduce<T, EPI_STORE_F32>), rgrid, rblock, 0, s, g, splits); break;
+    case EPI_ACC_F32: hipLaunchKernelGGL((splitk_reduce<T, EPI_ACC_F32>), rgrid, rblock, 0, s, g, splits); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
+}
+
+// Tile configuration and split count for a problem: the large tile when it
+// gives at least one workgroup per CU, else the 128x128 tile; a split over k
+// when even that leaves the CUs idle and k is long (weight gradients of
+// small layers), limited by the workspace.
+template <typename T, bool AKC, bool BKC>
+hipError_t launch_t(const GemmArgs& g, int epi, hipStream_t s) {
+  constexpr int CUS = 256;
+  const int tiles_big = ((g.M + Big::BM - 1) / Big::BM) * ((g.N + Big::BN - 1) / Big::BN);
+  if (tiles_big >= CUS) return launch_cfg<T, AKC, BKC, Big>(g, epi, 1, s);
+  const int tiles = ((g.M + Small::BM - 1) / Small::BM) * ((g.N + Small::BN - 1) / Small::BN);
+  const int nk = (g.K + Tile<T>::BK - 1) / Tile<T>::BK;
+  int splits = 1;
+  const bool can_split = epi == EPI_STORE || epi == EPI_STORE_F32 || epi == EPI_ACC_F32;
+  if (can_split && g.ws && tiles < 2 * CUS && nk >= 32) {
+    splits = std::min((2 * CUS + tiles - 1) / tiles, nk / 16);
+    const int64_t per = static_cast<int64_t>(g.M) * g.N * 4;
+    splits = static_cast<int>(std::min<int64_t>(splits, static_cast<int64_t>(g.ws_bytes / per)));
+    splits = std::max(1, std::min(splits, 16));
+  }
+  return launch_cfg<T, AKC, BKC, Small>(g, epi, splits, s);
 }
 
 }  // namespace

@@ -28,6 +28,8 @@ struct GemmArgs {
   void* aux;
   int64_t lda, ldb, ldc, ldaux;
   int M, N, K;
+  float* ws;          // optional fp32 workspace for a split over k (may be null)
+  uint64_t ws_bytes;  // its size; a split needs splits * M * N * 4 bytes
 };
 
 hipError_t gemm_check(const GemmArgs& g, int dtype, bool a_kcontig, bool b_kcontig);

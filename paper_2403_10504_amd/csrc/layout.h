@@ -19,6 +19,9 @@ inline int elem_bytes(const atom_config& c) { return c.dtype == ATOM_BF16 ? 2 : 
 // Rows of the logits chunk of the LM head (the [N][V] fp32 logits are never
 // held whole).
 constexpr int64_t HEAD_CHUNK = 2048;
+// fp32 workspace that lets weight-gradient GEMMs of narrow layers split their
+// long token dimension over workgroups.
+constexpr uint64_t SPLITK_BYTES = 64ull << 20;
 
 struct TensorDesc {
   std::string name;
@@ -39,6 +42,7 @@ struct ArenaLayout {
   uint64_t ckpt, ckpt_bytes_each;  // (L+1) x accum x [N][d] fp32 block inputs
   uint64_t dres, dres_lp;          // accum x [N][d] fp32 / working dtype
   uint64_t loss_rows, loss_out;
+  uint64_t splitk, splitk_bytes;   // fp32 workspace for GEMMs split over k
   uint64_t ws;                     // start of the union workspace
   // block workspace (offsets inside ws)
   uint64_t a, qkv, o, x1, c, u, g, mu1, rs1, mu2, rs2, lse, delta, du, dbuf, dout, dqkv, part;

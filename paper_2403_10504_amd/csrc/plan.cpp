@@ -97,6 +97,8 @@ ArenaLayout arena_layout(const atom_config& c, uint64_t slot_bytes, int n_slots)
   a.dres_lp = c.dtype == ATOM_BF16 ? take(C * N * d * 2) : a.dres;
   a.loss_rows = take(C * N * 4);
   a.loss_out = take(256);
+  a.splitk_bytes = SPLITK_BYTES;
+  a.splitk = take(a.splitk_bytes);
   // partial-sum scratch: column sums over ceil(N/64) row blocks, or LayerNorm
   // partials (one per 16-row block, two rows of d each)
   a.part_floats = std::max((N + 63) / 64 * std::max(3 * d, f), (N + 15) / 16 * 2 * d);

@@ -288,7 +288,10 @@ hipError_t run_gemm(atom_ctx* c, const GemmArgs& g, bool akc, bool bkc, int epi)
     hipError_t e = hipEventRecord(c->probe_ev[2 * c->probe_pending], c->cs);
     if (e != hipSuccess) return e;
   }
-  hipError_t e = gemm(g, c->dt, akc, bkc, epi, c->cs);
+  GemmArgs gw = g;
+  gw.ws = reinterpret_cast<float*>(A(c, c->lay.splitk));
+  gw.ws_bytes = c->lay.splitk_bytes;
+  hipError_t e = gemm(gw, c->dt, akc, bkc, epi, c->cs);
   if (e != hipSuccess || !probe) return e;
   e = hipEventRecord(c->probe_ev[2 * c->probe_pending + 1], c->cs);
   if (e != hipSuccess) return e;

@@ -84,6 +84,47 @@ def test_gemm_epilogues(dtype, epi):
         assert err < tol, (akc, bkc, err)
 
 
+def sampled_gemm_check(dtype, akc, bkc, M, N, K, ws_bytes=0, seed=0, rows=48):
+    """Large GEMM: compare a random sample of full output rows with fp64 dot products."""
+    r = U.rng(seed)
+    a_shape = (M, K) if akc else (K, M)
+    b_shape = (N, K) if bkc else (K, N)
+    Am = U.rep(r.standard_normal(a_shape), dtype)
+    Bm = U.rep(r.standard_normal(b_shape), dtype)
+    dA, dB = U.dev(Am, dtype), U.dev(Bm, dtype)
+    dC = U.empty((M, N), "f32")
+    ws = U.empty(max(1, ws_bytes // 4), "f32")
+    A.atom_k_gemm(U.dt_code(dtype), akc, bkc, A.ATOM_EPI_STORE_F32, M, N, K, U.ptr(dA), a_shape[1], U.ptr(dB),
+                  b_shape[1], U.ptr(dC), N, stream=stream(), ws=U.ptr(ws) if ws_bytes else None, ws_bytes=ws_bytes)
+    U.sync()
+    got = U.host(dC)
+    pick = np.sort(r.choice(M, size=min(rows, M), replace=False))
+    pick[-1] = M - 1  # always include the ragged last row
+    Aop = (Am if akc else Am.T)[pick].astype(np.float64)
+    Bop = (Bm.T if bkc else Bm).astype(np.float64)
+    return U.rel_err(got[pick], Aop @ Bop), got
+
+
+@pytest.mark.parametrize("akc,bkc", [(1, 1), (1, 0), (0, 0)])
+def test_gemm_large_tile_path(akc, bkc):
+    # >= 256 output tiles of 256x256 selects the large-tile kernel; ragged edges
+    err, _ = sampled_gemm_check("bf16", akc, bkc, 4100, 4104, 264, seed=akc + 2 * bkc)
+    assert err < 1e-4, err
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_gemm_split_k_is_exact_and_deterministic(dtype):
+    M, N, K = 256, 392, 8192  # few output tiles, long k: splits over k
+    ws = 16 * M * N * 4
+    err, c1 = sampled_gemm_check(dtype, 0, 0, M, N, K, ws_bytes=ws, seed=5, rows=M)
+    assert err < 1e-4, err
+    _, c2 = sampled_gemm_check(dtype, 0, 0, M, N, K, ws_bytes=ws, seed=5, rows=8)
+    assert np.array_equal(c1, c2)
+    err0, c0 = sampled_gemm_check(dtype, 0, 0, M, N, K, ws_bytes=0, seed=5, rows=M)
+    assert err0 < 1e-4
+    assert not np.array_equal(c0, c1)  # the split path really ran (different summation order)
+
+
 def test_gemm_rejects_unsupported_shapes():
     t = U.empty((64, 64), "bf16")
     with pytest.raises(A.AtomError):  # K not a multiple of 8
