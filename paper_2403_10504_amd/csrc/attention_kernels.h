@@ -1,5 +1,6 @@
 // Causal self-attention kernel templates; instantiated by attention.hip
 // (bf16) and attention_f32.hip (fp32 validation mode).
+//
 // Fused causal self-attention on CDNA4 matrix cores (tiled, online softmax;
 // the [T, T] score matrix never leaves registers).
 //
@@ -8,13 +9,16 @@
 // exp(scale * q.k) over the unmasked keys).  scale = 1/sqrt(dh); key j is
 // visible to query i iff j <= i.
 //
-// Workgroup = (64-row tile, batch*head), four waves of 16 rows each.
-//   forward : S^T = K Q^T per 64-key tile (lanes hold one query, so the
-//             accumulators feed the P V^T product as B operands directly);
-//   dK, dV  : one workgroup per 64-key tile loops over the query tiles at or
-//             below the diagonal; S = Q K^T, dP = dO V^T, dS = P (dP - D);
-//             dV += P^T dO, dK += dS^T Q;
-//   dQ      : one workgroup per 64-query tile loops over key tiles; dQ += dS K.
+// Each wave owns G groups of 16 rows; fragments read from LDS are reused by
+// all G groups.  Key/query tiles of 64 rows are staged in LDS and, when two
+// stages fit, double-buffered: the next tile is loaded into registers while
+// the current one is consumed, so global-memory latency overlaps the MFMAs.
+//   forward : S^T = K Q^T (lanes hold one query, so the accumulators feed the
+//             P V product as B operands directly); online softmax; O += V^T P^T.
+//   dK, dV  : a workgroup of W waves owns 16*W keys and loops over the query
+//             tiles at or below the diagonal; S = Q K^T, dP = dO V^T,
+//             dS = P (dP - D); dV += P^T dO, dK += dS^T Q.
+//   dQ      : a workgroup owns 64*G queries and loops over key tiles; dQ += dS K.
 // Splitting dQ from dK/dV makes every output owned by one workgroup, so the
 // backward needs no atomics and is bitwise reproducible.
 #pragma once
@@ -24,7 +28,16 @@
 namespace atom {
 namespace attn {
 
-constexpr int BT = 64;  // rows per tile (queries or keys)
+constexpr int BT = 64;  // rows per staged tile (keys or queries)
+// Lazy rescaling: the running row maximum is only raised when a new score
+// exceeds it by more than this (log2 units), so p = 2^(s - m) <= 2^8.  The
+// final division by the row sum makes the result independent of the
+// reference maximum.
+constexpr float RESCALE_LOG2 = 8.f;
+
+// 2^x by the hardware instruction (inputs here are finite or -inf; results
+// that would be denormal flush to zero, as p is later rounded anyway).
+__device__ __forceinline__ float ex2(float x) { return __builtin_amdgcn_exp2f(x); }
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 
@@ -36,53 +49,94 @@ struct ALay {
   static constexpr int TP = BT + PAD;        // pitch of a transposed [DH][64] tile
   static constexpr int NS = DH / 32;         // 32-wide k slices over dh
   static constexpr int NCT = DH / 16;        // 16-wide column tiles over dh
+  static constexpr int ROWS_BYTES = BT * RP * sizeof(T);
+  static constexpr int TRANS_BYTES = DH * TP * sizeof(T);
 };
 
-// Stage rows [r0, r0+64) of a head slice (row stride ld) into S[64][RP].
-template <typename T, int DH>
-__device__ __forceinline__ void stage_rows(T* S, const T* __restrict__ base, int64_t ld, int r0, int nrows,
-                                           int tid) {
+// Register staging of one 64-row tile of a head slice (row stride ld), in
+// the natural [row][c] layout (16-byte chunks) or transposed [c][row] (dword
+// loads of PAIR columns over KV consecutive rows, transposed in registers).
+template <typename T, int DH, int NT, bool TRANS>
+struct TileLoader {
   using L = ALay<T, DH>;
-  constexpr int CPR = DH / L::KV;  // 16-byte chunks per row
-  for (int c = tid; c < BT * CPR; c += 256) {
-    const int r = c / CPR, k = (c % CPR) * L::KV;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (r0 + r < nrows) v = *reinterpret_cast<const uint4*>(base + static_cast<int64_t>(r0 + r) * ld + k);
-    *reinterpret_cast<uint4*>(S + r * L::RP + k) = v;
-  }
-}
+  static constexpr int CPR = DH / L::KV;                   // natural: chunks per row
+  static constexpr int NCH = BT * CPR / NT;                 // natural: chunks per thread
+  static constexpr int PAIR = 4 / sizeof(T);
+  static constexpr int UC = DH / PAIR;                      // transposed: dword columns
+  static constexpr int UNITS = (BT / L::KV) * UC;
+  static constexpr int NU = (UNITS + NT - 1) / NT;          // transposed: units per thread
+  static constexpr int NREG = TRANS ? NU * L::KV : NCH * 4;
+  uint32_t r[NREG];
 
-// Stage the same rows transposed into S[DH][TP] (S[c][r] = x[r0 + r][c]).
-template <typename T, int DH>
-__device__ __forceinline__ void stage_rows_t(T* S, const T* __restrict__ base, int64_t ld, int r0, int nrows,
-                                             int tid) {
-  using L = ALay<T, DH>;
-  constexpr int PAIR = 4 / sizeof(T);
-  constexpr int UC = DH / PAIR;            // dword columns
-  constexpr int UNITS = (BT / L::KV) * UC; // (KV rows x PAIR cols) units
-  for (int u = tid; u < UNITS; u += 256) {
-    const int rb = u / UC, cc = (u % UC) * PAIR;
-    uint32_t d[L::KV];
+  // Rows r0 .. r0+63 of the tile; rows at or beyond nrows read as zero.
+  // A tile wholly inside [0, nrows) takes the unchecked path.
+  __device__ __forceinline__ void load(const T* __restrict__ base, int64_t ld, int r0, int nrows, int tid) {
+    const T* tb = base + static_cast<int64_t>(r0) * ld;
+    const bool full = r0 + BT <= nrows;
+    if constexpr (!TRANS) {
 #pragma unroll
-    for (int j = 0; j < L::KV; ++j) {
-      const int r = r0 + rb * L::KV + j;
-      d[j] = r < nrows ? *reinterpret_cast<const uint32_t*>(base + static_cast<int64_t>(r) * ld + cc) : 0u;
-    }
-    if constexpr (sizeof(T) == 2) {
-      uint4 lo, hi;
-      lo.x = (d[0] & 0xffffu) | (d[1] << 16); hi.x = (d[0] >> 16) | (d[1] & 0xffff0000u);
-      lo.y = (d[2] & 0xffffu) | (d[3] << 16); hi.y = (d[2] >> 16) | (d[3] & 0xffff0000u);
-      lo.z = (d[4] & 0xffffu) | (d[5] << 16); hi.z = (d[4] >> 16) | (d[5] & 0xffff0000u);
-      lo.w = (d[6] & 0xffffu) | (d[7] << 16); hi.w = (d[6] >> 16) | (d[7] & 0xffff0000u);
-      *reinterpret_cast<uint4*>(S + cc * L::TP + rb * 8) = lo;
-      *reinterpret_cast<uint4*>(S + (cc + 1) * L::TP + rb * 8) = hi;
+      for (int i = 0; i < NCH; ++i) {
+        const int c = tid + NT * i;
+        const int rr = c / CPR, k = (c % CPR) * L::KV;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (full || r0 + rr < nrows) v = *reinterpret_cast<const uint4*>(tb + static_cast<int64_t>(rr) * ld + k);
+        r[4 * i] = v.x;
+        r[4 * i + 1] = v.y;
+        r[4 * i + 2] = v.z;
+        r[4 * i + 3] = v.w;
+      }
     } else {
-      *reinterpret_cast<uint4*>(S + cc * L::TP + rb * 4) = make_uint4(d[0], d[1], d[2], d[3]);
+#pragma unroll
+      for (int i = 0; i < NU; ++i) {
+        const int u = tid + NT * i;
+        const int rb = u / UC, cc = (u % UC) * PAIR;
+        const T* p = tb + static_cast<int64_t>(rb * L::KV) * ld + cc;
+        if (full && (UNITS % NT == 0 || u < UNITS)) {
+#pragma unroll
+          for (int j = 0; j < L::KV; ++j) r[i * L::KV + j] = *reinterpret_cast<const uint32_t*>(p + j * ld);
+        } else {
+#pragma unroll
+          for (int j = 0; j < L::KV; ++j) {
+            const int rr = r0 + rb * L::KV + j;
+            r[i * L::KV + j] = (u < UNITS && rr < nrows) ? *reinterpret_cast<const uint32_t*>(p + j * ld) : 0u;
+          }
+        }
+      }
     }
   }
-}
 
-// Fragment of a head row (for a register-resident operand): row r, k slice s.
+  __device__ __forceinline__ void store(T* S, int tid) {
+    if constexpr (!TRANS) {
+#pragma unroll
+      for (int i = 0; i < NCH; ++i) {
+        const int c = tid + NT * i;
+        const int rr = c / CPR, k = (c % CPR) * L::KV;
+        *reinterpret_cast<uint4*>(S + rr * L::RP + k) = make_uint4(r[4 * i], r[4 * i + 1], r[4 * i + 2], r[4 * i + 3]);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < NU; ++i) {
+        const int u = tid + NT * i;
+        if (u >= UNITS) continue;
+        const int rb = u / UC, cc = (u % UC) * PAIR;
+        const uint32_t* d = r + i * L::KV;
+        if constexpr (sizeof(T) == 2) {
+          uint4 lo, hi;
+          lo.x = (d[0] & 0xffffu) | (d[1] << 16); hi.x = (d[0] >> 16) | (d[1] & 0xffff0000u);
+          lo.y = (d[2] & 0xffffu) | (d[3] << 16); hi.y = (d[2] >> 16) | (d[3] & 0xffff0000u);
+          lo.z = (d[4] & 0xffffu) | (d[5] << 16); hi.z = (d[4] >> 16) | (d[5] & 0xffff0000u);
+          lo.w = (d[6] & 0xffffu) | (d[7] << 16); hi.w = (d[6] >> 16) | (d[7] & 0xffff0000u);
+          *reinterpret_cast<uint4*>(S + cc * L::TP + rb * 8) = lo;
+          *reinterpret_cast<uint4*>(S + (cc + 1) * L::TP + rb * 8) = hi;
+        } else {
+          *reinterpret_cast<uint4*>(S + cc * L::TP + rb * 4) = make_uint4(d[0], d[1], d[2], d[3]);
+        }
+      }
+    }
+  }
+};
+
+// Fragment of a head row (for a register-resident operand): row r, column col.
 template <typename T>
 __device__ __forceinline__ void frag_global(Frag<T>& f, const T* __restrict__ base, int64_t ld, int r, int nrows,
                                             int col) {
@@ -90,9 +144,9 @@ __device__ __forceinline__ void frag_global(Frag<T>& f, const T* __restrict__ ba
   else frag_zero(f);
 }
 
-// Build the B-operand fragment for a 32-wide slice from two 16-row tiles of
-// per-lane accumulator values x[t][r] (t = 2s, 2s+1): element e < 4 takes
-// x[2s][e], e >= 4 takes x[2s+1][e-4].  The matching A operand reads rows
+// B-operand fragment for a 32-wide slice from two 16-row tiles of per-lane
+// accumulator values x[t][r] (t = 2s, 2s+1): element e < 4 takes x[2s][e],
+// e >= 4 takes x[2s+1][e-4].  The matching A operand reads rows
 // 32s + 4g + e and 32s + 16 + 4g + (e-4) (see frag_pair_rows).
 template <typename T>
 __device__ __forceinline__ void frag_from_pair(Frag<T>& f, const float (*x)[4], int s) {
@@ -109,28 +163,30 @@ __device__ __forceinline__ void frag_pair_rows(Frag<T>& f, const T* S, int c, in
 }
 
 template <typename T>
-__device__ __forceinline__ void store_row4(T* p, const float* v, int nvalid) {
-  if (nvalid == 4) {
-    if constexpr (sizeof(T) == 2) {
-      uint2 w;
-      w.x = static_cast<uint32_t>(f2bf(v[0])) | (static_cast<uint32_t>(f2bf(v[1])) << 16);
-      w.y = static_cast<uint32_t>(f2bf(v[2])) | (static_cast<uint32_t>(f2bf(v[3])) << 16);
-      *reinterpret_cast<uint2*>(p) = w;
-    } else {
-      *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
-    }
+__device__ __forceinline__ void store_row4(T* p, const float* v) {
+  if constexpr (sizeof(T) == 2) {
+    uint2 w;
+    w.x = static_cast<uint32_t>(f2bf(v[0])) | (static_cast<uint32_t>(f2bf(v[1])) << 16);
+    w.y = static_cast<uint32_t>(f2bf(v[2])) | (static_cast<uint32_t>(f2bf(v[3])) << 16);
+    *reinterpret_cast<uint2*>(p) = w;
   } else {
-    for (int r = 0; r < nvalid; ++r) p[r] = from_f<T>(v[r]);
+    *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
   }
 }
 
+// Two stages of `bytes` fit in the LDS budget of one workgroup.
+constexpr bool two_stages(int bytes) { return 2 * bytes <= 150 * 1024; }
+
 // ------------------------------------------------------------------ forward
-template <typename T, int DH>
+template <typename T, int DH, int G>
 __global__ void __launch_bounds__(256) attn_fwd_kernel(const T* __restrict__ qkv, T* __restrict__ o,
                                                        float* __restrict__ lse, int B, int Tn, int H) {
   using L = ALay<T, DH>;
-  __shared__ __attribute__((aligned(16))) T Ks[BT * L::RP];
-  __shared__ __attribute__((aligned(16))) T Vt[DH * L::TP];
+  constexpr int STAGE = L::ROWS_BYTES + L::TRANS_BYTES;
+  constexpr int NBUF = two_stages(STAGE) ? 2 : 1;
+  constexpr int BQ = 4 * 16 * G;  // queries per workgroup
+  __shared__ __attribute__((aligned(16))) T Ks[NBUF][BT * L::RP];
+  __shared__ __attribute__((aligned(16))) T Vt[NBUF][DH * L::TP];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
@@ -140,86 +196,141 @@ __global__ void __launch_bounds__(256) attn_fwd_kernel(const T* __restrict__ qkv
   const T* qb = qkv + static_cast<int64_t>(b) * Tn * ld + h * DH;
   const T* kb = qb + d;
   const T* vb = qb + 2 * d;
-  const int q0 = blockIdx.x * BT;
-  const int qi = q0 + w * 16 + lr;  // this lane's query
+  const int q0 = blockIdx.x * BQ;
+  const int qw = q0 + w * 16 * G;  // first query of this wave
   const float sc = LOG2E / sqrtf(static_cast<float>(DH));
 
-  Frag<T> qf[L::NS];
+  Frag<T> qf[G][L::NS];
 #pragma unroll
-  for (int s = 0; s < L::NS; ++s) frag_global(qf[s], qb, ld, qi, Tn, 32 * s + 8 * lg);
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int s = 0; s < L::NS; ++s) frag_global(qf[g][s], qb, ld, qw + g * 16 + lr, Tn, 32 * s + 8 * lg);
 
-  f32x4_t acc_o[L::NCT];
+  f32x4_t acc_o[G][L::NCT];
+  float m_i[G], l_i[G];
 #pragma unroll
-  for (int c = 0; c < L::NCT; ++c) acc_o[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m_i = -1e30f, l_i = 0.f;
-
-  const int n_kt = min((Tn + BT - 1) / BT, (q0 + BT - 1) / BT + 1);
-  for (int kt = 0; kt < n_kt; ++kt) {
-    const int j0 = kt * BT;
-    __syncthreads();
-    stage_rows<T, DH>(Ks, kb, ld, j0, Tn, tid);
-    stage_rows_t<T, DH>(Vt, vb, ld, j0, Tn, tid);
-    __syncthreads();
-
-    float p[4][4];
-    float mloc = -INFINITY;
+  for (int g = 0; g < G; ++g) {
+    m_i[g] = -1e30f;
+    l_i[g] = 0.f;
 #pragma unroll
-    for (int jt = 0; jt < 4; ++jt) {
-      f32x4_t a = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < L::NS; ++s) {
-        Frag<T> kf;
-        frag_load(kf, Ks + (jt * 16 + lr) * L::RP + 32 * s + 8 * lg);
-        mfma16(a, kf, qf[s]);
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int j = j0 + jt * 16 + 4 * lg + r;
-        const float x = (j <= qi && j < Tn) ? a[r] * sc : -INFINITY;
-        p[jt][r] = x;
-        mloc = fmaxf(mloc, x);
-      }
-    }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-    const float m_new = fmaxf(m_i, mloc);
-    const float alpha = exp2f(m_i - m_new);
-    float lsum = 0.f;
-#pragma unroll
-    for (int jt = 0; jt < 4; ++jt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        p[jt][r] = exp2f(p[jt][r] - m_new);
-        lsum += p[jt][r];
-      }
-    l_i = l_i * alpha + lsum;
-    m_i = m_new;
-#pragma unroll
-    for (int c = 0; c < L::NCT; ++c) acc_o[c] *= alpha;
-#pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) {
-      Frag<T> pf;
-      frag_from_pair(pf, p, s2);
-#pragma unroll
-      for (int c = 0; c < L::NCT; ++c) {
-        Frag<T> vf;
-        frag_pair_rows<T, DH>(vf, Vt, c * 16 + lr, s2, lg);
-        mfma16(acc_o[c], vf, pf);
-      }
-    }
+    for (int c = 0; c < L::NCT; ++c) acc_o[g][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
 
-  float l_tot = l_i + __shfl_xor(l_i, 16, 64);
-  l_tot += __shfl_xor(l_tot, 32, 64);
-  if (qi < Tn) {
-    const float inv = 1.f / l_tot;
-    T* orow = o + (static_cast<int64_t>(b) * Tn + qi) * d + h * DH;
-#pragma unroll
-    for (int c = 0; c < L::NCT; ++c) {
-      float v[4] = {acc_o[c][0] * inv, acc_o[c][1] * inv, acc_o[c][2] * inv, acc_o[c][3] * inv};
-      store_row4<T>(orow + c * 16 + 4 * lg, v, 4);
+  TileLoader<T, DH, 256, false> lk;
+  TileLoader<T, DH, 256, true> lv;
+  const int n_kt = min((Tn + BT - 1) / BT, (min(q0 + BQ, Tn) - 1) / BT + 1);
+  lk.load(kb, ld, 0, Tn, tid);
+  lv.load(vb, ld, 0, Tn, tid);
+  lk.store(Ks[0], tid);
+  lv.store(Vt[0], tid);
+  __syncthreads();
+
+  for (int kt = 0; kt < n_kt; ++kt) {
+    const int j0 = kt * BT;
+    const int cur = NBUF == 2 ? (kt & 1) : 0;
+    const bool more = kt + 1 < n_kt;
+    if (NBUF == 2 && more) {
+      lk.load(kb, ld, j0 + BT, Tn, tid);
+      lv.load(vb, ld, j0 + BT, Tn, tid);
     }
-    if (lg == 0) lse[(static_cast<int64_t>(b) * H + h) * Tn + qi] = (m_i + log2f(l_tot)) * LN2;
+    const T* ks = Ks[cur];
+    const T* vt = Vt[cur];
+    // the wave's queries that can see part of this key tile
+    if (j0 <= qw + 16 * G - 1) {
+      float p[G][4][4];
+      float mloc[G];
+#pragma unroll
+      for (int g = 0; g < G; ++g) mloc[g] = -INFINITY;
+#pragma unroll
+      for (int jt = 0; jt < 4; ++jt) {
+        f32x4_t a[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) a[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < L::NS; ++s) {
+          Frag<T> kf;
+          frag_load(kf, ks + (jt * 16 + lr) * L::RP + 32 * s + 8 * lg);
+#pragma unroll
+          for (int g = 0; g < G; ++g) mfma16(a[g], kf, qf[g][s]);
+        }
+        const bool edge = j0 + BT > qw || j0 + BT > Tn;  // tile touches the diagonal or the end
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const int qi = qw + g * 16 + lr;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int j = j0 + jt * 16 + 4 * lg + r;
+            const float x = (!edge || (j <= qi && j < Tn)) ? a[g][r] * sc : -INFINITY;
+            p[g][jt][r] = x;
+            mloc[g] = fmaxf(mloc[g], x);
+          }
+        }
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float mx = fmaxf(mloc[g], __shfl_xor(mloc[g], 16, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        // raise the reference maximum only when some lane of the wave needs it
+        // (a wave-uniform branch, so the rescale of O is skipped together)
+        if (__builtin_amdgcn_ballot_w64(mx > m_i[g] + RESCALE_LOG2) != 0) {
+          const float m_new = fmaxf(m_i[g], mx);
+          const float alpha = ex2(m_i[g] - m_new);
+          l_i[g] *= alpha;
+          m_i[g] = m_new;
+#pragma unroll
+          for (int c = 0; c < L::NCT; ++c) acc_o[g][c] *= alpha;
+        }
+        float lsum = 0.f;
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            p[g][jt][r] = ex2(p[g][jt][r] - m_i[g]);
+            lsum += p[g][jt][r];
+          }
+        l_i[g] += lsum;
+      }
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        Frag<T> pf[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) frag_from_pair(pf[g], p[g], s2);
+#pragma unroll
+        for (int c = 0; c < L::NCT; ++c) {
+          Frag<T> vf;
+          frag_pair_rows<T, DH>(vf, vt, c * 16 + lr, s2, lg);
+#pragma unroll
+          for (int g = 0; g < G; ++g) mfma16(acc_o[g][c], vf, pf[g]);
+        }
+      }
+    }
+    if (more) {
+      if (NBUF == 1) {
+        __syncthreads();
+        lk.load(kb, ld, j0 + BT, Tn, tid);
+        lv.load(vb, ld, j0 + BT, Tn, tid);
+      }
+      lk.store(Ks[NBUF == 2 ? (cur ^ 1) : 0], tid);
+      lv.store(Vt[NBUF == 2 ? (cur ^ 1) : 0], tid);
+    }
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const int qi = qw + g * 16 + lr;
+    float l_tot = l_i[g] + __shfl_xor(l_i[g], 16, 64);
+    l_tot += __shfl_xor(l_tot, 32, 64);
+    if (qi < Tn) {
+      const float inv = 1.f / l_tot;
+      T* orow = o + (static_cast<int64_t>(b) * Tn + qi) * d + h * DH;
+#pragma unroll
+      for (int c = 0; c < L::NCT; ++c) {
+        float v[4] = {acc_o[g][c][0] * inv, acc_o[g][c][1] * inv, acc_o[g][c][2] * inv, acc_o[g][c][3] * inv};
+        store_row4<T>(orow + c * 16 + 4 * lg, v);
+      }
+      if (lg == 0) lse[(static_cast<int64_t>(b) * H + h) * Tn + qi] = (m_i[g] + log2f(l_tot)) * LN2;
+    }
   }
 }
 
@@ -244,17 +355,22 @@ __global__ void __launch_bounds__(256) attn_delta_kernel(const T* __restrict__ o
 }
 
 // ------------------------------------------------------ backward: dK, dV
-template <typename T, int DH>
-__global__ void __launch_bounds__(256) attn_bwd_dkdv_kernel(const T* __restrict__ qkv, const T* __restrict__ dout,
-                                                            const float* __restrict__ lse,
-                                                            const float* __restrict__ delta, T* __restrict__ dqkv,
-                                                            int B, int Tn, int H) {
+template <typename T, int DH, int W>
+__global__ void __launch_bounds__(64 * W) attn_bwd_dkdv_kernel(const T* __restrict__ qkv,
+                                                               const T* __restrict__ dout,
+                                                               const float* __restrict__ lse,
+                                                               const float* __restrict__ delta,
+                                                               T* __restrict__ dqkv, int B, int Tn, int H) {
   using L = ALay<T, DH>;
-  __shared__ __attribute__((aligned(16))) T Qs[BT * L::RP];
-  __shared__ __attribute__((aligned(16))) T Qt[DH * L::TP];
-  __shared__ __attribute__((aligned(16))) T Os[BT * L::RP];
-  __shared__ __attribute__((aligned(16))) T Ot[DH * L::TP];
-  __shared__ float lse_s[BT], del_s[BT];
+  constexpr int NT = 64 * W;
+  constexpr int STAGE = 2 * (L::ROWS_BYTES + L::TRANS_BYTES);
+  constexpr int NBUF = two_stages(STAGE) ? 2 : 1;
+  constexpr int BKEYS = 16 * W;
+  __shared__ __attribute__((aligned(16))) T Qs[NBUF][BT * L::RP];
+  __shared__ __attribute__((aligned(16))) T Qt[NBUF][DH * L::TP];
+  __shared__ __attribute__((aligned(16))) T Os[NBUF][BT * L::RP];
+  __shared__ __attribute__((aligned(16))) T Ot[NBUF][DH * L::TP];
+  __shared__ float lse_s[NBUF][BT], del_s[NBUF][BT];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
@@ -267,8 +383,9 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_kernel(const T* __restrict_
   const T* ob = dout + static_cast<int64_t>(b) * Tn * d + h * DH;  // dO, row stride d
   const float* lse_b = lse + (static_cast<int64_t>(b) * H + h) * Tn;
   const float* del_b = delta + (static_cast<int64_t>(b) * H + h) * Tn;
-  const int j0 = blockIdx.x * BT;
-  const int kj = j0 + w * 16 + lr;  // this lane's key
+  const int k0 = blockIdx.x * BKEYS;
+  const int kw = k0 + w * 16;  // this wave's first key
+  const int kj = kw + lr;      // this lane's key
   const float sc = LOG2E / sqrtf(static_cast<float>(DH));
 
   Frag<T> kf[L::NS], vf[L::NS];
@@ -284,56 +401,93 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_kernel(const T* __restrict_
     acc_dv[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
 
-  const int n_qt = (Tn + BT - 1) / BT;
-  for (int qt = j0 / BT; qt < n_qt; ++qt) {
-    const int i0 = qt * BT;
-    __syncthreads();
-    stage_rows<T, DH>(Qs, qb, ld, i0, Tn, tid);
-    stage_rows_t<T, DH>(Qt, qb, ld, i0, Tn, tid);
-    stage_rows<T, DH>(Os, ob, d, i0, Tn, tid);
-    stage_rows_t<T, DH>(Ot, ob, d, i0, Tn, tid);
+  TileLoader<T, DH, NT, false> lq, lo;
+  TileLoader<T, DH, NT, true> lqt, lot;
+  const int qt0 = k0 / BT, n_qt = (Tn + BT - 1) / BT;
+  float pre_lse = 0.f, pre_del = 0.f;
+  auto load_tile = [&](int i0) {
+    lq.load(qb, ld, i0, Tn, tid);
+    lqt.load(qb, ld, i0, Tn, tid);
+    lo.load(ob, d, i0, Tn, tid);
+    lot.load(ob, d, i0, Tn, tid);
     if (tid < BT) {
       const int i = i0 + tid;
-      lse_s[tid] = i < Tn ? lse_b[i] * LOG2E : INFINITY;
-      del_s[tid] = i < Tn ? del_b[i] : 0.f;
+      pre_lse = i < Tn ? lse_b[i] * LOG2E : INFINITY;
+      pre_del = i < Tn ? del_b[i] : 0.f;
+    }
+  };
+  auto store_tile = [&](int buf) {
+    lq.store(Qs[buf], tid);
+    lqt.store(Qt[buf], tid);
+    lo.store(Os[buf], tid);
+    lot.store(Ot[buf], tid);
+    if (tid < BT) {
+      lse_s[buf][tid] = pre_lse;
+      del_s[buf][tid] = pre_del;
+    }
+  };
+  if (qt0 < n_qt) {
+    load_tile(qt0 * BT);
+    store_tile(0);
+  }
+  __syncthreads();
+
+  for (int qt = qt0; qt < n_qt; ++qt) {
+    const int i0 = qt * BT;
+    const int cur = NBUF == 2 ? ((qt - qt0) & 1) : 0;
+    const bool more = qt + 1 < n_qt;
+    if (NBUF == 2 && more) load_tile(i0 + BT);
+    if (i0 + BT - 1 >= kw && kw < Tn) {  // some query of the tile sees some key of this wave
+      const T* qs = Qs[cur];
+      const T* os = Os[cur];
+      const bool edge = i0 < kw + 15;  // diagonal tile: mask
+      float p[4][4], ds[4][4];
+#pragma unroll
+      for (int it = 0; it < 4; ++it) {
+        f32x4_t sa = f32x4_t{0.f, 0.f, 0.f, 0.f}, dp = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < L::NS; ++s) {
+          Frag<T> qf, of;
+          frag_load(qf, qs + (it * 16 + lr) * L::RP + 32 * s + 8 * lg);
+          frag_load(of, os + (it * 16 + lr) * L::RP + 32 * s + 8 * lg);
+          mfma16(sa, qf, kf[s]);  // S[i][j]: lane holds key kj, queries 4lg + r
+          mfma16(dp, of, vf[s]);  // dP[i][j]
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int il = it * 16 + 4 * lg + r;
+          const int i = i0 + il;
+          const bool vis = !edge || (kj <= i);
+          const float pv = (vis && kj < Tn) ? ex2(sa[r] * sc - lse_s[cur][il]) : 0.f;
+          p[it][r] = pv;
+          ds[it][r] = pv * (dp[r] - del_s[cur][il]);
+        }
+      }
+      const T* ot = Ot[cur];
+      const T* qtt = Qt[cur];
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        Frag<T> pf, dsf;
+        frag_from_pair(pf, p, s2);
+        frag_from_pair(dsf, ds, s2);
+#pragma unroll
+        for (int c = 0; c < L::NCT; ++c) {
+          Frag<T> of2, qf2;
+          frag_pair_rows<T, DH>(of2, ot, c * 16 + lr, s2, lg);
+          frag_pair_rows<T, DH>(qf2, qtt, c * 16 + lr, s2, lg);
+          mfma16(acc_dv[c], of2, pf);   // dV^T[c][j]
+          mfma16(acc_dk[c], qf2, dsf);  // dK^T[c][j]
+        }
+      }
+    }
+    if (more) {
+      if (NBUF == 1) {
+        __syncthreads();
+        load_tile(i0 + BT);
+      }
+      store_tile(NBUF == 2 ? (cur ^ 1) : 0);
     }
     __syncthreads();
-
-    float p[4][4], ds[4][4];
-#pragma unroll
-    for (int it = 0; it < 4; ++it) {
-      f32x4_t sa = f32x4_t{0.f, 0.f, 0.f, 0.f}, dp = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int s = 0; s < L::NS; ++s) {
-        Frag<T> qf, of;
-        frag_load(qf, Qs + (it * 16 + lr) * L::RP + 32 * s + 8 * lg);
-        frag_load(of, Os + (it * 16 + lr) * L::RP + 32 * s + 8 * lg);
-        mfma16(sa, qf, kf[s]);  // S[i][j]: lane holds key kj, queries 4lg + r
-        mfma16(dp, of, vf[s]);  // dP[i][j]
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int il = it * 16 + 4 * lg + r;
-        const int i = i0 + il;
-        const float pv = (kj <= i && kj < Tn) ? exp2f(sa[r] * sc - lse_s[il]) : 0.f;
-        p[it][r] = pv;
-        ds[it][r] = pv * (dp[r] - del_s[il]);
-      }
-    }
-#pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) {
-      Frag<T> pf, dsf;
-      frag_from_pair(pf, p, s2);
-      frag_from_pair(dsf, ds, s2);
-#pragma unroll
-      for (int c = 0; c < L::NCT; ++c) {
-        Frag<T> of, qf;
-        frag_pair_rows<T, DH>(of, Ot, c * 16 + lr, s2, lg);
-        frag_pair_rows<T, DH>(qf, Qt, c * 16 + lr, s2, lg);
-        mfma16(acc_dv[c], of, pf);   // dV^T[c][j]
-        mfma16(acc_dk[c], qf, dsf);  // dK^T[c][j]
-      }
-    }
   }
 
   if (kj < Tn) {
@@ -343,22 +497,25 @@ __global__ void __launch_bounds__(256) attn_bwd_dkdv_kernel(const T* __restrict_
     for (int c = 0; c < L::NCT; ++c) {
       float vk[4] = {acc_dk[c][0] * scale, acc_dk[c][1] * scale, acc_dk[c][2] * scale, acc_dk[c][3] * scale};
       float vv[4] = {acc_dv[c][0], acc_dv[c][1], acc_dv[c][2], acc_dv[c][3]};
-      store_row4<T>(row + d + c * 16 + 4 * lg, vk, 4);
-      store_row4<T>(row + 2 * d + c * 16 + 4 * lg, vv, 4);
+      store_row4<T>(row + d + c * 16 + 4 * lg, vk);
+      store_row4<T>(row + 2 * d + c * 16 + 4 * lg, vv);
     }
   }
 }
 
 // ----------------------------------------------------------- backward: dQ
-template <typename T, int DH>
+template <typename T, int DH, int G>
 __global__ void __launch_bounds__(256) attn_bwd_dq_kernel(const T* __restrict__ qkv, const T* __restrict__ dout,
                                                           const float* __restrict__ lse,
                                                           const float* __restrict__ delta, T* __restrict__ dqkv,
                                                           int B, int Tn, int H) {
   using L = ALay<T, DH>;
-  __shared__ __attribute__((aligned(16))) T Ks[BT * L::RP];
-  __shared__ __attribute__((aligned(16))) T Kt[DH * L::TP];
-  __shared__ __attribute__((aligned(16))) T Vs[BT * L::RP];
+  constexpr int STAGE = 2 * L::ROWS_BYTES + L::TRANS_BYTES;
+  constexpr int NBUF = two_stages(STAGE) ? 2 : 1;
+  constexpr int BQ = 4 * 16 * G;
+  __shared__ __attribute__((aligned(16))) T Ks[NBUF][BT * L::RP];
+  __shared__ __attribute__((aligned(16))) T Kt[NBUF][DH * L::TP];
+  __shared__ __attribute__((aligned(16))) T Vs[NBUF][BT * L::RP];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
@@ -369,78 +526,142 @@ __global__ void __launch_bounds__(256) attn_bwd_dq_kernel(const T* __restrict__ 
   const T* kb = qb + d;
   const T* vb = qb + 2 * d;
   const T* ob = dout + static_cast<int64_t>(b) * Tn * d + h * DH;
-  const int q0 = blockIdx.x * BT;
-  const int qi = q0 + w * 16 + lr;
+  const int q0 = blockIdx.x * BQ;
+  const int qw = q0 + w * 16 * G;
   const float sc = LOG2E / sqrtf(static_cast<float>(DH));
-  const float lse_i = qi < Tn ? lse[(static_cast<int64_t>(b) * H + h) * Tn + qi] * LOG2E : INFINITY;
-  const float del_i = qi < Tn ? delta[(static_cast<int64_t>(b) * H + h) * Tn + qi] : 0.f;
 
-  Frag<T> qf[L::NS], of[L::NS];
+  Frag<T> qf[G][L::NS], of[G][L::NS];
+  float lse_i[G], del_i[G];
 #pragma unroll
-  for (int s = 0; s < L::NS; ++s) {
-    frag_global(qf[s], qb, ld, qi, Tn, 32 * s + 8 * lg);
-    frag_global(of[s], ob, d, qi, Tn, 32 * s + 8 * lg);
+  for (int g = 0; g < G; ++g) {
+    const int qi = qw + g * 16 + lr;
+    lse_i[g] = qi < Tn ? lse[(static_cast<int64_t>(b) * H + h) * Tn + qi] * LOG2E : INFINITY;
+    del_i[g] = qi < Tn ? delta[(static_cast<int64_t>(b) * H + h) * Tn + qi] : 0.f;
+#pragma unroll
+    for (int s = 0; s < L::NS; ++s) {
+      frag_global(qf[g][s], qb, ld, qi, Tn, 32 * s + 8 * lg);
+      frag_global(of[g][s], ob, d, qi, Tn, 32 * s + 8 * lg);
+    }
   }
-  f32x4_t acc_dq[L::NCT];
+  f32x4_t acc_dq[G][L::NCT];
 #pragma unroll
-  for (int c = 0; c < L::NCT; ++c) acc_dq[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int c = 0; c < L::NCT; ++c) acc_dq[g][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  const int n_kt = min((Tn + BT - 1) / BT, (q0 + BT - 1) / BT + 1);
+  TileLoader<T, DH, 256, false> lk, lv;
+  TileLoader<T, DH, 256, true> lkt;
+  const int n_kt = min((Tn + BT - 1) / BT, (min(q0 + BQ, Tn) - 1) / BT + 1);
+  lk.load(kb, ld, 0, Tn, tid);
+  lkt.load(kb, ld, 0, Tn, tid);
+  lv.load(vb, ld, 0, Tn, tid);
+  lk.store(Ks[0], tid);
+  lkt.store(Kt[0], tid);
+  lv.store(Vs[0], tid);
+  __syncthreads();
+
   for (int kt = 0; kt < n_kt; ++kt) {
     const int j0 = kt * BT;
-    __syncthreads();
-    stage_rows<T, DH>(Ks, kb, ld, j0, Tn, tid);
-    stage_rows_t<T, DH>(Kt, kb, ld, j0, Tn, tid);
-    stage_rows<T, DH>(Vs, vb, ld, j0, Tn, tid);
-    __syncthreads();
-
-    float ds[4][4];
+    const int cur = NBUF == 2 ? (kt & 1) : 0;
+    const bool more = kt + 1 < n_kt;
+    if (NBUF == 2 && more) {
+      lk.load(kb, ld, j0 + BT, Tn, tid);
+      lkt.load(kb, ld, j0 + BT, Tn, tid);
+      lv.load(vb, ld, j0 + BT, Tn, tid);
+    }
+    if (j0 <= qw + 16 * G - 1) {
+      const T* ks = Ks[cur];
+      const T* vs = Vs[cur];
+      const bool edge = j0 + BT > qw || j0 + BT > Tn;
+      float ds[G][4][4];
 #pragma unroll
-    for (int jt = 0; jt < 4; ++jt) {
-      f32x4_t sa = f32x4_t{0.f, 0.f, 0.f, 0.f}, dp = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int jt = 0; jt < 4; ++jt) {
+        f32x4_t sa[G], dp[G];
 #pragma unroll
-      for (int s = 0; s < L::NS; ++s) {
-        Frag<T> kf, vf;
-        frag_load(kf, Ks + (jt * 16 + lr) * L::RP + 32 * s + 8 * lg);
-        frag_load(vf, Vs + (jt * 16 + lr) * L::RP + 32 * s + 8 * lg);
-        mfma16(sa, kf, qf[s]);  // S^T[j][i]: lane holds query qi, keys 4lg + r
-        mfma16(dp, vf, of[s]);  // dP^T[j][i]
+        for (int g = 0; g < G; ++g) {
+          sa[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+          dp[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int s = 0; s < L::NS; ++s) {
+          Frag<T> kf, vf;
+          frag_load(kf, ks + (jt * 16 + lr) * L::RP + 32 * s + 8 * lg);
+          frag_load(vf, vs + (jt * 16 + lr) * L::RP + 32 * s + 8 * lg);
+#pragma unroll
+          for (int g = 0; g < G; ++g) {
+            mfma16(sa[g], kf, qf[g][s]);  // S^T[j][i]: lane holds one query, keys 4lg + r
+            mfma16(dp[g], vf, of[g][s]);  // dP^T[j][i]
+          }
+        }
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const int qi = qw + g * 16 + lr;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int j = j0 + jt * 16 + 4 * lg + r;
+            const bool vis = !edge || (j <= qi && j < Tn);
+            const float pv = vis ? ex2(sa[g][r] * sc - lse_i[g]) : 0.f;
+            ds[g][jt][r] = pv * (dp[g][r] - del_i[g]);
+          }
+        }
       }
+      const T* kt_s = Kt[cur];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int j = j0 + jt * 16 + 4 * lg + r;
-        const float pv = (j <= qi && j < Tn) ? exp2f(sa[r] * sc - lse_i) : 0.f;
-        ds[jt][r] = pv * (dp[r] - del_i);
+      for (int s2 = 0; s2 < 2; ++s2) {
+        Frag<T> dsf[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) frag_from_pair(dsf[g], ds[g], s2);
+#pragma unroll
+        for (int c = 0; c < L::NCT; ++c) {
+          Frag<T> kf2;
+          frag_pair_rows<T, DH>(kf2, kt_s, c * 16 + lr, s2, lg);
+#pragma unroll
+          for (int g = 0; g < G; ++g) mfma16(acc_dq[g][c], kf2, dsf[g]);  // dQ^T[c][i]
+        }
       }
     }
-#pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) {
-      Frag<T> dsf;
-      frag_from_pair(dsf, ds, s2);
-#pragma unroll
-      for (int c = 0; c < L::NCT; ++c) {
-        Frag<T> kf;
-        frag_pair_rows<T, DH>(kf, Kt, c * 16 + lr, s2, lg);
-        mfma16(acc_dq[c], kf, dsf);  // dQ^T[c][i]
+    if (more) {
+      if (NBUF == 1) {
+        __syncthreads();
+        lk.load(kb, ld, j0 + BT, Tn, tid);
+        lkt.load(kb, ld, j0 + BT, Tn, tid);
+        lv.load(vb, ld, j0 + BT, Tn, tid);
       }
+      lk.store(Ks[NBUF == 2 ? (cur ^ 1) : 0], tid);
+      lkt.store(Kt[NBUF == 2 ? (cur ^ 1) : 0], tid);
+      lv.store(Vs[NBUF == 2 ? (cur ^ 1) : 0], tid);
     }
+    __syncthreads();
   }
 
-  if (qi < Tn) {
-    const float scale = 1.f / sqrtf(static_cast<float>(DH));
-    T* row = dqkv + (static_cast<int64_t>(b) * Tn + qi) * ld + h * DH;
+  const float scale = 1.f / sqrtf(static_cast<float>(DH));
 #pragma unroll
-    for (int c = 0; c < L::NCT; ++c) {
-      float v[4] = {acc_dq[c][0] * scale, acc_dq[c][1] * scale, acc_dq[c][2] * scale, acc_dq[c][3] * scale};
-      store_row4<T>(row + c * 16 + 4 * lg, v, 4);
+  for (int g = 0; g < G; ++g) {
+    const int qi = qw + g * 16 + lr;
+    if (qi < Tn) {
+      T* row = dqkv + (static_cast<int64_t>(b) * Tn + qi) * ld + h * DH;
+#pragma unroll
+      for (int c = 0; c < L::NCT; ++c) {
+        float v[4] = {acc_dq[g][c][0] * scale, acc_dq[g][c][1] * scale, acc_dq[g][c][2] * scale,
+                      acc_dq[g][c][3] * scale};
+        store_row4<T>(row + c * 16 + 4 * lg, v);
+      }
     }
   }
 }
 
+// Query groups per wave (forward and dQ) and waves per dK/dV workgroup.
+template <typename T, int DH>
+struct ACfg {
+  static constexpr int G = sizeof(T) == 2 ? 2 : 1;
+  static constexpr int W = sizeof(T) == 2 ? 8 : 4;
+};
+
 template <typename T, int DH>
 hipError_t fwd_t(const void* qkv, void* o, float* lse, int B, int Tn, int H, hipStream_t s) {
-  dim3 grid((Tn + BT - 1) / BT, B * H), block(256);
-  hipLaunchKernelGGL((attn_fwd_kernel<T, DH>), grid, block, 0, s, static_cast<const T*>(qkv), static_cast<T*>(o),
+  constexpr int G = ACfg<T, DH>::G;
+  dim3 grid((Tn + 64 * G - 1) / (64 * G), B * H), block(256);
+  hipLaunchKernelGGL((attn_fwd_kernel<T, DH, G>), grid, block, 0, s, static_cast<const T*>(qkv), static_cast<T*>(o),
                      lse, B, Tn, H);
   return hipGetLastError();
 }
@@ -448,17 +669,19 @@ hipError_t fwd_t(const void* qkv, void* o, float* lse, int B, int Tn, int H, hip
 template <typename T, int DH>
 hipError_t bwd_t(const void* qkv, const void* o, const void* dout, const float* lse, float* delta, void* dqkv, int B,
                  int Tn, int H, hipStream_t s) {
+  constexpr int G = ACfg<T, DH>::G, W = ACfg<T, DH>::W;
   const int64_t n_rows = static_cast<int64_t>(B) * Tn;
   hipLaunchKernelGGL(attn_delta_kernel<T>, dim3(static_cast<unsigned>((n_rows * H + 3) / 4)), dim3(256), 0, s,
                      static_cast<const T*>(o), static_cast<const T*>(dout), delta, n_rows, Tn, H, DH);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  dim3 grid((Tn + BT - 1) / BT, B * H), block(256);
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<T, DH>), grid, block, 0, s, static_cast<const T*>(qkv),
-                     static_cast<const T*>(dout), lse, delta, static_cast<T*>(dqkv), B, Tn, H);
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<T, DH, W>), dim3((Tn + 16 * W - 1) / (16 * W), B * H), dim3(64 * W), 0,
+                     s, static_cast<const T*>(qkv), static_cast<const T*>(dout), lse, delta, static_cast<T*>(dqkv), B,
+                     Tn, H);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_bwd_dq_kernel<T, DH>), grid, block, 0, s, static_cast<const T*>(qkv),
-                     static_cast<const T*>(dout), lse, delta, static_cast<T*>(dqkv), B, Tn, H);
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<T, DH, G>), dim3((Tn + 64 * G - 1) / (64 * G), B * H), dim3(256), 0, s,
+                     static_cast<const T*>(qkv), static_cast<const T*>(dout), lse, delta, static_cast<T*>(dqkv), B,
+                     Tn, H);
   return hipGetLastError();
 }
 

@@ -26,13 +26,9 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 ATOM_DEV float bf2f(bf16_t h) { return __uint_as_float(static_cast<uint32_t>(h) << 16); }
 
-// fp32 -> bf16, round to nearest even; NaN stays NaN.
-ATOM_DEV bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<bf16_t>(u >> 16);
-}
+// fp32 -> bf16, round to nearest even, NaN stays NaN: the gfx950 hardware
+// conversion (pairs of calls fuse into one v_cvt_pk_bf16_f32).
+ATOM_DEV bf16_t f2bf(float f) { return __builtin_bit_cast(bf16_t, static_cast<__bf16>(f)); }
 
 template <typename T> ATOM_DEV float to_f(T v);
 template <> ATOM_DEV float to_f<float>(float v) { return v; }
