@@ -5,10 +5,14 @@ python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 6.7b] [--accum C]
 
 One step = the whole hot path over one batch: swap-in of every group,
 forward, LM head and cross-entropy, backward with recompute, gradient
-swap-out and host fp32 accumulation (atom_step).  Inputs are synthetic and
-seeded (weights N(0, 0.02), uniform tokens) with the shapes of the named
-GPT-3 configuration; the host model is already in pinned memory when timing
-starts, and each timed step starts with no weights on the device.
+swap-out and host fp32 accumulation.  The timed steps are the steps of one
+global batch, run by one pipelined call (atom_steps: the next step's first
+groups are swapped in during the current step's backward; every step still
+loads every weight and copies out every gradient); --sequential times one
+atom_step call per step instead, each starting with no weights on the device.
+Inputs are synthetic and seeded (weights N(0, 0.02), uniform tokens, a
+different batch per step) with the shapes of the named GPT-3 configuration;
+the host model is already in pinned memory when timing starts.
 
 Prints one JSON line.  `value` is training tokens/s.  `roofline` is the
 dominant kernel (the weight-gradient GEMM) against the bf16 MFMA peak, its
@@ -117,6 +121,7 @@ def main():
     ap.add_argument("--accum", type=int, default=None, help="gradient-accumulation degree C")
     ap.add_argument("--budget-gb", type=float, default=None, help="device budget (default: the config's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sequential", action="store_true", help="one atom_step call per step (no cross-step overlap)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -145,15 +150,30 @@ def main():
     t0 = time.time()
     sess.load_weights()
     log(f"host model filled ({time.time() - t0:.1f} s)")
-    tokens = synthetic.gen_tokens(cfg)
+    n_batches = max(args.steps, args.warmup, 1)
+    tokens = np.stack([synthetic.gen_tokens(cfg, seed=synthetic.TOKEN_SEED + i) for i in range(n_batches)])
 
     link_bytes = min(1 << 30, plan.n_slots * plan.slot_bytes // 2)
     h2d_gbs, d2h_gbs, bidir_gbs = A.atom_link_bench(sess.ctx, link_bytes, 4)
     log(f"host link: H2D {h2d_gbs:.1f} GB/s, D2H {d2h_gbs:.1f} GB/s, both {bidir_gbs:.1f} GB/s")
 
-    for i in range(args.warmup):
-        loss = sess.step(tokens)
-        log(f"warmup step {i}: loss {loss:.5f} ({sess.stats().step_s * 1e3:.1f} ms)")
+    def run(n):
+        """n steps (tokens[i] for step i); returns the losses."""
+        if args.sequential:
+            out = []
+            for i in range(n):
+                out.append(sess.step(tokens[i]))
+                log(f"step {i}: loss {out[-1]:.5f} ({sess.stats().step_s * 1e3:.1f} ms)")
+            return out
+        out = []
+        for i0 in range(0, n, A.MAX_STEPS_PER_CALL):
+            out.extend(sess.steps(tokens[i0:min(n, i0 + A.MAX_STEPS_PER_CALL)]).tolist())
+            log(f"steps {i0}..{i0 + len(out) - 1}: {sess.stats().step_s * 1e3:.1f} ms/step")
+        return out
+
+    if args.warmup:
+        losses = run(args.warmup)
+        log(f"warmup: losses {[round(l, 5) for l in losses]}")
 
     # dominant kernel: weight-gradient GEMM (A and B not k-contiguous)
     # (bf16 at C = 1 writes bf16 gradients; otherwise micro-batch 0 stores fp32)
@@ -161,10 +181,7 @@ def main():
     A.atom_probe_gemm(sess.ctx, 0, 0, wgrad_epi)
     torch.cuda.synchronize()
     t_start = time.perf_counter()
-    step_times, losses = [], []
-    for i in range(args.steps):
-        losses.append(sess.step(tokens))
-        step_times.append(sess.stats().step_s)
+    losses = run(args.steps)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     launches, probe_s, probe_flops = A.atom_probe_read(sess.ctx)
@@ -203,6 +220,8 @@ def main():
             "workload": (f"GPT-3 {args.config} swapped training step: {cfg.n_layer} layers, d_model {cfg.d_model}, "
                          f"{cfg.n_head} heads, MLP {cfg.d_mlp}, vocab {cfg.vocab}; batch {cfg.batch} x seq "
                          f"{cfg.seq_len}, accum {cfg.accum}; "
+                         + ("one step per call; " if args.sequential else
+                            f"{args.steps} steps of one global batch in one pipelined call; ")
                          + (f"device budget {budget / 1e9:.0f} GB" if budget < (1 << 49) else "whole model resident")),
             "global_batch": cfg.accum * cfg.batch,
             "seq_len": cfg.seq_len,

@@ -28,7 +28,9 @@
  * host gradient buffers and the fp32 gradient accumulators.
  *
  * Errors.  Every call returns an atom_status; nothing throws across the ABI.
- * atom_last_error(ctx) describes the last failure on a context.  Calls that
+ * atom_last_error(ctx) describes the last failure on a context;
+ * atom_last_error(NULL) the last failed atom_ctx_create of the calling
+ * thread.  Calls that
  * enqueue GPU work report launch errors at once; execution errors surface at
  * the next synchronising call (atom_step, atom_sync, atom_ctx_destroy).
  * Threading: one context per host thread.
@@ -195,7 +197,21 @@ int atom_sync(atom_ctx* ctx, float* loss_out);
  * loss goes to *loss_out.  Synchronous. */
 int atom_step(atom_ctx* ctx, const int32_t* tokens, float* loss_out);
 
-/* Per-step counters of the last atom_step. */
+/* `n_steps` (1..64) training steps of one global batch, pipelined: the host
+ * model is not changed between them (the optimizer runs after the global
+ * batch, Section III-E), so the next step's first groups are swapped in while
+ * the current step's backward runs and its gradients are swapped out (the
+ * overlap of Section IV carried across the step boundary).  Every step still
+ * loads every weight and copies out every gradient, and the fp32 host
+ * accumulators receive the gradients of all steps.  tokens: host int32
+ * [n_steps][accum][batch][seq_len + 1]; losses: host float[n_steps] (may be
+ * NULL), the mean loss of each step.  The result is bitwise that of n_steps
+ * calls of atom_step.  All token ids are validated before anything runs
+ * (ATOM_EINVAL; nothing is changed).  Synchronous. */
+int atom_steps(atom_ctx* ctx, const int32_t* tokens, int32_t n_steps, float* losses);
+
+/* Per-step counters of the last atom_step / atom_steps call (bytes and
+ * swap counts summed over its steps; times per step). */
 typedef struct atom_stats {
   uint64_t h2d_bytes, d2h_bytes;
   double step_s, host_accum_s;

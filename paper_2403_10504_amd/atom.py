@@ -18,6 +18,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libatom.so")
 
 ATOM_MAX_NODES = 256
+MAX_STEPS_PER_CALL = 64  # atom_steps limit
 ATOM_OK, ATOM_EINVAL, ATOM_ENOPLAN, ATOM_EBUDGET, ATOM_EHIP, ATOM_ESTATE, ATOM_ENOMEM_HOST = 0, -1, -2, -3, -4, -5, -6
 ATOM_F32, ATOM_BF16 = 0, 1
 ATOM_CKPT_DEVICE, ATOM_CKPT_HOST = 0, 1
@@ -89,6 +90,7 @@ _SIGS = {
     "atom_swap_out": (ctypes.c_int, [P, I32]),
     "atom_sync": (ctypes.c_int, [P, P]),
     "atom_step": (ctypes.c_int, [P, P, P]),
+    "atom_steps": (ctypes.c_int, [P, P, ctypes.c_int32, P]),
     "atom_get_stats": (ctypes.c_int, [P, P]),
     "atom_probe_gemm": (ctypes.c_int, [P, I32, I32, I32]),
     "atom_probe_read": (ctypes.c_int, [P, P, P, P]),
@@ -109,13 +111,33 @@ _SIGS = {
 EXPORTED = tuple(_SIGS)
 
 
+def _hip_runtimes():
+    """Files of the HIP runtime mapped into this process (Linux)."""
+    try:
+        with open("/proc/self/maps") as f:
+            return sorted({ln.split()[-1] for ln in f if "libamdhip64" in ln})
+    except OSError:
+        return []
+
+
 def lib():
-    """The loaded libatom (raises if it was not built)."""
+    """The loaded libatom (raises if it was not built).
+
+    libatom must run on the same HIP runtime as torch, which owns the device
+    memory and the streams it is handed: torch is imported first, so the
+    runtime it loaded satisfies libatom's dependency (same soname).  Loading
+    libatom first would bring in a second runtime, which fails to find the
+    device or mixes two device contexts; that is checked here."""
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2403_10504_amd.build`")
+        import torch  # noqa: F401  (loads torch's HIP runtime first)
+
         h = ctypes.CDLL(LIB_PATH)
+        runtimes = _hip_runtimes()
+        if len(runtimes) > 1:
+            raise RuntimeError(f"two HIP runtimes in one process ({runtimes}): libatom must bind to torch's")
         for name, (res, args) in _SIGS.items():
             fn = getattr(h, name)
             fn.restype = res
@@ -206,7 +228,9 @@ def atom_plan_fixed(c: atom_config, last_nodes, n_slots: int) -> atom_plan:
 # ------------------------------------------------------------------ context
 def atom_ctx_create(c: atom_config, plan: atom_plan, arena_ptr: int, arena_bytes: int, cs: int, hs: int, ds: int):
     ctx = P()
-    _check(lib().atom_ctx_create(_ref(c), _ref(plan), arena_ptr, arena_bytes, cs, hs, ds, _ref(ctx)))
+    status = lib().atom_ctx_create(_ref(c), _ref(plan), arena_ptr, arena_bytes, cs, hs, ds, _ref(ctx))
+    if status != ATOM_OK:
+        raise AtomError(status, lib().atom_last_error(None).decode())
     return ctx
 
 
@@ -262,6 +286,17 @@ def atom_step(ctx, tokens) -> float:
     v = ctypes.c_float()
     _check(lib().atom_step(ctx, p, _ref(v)), ctx)
     return v.value
+
+
+def atom_steps(ctx, tokens) -> np.ndarray:
+    """tokens: int32 [n_steps][accum][batch][seq_len + 1]; returns the losses."""
+    t, p = _tokens_ptr(tokens)
+    if t.ndim != 4:
+        raise ValueError("tokens must be [n_steps][accum][batch][seq_len + 1]")
+    n = t.shape[0]
+    out = np.zeros(n, dtype=np.float32)
+    _check(lib().atom_steps(ctx, p, n, out.ctypes.data_as(P)), ctx)
+    return out
 
 
 def atom_get_stats(ctx) -> atom_stats:

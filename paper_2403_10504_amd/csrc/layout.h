@@ -22,6 +22,8 @@ constexpr int64_t HEAD_CHUNK = 2048;
 // fp32 workspace that lets weight-gradient GEMMs of narrow layers split their
 // long token dimension over workgroups.
 constexpr uint64_t SPLITK_BYTES = 64ull << 20;
+// Steps one pipelined call may run (one loss slot each).
+constexpr int MAX_STEPS_PER_CALL = 64;
 
 struct TensorDesc {
   std::string name;
@@ -38,7 +40,8 @@ std::string check_config(const atom_config& c);
 // Offsets (bytes from the arena base) of every region of the device arena.
 struct ArenaLayout {
   // reserve regions
-  uint64_t tok_in, tok_tgt, emb_perm, emb_seg, emb_uniq;
+  uint64_t tok_in, tok_tgt, emb_perm, emb_seg, emb_uniq;  // slot 0; slot 1 at + tok_stride
+  uint64_t tok_stride;
   uint64_t ckpt, ckpt_bytes_each;  // (L+1) x accum x [N][d] fp32 block inputs
   uint64_t dres, dres_lp;          // accum x [N][d] fp32 / working dtype
   uint64_t loss_rows, loss_out;

@@ -86,17 +86,21 @@ ArenaLayout arena_layout(const atom_config& c, uint64_t slot_bytes, int n_slots)
     off = align_up(off + bytes);
     return o;
   };
+  // token arrays, twice: consecutive steps of a pipelined call alternate
+  const uint64_t tok0 = off;
   a.tok_in = take(C * N * 4);
   a.tok_tgt = take(C * N * 4);
   a.emb_perm = take(C * N * 4);
   a.emb_seg = take(C * (N + 1) * 4);
   a.emb_uniq = take(C * N * 4);
+  a.tok_stride = off - tok0;
+  take(a.tok_stride);
   a.ckpt_bytes_each = N * d * 4;
   a.ckpt = take((c.ckpt == ATOM_CKPT_DEVICE ? (L + 1) * C : 4) * a.ckpt_bytes_each);
   a.dres = take(C * N * d * 4);
   a.dres_lp = c.dtype == ATOM_BF16 ? take(C * N * d * 2) : a.dres;
   a.loss_rows = take(C * N * 4);
-  a.loss_out = take(256);
+  a.loss_out = take(MAX_STEPS_PER_CALL * 4);
   a.splitk_bytes = SPLITK_BYTES;
   a.splitk = take(a.splitk_bytes);
   // partial-sum scratch: column sums over ceil(N/64) row blocks, or LayerNorm

@@ -2,27 +2,36 @@
 // swap engine (weights in on the H2D stream, gradients out on the D2H stream,
 // events between them and the compute stream), the composition of each
 // node's forward and backward from the kernels, host-side gradient
-// accumulation, and the schedule of a whole step.
+// accumulation, and the schedule of whole steps.
 //
 // Schedule (Section IV: one stream runs the current sub-model, another
 // prefetches the next; completed sub-models are swapped out; the last forward
-// sub-model is not swapped out before the backward).  With K weight slots,
-// group j lives in slot j % K:
+// sub-model is not swapped out before the backward).  With K weight slots:
 //   forward : load groups 0..K-1; after group j's forward is enqueued, load
-//             group j+K (its slot frees when group j's compute ends);
+//             group j+K into the slot group j frees;
 //   backward: the last K groups are still resident; after group j's backward
-//             its gradients are copied out and group j-K is reloaded into
-//             the slot group j just freed.
+//             its gradients are copied out and group j-K is reloaded into the
+//             slot group j just freed.
+// A pipelined call runs several steps of one global batch back to back (the
+// host model does not change inside it, as the optimizer runs only when the
+// global batch is complete, Section III-E): once the backward has freed the
+// slot of one of the last K groups, the next step's swap-in of a first group
+// starts in it, so the next step's weights stream in while this step's
+// backward computes and its gradients stream out.  Consecutive steps use
+// opposite slot orders (group j in slot j mod K, then K-1-(j mod K)), which
+// makes the slots free in exactly the order the next step needs them.  Each
+// step still loads every weight and drains every gradient.
+//
 // Gradients of a group go to one of two gradient slots (by backward order),
-// are copied to pinned host memory, and a host thread adds them to the fp32
-// accumulators.  Every kernel reduces in a fixed order, so a step gives
-// bitwise the same result for any plan (swapping or not).
+// are copied to pinned host memory (two buffers, by step parity), and a host
+// thread adds them to the fp32 accumulators.  Every kernel reduces in a fixed
+// order, so a step gives bitwise the same result for any plan and any
+// pipelining.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <string.h>
 
 #include <algorithm>
-#include <atomic>
 #include <chrono>
 #include <condition_variable>
 #include <deque>
@@ -106,6 +115,9 @@ struct Range {
   uint64_t off, n;  // element offset and count within the host model
 };
 
+// Group g of a step with parity p is the "instance" gi = p * G + g: the two
+// steps a pipelined call keeps in flight have separate residency, events and
+// host gradient buffers.
 struct atom_ctx {
   atom_config cfg{};
   atom_plan plan{};
@@ -114,11 +126,13 @@ struct atom_ctx {
   hipStream_t cs = nullptr, hs = nullptr, ds = nullptr;
   int L = 0, G = 0, K = 0, C = 0, H = 0, dh = 0, dt = 0, e = 0, d = 0, f = 0, V = 0, B = 0, T = 0;
   int64_t N = 0, Vp = 0;
+  int par = 0;       // parity of the step the compute stream is being given work for
+  int last_par = 0;  // parity of the last step whose gradients reached the host
 
   // host model (pinned), per-node ranges
-  uint8_t* h_w = nullptr;   // weights, working dtype
-  uint8_t* h_g = nullptr;   // gradients of the last step, working dtype
-  float* h_acc = nullptr;   // fp32 accumulators (element-indexed like h_w)
+  uint8_t* h_w = nullptr;             // weights, working dtype
+  uint8_t* h_g[2] = {nullptr, nullptr};  // gradients of a step (by parity), working dtype
+  float* h_acc = nullptr;             // fp32 accumulators (element-indexed like h_w)
   uint64_t model_bytes = 0;
   std::vector<uint64_t> node_off, node_bytes;
   std::vector<std::vector<TensorDesc>> tens;
@@ -126,24 +140,27 @@ struct atom_ctx {
   std::vector<uint64_t> group_off, group_bytes;
   std::vector<std::vector<Range>> group_ranges;  // tensors of each group (for accumulation)
 
-  // residency and events
-  std::vector<int> slot_owner;            // group whose weights occupy the slot
-  std::vector<char> resident, need_wait, gclaimed;
+  // residency and events, indexed by group instance
+  std::vector<int> slot_owner;  // instance whose weights occupy the slot (-1: none)
+  std::vector<char> resident, need_wait, gclaimed, lastuse_recorded, stored_recorded;
   std::vector<hipEvent_t> ev_loaded, ev_lastuse, ev_gready, ev_stored;
-  std::vector<char> lastuse_recorded, stored_recorded;
   int gslot_last[2] = {-1, -1};
 
-  // per-step validation state
-  bool tokens_ok = false;
-  std::vector<char> fwd_done, bwd_done;   // [node][micro]
-  std::vector<int> n_uniq;                // per micro
+  // per-step validation state, by parity
+  bool tokens_ok[2] = {false, false};
+  std::vector<char> fwd_done[2], bwd_done[2];  // [node][micro]
+  std::vector<int> n_uniq[2];                  // per micro
+  int32_t* h_tok[2] = {nullptr, nullptr};      // pinned token staging
+  hipEvent_t ev_tok[2] = {nullptr, nullptr};
+  bool tok_recorded[2] = {false, false};
 
   // host accumulation
   HostPool* pool = nullptr;
   std::thread acc_thread;
   std::mutex acc_m;
   std::condition_variable acc_cv, acc_done_cv;
-  std::deque<int> acc_q;
+  std::deque<int> acc_q;  // group instances
+  std::vector<int> acc_pending;
   int acc_busy = 0;
   bool acc_stop = false;
   int acc_error = 0;
@@ -164,6 +181,10 @@ struct atom_ctx {
 
 namespace {
 
+// Failure text of the last atom_ctx_create on this thread (no context exists
+// to hold it).
+thread_local std::string g_create_error;
+
 int fail(atom_ctx* c, int code, const std::string& msg) {
   if (c) c->err = msg;
   return code;
@@ -178,6 +199,13 @@ int fail(atom_ctx* c, int code, const std::string& msg) {
 
 inline uint8_t* A(atom_ctx* c, uint64_t off) { return c->arena + off; }
 inline uint8_t* WS(atom_ctx* c, uint64_t off) { return c->arena + c->lay.ws + off; }
+inline int GI(atom_ctx* c, int par, int g) { return par * c->G + g; }
+
+// Weight slot of group g in a step of parity par (see the file comment).
+inline int slot_of(atom_ctx* c, int par, int g) {
+  const int r = g % c->K;
+  return par == 0 ? r : c->K - 1 - r;
+}
 
 float* ckpt_ptr(atom_ctx* c, int idx, int micro) {
   return reinterpret_cast<float*>(A(c, c->lay.ckpt) +
@@ -188,7 +216,7 @@ float* ckpt_ptr(atom_ctx* c, int idx, int micro) {
 const void* wptr(atom_ctx* c, int node, int t) {
   const int g = c->node_group[node];
   const uint64_t in_group = c->node_off[node] - c->group_off[g];
-  return A(c, c->lay.wslots + static_cast<uint64_t>(g % c->K) * c->plan.slot_bytes + in_group +
+  return A(c, c->lay.wslots + static_cast<uint64_t>(slot_of(c, c->par, g)) * c->plan.slot_bytes + in_group +
                   c->tens[node][t].offset);
 }
 
@@ -196,7 +224,7 @@ const void* wptr(atom_ctx* c, int node, int t) {
 // the group's gradient slot in the working dtype.
 struct GradTarget {
   void* p;
-  int dtype;      // DT_F32 or DT_BF16
+  int dtype;  // DT_F32 or DT_BF16
   bool accumulate;
 };
 
@@ -220,25 +248,27 @@ int wgrad_epi(const GradTarget& t) {
 // the gradient slot the group will write.
 int prepare_group(atom_ctx* c, int node, bool grads) {
   const int g = c->node_group[node];
-  if (!c->resident[g]) return fail(c, ATOM_ESTATE, "group " + std::to_string(g) + " is not swapped in");
-  if (c->need_wait[g]) {
-    HIPCHK(c, hipStreamWaitEvent(c->cs, c->ev_loaded[g], 0));
-    c->need_wait[g] = 0;
+  const int gi = GI(c, c->par, g);
+  if (!c->resident[gi]) return fail(c, ATOM_ESTATE, "group " + std::to_string(g) + " is not swapped in");
+  if (c->need_wait[gi]) {
+    HIPCHK(c, hipStreamWaitEvent(c->cs, c->ev_loaded[gi], 0));
+    c->need_wait[gi] = 0;
   }
-  if (grads && !c->gclaimed[g]) {
+  if (grads && !c->gclaimed[gi]) {
     const int gs = (c->G - 1 - g) & 1;
     const int prev = c->gslot_last[gs];
-    if (prev >= 0 && prev != g && c->stored_recorded[prev]) HIPCHK(c, hipStreamWaitEvent(c->cs, c->ev_stored[prev], 0));
-    c->gslot_last[gs] = g;
-    c->gclaimed[g] = 1;
+    if (prev >= 0 && c->stored_recorded[prev])
+      HIPCHK(c, hipStreamWaitEvent(c->cs, c->ev_stored[prev], 0));
+    c->gslot_last[gs] = gi;
+    c->gclaimed[gi] = 1;
   }
   return ATOM_OK;
 }
 
 int finish_group_use(atom_ctx* c, int node) {
-  const int g = c->node_group[node];
-  HIPCHK(c, hipEventRecord(c->ev_lastuse[g], c->cs));
-  c->lastuse_recorded[g] = 1;
+  const int gi = GI(c, c->par, c->node_group[node]);
+  HIPCHK(c, hipEventRecord(c->ev_lastuse[gi], c->cs));
+  c->lastuse_recorded[gi] = 1;
   return ATOM_OK;
 }
 
@@ -455,7 +485,8 @@ int head_forward_backward(atom_ctx* c, int node, int micro) {
   float* dres = reinterpret_cast<float*>(A(c, L.dres)) + static_cast<int64_t>(micro) * N * d;
   void* dres_lp_out = dt == DT_BF16 ? static_cast<void*>(A(c, L.dres_lp) + static_cast<uint64_t>(micro) * N * d * 2)
                                     : nullptr;
-  const int32_t* tgt = reinterpret_cast<const int32_t*>(A(c, L.tok_tgt)) + static_cast<int64_t>(micro) * N;
+  const int32_t* tgt = reinterpret_cast<const int32_t*>(A(c, L.tok_tgt + c->par * L.tok_stride)) +
+                       static_cast<int64_t>(micro) * N;
   float* loss_rows = reinterpret_cast<float*>(A(c, L.loss_rows)) + static_cast<int64_t>(micro) * N;
   const float scale = 1.0f / static_cast<float>(static_cast<double>(c->C) * static_cast<double>(N));
 
@@ -478,7 +509,8 @@ int head_forward_backward(atom_ctx* c, int node, int micro) {
 }
 
 int embed_forward(atom_ctx* c, int micro) {
-  const int32_t* tok = reinterpret_cast<const int32_t*>(A(c, c->lay.tok_in)) + static_cast<int64_t>(micro) * c->N;
+  const int32_t* tok = reinterpret_cast<const int32_t*>(A(c, c->lay.tok_in + c->par * c->lay.tok_stride)) +
+                       static_cast<int64_t>(micro) * c->N;
   KCHK(c, embed_fwd(c->dt, tok, wptr(c, 0, T_WTE), wptr(c, 0, T_WPE), ckpt_ptr(c, 0, micro), c->N, c->T, c->V, c->d,
                     c->cs));
   return ATOM_OK;
@@ -487,12 +519,13 @@ int embed_forward(atom_ctx* c, int micro) {
 int embed_backward(atom_ctx* c, int micro) {
   const auto& L = c->lay;
   const int64_t N = c->N;
+  const uint64_t ts = c->par * L.tok_stride;
   const float* dres = reinterpret_cast<const float*>(A(c, L.dres)) + static_cast<int64_t>(micro) * N * c->d;
-  const int32_t* perm = reinterpret_cast<const int32_t*>(A(c, L.emb_perm)) + static_cast<int64_t>(micro) * N;
-  const int32_t* seg = reinterpret_cast<const int32_t*>(A(c, L.emb_seg)) + static_cast<int64_t>(micro) * (N + 1);
-  const int32_t* uniq = reinterpret_cast<const int32_t*>(A(c, L.emb_uniq)) + static_cast<int64_t>(micro) * N;
+  const int32_t* perm = reinterpret_cast<const int32_t*>(A(c, L.emb_perm + ts)) + static_cast<int64_t>(micro) * N;
+  const int32_t* seg = reinterpret_cast<const int32_t*>(A(c, L.emb_seg + ts)) + static_cast<int64_t>(micro) * (N + 1);
+  const int32_t* uniq = reinterpret_cast<const int32_t*>(A(c, L.emb_uniq + ts)) + static_cast<int64_t>(micro) * N;
   GradTarget te = gptr(c, 0, T_WTE, micro), tp = gptr(c, 0, T_WPE, micro);
-  KCHK(c, embed_bwd(te.dtype, dres, perm, seg, uniq, c->n_uniq[micro], te.p, tp.p, c->V, c->T, c->B, c->d,
+  KCHK(c, embed_bwd(te.dtype, dres, perm, seg, uniq, c->n_uniq[c->par][micro], te.p, tp.p, c->V, c->T, c->B, c->d,
                     te.accumulate, c->cs));
   return ATOM_OK;
 }
@@ -514,7 +547,9 @@ void accum_range<uint16_t>(float* acc, const uint16_t* g, uint64_t n) {
   }
 }
 
-void accumulate_group(atom_ctx* c, int g) {
+void accumulate_group(atom_ctx* c, int gi) {
+  const int par = gi / c->G, g = gi % c->G;
+  const uint8_t* hg = c->h_g[par];
   const auto& rs = c->group_ranges[g];
   uint64_t total = 0;
   for (auto& r : rs) total += r.n;
@@ -528,9 +563,9 @@ void accumulate_group(atom_ctx* c, int g) {
       if (a < b) {
         const uint64_t off = r.off + (a - pos);
         if (c->dt == DT_BF16)
-          accum_range<uint16_t>(c->h_acc + off, reinterpret_cast<const uint16_t*>(c->h_g) + off, b - a);
+          accum_range<uint16_t>(c->h_acc + off, reinterpret_cast<const uint16_t*>(hg) + off, b - a);
         else
-          accum_range<float>(c->h_acc + off, reinterpret_cast<const float*>(c->h_g) + off, b - a);
+          accum_range<float>(c->h_acc + off, reinterpret_cast<const float*>(hg) + off, b - a);
       }
       pos += r.n;
     }
@@ -539,18 +574,18 @@ void accumulate_group(atom_ctx* c, int g) {
 
 void acc_loop(atom_ctx* c) {
   for (;;) {
-    int g;
+    int gi;
     {
       std::unique_lock<std::mutex> l(c->acc_m);
       c->acc_cv.wait(l, [c] { return c->acc_stop || !c->acc_q.empty(); });
       if (c->acc_q.empty()) return;
-      g = c->acc_q.front();
+      gi = c->acc_q.front();
       c->acc_q.pop_front();
     }
-    hipError_t e = hipEventSynchronize(c->ev_stored[g]);
+    hipError_t e = hipEventSynchronize(c->ev_stored[gi]);
     if (e == hipSuccess) {
       auto t0 = std::chrono::steady_clock::now();
-      accumulate_group(c, g);
+      accumulate_group(c, gi);
       c->acc_seconds += std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
     }
     {
@@ -559,6 +594,7 @@ void acc_loop(atom_ctx* c) {
         c->acc_error = ATOM_EHIP;
         c->acc_errmsg = std::string("gradient copy failed: ") + hipGetErrorString(e);
       }
+      --c->acc_pending[gi];
       --c->acc_busy;
     }
     c->acc_done_cv.notify_all();
@@ -576,21 +612,247 @@ int wait_accum(atom_ctx* c) {
   return ATOM_OK;
 }
 
-bool group_bwd_complete(atom_ctx* c, int g) {
+// The host buffer of instance gi is rewritten by its next gradient copy only
+// after the previous one has been added to the accumulators.
+void wait_accum_instance(atom_ctx* c, int gi) {
+  std::unique_lock<std::mutex> l(c->acc_m);
+  c->acc_done_cv.wait(l, [c, gi] { return c->acc_pending[gi] == 0; });
+}
+
+bool group_bwd_complete(atom_ctx* c, int par, int g) {
   for (int n = c->plan.first[g]; n <= c->plan.last[g]; ++n)
     for (int m = 0; m < c->C; ++m) {
       const size_t k = static_cast<size_t>(n) * c->C + m;
-      if (n == c->L + 1 ? !c->fwd_done[k] : !c->bwd_done[k]) return false;
+      if (n == c->L + 1 ? !c->fwd_done[par][k] : !c->bwd_done[par][k]) return false;
     }
   return true;
 }
 
-void reset_step_state(atom_ctx* c) {
-  std::fill(c->fwd_done.begin(), c->fwd_done.end(), 0);
-  std::fill(c->bwd_done.begin(), c->bwd_done.end(), 0);
-  std::fill(c->gclaimed.begin(), c->gclaimed.end(), 0);
+// Clears the per-step state of parity par (called when a step's tokens are set).
+void reset_step_state(atom_ctx* c, int par) {
+  std::fill(c->fwd_done[par].begin(), c->fwd_done[par].end(), 0);
+  std::fill(c->bwd_done[par].begin(), c->bwd_done[par].end(), 0);
+  for (int g = 0; g < c->G; ++g) c->gclaimed[GI(c, par, g)] = 0;
+}
+
+// Every group of both parities is considered not resident: the next step
+// loads all weights again (the host model may have changed).
+void drop_residency(atom_ctx* c) {
   std::fill(c->resident.begin(), c->resident.end(), 0);
   std::fill(c->need_wait.begin(), c->need_wait.end(), 0);
+}
+
+// Token preprocessing on the host and an asynchronous upload on the compute
+// stream into token slot par.  Ids are validated before anything is copied.
+int upload_tokens(atom_ctx* c, int par, const int32_t* tokens) {
+  const int64_t N = c->N, T = c->T, C = c->C;
+  for (int64_t i = 0; i < C * c->B * (T + 1); ++i)
+    if (tokens[i] < 0 || tokens[i] >= c->V) return fail(c, ATOM_EINVAL, "token id out of range");
+  if (c->tok_recorded[par]) HIPCHK(c, hipEventSynchronize(c->ev_tok[par]));  // staging slot free
+  // staging layout: [inp C*N][tgt C*N][perm C*N][seg C*(N+1)][uniq C*N]
+  int32_t* inp = c->h_tok[par];
+  int32_t* tgt = inp + C * N;
+  int32_t* perm = tgt + C * N;
+  int32_t* seg = perm + C * N;
+  int32_t* uniq = seg + C * (N + 1);
+  std::vector<int32_t> count(c->V), start(c->V);
+  for (int64_t m = 0; m < C; ++m) {
+    for (int64_t b = 0; b < c->B; ++b)
+      for (int64_t t = 0; t < T; ++t) {
+        inp[m * N + b * T + t] = tokens[(m * c->B + b) * (T + 1) + t];
+        tgt[m * N + b * T + t] = tokens[(m * c->B + b) * (T + 1) + t + 1];
+      }
+    // stable counting sort of token positions by token id
+    std::fill(count.begin(), count.end(), 0);
+    for (int64_t n = 0; n < N; ++n) ++count[inp[m * N + n]];
+    int nu = 0, pos = 0;
+    for (int v = 0; v < c->V; ++v) {
+      start[v] = pos;
+      if (count[v]) {
+        uniq[m * N + nu] = v;
+        seg[m * (N + 1) + nu] = pos;
+        ++nu;
+      }
+      pos += count[v];
+    }
+    seg[m * (N + 1) + nu] = pos;
+    for (int64_t n = 0; n < N; ++n) perm[m * N + start[inp[m * N + n]]++] = static_cast<int32_t>(n);
+    c->n_uniq[par][m] = nu;
+  }
+  const auto& L = c->lay;
+  const uint64_t ts = par * L.tok_stride;
+  HIPCHK(c, hipMemcpyAsync(A(c, L.tok_in + ts), inp, C * N * 4, hipMemcpyHostToDevice, c->cs));
+  HIPCHK(c, hipMemcpyAsync(A(c, L.tok_tgt + ts), tgt, C * N * 4, hipMemcpyHostToDevice, c->cs));
+  HIPCHK(c, hipMemcpyAsync(A(c, L.emb_perm + ts), perm, C * N * 4, hipMemcpyHostToDevice, c->cs));
+  HIPCHK(c, hipMemcpyAsync(A(c, L.emb_seg + ts), seg, C * (N + 1) * 4, hipMemcpyHostToDevice, c->cs));
+  HIPCHK(c, hipMemcpyAsync(A(c, L.emb_uniq + ts), uniq, C * N * 4, hipMemcpyHostToDevice, c->cs));
+  HIPCHK(c, hipEventRecord(c->ev_tok[par], c->cs));
+  c->tok_recorded[par] = true;
+  c->tokens_ok[par] = true;
+  reset_step_state(c, par);
+  return ATOM_OK;
+}
+
+int swap_in_impl(atom_ctx* c, int par, int g) {
+  const int gi = GI(c, par, g);
+  if (c->resident[gi]) return fail(c, ATOM_ESTATE, "group " + std::to_string(g) + " is already resident");
+  const int s = slot_of(c, par, g);
+  const int prev = c->slot_owner[s];
+  if (prev >= 0 && prev != gi) {
+    if (c->resident[prev]) {
+      // the previous occupant must have been used since it was loaded
+      if (!c->lastuse_recorded[prev] && c->need_wait[prev])
+        return fail(c, ATOM_ESTATE, "slot holds group " + std::to_string(prev % c->G) + " that was never used");
+      c->resident[prev] = 0;
+    }
+    if (c->lastuse_recorded[prev]) HIPCHK(c, hipStreamWaitEvent(c->hs, c->ev_lastuse[prev], 0));
+  } else if (prev == gi && c->lastuse_recorded[gi]) {
+    HIPCHK(c, hipStreamWaitEvent(c->hs, c->ev_lastuse[gi], 0));
+  }
+  uint8_t* dst = A(c, c->lay.wslots + static_cast<uint64_t>(s) * c->plan.slot_bytes);
+  HIPCHK(c, hipMemcpyAsync(dst, c->h_w + c->group_off[g], c->group_bytes[g], hipMemcpyHostToDevice, c->hs));
+  HIPCHK(c, hipEventRecord(c->ev_loaded[gi], c->hs));
+  c->slot_owner[s] = gi;
+  c->resident[gi] = 1;
+  c->need_wait[gi] = 1;
+  c->lastuse_recorded[gi] = 0;
+  c->stats.h2d_bytes += c->group_bytes[g];
+  c->stats.swap_ins += 1;
+  return ATOM_OK;
+}
+
+int fwd_impl(atom_ctx* c, int node, int micro) {
+  const int par = c->par;
+  if (!c->tokens_ok[par]) return fail(c, ATOM_ESTATE, "tokens not set");
+  if (node > 0 && !c->fwd_done[par][static_cast<size_t>(node - 1) * c->C + micro])
+    return fail(c, ATOM_ESTATE, "input of node " + std::to_string(node) + " not computed");
+  int st = prepare_group(c, node, node == c->L + 1);
+  if (st != ATOM_OK) return st;
+  if (node == 0) st = embed_forward(c, micro);
+  else if (node <= c->L) st = block_forward(c, node, micro, false);
+  else st = head_forward_backward(c, node, micro);
+  if (st != ATOM_OK) return st;
+  c->fwd_done[par][static_cast<size_t>(node) * c->C + micro] = 1;
+  return finish_group_use(c, node);
+}
+
+int bwd_impl(atom_ctx* c, int node, int micro) {
+  const int par = c->par;
+  const size_t k = static_cast<size_t>(node) * c->C + micro;
+  const size_t up = static_cast<size_t>(node + 1) * c->C + micro;
+  const bool up_done = node + 1 == c->L + 1 ? c->fwd_done[par][up] : c->bwd_done[par][up];
+  if (!up_done) return fail(c, ATOM_ESTATE, "gradient of node " + std::to_string(node) + " output not computed");
+  if (c->bwd_done[par][k]) return fail(c, ATOM_ESTATE, "backward already done");
+  int st = prepare_group(c, node, true);
+  if (st != ATOM_OK) return st;
+  st = node == 0 ? embed_backward(c, micro) : block_backward(c, node, micro);
+  if (st != ATOM_OK) return st;
+  c->bwd_done[par][k] = 1;
+  return finish_group_use(c, node);
+}
+
+int swap_out_impl(atom_ctx* c, int par, int g) {
+  const int gi = GI(c, par, g);
+  if (!group_bwd_complete(c, par, g))
+    return fail(c, ATOM_ESTATE, "group " + std::to_string(g) + " backward incomplete");
+  const int gs = (c->G - 1 - g) & 1;
+  uint8_t* gsl = A(c, c->lay.gslots + static_cast<uint64_t>(gs) * c->plan.slot_bytes);
+  if (use_accslot(c)) {
+    // fp32 accumulation slot -> working dtype in the gradient slot, per tensor
+    for (int n = c->plan.first[g]; n <= c->plan.last[g]; ++n)
+      for (auto& t : c->tens[n]) {
+        const uint64_t in_group = c->node_off[n] - c->group_off[g] + t.offset;
+        KCHK(c, convert_f32(c->dt, reinterpret_cast<const float*>(A(c, c->lay.accslot + 2 * in_group)),
+                            gsl + in_group, static_cast<int64_t>(t.bytes / c->e), c->cs));
+      }
+  }
+  wait_accum_instance(c, gi);  // host buffer of this parity is free again
+  HIPCHK(c, hipEventRecord(c->ev_gready[gi], c->cs));
+  HIPCHK(c, hipStreamWaitEvent(c->ds, c->ev_gready[gi], 0));
+  HIPCHK(c, hipMemcpyAsync(c->h_g[par] + c->group_off[g], gsl, c->group_bytes[g], hipMemcpyDeviceToHost, c->ds));
+  HIPCHK(c, hipEventRecord(c->ev_stored[gi], c->ds));
+  c->stored_recorded[gi] = 1;
+  c->last_par = par;
+  c->stats.d2h_bytes += c->group_bytes[g];
+  c->stats.swap_outs += 1;
+  {
+    std::lock_guard<std::mutex> l(c->acc_m);
+    c->acc_q.push_back(gi);
+    ++c->acc_pending[gi];
+    ++c->acc_busy;
+  }
+  c->acc_cv.notify_one();
+  return ATOM_OK;
+}
+
+// Sum of the step's per-token losses into loss slot `slot` (compute stream).
+int reduce_loss(atom_ctx* c, int slot) {
+  float* lr = reinterpret_cast<float*>(A(c, c->lay.loss_rows));
+  float* lo = reinterpret_cast<float*>(A(c, c->lay.loss_out)) + slot;
+  KCHK(c, sum_fixed(lr, static_cast<int64_t>(c->C) * c->N, lo, c->cs));
+  return ATOM_OK;
+}
+
+int sync_all(atom_ctx* c) {
+  HIPCHK(c, hipStreamSynchronize(c->cs));
+  HIPCHK(c, hipStreamSynchronize(c->hs));
+  HIPCHK(c, hipStreamSynchronize(c->ds));
+  int st = probe_collect(c);
+  if (st != ATOM_OK) return st;
+  return wait_accum(c);
+}
+
+// n steps with pipelined swapping (see the file comment); losses[s] is the
+// mean loss of step s.
+int run_steps(atom_ctx* c, const int32_t* tokens, int n, float* losses) {
+  const int G = c->G, K = c->K, C = c->C;
+  const atom_plan& p = c->plan;
+  const int64_t tok_per_step = static_cast<int64_t>(C) * c->B * (c->T + 1);
+  int st = sync_all(c);
+  if (st != ATOM_OK) return st;
+  drop_residency(c);
+  std::fill(c->slot_owner.begin(), c->slot_owner.end(), -1);
+  c->gslot_last[0] = c->gslot_last[1] = -1;
+#define STEP(expr)                  \
+  do {                              \
+    if ((st = (expr)) != ATOM_OK) { \
+      sync_all(c);                  \
+      return st;                    \
+    }                               \
+  } while (0)
+  STEP(upload_tokens(c, 0, tokens));
+  for (int j = 0; j < std::min(G, K); ++j) STEP(swap_in_impl(c, 0, j));
+  for (int s = 0; s < n; ++s) {
+    const int par = s & 1, nxt = par ^ 1;
+    const bool more = s + 1 < n;
+    c->par = par;
+    // forward (the head also runs its backward and starts the residual gradient)
+    for (int j = 0; j < G; ++j) {
+      for (int node = p.first[j]; node <= p.last[j]; ++node)
+        for (int m = 0; m < C; ++m) STEP(fwd_impl(c, node, m));
+      if (j + K < G) STEP(swap_in_impl(c, par, j + K));
+    }
+    STEP(reduce_loss(c, s));
+    if (more) STEP(upload_tokens(c, nxt, tokens + (s + 1) * tok_per_step));
+    // backward, with reloads; slots the last K groups free take the next step's first groups
+    for (int j = G - 1; j >= 0; --j) {
+      for (int node = std::min(p.last[j], c->L); node >= p.first[j]; --node)
+        for (int m = 0; m < C; ++m) STEP(bwd_impl(c, node, m));
+      STEP(swap_out_impl(c, par, j));
+      if (j - K >= 0) STEP(swap_in_impl(c, par, j - K));
+      else if (more) STEP(swap_in_impl(c, nxt, K - 1 - j));
+    }
+  }
+#undef STEP
+  c->par = 0;
+  st = sync_all(c);
+  if (st != ATOM_OK) return st;
+  if (losses) {
+    HIPCHK(c, hipMemcpy(losses, A(c, c->lay.loss_out), n * sizeof(float), hipMemcpyDeviceToHost));
+    const float inv = 1.0f / static_cast<float>(static_cast<double>(C) * static_cast<double>(c->N));
+    for (int s = 0; s < n; ++s) losses[s] *= inv;
+  }
+  return ATOM_OK;
 }
 
 }  // namespace
@@ -602,6 +864,7 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
                     void* compute_stream, void* h2d_stream, void* d2h_stream, atom_ctx** out) {
   if (!out) return ATOM_EINVAL;
   *out = nullptr;
+  g_create_error = "invalid argument";
   if (!cfg || !plan || !dev_arena || !compute_stream || !h2d_stream || !d2h_stream) return ATOM_EINVAL;
   if (!check_config(*cfg).empty()) return ATOM_EINVAL;
   if (compute_stream == h2d_stream || compute_stream == d2h_stream || h2d_stream == d2h_stream) return ATOM_EINVAL;
@@ -679,15 +942,34 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
   c->hs = static_cast<hipStream_t>(h2d_stream);
   c->ds = static_cast<hipStream_t>(d2h_stream);
 
-  // pinned host model
-  if (hipHostMalloc(reinterpret_cast<void**>(&c->h_w), c->model_bytes, hipHostMallocDefault) != hipSuccess ||
-      hipHostMalloc(reinterpret_cast<void**>(&c->h_g), c->model_bytes, hipHostMallocDefault) != hipSuccess) {
-    atom_ctx_destroy(c);
-    return ATOM_ENOMEM_HOST;
+  // pinned host model, two gradient buffers, token staging
+  const int64_t tok_words = static_cast<int64_t>(c->C) * (5 * c->N + 1);
+  struct PinnedBuf {
+    uint8_t** p;
+    uint64_t bytes;
+    const char* what;
+  };
+  const PinnedBuf bufs[] = {{&c->h_w, c->model_bytes, "host weights"},
+                            {&c->h_g[0], c->model_bytes, "host gradients (even steps)"},
+                            {&c->h_g[1], c->model_bytes, "host gradients (odd steps)"},
+                            {reinterpret_cast<uint8_t**>(&c->h_tok[0]), static_cast<uint64_t>(tok_words) * 4,
+                             "token staging (even steps)"},
+                            {reinterpret_cast<uint8_t**>(&c->h_tok[1]), static_cast<uint64_t>(tok_words) * 4,
+                             "token staging (odd steps)"}};
+  for (const auto& b : bufs) {
+    const hipError_t e = hipHostMalloc(reinterpret_cast<void**>(b.p), b.bytes, hipHostMallocDefault);
+    if (e != hipSuccess) {
+      *b.p = nullptr;
+      g_create_error = std::string("hipHostMalloc of ") + std::to_string(b.bytes) + " bytes for " + b.what +
+                       " failed: " + hipGetErrorString(e);
+      atom_ctx_destroy(c);
+      return ATOM_ENOMEM_HOST;
+    }
   }
   const uint64_t n_elem = c->model_bytes / c->e;
   if (posix_memalign(reinterpret_cast<void**>(&c->h_acc), 4096, n_elem * 4) != 0) {
     c->h_acc = nullptr;
+    g_create_error = "allocation of " + std::to_string(n_elem * 4) + " bytes for the fp32 accumulators failed";
     atom_ctx_destroy(c);
     return ATOM_ENOMEM_HOST;
   }
@@ -701,27 +983,35 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
       const int nt = c->pool->size();
       const uint64_t lo = nb * ti / nt, hi = nb * (ti + 1) / nt;
       memset(c->h_w + lo, 0, hi - lo);
-      memset(c->h_g + lo, 0, hi - lo);
+      memset(c->h_g[0] + lo, 0, hi - lo);
+      memset(c->h_g[1] + lo, 0, hi - lo);
       const uint64_t elo = n_elem * ti / nt, ehi = n_elem * (ti + 1) / nt;
       memset(c->h_acc + elo, 0, (ehi - elo) * 4);
     });
   }
+  const int GI2 = 2 * c->G;
   c->slot_owner.assign(c->K, -1);
-  c->resident.assign(c->G, 0);
-  c->need_wait.assign(c->G, 0);
-  c->gclaimed.assign(c->G, 0);
-  c->lastuse_recorded.assign(c->G, 0);
-  c->stored_recorded.assign(c->G, 0);
-  c->fwd_done.assign(static_cast<size_t>(n) * c->C, 0);
-  c->bwd_done.assign(static_cast<size_t>(n) * c->C, 0);
-  c->n_uniq.assign(c->C, 0);
+  c->resident.assign(GI2, 0);
+  c->need_wait.assign(GI2, 0);
+  c->gclaimed.assign(GI2, 0);
+  c->lastuse_recorded.assign(GI2, 0);
+  c->stored_recorded.assign(GI2, 0);
+  c->acc_pending.assign(GI2, 0);
+  for (int par = 0; par < 2; ++par) {
+    c->fwd_done[par].assign(static_cast<size_t>(n) * c->C, 0);
+    c->bwd_done[par].assign(static_cast<size_t>(n) * c->C, 0);
+    c->n_uniq[par].assign(c->C, 0);
+  }
   auto mk = [&](std::vector<hipEvent_t>& v) {
-    v.assign(c->G, nullptr);
+    v.assign(GI2, nullptr);
     for (auto& e : v)
       if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return false;
     return true;
   };
-  if (!mk(c->ev_loaded) || !mk(c->ev_lastuse) || !mk(c->ev_gready) || !mk(c->ev_stored)) {
+  if (!mk(c->ev_loaded) || !mk(c->ev_lastuse) || !mk(c->ev_gready) || !mk(c->ev_stored) ||
+      hipEventCreateWithFlags(&c->ev_tok[0], hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c->ev_tok[1], hipEventDisableTiming) != hipSuccess) {
+    g_create_error = "event creation failed";
     atom_ctx_destroy(c);
     return ATOM_EHIP;
   }
@@ -739,9 +1029,9 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
 
 void atom_ctx_destroy(atom_ctx* c) {
   if (!c) return;
-  if (c->cs) hipStreamSynchronize(c->cs);
-  if (c->hs) hipStreamSynchronize(c->hs);
-  if (c->ds) hipStreamSynchronize(c->ds);
+  if (c->cs) (void)hipStreamSynchronize(c->cs);
+  if (c->hs) (void)hipStreamSynchronize(c->hs);
+  if (c->ds) (void)hipStreamSynchronize(c->ds);
   if (c->acc_thread.joinable()) {
     {
       std::lock_guard<std::mutex> l(c->acc_m);
@@ -752,10 +1042,15 @@ void atom_ctx_destroy(atom_ctx* c) {
   }
   for (auto* v : {&c->ev_loaded, &c->ev_lastuse, &c->ev_gready, &c->ev_stored, &c->probe_ev})
     for (auto e : *v)
-      if (e) hipEventDestroy(e);
+      if (e) (void)hipEventDestroy(e);
+  for (auto e : c->ev_tok)
+    if (e) (void)hipEventDestroy(e);
   delete c->pool;
-  if (c->h_w) hipHostFree(c->h_w);
-  if (c->h_g) hipHostFree(c->h_g);
+  if (c->h_w) (void)hipHostFree(c->h_w);
+  for (auto p : c->h_g)
+    if (p) (void)hipHostFree(p);
+  for (auto p : c->h_tok)
+    if (p) (void)hipHostFree(p);
   free(c->h_acc);
   delete c;
 }
@@ -765,7 +1060,7 @@ int atom_host_tensor(atom_ctx* c, int32_t node, int32_t which, void** ptr, uint6
   const uint64_t off = c->node_off[node];
   if (which == 0) *ptr = c->h_w + off;
   else if (which == 1) *ptr = c->h_acc + off / c->e;
-  else *ptr = c->h_g + off;
+  else *ptr = c->h_g[c->last_par] + off;
   if (bytes) *bytes = which == 1 ? c->node_bytes[node] / c->e * 4 : c->node_bytes[node];
   return ATOM_OK;
 }
@@ -780,189 +1075,65 @@ int atom_zero_grads(atom_ctx* c) {
 
 int atom_set_tokens(atom_ctx* c, const int32_t* tokens) {
   if (!c || !tokens) return fail(c, ATOM_EINVAL, "null tokens");
-  const int64_t N = c->N, T = c->T, C = c->C;
-  for (int64_t i = 0; i < C * c->B * (T + 1); ++i)
-    if (tokens[i] < 0 || tokens[i] >= c->V) return fail(c, ATOM_EINVAL, "token id out of range");
-  // [inp C*N][tgt C*N][perm C*N][seg C*(N+1)][uniq C*N]
-  std::vector<int32_t> inp(C * N), tgt(C * N), perm(C * N), seg(C * (N + 1)), uniq(C * N);
-  std::vector<int32_t> count(c->V);
-  for (int64_t m = 0; m < C; ++m) {
-    for (int64_t b = 0; b < c->B; ++b)
-      for (int64_t t = 0; t < T; ++t) {
-        inp[m * N + b * T + t] = tokens[(m * c->B + b) * (T + 1) + t];
-        tgt[m * N + b * T + t] = tokens[(m * c->B + b) * (T + 1) + t + 1];
-      }
-    // stable counting sort of token positions by token id
-    std::fill(count.begin(), count.end(), 0);
-    for (int64_t n = 0; n < N; ++n) ++count[inp[m * N + n]];
-    int nu = 0, pos = 0;
-    std::vector<int32_t> start(c->V);
-    for (int v = 0; v < c->V; ++v) {
-      start[v] = pos;
-      if (count[v]) {
-        uniq[m * N + nu] = v;
-        seg[m * (N + 1) + nu] = pos;
-        ++nu;
-      }
-      pos += count[v];
-    }
-    seg[m * (N + 1) + nu] = pos;
-    for (int64_t n = 0; n < N; ++n) perm[m * N + start[inp[m * N + n]]++] = static_cast<int32_t>(n);
-    c->n_uniq[m] = nu;
-  }
-  const auto& L = c->lay;
-  HIPCHK(c, hipMemcpyAsync(A(c, L.tok_in), inp.data(), C * N * 4, hipMemcpyHostToDevice, c->cs));
-  HIPCHK(c, hipMemcpyAsync(A(c, L.tok_tgt), tgt.data(), C * N * 4, hipMemcpyHostToDevice, c->cs));
-  HIPCHK(c, hipMemcpyAsync(A(c, L.emb_perm), perm.data(), C * N * 4, hipMemcpyHostToDevice, c->cs));
-  HIPCHK(c, hipMemcpyAsync(A(c, L.emb_seg), seg.data(), C * (N + 1) * 4, hipMemcpyHostToDevice, c->cs));
-  HIPCHK(c, hipMemcpyAsync(A(c, L.emb_uniq), uniq.data(), C * N * 4, hipMemcpyHostToDevice, c->cs));
+  c->par = 0;
+  int st = upload_tokens(c, 0, tokens);
+  if (st != ATOM_OK) return st;
   HIPCHK(c, hipStreamSynchronize(c->cs));
-  c->tokens_ok = true;
-  reset_step_state(c);
+  drop_residency(c);
   return ATOM_OK;
 }
 
 int atom_swap_in(atom_ctx* c, int32_t g) {
   if (!c || g < 0 || g >= c->G) return fail(c, ATOM_EINVAL, "bad group");
-  if (c->resident[g]) return fail(c, ATOM_ESTATE, "group " + std::to_string(g) + " is already resident");
-  const int s = g % c->K;
-  const int prev = c->slot_owner[s];
-  if (prev >= 0 && prev != g) {
-    if (c->resident[prev]) {
-      // the previous occupant must have been used since it was loaded
-      if (!c->lastuse_recorded[prev] && c->need_wait[prev])
-        return fail(c, ATOM_ESTATE, "slot holds group " + std::to_string(prev) + " that was never used");
-      c->resident[prev] = 0;
-    }
-    if (c->lastuse_recorded[prev]) HIPCHK(c, hipStreamWaitEvent(c->hs, c->ev_lastuse[prev], 0));
-  } else if (prev == g && c->lastuse_recorded[g]) {
-    HIPCHK(c, hipStreamWaitEvent(c->hs, c->ev_lastuse[g], 0));
-  }
-  uint8_t* dst = A(c, c->lay.wslots + static_cast<uint64_t>(s) * c->plan.slot_bytes);
-  HIPCHK(c, hipMemcpyAsync(dst, c->h_w + c->group_off[g], c->group_bytes[g], hipMemcpyHostToDevice, c->hs));
-  HIPCHK(c, hipEventRecord(c->ev_loaded[g], c->hs));
-  c->slot_owner[s] = g;
-  c->resident[g] = 1;
-  c->need_wait[g] = 1;
-  c->lastuse_recorded[g] = 0;
-  c->stats.h2d_bytes += c->group_bytes[g];
-  c->stats.swap_ins += 1;
-  return ATOM_OK;
+  return swap_in_impl(c, c->par, g);
 }
 
 int atom_block_fwd(atom_ctx* c, int32_t node, int32_t micro) {
   if (!c || node < 0 || node > c->L + 1 || micro < 0 || micro >= c->C) return fail(c, ATOM_EINVAL, "bad node/micro");
-  if (!c->tokens_ok) return fail(c, ATOM_ESTATE, "tokens not set");
-  if (node > 0 && !c->fwd_done[static_cast<size_t>(node - 1) * c->C + micro])
-    return fail(c, ATOM_ESTATE, "input of node " + std::to_string(node) + " not computed");
-  int st = prepare_group(c, node, node == c->L + 1);
-  if (st != ATOM_OK) return st;
-  if (node == 0) st = embed_forward(c, micro);
-  else if (node <= c->L) st = block_forward(c, node, micro, false);
-  else st = head_forward_backward(c, node, micro);
-  if (st != ATOM_OK) return st;
-  c->fwd_done[static_cast<size_t>(node) * c->C + micro] = 1;
-  return finish_group_use(c, node);
+  return fwd_impl(c, node, micro);
 }
 
 int atom_block_bwd(atom_ctx* c, int32_t node, int32_t micro) {
   if (!c || node < 0 || node > c->L || micro < 0 || micro >= c->C) return fail(c, ATOM_EINVAL, "bad node/micro");
-  const size_t k = static_cast<size_t>(node) * c->C + micro;
-  const size_t up = static_cast<size_t>(node + 1) * c->C + micro;
-  const bool up_done = node + 1 == c->L + 1 ? c->fwd_done[up] : c->bwd_done[up];
-  if (!up_done) return fail(c, ATOM_ESTATE, "gradient of node " + std::to_string(node) + " output not computed");
-  if (c->bwd_done[k]) return fail(c, ATOM_ESTATE, "backward already done");
-  int st = prepare_group(c, node, true);
-  if (st != ATOM_OK) return st;
-  st = node == 0 ? embed_backward(c, micro) : block_backward(c, node, micro);
-  if (st != ATOM_OK) return st;
-  c->bwd_done[k] = 1;
-  return finish_group_use(c, node);
+  return bwd_impl(c, node, micro);
 }
 
 int atom_swap_out(atom_ctx* c, int32_t g) {
   if (!c || g < 0 || g >= c->G) return fail(c, ATOM_EINVAL, "bad group");
-  if (!group_bwd_complete(c, g)) return fail(c, ATOM_ESTATE, "group " + std::to_string(g) + " backward incomplete");
-  const int gs = (c->G - 1 - g) & 1;
-  uint8_t* gsl = A(c, c->lay.gslots + static_cast<uint64_t>(gs) * c->plan.slot_bytes);
-  if (use_accslot(c)) {
-    // fp32 accumulation slot -> working dtype in the gradient slot, per tensor
-    for (int n = c->plan.first[g]; n <= c->plan.last[g]; ++n)
-      for (auto& t : c->tens[n]) {
-        const uint64_t in_group = c->node_off[n] - c->group_off[g] + t.offset;
-        KCHK(c, convert_f32(c->dt, reinterpret_cast<const float*>(A(c, c->lay.accslot + 2 * in_group)), gsl + in_group,
-                            static_cast<int64_t>(t.bytes / c->e), c->cs));
-      }
-  }
-  HIPCHK(c, hipEventRecord(c->ev_gready[g], c->cs));
-  HIPCHK(c, hipStreamWaitEvent(c->ds, c->ev_gready[g], 0));
-  HIPCHK(c, hipMemcpyAsync(c->h_g + c->group_off[g], gsl, c->group_bytes[g], hipMemcpyDeviceToHost, c->ds));
-  HIPCHK(c, hipEventRecord(c->ev_stored[g], c->ds));
-  c->stored_recorded[g] = 1;
-  c->stats.d2h_bytes += c->group_bytes[g];
-  c->stats.swap_outs += 1;
-  {
-    std::lock_guard<std::mutex> l(c->acc_m);
-    c->acc_q.push_back(g);
-    ++c->acc_busy;
-  }
-  c->acc_cv.notify_one();
-  return ATOM_OK;
+  return swap_out_impl(c, c->par, g);
 }
 
 int atom_sync(atom_ctx* c, float* loss_out) {
   if (!c) return ATOM_EINVAL;
   if (loss_out) {
-    float* lr = reinterpret_cast<float*>(A(c, c->lay.loss_rows));
-    float* lo = reinterpret_cast<float*>(A(c, c->lay.loss_out));
-    KCHK(c, sum_fixed(lr, static_cast<int64_t>(c->C) * c->N, lo, c->cs));
+    int st = reduce_loss(c, 0);
+    if (st != ATOM_OK) return st;
     float v = 0.f;
-    HIPCHK(c, hipMemcpyAsync(&v, lo, 4, hipMemcpyDeviceToHost, c->cs));
+    HIPCHK(c, hipMemcpyAsync(&v, A(c, c->lay.loss_out), 4, hipMemcpyDeviceToHost, c->cs));
     HIPCHK(c, hipStreamSynchronize(c->cs));
     *loss_out = v / static_cast<float>(static_cast<double>(c->C) * static_cast<double>(c->N));
   }
-  HIPCHK(c, hipStreamSynchronize(c->cs));
-  HIPCHK(c, hipStreamSynchronize(c->hs));
-  HIPCHK(c, hipStreamSynchronize(c->ds));
-  int st = probe_collect(c);
-  if (st != ATOM_OK) return st;
-  return wait_accum(c);
+  return sync_all(c);
 }
 
-int atom_step(atom_ctx* c, const int32_t* tokens, float* loss_out) {
-  if (!c) return ATOM_EINVAL;
+int atom_steps(atom_ctx* c, const int32_t* tokens, int32_t n, float* losses) {
+  if (!c || !tokens || n < 1 || n > MAX_STEPS_PER_CALL) return fail(c, ATOM_EINVAL, "bad step count");
+  const int64_t total = static_cast<int64_t>(n) * c->C * c->B * (c->T + 1);
+  for (int64_t i = 0; i < total; ++i)
+    if (tokens[i] < 0 || tokens[i] >= c->V) return fail(c, ATOM_EINVAL, "token id out of range");
   auto t0 = std::chrono::steady_clock::now();
   c->stats = atom_stats{};
   c->acc_seconds = 0;
-  int st = atom_set_tokens(c, tokens);
-  if (st != ATOM_OK) return st;
-  const int G = c->G, K = c->K, C = c->C;
-  const atom_plan& p = c->plan;
-#define STEP(expr)                 \
-  do {                             \
-    if ((st = (expr)) != ATOM_OK) { \
-      atom_sync(c, nullptr);       \
-      return st;                   \
-    }                              \
-  } while (0)
-  // forward
-  for (int j = 0; j < std::min(G, K); ++j) STEP(atom_swap_in(c, j));
-  for (int j = 0; j < G; ++j) {
-    for (int n = p.first[j]; n <= p.last[j]; ++n)
-      for (int m = 0; m < C; ++m) STEP(atom_block_fwd(c, n, m));
-    if (j + K < G) STEP(atom_swap_in(c, j + K));
-  }
-  // backward
-  for (int j = G - 1; j >= 0; --j) {
-    for (int n = std::min(p.last[j], c->L); n >= p.first[j]; --n)
-      for (int m = 0; m < C; ++m) STEP(atom_block_bwd(c, n, m));
-    STEP(atom_swap_out(c, j));
-    if (j - K >= 0) STEP(atom_swap_in(c, j - K));
-  }
-#undef STEP
-  st = atom_sync(c, loss_out);
-  c->stats.step_s = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
-  c->stats.host_accum_s = c->acc_seconds;
+  const int st = run_steps(c, tokens, n, losses);
+  c->stats.step_s = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count() / n;
+  c->stats.host_accum_s = c->acc_seconds / n;
+  return st;
+}
+
+int atom_step(atom_ctx* c, const int32_t* tokens, float* loss_out) {
+  float loss = 0.f;
+  const int st = atom_steps(c, tokens, 1, &loss);
+  if (st == ATOM_OK && loss_out) *loss_out = loss;
   return st;
 }
 
@@ -993,9 +1164,8 @@ int atom_probe_read(atom_ctx* c, int64_t* launches, double* seconds, double* flo
 
 int atom_link_bench(atom_ctx* c, uint64_t bytes, int32_t iters, double* h2d, double* d2h, double* bidir) {
   if (!c || iters < 1) return ATOM_EINVAL;
-  HIPCHK(c, hipStreamSynchronize(c->cs));
-  HIPCHK(c, hipStreamSynchronize(c->hs));
-  HIPCHK(c, hipStreamSynchronize(c->ds));
+  int st = sync_all(c);
+  if (st != ATOM_OK) return st;
   const uint64_t region = static_cast<uint64_t>(c->K) * c->plan.slot_bytes;
   // two device halves so both directions can run at once on distinct memory
   const uint64_t n = std::min<uint64_t>(std::min<uint64_t>(bytes, region / 2), c->model_bytes);
@@ -1006,7 +1176,7 @@ int atom_link_bench(atom_ctx* c, uint64_t bytes, int32_t iters, double* h2d, dou
     auto t0 = std::chrono::steady_clock::now();
     for (int i = 0; i < iters; ++i) {
       if (up) (void)hipMemcpyAsync(dev0, c->h_w, n, hipMemcpyHostToDevice, c->hs);
-      if (down) (void)hipMemcpyAsync(c->h_g, dev1, n, hipMemcpyDeviceToHost, c->ds);
+      if (down) (void)hipMemcpyAsync(c->h_g[0], dev1, n, hipMemcpyDeviceToHost, c->ds);
     }
     (void)hipStreamSynchronize(c->hs);
     (void)hipStreamSynchronize(c->ds);
@@ -1017,7 +1187,7 @@ int atom_link_bench(atom_ctx* c, uint64_t bytes, int32_t iters, double* h2d, dou
   HIPCHK(c, hipGetLastError());
   // slots no longer hold any group's weights
   std::fill(c->slot_owner.begin(), c->slot_owner.end(), -1);
-  std::fill(c->resident.begin(), c->resident.end(), 0);
+  drop_residency(c);
   const double gb = static_cast<double>(n) * iters / 1e9;
   if (h2d) *h2d = gb / tu;
   if (d2h) *d2h = gb / td;
@@ -1032,7 +1202,7 @@ int atom_get_stats(atom_ctx* c, atom_stats* out) {
 }
 
 const char* atom_last_error(const atom_ctx* c) {
-  if (!c) return "null context";
+  if (!c) return g_create_error.c_str();
   return c->err.c_str();
 }
 

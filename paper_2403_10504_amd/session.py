@@ -96,6 +96,10 @@ class Session:
     def step(self, tokens) -> float:
         return A.atom_step(self.ctx, tokens)
 
+    def steps(self, tokens) -> np.ndarray:
+        """Pipelined steps of one global batch; tokens [n][C][B][T+1]."""
+        return A.atom_steps(self.ctx, tokens)
+
     def zero_grads(self):
         A.atom_zero_grads(self.ctx)
 
