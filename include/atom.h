@@ -22,8 +22,10 @@
  * a group swaps with one copy.
  *
  * Ownership.  The caller owns the device arena (one allocation of exactly
- * atom_plan.arena_bytes, e.g. a torch uint8 tensor) and the three streams;
- * both must outlive the context.  The library never allocates device memory.
+ * atom_plan.arena_bytes, e.g. a torch uint8 tensor) and the compute
+ * stream; both must outlive the context.  The library never allocates
+ * device memory.  Weight and gradient copies run on the GPU's system DMA
+ * engines (one fixed engine per direction), issued by library threads.
  * The library owns the pinned host model (weights in the working dtype), the
  * host gradient buffers and the fp32 gradient accumulators.
  *
@@ -81,9 +83,14 @@ typedef struct atom_node_cost {
 /* A partition of the chain into contiguous groups and its static layout.
  * Group g holds nodes first[g]..last[g] and uses weight slot g % n_slots;
  * the last n_slots groups stay resident from the forward into the backward.
- * arena_bytes = reserve_bytes + n_slots * slot_bytes + gradient slots. */
+ * Gradients of a group go to one of n_gslots gradient slots (2 to 16, used
+ * round-robin in backward order); a copy out to the host must finish before
+ * its slot is reused, so more slots let the copies lag further behind the
+ * backward.  arena_bytes = reserve_bytes + (n_slots + n_gslots) * slot_bytes
+ * (+ 2 * slot_bytes fp32 accumulation slot for bf16 with accum > 1). */
+#define ATOM_MAX_GSLOTS 16
 typedef struct atom_plan {
-  int32_t n_nodes, n_groups, n_slots, overlap_ok, exhaustive, accum;
+  int32_t n_nodes, n_groups, n_slots, overlap_ok, exhaustive, accum, n_gslots;
   int32_t first[ATOM_MAX_NODES], last[ATOM_MAX_NODES];
   uint64_t budget_bytes, reserve_bytes, slot_bytes, arena_bytes;
   uint64_t h2d_bytes, d2h_bytes, forced_h2d_bytes;
@@ -125,31 +132,39 @@ int atom_reserve_bytes(const atom_config* cfg, uint64_t* out);
  * partitions of `n` nodes with the given costs, a device budget and
  * `reserve` bytes of non-slot memory.  Exhaustive for n <= 20 nodes; for
  * longer chains it searches the structured family that identical decoder
- * blocks allow.  Returns ATOM_ENOPLAN when no partition fits. */
+ * blocks allow.  The memory model counts two gradient slots (n_gslots = 2).
+ * Returns ATOM_ENOPLAN when no partition fits. */
 int atom_plan_search(const atom_config* cfg, uint64_t budget_bytes, uint64_t reserve_bytes,
                      const atom_node_cost* costs, int32_t n, atom_plan* out);
 
 /* atom_plan_partition: the static analysis of Section III-D for cfg under
  * a device budget.  costs == NULL uses atom_node_costs; the reserve comes
- * from atom_reserve_bytes.  Errors: ATOM_EINVAL, ATOM_ENOPLAN. */
+ * from atom_reserve_bytes.  Budget the search leaves unused becomes extra
+ * gradient slots (up to ATOM_MAX_GSLOTS), which changes no transfer and no
+ * result, only how far gradient copies may lag the backward.  Errors:
+ * ATOM_EINVAL, ATOM_ENOPLAN. */
 int atom_plan_partition(const atom_config* cfg, uint64_t device_budget_bytes, const atom_node_cost* costs,
                         int32_t n_costs, atom_plan* out);
 
 /* A plan for a given partition: group g ends at node last[g] (strictly
  * increasing, last[n_groups-1] = n_layer + 1), with n_slots weight slots
- * (1 <= n_slots <= n_groups, at least min(n_groups, 2)).  Fills the slot
+ * (1 <= n_slots <= n_groups, at least min(n_groups, 2)) and n_gslots
+ * gradient slots (2..ATOM_MAX_GSLOTS).  Fills the slot
  * size, arena size and transfer bytes from the layout; predicted times use
  * the analytic costs.  ATOM_EINVAL for a malformed partition. */
-int atom_plan_fixed(const atom_config* cfg, int32_t n_groups, const int32_t* last, int32_t n_slots, atom_plan* out);
+int atom_plan_fixed(const atom_config* cfg, int32_t n_groups, const int32_t* last, int32_t n_slots,
+                    int32_t n_gslots, atom_plan* out);
 
 /* Create a context: validates cfg against plan, carves the arena, allocates
  * the pinned host model (zero weights; fill them through atom_host_tensor)
- * and the host gradient buffers.  Streams are hipStream_t handles (e.g.
- * torch.cuda.Stream().cuda_stream); they must be distinct.  Errors:
+ * and the host gradient buffers, and opens the two DMA engines on the
+ * current HIP device.  compute_stream is a hipStream_t handle (e.g.
+ * torch.cuda.Stream().cuda_stream) that receives every kernel; the library
+ * also runs a few threads of its own (copies, host accumulation).  Errors:
  * ATOM_EINVAL, ATOM_EBUDGET (arena_bytes < plan->arena_bytes),
  * ATOM_ENOMEM_HOST, ATOM_EHIP. */
 int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_arena, uint64_t arena_bytes,
-                    void* compute_stream, void* h2d_stream, void* d2h_stream, atom_ctx** out);
+                    void* compute_stream, atom_ctx** out);
 /* Waits for all work, frees host memory and events.  NULL is ignored. */
 void atom_ctx_destroy(atom_ctx* ctx);
 
@@ -232,7 +247,7 @@ int atom_probe_read(atom_ctx* ctx, int64_t* launches, double* seconds, double* f
  * (weight-slot region; call between steps): `bytes` per copy (clamped to the
  * slot region), `iters` repetitions.  Rates in GB/s (1e9 bytes/s): pinned
  * host to device alone, device to pinned host alone, and both directions at
- * once on the H2D and D2H streams (sum of both directions). */
+ * once (sum of both directions), on the DMA engines a step uses. */
 int atom_link_bench(atom_ctx* ctx, uint64_t bytes, int32_t iters, double* h2d_gbs, double* d2h_gbs,
                     double* bidir_gbs);
 

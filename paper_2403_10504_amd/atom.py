@@ -2,7 +2,7 @@
 
 Argument marshalling only: every function here forwards to the C ABI function
 of the same name; no step of the method runs in Python.  PyTorch is used by
-`Session` for the device arena (one uint8 tensor) and the three streams.
+`Session` for the device arena (one uint8 tensor) and the compute stream.
 
 The library must have been built (`python -m paper_2403_10504_amd.build`);
 loading fails loudly otherwise.  There is no fallback path.
@@ -18,6 +18,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libatom.so")
 
 ATOM_MAX_NODES = 256
+ATOM_MAX_GSLOTS = 16
 MAX_STEPS_PER_CALL = 64  # atom_steps limit
 ATOM_OK, ATOM_EINVAL, ATOM_ENOPLAN, ATOM_EBUDGET, ATOM_EHIP, ATOM_ESTATE, ATOM_ENOMEM_HOST = 0, -1, -2, -3, -4, -5, -6
 ATOM_F32, ATOM_BF16 = 0, 1
@@ -40,6 +41,7 @@ class atom_node_cost(ctypes.Structure):
 class atom_plan(ctypes.Structure):
     _fields_ = [("n_nodes", ctypes.c_int32), ("n_groups", ctypes.c_int32), ("n_slots", ctypes.c_int32),
                 ("overlap_ok", ctypes.c_int32), ("exhaustive", ctypes.c_int32), ("accum", ctypes.c_int32),
+                ("n_gslots", ctypes.c_int32),
                 ("first", ctypes.c_int32 * ATOM_MAX_NODES), ("last", ctypes.c_int32 * ATOM_MAX_NODES),
                 ("budget_bytes", ctypes.c_uint64), ("reserve_bytes", ctypes.c_uint64),
                 ("slot_bytes", ctypes.c_uint64), ("arena_bytes", ctypes.c_uint64),
@@ -78,8 +80,8 @@ _SIGS = {
     "atom_reserve_bytes": (ctypes.c_int, [P, P]),
     "atom_plan_search": (ctypes.c_int, [P, U64, U64, P, I32, P]),
     "atom_plan_partition": (ctypes.c_int, [P, U64, P, I32, P]),
-    "atom_plan_fixed": (ctypes.c_int, [P, I32, P, I32, P]),
-    "atom_ctx_create": (ctypes.c_int, [P, P, P, U64, P, P, P, P]),
+    "atom_plan_fixed": (ctypes.c_int, [P, I32, P, I32, I32, P]),
+    "atom_ctx_create": (ctypes.c_int, [P, P, P, U64, P, P]),
     "atom_ctx_destroy": (None, [P]),
     "atom_host_tensor": (ctypes.c_int, [P, I32, I32, P, P]),
     "atom_zero_grads": (ctypes.c_int, [P]),
@@ -111,11 +113,11 @@ _SIGS = {
 EXPORTED = tuple(_SIGS)
 
 
-def _hip_runtimes():
-    """Files of the HIP runtime mapped into this process (Linux)."""
+def _mapped(name):
+    """Files whose path contains `name` mapped into this process (Linux)."""
     try:
         with open("/proc/self/maps") as f:
-            return sorted({ln.split()[-1] for ln in f if "libamdhip64" in ln})
+            return sorted({ln.split()[-1] for ln in f if name in ln})
     except OSError:
         return []
 
@@ -125,9 +127,9 @@ def lib():
 
     libatom must run on the same HIP runtime as torch, which owns the device
     memory and the streams it is handed: torch is imported first, so the
-    runtime it loaded satisfies libatom's dependency (same soname).  Loading
-    libatom first would bring in a second runtime, which fails to find the
-    device or mixes two device contexts; that is checked here."""
+    runtime it loaded (HIP and ROCr) satisfies libatom's dependencies (same
+    sonames).  Loading libatom first would bring in second runtimes, which
+    fail to find the device or mix two device contexts; that is checked here."""
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
@@ -135,9 +137,10 @@ def lib():
         import torch  # noqa: F401  (loads torch's HIP runtime first)
 
         h = ctypes.CDLL(LIB_PATH)
-        runtimes = _hip_runtimes()
-        if len(runtimes) > 1:
-            raise RuntimeError(f"two HIP runtimes in one process ({runtimes}): libatom must bind to torch's")
+        for name in ("libamdhip64", "libhsa-runtime64"):
+            runtimes = _mapped(name)
+            if len(runtimes) > 1:
+                raise RuntimeError(f"two copies of {name} in one process ({runtimes}): libatom must bind to torch's")
         for name, (res, args) in _SIGS.items():
             fn = getattr(h, name)
             fn.restype = res
@@ -218,17 +221,17 @@ def atom_plan_partition(c: atom_config, budget: int, costs=None) -> atom_plan:
     return p
 
 
-def atom_plan_fixed(c: atom_config, last_nodes, n_slots: int) -> atom_plan:
+def atom_plan_fixed(c: atom_config, last_nodes, n_slots: int, n_gslots: int = 2) -> atom_plan:
     p = atom_plan()
     arr = (I32 * len(last_nodes))(*last_nodes)
-    _check(lib().atom_plan_fixed(_ref(c), len(last_nodes), arr, n_slots, _ref(p)))
+    _check(lib().atom_plan_fixed(_ref(c), len(last_nodes), arr, n_slots, n_gslots, _ref(p)))
     return p
 
 
 # ------------------------------------------------------------------ context
-def atom_ctx_create(c: atom_config, plan: atom_plan, arena_ptr: int, arena_bytes: int, cs: int, hs: int, ds: int):
+def atom_ctx_create(c: atom_config, plan: atom_plan, arena_ptr: int, arena_bytes: int, cs: int):
     ctx = P()
-    status = lib().atom_ctx_create(_ref(c), _ref(plan), arena_ptr, arena_bytes, cs, hs, ds, _ref(ctx))
+    status = lib().atom_ctx_create(_ref(c), _ref(plan), arena_ptr, arena_bytes, cs, _ref(ctx))
     if status != ATOM_OK:
         raise AtomError(status, lib().atom_last_error(None).decode())
     return ctx

@@ -21,7 +21,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libatom.so")
 ARCH = "gfx950"
 
-HIP_SOURCES = ["gemm.hip", "attention.hip", "attention_f32.hip", "rowops.hip", "runtime.cpp", "capi_kernels.cpp"]
+HIP_SOURCES = ["gemm.hip", "attention.hip", "attention_f32.hip", "rowops.hip", "runtime.cpp", "transfer.cpp", "capi_kernels.cpp"]
 # per-source optimisation level (see attention_f32.hip)
 OPT = {"attention_f32.hip": "-O1"}
 CXX_SOURCES = ["plan.cpp"]
@@ -67,7 +67,7 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
     with ThreadPoolExecutor(jobs) as ex:
         list(ex.map(lambda c: _run(c, verbose), cmds))
     tmp = LIB + ".tmp"
-    _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-o", tmp, *objs, "-lpthread"], verbose)
+    _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-o", tmp, *objs, "-lhsa-runtime64", "-lpthread"], verbose)
     os.replace(tmp, LIB)
     return LIB
 

@@ -58,6 +58,6 @@ struct ArenaLayout {
   uint64_t arena_bytes;
 };
 
-ArenaLayout arena_layout(const atom_config& c, uint64_t slot_bytes, int n_slots);
+ArenaLayout arena_layout(const atom_config& c, uint64_t slot_bytes, int n_slots, int n_gslots);
 
 }  // namespace atom

@@ -74,7 +74,7 @@ uint64_t node_tensors(const atom_config& c, int node, std::vector<TensorDesc>* o
   return off;
 }
 
-ArenaLayout arena_layout(const atom_config& c, uint64_t slot_bytes, int n_slots) {
+ArenaLayout arena_layout(const atom_config& c, uint64_t slot_bytes, int n_slots, int n_gslots) {
   ArenaLayout a{};
   const uint64_t N = static_cast<uint64_t>(c.batch) * c.seq_len, d = c.d_model, f = c.d_mlp, C = c.accum;
   const uint64_t L = c.n_layer, H = c.n_head, e = elem_bytes(c);
@@ -146,7 +146,7 @@ ArenaLayout arena_layout(const atom_config& c, uint64_t slot_bytes, int n_slots)
   a.ws = take(a.ws_bytes);
   a.reserve_bytes = off;
   a.wslots = take(static_cast<uint64_t>(n_slots) * slot_bytes);
-  a.gslots = take(2 * slot_bytes);
+  a.gslots = take(static_cast<uint64_t>(n_gslots) * slot_bytes);
   a.accslot = (c.dtype == ATOM_BF16 && c.accum > 1) ? take(2 * slot_bytes) : 0;
   a.arena_bytes = off;
   return a;
@@ -330,7 +330,7 @@ int atom_node_costs(const atom_config* cfg, atom_node_cost* out, int32_t n) {
 
 int atom_reserve_bytes(const atom_config* cfg, uint64_t* out) {
   if (!cfg || !out || !check_config(*cfg).empty()) return ATOM_EINVAL;
-  *out = arena_layout(*cfg, 0, 0).reserve_bytes;
+  *out = arena_layout(*cfg, 0, 0, 0).reserve_bytes;
   return ATOM_OK;
 }
 
@@ -395,6 +395,7 @@ int atom_plan_search(const atom_config* cfg, uint64_t budget, uint64_t reserve, 
   out->n_nodes = n;
   out->n_groups = static_cast<int32_t>(best_g.size());
   out->n_slots = best.K;
+  out->n_gslots = 2;
   out->overlap_ok = best.overlap ? 1 : 0;
   out->exhaustive = exhaustive ? 1 : 0;
   out->accum = accum;
@@ -426,8 +427,9 @@ int atom_plan_search(const atom_config* cfg, uint64_t budget, uint64_t reserve, 
 }
 
 int atom_plan_fixed(const atom_config* cfg, int32_t n_groups, const int32_t* last, int32_t n_slots,
-                    atom_plan* out) {
+                    int32_t n_gslots, atom_plan* out) {
   if (!cfg || !last || !out || !check_config(*cfg).empty()) return ATOM_EINVAL;
+  if (n_gslots < 2 || n_gslots > ATOM_MAX_GSLOTS) return ATOM_EINVAL;
   const int n = cfg->n_layer + 2;
   if (n_groups < 1 || n_groups > n || n_slots < std::min<int32_t>(n_groups, 2) || n_slots > n_groups) return ATOM_EINVAL;
   std::vector<std::pair<int, int>> g;
@@ -456,16 +458,17 @@ int atom_plan_fixed(const atom_config* cfg, int32_t n_groups, const int32_t* las
   out->n_nodes = n;
   out->n_groups = n_groups;
   out->n_slots = n_slots;
+  out->n_gslots = n_gslots;
   out->overlap_ok = ev.overlap ? 1 : 0;
   out->accum = cfg->accum;
   for (int i = 0; i < n_groups; ++i) {
     out->first[i] = g[i].first;
     out->last[i] = g[i].second;
   }
-  out->budget_bytes = budget;
   out->reserve_bytes = reserve;
   out->slot_bytes = S;
-  out->arena_bytes = arena_layout(*cfg, S, n_slots).arena_bytes;
+  out->arena_bytes = arena_layout(*cfg, S, n_slots, n_gslots).arena_bytes;
+  out->budget_bytes = out->arena_bytes;
   out->h2d_bytes = ev.h2d;
   out->d2h_bytes = ev.d2h;
   out->forced_h2d_bytes = ev.h2d;
@@ -494,8 +497,13 @@ int atom_plan_partition(const atom_config* cfg, uint64_t budget, const atom_node
   // Slot sizes are multiples of the 256-byte alignment and the reserve
   // already includes its padding, so the carved arena is exactly the size the
   // search assumed.
-  const ArenaLayout a = arena_layout(*cfg, out->slot_bytes, out->n_slots);
+  const ArenaLayout a = arena_layout(*cfg, out->slot_bytes, out->n_slots, 2);
   if (a.arena_bytes != out->arena_bytes || a.arena_bytes > budget) return ATOM_ENOPLAN;
+  // leftover budget -> extra gradient slots
+  const uint64_t extra = (budget - a.arena_bytes) / out->slot_bytes;
+  out->n_gslots = static_cast<int32_t>(std::min<uint64_t>(ATOM_MAX_GSLOTS, 2 + extra));
+  out->arena_bytes = arena_layout(*cfg, out->slot_bytes, out->n_slots, out->n_gslots).arena_bytes;
+  if (out->arena_bytes > budget) return ATOM_ENOPLAN;
   return ATOM_OK;
 }
 

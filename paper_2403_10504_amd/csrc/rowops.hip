@@ -280,6 +280,21 @@ __global__ void __launch_bounds__(256) fill_zero_kernel(uint4* __restrict__ p, i
   if (blockIdx.x == 0 && static_cast<int>(threadIdx.x) < ntail) tail[threadIdx.x] = 0;
 }
 
+// Word copy whose source may be mapped pinned host memory (read over the host
+// link by the kernel itself).
+__global__ void __launch_bounds__(256) copy_words_kernel(const uint32_t* __restrict__ src,
+                                                         uint32_t* __restrict__ dst, int64_t n) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * 256)
+    dst[i] = src[i];
+}
+
+// System-scope acquire on every compute unit and L2: lines cached before a
+// DMA engine rewrote device memory are dropped, so later kernels read the new
+// contents.  256 workgroups reach every XCD's L2 (workgroups are spread over
+// the XCDs round-robin).
+__global__ void __launch_bounds__(64) dma_acquire_kernel() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, ""); }
+
 inline unsigned grid_for(int64_t n) {
   int64_t g = (n + 255) / 256;
   return static_cast<unsigned>(g < 1 ? 1 : (g > 65536 ? 65536 : g));
@@ -442,6 +457,17 @@ hipError_t convert_f32(int dtype, const float* x, void* y, int64_t n, hipStream_
     hipLaunchKernelGGL(convert_kernel<bf16_t>, dim3(grid_for(n)), dim3(256), 0, s, x, static_cast<bf16_t*>(y), n);
   else
     hipLaunchKernelGGL(convert_kernel<float>, dim3(grid_for(n)), dim3(256), 0, s, x, static_cast<float*>(y), n);
+  return hipGetLastError();
+}
+
+hipError_t dma_acquire(hipStream_t s) {
+  hipLaunchKernelGGL(dma_acquire_kernel, dim3(256), dim3(64), 0, s);
+  return hipGetLastError();
+}
+
+hipError_t copy_words(const uint32_t* src, uint32_t* dst, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(copy_words_kernel, dim3(grid_for(n)), dim3(256), 0, s, src, dst, n);
   return hipGetLastError();
 }
 

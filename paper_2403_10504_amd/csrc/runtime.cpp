@@ -22,14 +22,28 @@
 // makes the slots free in exactly the order the next step needs them.  Each
 // step still loads every weight and drains every gradient.
 //
-// Gradients of a group go to one of two gradient slots (by backward order),
-// are copied to pinned host memory (two buffers, by step parity), and a host
-// thread adds them to the fp32 accumulators.  Every kernel reduces in a fixed
+// Gradients of a group go to one of the plan's gradient slots (claimed
+// round-robin in backward order), are copied to pinned host memory (two buffers, by step parity) on the
+// system DMA engine, and a host thread adds them to the fp32 accumulators.
+//
+// Transfers.  Both directions run on the GPU's system DMA (SDMA) engines
+// through ROCr, each on its own fixed engine and its own worker thread, so
+// they never queue behind each other or behind HIP's own copies, and take no
+// compute unit (HIP moves device-to-host data with a copy kernel, which the
+// training kernels starve).  A weight copy waits (on the host) for the last
+// compute that used its slot; a gradient copy waits for the group's backward.
+// The calling thread only enqueues compute: before a group's first kernel it
+// waits on the host for the group's weight copy to have finished (then
+// enqueues a cache acquire so kernels see the DMA-written weights), and
+// before a group reuses a gradient slot, for the copy out of that slot (so
+// gradient copies may lag the backward by as many groups as there are
+// gradient slots).  Every kernel reduces in a fixed
 // order, so a step gives bitwise the same result for any plan and any
 // pipelining.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <string.h>
+#include <unistd.h>
 
 #include <algorithm>
 #include <chrono>
@@ -43,6 +57,7 @@
 
 #include "launch.h"
 #include "layout.h"
+#include "transfer.h"
 
 namespace atom {
 
@@ -123,7 +138,7 @@ struct atom_ctx {
   atom_plan plan{};
   ArenaLayout lay{};
   uint8_t* arena = nullptr;
-  hipStream_t cs = nullptr, hs = nullptr, ds = nullptr;
+  hipStream_t cs = nullptr;
   int L = 0, G = 0, K = 0, C = 0, H = 0, dh = 0, dt = 0, e = 0, d = 0, f = 0, V = 0, B = 0, T = 0;
   int64_t N = 0, Vp = 0;
   int par = 0;       // parity of the step the compute stream is being given work for
@@ -142,9 +157,22 @@ struct atom_ctx {
 
   // residency and events, indexed by group instance
   std::vector<int> slot_owner;  // instance whose weights occupy the slot (-1: none)
-  std::vector<char> resident, need_wait, gclaimed, lastuse_recorded, stored_recorded;
-  std::vector<hipEvent_t> ev_loaded, ev_lastuse, ev_gready, ev_stored;
-  int gslot_last[2] = {-1, -1};
+  std::vector<char> resident, need_wait, gclaimed, lastuse_recorded;
+  std::vector<hipEvent_t> ev_lastuse, ev_gready;
+
+  // transfers (see the file comment); counters are guarded by xm
+  Worker* h2d_worker = nullptr;
+  Worker* d2h_worker = nullptr;
+  DmaEngine dma;     // device-to-host
+  DmaEngine dma_in;  // host-to-device
+  std::mutex xm;
+  std::condition_variable xcv;
+  std::vector<uint64_t> load_req, load_done;  // per instance: weight copies requested / finished
+  std::vector<int> d2h_pending;               // per instance: gradient copies not yet finished
+  int R = 2;                                // gradient slots
+  std::vector<uint64_t> gs_issued, gs_freed;  // per gradient slot: copies out issued / finished
+  std::vector<int> gslot_of;                // per instance: gradient slot of its current claim
+  int next_gslot = 0;                       // round-robin claim order
 
   // per-step validation state, by parity
   bool tokens_ok[2] = {false, false};
@@ -197,6 +225,13 @@ int fail(atom_ctx* c, int code, const std::string& msg) {
       return fail(ctx, ATOM_EHIP, std::string(#expr) + ": " + hipGetErrorString(_e));     \
   } while (0)
 
+#define KCHK(ctx, expr)                                                                       \
+  do {                                                                                        \
+    hipError_t _e = (expr);                                                                   \
+    if (_e != hipSuccess)                                                                     \
+      return fail(ctx, ATOM_EHIP, std::string("kernel launch ") + #expr + ": " + hipGetErrorString(_e)); \
+  } while (0)
+
 inline uint8_t* A(atom_ctx* c, uint64_t off) { return c->arena + off; }
 inline uint8_t* WS(atom_ctx* c, uint64_t off) { return c->arena + c->lay.ws + off; }
 inline int GI(atom_ctx* c, int par, int g) { return par * c->G + g; }
@@ -234,7 +269,7 @@ GradTarget gptr(atom_ctx* c, int node, int t, int micro) {
   const int g = c->node_group[node];
   const uint64_t in_group = c->node_off[node] - c->group_off[g] + c->tens[node][t].offset;
   if (use_accslot(c)) return {A(c, c->lay.accslot + 2 * in_group), DT_F32, micro > 0};
-  const int gs = (c->G - 1 - g) & 1;
+  const int gs = c->gslot_of[GI(c, c->par, g)];
   return {A(c, c->lay.gslots + static_cast<uint64_t>(gs) * c->plan.slot_bytes + in_group),
           c->dt == DT_BF16 ? DT_BF16 : DT_F32, micro > 0};
 }
@@ -251,15 +286,20 @@ int prepare_group(atom_ctx* c, int node, bool grads) {
   const int gi = GI(c, c->par, g);
   if (!c->resident[gi]) return fail(c, ATOM_ESTATE, "group " + std::to_string(g) + " is not swapped in");
   if (c->need_wait[gi]) {
-    HIPCHK(c, hipStreamWaitEvent(c->cs, c->ev_loaded[gi], 0));
+    {
+      std::unique_lock<std::mutex> l(c->xm);
+      c->xcv.wait(l, [c, gi] { return c->load_done[gi] >= c->load_req[gi]; });
+    }
+    KCHK(c, dma_acquire(c->cs));
     c->need_wait[gi] = 0;
   }
   if (grads && !c->gclaimed[gi]) {
-    const int gs = (c->G - 1 - g) & 1;
-    const int prev = c->gslot_last[gs];
-    if (prev >= 0 && c->stored_recorded[prev])
-      HIPCHK(c, hipStreamWaitEvent(c->cs, c->ev_stored[prev], 0));
-    c->gslot_last[gs] = gi;
+    // every copy out of the gradient slot issued so far must have finished
+    const int gs = c->next_gslot;
+    c->next_gslot = (gs + 1) % c->R;
+    std::unique_lock<std::mutex> l(c->xm);
+    c->xcv.wait(l, [c, gs] { return c->gs_freed[gs] >= c->gs_issued[gs]; });
+    c->gslot_of[gi] = gs;
     c->gclaimed[gi] = 1;
   }
   return ATOM_OK;
@@ -271,13 +311,6 @@ int finish_group_use(atom_ctx* c, int node) {
   c->lastuse_recorded[gi] = 1;
   return ATOM_OK;
 }
-
-#define KCHK(ctx, expr)                                                                       \
-  do {                                                                                        \
-    hipError_t _e = (expr);                                                                   \
-    if (_e != hipSuccess)                                                                     \
-      return fail(ctx, ATOM_EHIP, std::string("kernel launch ") + #expr + ": " + hipGetErrorString(_e)); \
-  } while (0)
 
 GemmArgs gargs(const void* A_, int64_t lda, const void* B_, int64_t ldb, void* C_, int64_t ldc, int M, int N,
                int K) {
@@ -582,18 +615,12 @@ void acc_loop(atom_ctx* c) {
       gi = c->acc_q.front();
       c->acc_q.pop_front();
     }
-    hipError_t e = hipEventSynchronize(c->ev_stored[gi]);
-    if (e == hipSuccess) {
-      auto t0 = std::chrono::steady_clock::now();
-      accumulate_group(c, gi);
-      c->acc_seconds += std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
-    }
+    // queued only once its gradient copy has finished
+    auto t0 = std::chrono::steady_clock::now();
+    accumulate_group(c, gi);
+    c->acc_seconds += std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
     {
       std::lock_guard<std::mutex> l(c->acc_m);
-      if (e != hipSuccess && !c->acc_error) {
-        c->acc_error = ATOM_EHIP;
-        c->acc_errmsg = std::string("gradient copy failed: ") + hipGetErrorString(e);
-      }
       --c->acc_pending[gi];
       --c->acc_busy;
     }
@@ -681,11 +708,17 @@ int upload_tokens(atom_ctx* c, int par, const int32_t* tokens) {
   }
   const auto& L = c->lay;
   const uint64_t ts = par * L.tok_stride;
-  HIPCHK(c, hipMemcpyAsync(A(c, L.tok_in + ts), inp, C * N * 4, hipMemcpyHostToDevice, c->cs));
-  HIPCHK(c, hipMemcpyAsync(A(c, L.tok_tgt + ts), tgt, C * N * 4, hipMemcpyHostToDevice, c->cs));
-  HIPCHK(c, hipMemcpyAsync(A(c, L.emb_perm + ts), perm, C * N * 4, hipMemcpyHostToDevice, c->cs));
-  HIPCHK(c, hipMemcpyAsync(A(c, L.emb_seg + ts), seg, C * (N + 1) * 4, hipMemcpyHostToDevice, c->cs));
-  HIPCHK(c, hipMemcpyAsync(A(c, L.emb_uniq + ts), uniq, C * N * 4, hipMemcpyHostToDevice, c->cs));
+  // Uploaded by a kernel on the compute stream, reading the pinned staging
+  // buffer: a DMA copy queued on the compute stream would hold its DMA engine
+  // until the compute stream reached it, delaying transfers queued behind it.
+  auto up = [&](uint64_t off, const int32_t* src, int64_t n) {
+    return copy_words(reinterpret_cast<const uint32_t*>(src), reinterpret_cast<uint32_t*>(A(c, off + ts)), n, c->cs);
+  };
+  KCHK(c, up(L.tok_in, inp, C * N));
+  KCHK(c, up(L.tok_tgt, tgt, C * N));
+  KCHK(c, up(L.emb_perm, perm, C * N));
+  KCHK(c, up(L.emb_seg, seg, C * (N + 1)));
+  KCHK(c, up(L.emb_uniq, uniq, C * N));
   HIPCHK(c, hipEventRecord(c->ev_tok[par], c->cs));
   c->tok_recorded[par] = true;
   c->tokens_ok[par] = true;
@@ -698,6 +731,8 @@ int swap_in_impl(atom_ctx* c, int par, int g) {
   if (c->resident[gi]) return fail(c, ATOM_ESTATE, "group " + std::to_string(g) + " is already resident");
   const int s = slot_of(c, par, g);
   const int prev = c->slot_owner[s];
+  // the copy waits for the last compute that used the slot's previous occupant
+  hipEvent_t wait_ev = nullptr;
   if (prev >= 0 && prev != gi) {
     if (c->resident[prev]) {
       // the previous occupant must have been used since it was loaded
@@ -705,18 +740,38 @@ int swap_in_impl(atom_ctx* c, int par, int g) {
         return fail(c, ATOM_ESTATE, "slot holds group " + std::to_string(prev % c->G) + " that was never used");
       c->resident[prev] = 0;
     }
-    if (c->lastuse_recorded[prev]) HIPCHK(c, hipStreamWaitEvent(c->hs, c->ev_lastuse[prev], 0));
+    if (c->lastuse_recorded[prev]) wait_ev = c->ev_lastuse[prev];
   } else if (prev == gi && c->lastuse_recorded[gi]) {
-    HIPCHK(c, hipStreamWaitEvent(c->hs, c->ev_lastuse[gi], 0));
+    wait_ev = c->ev_lastuse[gi];
   }
   uint8_t* dst = A(c, c->lay.wslots + static_cast<uint64_t>(s) * c->plan.slot_bytes);
-  HIPCHK(c, hipMemcpyAsync(dst, c->h_w + c->group_off[g], c->group_bytes[g], hipMemcpyHostToDevice, c->hs));
-  HIPCHK(c, hipEventRecord(c->ev_loaded[gi], c->hs));
+  const uint8_t* src = c->h_w + c->group_off[g];
+  const uint64_t bytes = c->group_bytes[g];
+  uint64_t gen;
+  {
+    std::lock_guard<std::mutex> l(c->xm);
+    gen = ++c->load_req[gi];
+  }
+  c->h2d_worker->submit([c, gi, wait_ev, dst, src, bytes, gen]() -> std::string {
+    std::string err;
+    hipError_t e = hipSuccess;
+    if (wait_ev)
+      while ((e = hipEventQuery(wait_ev)) == hipErrorNotReady) usleep(POLL_US);
+    if (e != hipSuccess) err = std::string("waiting for the slot: ") + hipGetErrorString(e);
+    if (err.empty()) err = c->dma_in.copy(dst, src, bytes);
+    {
+      // published even on failure, so no waiter hangs; the error surfaces at the next sync
+      std::lock_guard<std::mutex> l(c->xm);
+      c->load_done[gi] = gen;
+    }
+    c->xcv.notify_all();
+    return err;
+  });
   c->slot_owner[s] = gi;
   c->resident[gi] = 1;
   c->need_wait[gi] = 1;
   c->lastuse_recorded[gi] = 0;
-  c->stats.h2d_bytes += c->group_bytes[g];
+  c->stats.h2d_bytes += bytes;
   c->stats.swap_ins += 1;
   return ATOM_OK;
 }
@@ -755,7 +810,7 @@ int swap_out_impl(atom_ctx* c, int par, int g) {
   const int gi = GI(c, par, g);
   if (!group_bwd_complete(c, par, g))
     return fail(c, ATOM_ESTATE, "group " + std::to_string(g) + " backward incomplete");
-  const int gs = (c->G - 1 - g) & 1;
+  const int gs = c->gslot_of[gi];
   uint8_t* gsl = A(c, c->lay.gslots + static_cast<uint64_t>(gs) * c->plan.slot_bytes);
   if (use_accslot(c)) {
     // fp32 accumulation slot -> working dtype in the gradient slot, per tensor
@@ -766,22 +821,41 @@ int swap_out_impl(atom_ctx* c, int par, int g) {
                             gsl + in_group, static_cast<int64_t>(t.bytes / c->e), c->cs));
       }
   }
-  wait_accum_instance(c, gi);  // host buffer of this parity is free again
-  HIPCHK(c, hipEventRecord(c->ev_gready[gi], c->cs));
-  HIPCHK(c, hipStreamWaitEvent(c->ds, c->ev_gready[gi], 0));
-  HIPCHK(c, hipMemcpyAsync(c->h_g[par] + c->group_off[g], gsl, c->group_bytes[g], hipMemcpyDeviceToHost, c->ds));
-  HIPCHK(c, hipEventRecord(c->ev_stored[gi], c->ds));
-  c->stored_recorded[gi] = 1;
-  c->last_par = par;
-  c->stats.d2h_bytes += c->group_bytes[g];
-  c->stats.swap_outs += 1;
   {
-    std::lock_guard<std::mutex> l(c->acc_m);
-    c->acc_q.push_back(gi);
-    ++c->acc_pending[gi];
-    ++c->acc_busy;
+    // the instance's previous copy (two steps back) has finished with its event
+    std::unique_lock<std::mutex> l(c->xm);
+    c->xcv.wait(l, [c, gi] { return c->d2h_pending[gi] == 0; });
+    c->d2h_pending[gi] += 1;
+    c->gs_issued[gs] += 1;
   }
-  c->acc_cv.notify_one();
+  HIPCHK(c, hipEventRecord(c->ev_gready[gi], c->cs));
+  uint8_t* dst = c->h_g[par] + c->group_off[g];
+  const uint64_t bytes = c->group_bytes[g];
+  c->d2h_worker->submit([c, gi, gs, dst, gsl, bytes]() -> std::string {
+    wait_accum_instance(c, gi);  // the host buffer of this parity is free again
+    std::string err;
+    hipError_t e;
+    while ((e = hipEventQuery(c->ev_gready[gi])) == hipErrorNotReady) usleep(POLL_US);
+    if (e != hipSuccess) err = std::string("waiting for gradients: ") + hipGetErrorString(e);
+    if (err.empty()) err = c->dma.copy(dst, gsl, bytes);
+    if (err.empty()) {
+      std::lock_guard<std::mutex> l(c->acc_m);
+      c->acc_q.push_back(gi);
+      ++c->acc_pending[gi];
+      ++c->acc_busy;
+    }
+    c->acc_cv.notify_one();
+    {
+      std::lock_guard<std::mutex> l(c->xm);
+      c->gs_freed[gs] += 1;
+      c->d2h_pending[gi] -= 1;
+    }
+    c->xcv.notify_all();
+    return err;
+  });
+  c->last_par = par;
+  c->stats.d2h_bytes += bytes;
+  c->stats.swap_outs += 1;
   return ATOM_OK;
 }
 
@@ -794,9 +868,12 @@ int reduce_loss(atom_ctx* c, int slot) {
 }
 
 int sync_all(atom_ctx* c) {
+  // the workers only wait for work already enqueued, so they drain
+  const std::string e_in = c->h2d_worker->drain();
+  const std::string e_out = c->d2h_worker->drain();
   HIPCHK(c, hipStreamSynchronize(c->cs));
-  HIPCHK(c, hipStreamSynchronize(c->hs));
-  HIPCHK(c, hipStreamSynchronize(c->ds));
+  if (!e_in.empty()) return fail(c, ATOM_EHIP, e_in);
+  if (!e_out.empty()) return fail(c, ATOM_EHIP, e_out);
   int st = probe_collect(c);
   if (st != ATOM_OK) return st;
   return wait_accum(c);
@@ -812,7 +889,6 @@ int run_steps(atom_ctx* c, const int32_t* tokens, int n, float* losses) {
   if (st != ATOM_OK) return st;
   drop_residency(c);
   std::fill(c->slot_owner.begin(), c->slot_owner.end(), -1);
-  c->gslot_last[0] = c->gslot_last[1] = -1;
 #define STEP(expr)                  \
   do {                              \
     if ((st = (expr)) != ATOM_OK) { \
@@ -861,13 +937,12 @@ int run_steps(atom_ctx* c, const int32_t* tokens, int n, float* losses) {
 extern "C" {
 
 int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_arena, uint64_t arena_bytes,
-                    void* compute_stream, void* h2d_stream, void* d2h_stream, atom_ctx** out) {
+                    void* compute_stream, atom_ctx** out) {
   if (!out) return ATOM_EINVAL;
   *out = nullptr;
   g_create_error = "invalid argument";
-  if (!cfg || !plan || !dev_arena || !compute_stream || !h2d_stream || !d2h_stream) return ATOM_EINVAL;
+  if (!cfg || !plan || !dev_arena || !compute_stream) return ATOM_EINVAL;
   if (!check_config(*cfg).empty()) return ATOM_EINVAL;
-  if (compute_stream == h2d_stream || compute_stream == d2h_stream || h2d_stream == d2h_stream) return ATOM_EINVAL;
   if (cfg->ckpt != ATOM_CKPT_DEVICE) return ATOM_EINVAL;  // host checkpoints: not supported by this build
   const int n = cfg->n_layer + 2;
   if (plan->n_nodes != n || plan->n_groups < 1 || plan->n_groups > n || plan->n_slots < 1 ||
@@ -879,6 +954,7 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
     if (g > 0 && plan->first[g] != plan->last[g - 1] + 1) return ATOM_EINVAL;
   }
   if (plan->n_slots < std::min(plan->n_groups, 2)) return ATOM_EINVAL;
+  if (plan->n_gslots < 2 || plan->n_gslots > ATOM_MAX_GSLOTS) return ATOM_EINVAL;
   if (reinterpret_cast<uintptr_t>(dev_arena) & (ALIGN - 1)) return ATOM_EINVAL;
 
   atom_ctx* c = new atom_ctx();
@@ -932,15 +1008,16 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
     delete c;
     return ATOM_EINVAL;
   }
-  c->lay = arena_layout(*cfg, plan->slot_bytes, plan->n_slots);
+  c->lay = arena_layout(*cfg, plan->slot_bytes, plan->n_slots, plan->n_gslots);
+  c->R = plan->n_gslots;
+  c->gs_issued.assign(c->R, 0);
+  c->gs_freed.assign(c->R, 0);
   if (arena_bytes < c->lay.arena_bytes) {
     delete c;
     return ATOM_EBUDGET;
   }
   c->arena = static_cast<uint8_t*>(dev_arena);
   c->cs = static_cast<hipStream_t>(compute_stream);
-  c->hs = static_cast<hipStream_t>(h2d_stream);
-  c->ds = static_cast<hipStream_t>(d2h_stream);
 
   // pinned host model, two gradient buffers, token staging
   const int64_t tok_words = static_cast<int64_t>(c->C) * (5 * c->N + 1);
@@ -973,8 +1050,10 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
     atom_ctx_destroy(c);
     return ATOM_ENOMEM_HOST;
   }
+  // accumulation threads: the cores minus two for the calling thread and the
+  // transfer workers (at most 16; the sum is bound by host memory bandwidth)
   unsigned hw = std::thread::hardware_concurrency();
-  int nthreads = static_cast<int>(std::min(16u, std::max(1u, hw)));
+  int nthreads = static_cast<int>(std::min(16u, std::max(1u, hw > 3 ? hw - 2 : 1u)));
   c->pool = new HostPool(nthreads);
   {
     // zero host buffers in parallel
@@ -995,20 +1074,24 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
   c->need_wait.assign(GI2, 0);
   c->gclaimed.assign(GI2, 0);
   c->lastuse_recorded.assign(GI2, 0);
-  c->stored_recorded.assign(GI2, 0);
   c->acc_pending.assign(GI2, 0);
+  c->load_req.assign(GI2, 0);
+  c->load_done.assign(GI2, 0);
+  c->d2h_pending.assign(GI2, 0);
+  c->gslot_of.assign(GI2, 0);
   for (int par = 0; par < 2; ++par) {
     c->fwd_done[par].assign(static_cast<size_t>(n) * c->C, 0);
     c->bwd_done[par].assign(static_cast<size_t>(n) * c->C, 0);
     c->n_uniq[par].assign(c->C, 0);
   }
-  auto mk = [&](std::vector<hipEvent_t>& v) {
+  auto mk = [&](std::vector<hipEvent_t>& v, unsigned flags) {
     v.assign(GI2, nullptr);
     for (auto& e : v)
-      if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return false;
+      if (hipEventCreateWithFlags(&e, flags) != hipSuccess) return false;
     return true;
   };
-  if (!mk(c->ev_loaded) || !mk(c->ev_lastuse) || !mk(c->ev_gready) || !mk(c->ev_stored) ||
+  if (!mk(c->ev_lastuse, hipEventDisableTiming) ||
+      !mk(c->ev_gready, hipEventDisableTiming) ||
       hipEventCreateWithFlags(&c->ev_tok[0], hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&c->ev_tok[1], hipEventDisableTiming) != hipSuccess) {
     g_create_error = "event creation failed";
@@ -1022,16 +1105,31 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
       atom_ctx_destroy(c);
       return ATOM_EHIP;
     }
+  {
+    int dev = 0;
+    std::string e = hipGetDevice(&dev) == hipSuccess ? c->dma.init(dev, true) : "hipGetDevice failed";
+    if (e.empty()) e = c->dma_in.init(dev, false);
+    if (!e.empty()) {
+      g_create_error = "DMA engines: " + e;
+      atom_ctx_destroy(c);
+      return ATOM_EHIP;
+    }
+  }
   c->acc_thread = std::thread(acc_loop, c);
+  c->h2d_worker = new Worker();
+  c->d2h_worker = new Worker();
   *out = c;
   return ATOM_OK;
 }
 
 void atom_ctx_destroy(atom_ctx* c) {
   if (!c) return;
+  // workers first (gradient copies hand work to the accumulation thread)
+  if (c->h2d_worker) (void)c->h2d_worker->drain();
+  if (c->d2h_worker) (void)c->d2h_worker->drain();
+  delete c->h2d_worker;
+  delete c->d2h_worker;
   if (c->cs) (void)hipStreamSynchronize(c->cs);
-  if (c->hs) (void)hipStreamSynchronize(c->hs);
-  if (c->ds) (void)hipStreamSynchronize(c->ds);
   if (c->acc_thread.joinable()) {
     {
       std::lock_guard<std::mutex> l(c->acc_m);
@@ -1040,7 +1138,7 @@ void atom_ctx_destroy(atom_ctx* c) {
     c->acc_cv.notify_all();
     c->acc_thread.join();
   }
-  for (auto* v : {&c->ev_loaded, &c->ev_lastuse, &c->ev_gready, &c->ev_stored, &c->probe_ev})
+  for (auto* v : {&c->ev_lastuse, &c->ev_gready, &c->probe_ev})
     for (auto e : *v)
       if (e) (void)hipEventDestroy(e);
   for (auto e : c->ev_tok)
@@ -1168,26 +1266,29 @@ int atom_link_bench(atom_ctx* c, uint64_t bytes, int32_t iters, double* h2d, dou
   if (st != ATOM_OK) return st;
   const uint64_t region = static_cast<uint64_t>(c->K) * c->plan.slot_bytes;
   // two device halves so both directions can run at once on distinct memory
-  const uint64_t n = std::min<uint64_t>(std::min<uint64_t>(bytes, region / 2), c->model_bytes);
+  const uint64_t n = std::min<uint64_t>(std::min<uint64_t>(bytes, region / 2), c->model_bytes) / 256 * 256;
   if (n == 0) return fail(c, ATOM_EINVAL, "no room for the link benchmark");
   uint8_t* dev0 = A(c, c->lay.wslots);
   uint8_t* dev1 = dev0 + n;
+  std::string err;
+  // the engines a step uses, each direction on its own thread
+  std::string err_in;
   auto timed = [&](bool up, bool down) -> double {
     auto t0 = std::chrono::steady_clock::now();
-    for (int i = 0; i < iters; ++i) {
-      if (up) (void)hipMemcpyAsync(dev0, c->h_w, n, hipMemcpyHostToDevice, c->hs);
-      if (down) (void)hipMemcpyAsync(c->h_g[0], dev1, n, hipMemcpyDeviceToHost, c->ds);
-    }
-    (void)hipStreamSynchronize(c->hs);
-    (void)hipStreamSynchronize(c->ds);
+    std::thread t_in([&] {
+      for (int i = 0; i < iters && up && err_in.empty(); ++i) err_in = c->dma_in.copy(dev0, c->h_w, n);
+    });
+    for (int i = 0; i < iters && down && err.empty(); ++i) err = c->dma.copy(c->h_g[0], dev1, n);
+    t_in.join();
     return std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
   };
   timed(true, true);  // warm-up
   const double tu = timed(true, false), td = timed(false, true), tb = timed(true, true);
-  HIPCHK(c, hipGetLastError());
   // slots no longer hold any group's weights
   std::fill(c->slot_owner.begin(), c->slot_owner.end(), -1);
   drop_residency(c);
+  if (err.empty()) err = err_in;
+  if (!err.empty()) return fail(c, ATOM_EHIP, err);
   const double gb = static_cast<double>(n) * iters / 1e9;
   if (h2d) *h2d = gb / tu;
   if (d2h) *d2h = gb / td;

@@ -1,8 +1,8 @@
-"""Session: a context whose device arena and streams come from PyTorch.
+"""Session: a context whose device arena and compute stream come from PyTorch.
 
 Plumbing only.  The arena is one torch uint8 tensor of exactly the plan's
-arena size (so the device budget is enforced by construction), the three
-streams are torch streams at the default priority, and the host model lives
+arena size (so the device budget is enforced by construction), the compute
+stream is a torch stream at the default priority, and the host model lives
 in the library's pinned buffers, exposed here as numpy views.
 """
 from __future__ import annotations
@@ -26,9 +26,8 @@ class Session:
             plan = A.atom_plan_partition(self.c, budget)
         self.plan = plan
         self.arena = torch.empty(plan.arena_bytes, dtype=torch.uint8, device="cuda")
-        self.streams = [torch.cuda.Stream() for _ in range(3)]
-        self.ctx = A.atom_ctx_create(self.c, plan, self.arena.data_ptr(), plan.arena_bytes,
-                                     *[s.cuda_stream for s in self.streams])
+        self.stream = torch.cuda.Stream()
+        self.ctx = A.atom_ctx_create(self.c, plan, self.arena.data_ptr(), plan.arena_bytes, self.stream.cuda_stream)
         self.n_nodes = cfg.n_layer + 2
         self.layout = [A.atom_node_layout(self.c, n)[0] for n in range(self.n_nodes)]
         self.elem = np.uint16 if cfg.dtype == "bf16" else np.float32

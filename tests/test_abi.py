@@ -85,10 +85,20 @@ def test_reserve_and_partition_fit_budget():
         p = A.atom_plan_partition(c, budget)
         assert p.reserve_bytes == r
         assert p.arena_bytes <= budget
-        assert p.arena_bytes == r + p.n_slots * p.slot_bytes + 2 * p.slot_bytes
+        assert p.arena_bytes == r + p.n_slots * p.slot_bytes + p.n_gslots * p.slot_bytes
         assert p.n_slots >= min(p.n_groups, 2)
+        # leftover budget becomes gradient slots, up to the limit
+        assert 2 <= p.n_gslots <= A.ATOM_MAX_GSLOTS
+        assert p.n_gslots == A.ATOM_MAX_GSLOTS or budget - p.arena_bytes < p.slot_bytes
+        # the search itself (Algorithm 1's memory model) counts two gradient slots
+        q = A.atom_plan_search(c, budget, r, A.atom_node_costs(c))
+        assert q.n_gslots == 2 and q.groups() == groups_of(p) and q.n_slots == p.n_slots
         groups = p.groups()
         assert groups[0][0] == 0 and groups[-1][1] == cfg.n_layer + 1
+
+
+def groups_of(p):
+    return p.groups()
 
 
 def test_budget_too_small_is_enoplan():
@@ -186,18 +196,18 @@ def test_ctx_create_rejects_bad_arguments_without_gpu():
     c = A.make_config(TINY)
     p = A.atom_plan_partition(c, 1 << 40)
     with pytest.raises(A.AtomError) as e:
-        A.atom_ctx_create(c, p, 0, p.arena_bytes, 1, 2, 3)
+        A.atom_ctx_create(c, p, 0, p.arena_bytes, 1)
     assert e.value.status == A.ATOM_EINVAL
     with pytest.raises(A.AtomError) as e:
-        A.atom_ctx_create(c, p, 4096, p.arena_bytes, 1, 1, 3)
+        A.atom_ctx_create(c, p, 4096, p.arena_bytes, 0)  # no compute stream
     assert e.value.status == A.ATOM_EINVAL
     p2 = A.atom_plan_partition(c, 1 << 40)
     p2.n_slots = 0
     with pytest.raises(A.AtomError) as e:
-        A.atom_ctx_create(c, p2, 4096, p.arena_bytes, 1, 2, 3)
+        A.atom_ctx_create(c, p2, 4096, p.arena_bytes, 1)
     assert e.value.status == A.ATOM_EINVAL
     with pytest.raises(A.AtomError) as e:
-        A.atom_ctx_create(c, p, 4096, p.arena_bytes - 256, 1, 2, 3)
+        A.atom_ctx_create(c, p, 4096, p.arena_bytes - 256, 1)
     assert e.value.status == A.ATOM_EBUDGET
 
 

@@ -22,8 +22,8 @@ def tokens_for(cfg, n):
     return np.stack([synthetic.gen_tokens(cfg, seed=100 + s) for s in range(n)])
 
 
-def plan_for(cfg, last, k):
-    return A.atom_plan_fixed(A.make_config(cfg), last, k)
+def plan_for(cfg, last, k, gslots=2):
+    return A.atom_plan_fixed(A.make_config(cfg), last, k, gslots)
 
 
 def sequential(cfg, plan, tok):
@@ -59,17 +59,21 @@ CASES = {
     "bf16_pairs_all_slots": (TINY.with_(dtype="bf16", n_layer=4), lambda n: [1, 3, 5], 3),
     # odd number of groups with K = 2 (slot order alternates between steps)
     "f32_three_groups_k2": (TINY.with_(n_layer=3), lambda n: [0, 2, 4], 2),
+    # more gradient slots than groups per step: copies lag across the step boundary
+    "bf16_singletons_k2_g7": (TINY.with_(dtype="bf16", n_layer=3), lambda n: list(range(n)), 2, 7),
+    # three gradient slots with five groups (claims wrap unevenly across steps)
+    "f32_singletons_k3_g3": (TINY.with_(n_layer=3), lambda n: list(range(n)), 3, 3),
 }
 
 
 @pytest.mark.parametrize("case", sorted(CASES))
 def test_pipelined_steps_equal_sequential_steps(case):
-    cfg, last_fn, k = CASES[case]
+    cfg, last_fn, k, *gs = CASES[case]
     n = cfg.n_layer + 2
     last = last_fn(n)
     if last[-1] != n - 1:
         last = last + [n - 1]
-    plan = plan_for(cfg, last, k)
+    plan = plan_for(cfg, last, k, *gs)
     tok = tokens_for(cfg, 3)
     l_seq, acc_seq, last_seq, st_seq = sequential(cfg, plan, tok)
     l_pipe, acc_pipe, last_pipe, st_pipe = pipelined(cfg, plan, tok)
@@ -120,3 +124,20 @@ def test_steps_rejects_bad_count_and_bad_ids():
         s.load_weights()
         ref = s.step(tok[0])
     assert good[0] == ref
+
+
+def test_gradient_slot_count_does_not_change_results():
+    cfg = TINY.with_(dtype="bf16", n_layer=3)
+    last = list(range(cfg.n_nodes))
+    tok = tokens_for(cfg, 2)
+    ref = pipelined(cfg, plan_for(cfg, last, 2, 2), tok)
+    for gslots in (3, 16):
+        plan = plan_for(cfg, last, 2, gslots)
+        assert plan.n_gslots == gslots
+        got = pipelined(cfg, plan, tok)
+        assert np.array_equal(ref[0], got[0])
+        assert_same(ref[1], got[1])
+    with pytest.raises(A.AtomError):
+        plan_for(cfg, last, 2, 1)
+    with pytest.raises(A.AtomError):
+        plan_for(cfg, last, 2, A.ATOM_MAX_GSLOTS + 1)
