@@ -128,8 +128,12 @@ def lib():
     libatom must run on the same HIP runtime as torch, which owns the device
     memory and the streams it is handed: torch is imported first, so the
     runtime it loaded (HIP and ROCr) satisfies libatom's dependencies (same
-    sonames).  Loading libatom first would bring in second runtimes, which
-    fail to find the device or mix two device contexts; that is checked here."""
+    sonames).  Loading libatom first would bring in a second HIP runtime,
+    which fails to find the device or mixes two device contexts; that is
+    checked here.  A second ROCr copy can be present when a profiler preloads
+    its own; libatom's direct ROCr calls (the DMA copies) must then reach the
+    instance HIP uses, which atom_ctx_create checks on the arena and the
+    pinned host model (ATOM_EHIP otherwise)."""
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
@@ -137,7 +141,7 @@ def lib():
         import torch  # noqa: F401  (loads torch's HIP runtime first)
 
         h = ctypes.CDLL(LIB_PATH)
-        for name in ("libamdhip64", "libhsa-runtime64"):
+        for name in ("libamdhip64",):
             runtimes = _mapped(name)
             if len(runtimes) > 1:
                 raise RuntimeError(f"two copies of {name} in one process ({runtimes}): libatom must bind to torch's")

@@ -1109,6 +1109,8 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
     int dev = 0;
     std::string e = hipGetDevice(&dev) == hipSuccess ? c->dma.init(dev, true) : "hipGetDevice failed";
     if (e.empty()) e = c->dma_in.init(dev, false);
+    if (e.empty()) e = c->dma.check_known(c->arena, "the device arena");
+    if (e.empty()) e = c->dma.check_known(c->h_w, "the pinned host model");
     if (!e.empty()) {
       g_create_error = "DMA engines: " + e;
       atom_ctx_destroy(c);

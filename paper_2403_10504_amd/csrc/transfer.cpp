@@ -149,6 +149,17 @@ std::string DmaEngine::init(int hip_device, bool to_host) {
   return "";
 }
 
+std::string DmaEngine::check_known(const void* p, const char* what) {
+  hsa_amd_pointer_info_t info{};
+  info.size = sizeof(info);
+  const hsa_status_t st = hsa_amd_pointer_info(const_cast<void*>(p), &info, nullptr, nullptr, nullptr);
+  if (st != HSA_STATUS_SUCCESS) return hsa_err("hsa_amd_pointer_info", st);
+  if (info.type == HSA_EXT_POINTER_TYPE_UNKNOWN)
+    return std::string(what) + " is unknown to the ROCr runtime this library is bound to (a second ROCr copy "
+           "in the process?)";
+  return "";
+}
+
 std::string DmaEngine::copy(void* dst, const void* src, uint64_t bytes) {
   if (!ready_) return "DMA engine is not initialised";
   if (bytes == 0) return "";

@@ -65,6 +65,11 @@ class DmaEngine {
   // Copies `bytes` (device -> pinned host if to_host, else the reverse) on
   // the engine and waits for the copy to finish.  Empty string on success.
   std::string copy(void* dst, const void* src, uint64_t bytes);
+  // Checks that `p` (device memory or pinned host memory the HIP runtime
+  // allocated) is known to the ROCr instance this library calls.  A process
+  // can hold two ROCr copies (a profiler may preload its own); the copies
+  // must run on the one the HIP runtime uses.  Empty string on success.
+  std::string check_known(const void* p, const char* what);
   bool ready() const { return ready_; }
 
  private:
