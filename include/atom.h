@@ -27,7 +27,9 @@
  * device memory.  Weight and gradient copies run on the GPU's system DMA
  * engines (one fixed engine per direction), issued by library threads.
  * The library owns the pinned host model (weights in the working dtype), the
- * host gradient buffers and the fp32 gradient accumulators.
+ * host gradient buffer (the last step's gradients in the working dtype) and
+ * the fp32 gradient accumulators.  Pinned host memory: the weights, one
+ * gradient buffer and, with host checkpoints, the evicted block inputs.
  *
  * Errors.  Every call returns an atom_status; nothing throws across the ABI.
  * atom_last_error(ctx) describes the last failure on a context;
@@ -67,7 +69,14 @@ typedef enum atom_ckpt_policy { ATOM_CKPT_DEVICE = 0, ATOM_CKPT_HOST = 1 } atom_
 typedef struct atom_config {
   int32_t n_layer, d_model, n_head, d_mlp, vocab, seq_len, batch, accum;
   int32_t dtype; /* atom_dtype: working precision of weights and activations */
-  int32_t ckpt;  /* atom_ckpt_policy: where block-input checkpoints live */
+  int32_t ckpt;  /* atom_ckpt_policy: where block-input checkpoints live.
+                  * ATOM_CKPT_DEVICE keeps all L+1 block inputs (fp32 [N][d]
+                  * per micro-batch) in the arena.  ATOM_CKPT_HOST keeps a ring
+                  * of 4 per micro-batch: the forward copies inputs 0..L-4 to
+                  * pinned host memory (D2H engine) after the kernel that wrote
+                  * them, and the backward restores each (H2D engine) before the
+                  * block that reads it; results are bitwise unchanged.  The
+                  * plan's h2d/d2h/forced byte counts include these copies. */
 } atom_config;
 
 /* Cost of one node of the augmented graph (Section III-D: the node's
@@ -120,7 +129,9 @@ int atom_node_layout(const atom_config* cfg, int32_t node, atom_tensor_desc* out
 
 /* Analytic node costs for cfg (n = n_layer + 2 entries): FLOP counts at an
  * assumed MFMA rate and bytes at an assumed host-link rate (the values are
- * stated in the design notes); callers may substitute measured costs. */
+ * half the dense MFMA peak, i.e. 1.25 PFLOP/s bf16 or 78.65 TFLOP/s fp32, 50 GB/s
+ * host link each way, 4 TB/s HBM for the embedding); callers may substitute
+ * measured costs. */
 int atom_node_costs(const atom_config* cfg, atom_node_cost* out, int32_t n);
 
 /* Device bytes the step needs besides weight and gradient slots
@@ -128,7 +139,9 @@ int atom_node_costs(const atom_config* cfg, atom_node_cost* out, int32_t n);
 int atom_reserve_bytes(const atom_config* cfg, uint64_t* out);
 
 /* Planner core (Algorithm 1 with the constraints and selection rule of
- * Section III-D as read in the design notes): searches contiguous
+ * Section III-D: co-resident executing and prefetched groups, overlap as a
+ * reported soft constraint, smallest predicted step time then fewest groups
+ * then smallest end-node list): searches contiguous
  * partitions of `n` nodes with the given costs, a device budget and
  * `reserve` bytes of non-slot memory.  Exhaustive for n <= 20 nodes; for
  * longer chains it searches the structured family that identical decoder
@@ -157,7 +170,7 @@ int atom_plan_fixed(const atom_config* cfg, int32_t n_groups, const int32_t* las
 
 /* Create a context: validates cfg against plan, carves the arena, allocates
  * the pinned host model (zero weights; fill them through atom_host_tensor)
- * and the host gradient buffers, and opens the two DMA engines on the
+ * and the host gradient buffer, and opens the two DMA engines on the
  * current HIP device.  compute_stream is a hipStream_t handle (e.g.
  * torch.cuda.Stream().cuda_stream) that receives every kernel; the library
  * also runs a few threads of its own (copies, host accumulation).  Errors:

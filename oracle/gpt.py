@@ -15,7 +15,7 @@ definition.  The model is the minGPT GPT used for the paper's profiling
 decoder blocks, and a final LayerNorm with the "Logits" layer (Section III-B,
 layer loading; Section III-C, embedding).  Shapes follow Table II.
 
-Readings where the paper is silent (the full list is in the design notes):
+Readings where the paper is silent:
 GELU in its tanh form; LayerNorm with biased variance and eps 1e-5; no
 dropout; attention scale 1/sqrt(d_head) with a strict causal mask; biases on
 every block linear, none on the LM head; the LM head is untied from the token

@@ -13,7 +13,7 @@ minimises computation time.
 Because step size 1 makes the search exhaustive, its result is defined by the
 set of all compositions of the chain into contiguous groups, which this module
 enumerates directly (2^(n-1) of them, so only small n).  The readings of the
-constraints and of the objective, written out here and in the design notes:
+constraints and of the objective:
 
 Memory (hard).  Groups are staged in equal weight slots of S = the largest
 group's weight bytes.  Gradients drain through two gradient slots of S bytes;

@@ -51,7 +51,7 @@ int atom_k_layernorm_fwd(int dtype, const float* x, const void* gamma, const voi
   return st(layernorm_fwd(dtype, x, gamma, beta, y, mean, rstd, rows, d, S(stream)));
 }
 
-int64_t atom_k_layernorm_bwd_part_floats(int64_t rows, int d) { return layernorm_bwd_blocks(rows) * 2 * d; }
+int64_t atom_k_layernorm_bwd_part_floats(int64_t rows, int d) { return layernorm_bwd_blocks(rows, d) * 2 * d; }
 
 int atom_k_layernorm_bwd(int dtype, const void* dy, const float* x, const float* mean, const float* rstd,
                          const void* gamma, float* dres, void* dres_lp, int accumulate, float* dgamma, float* dbeta,
@@ -59,7 +59,7 @@ int atom_k_layernorm_bwd(int dtype, const void* dy, const float* x, const float*
   if (!dt_ok(dtype) || !dy || !x || !mean || !rstd || !gamma || !dres || !dgamma || !dbeta || !part) return ATOM_EINVAL;
   int s = st(layernorm_bwd(dtype, dy, x, mean, rstd, gamma, dres, dres_lp, accumulate != 0, part, rows, d, S(stream)));
   if (s != ATOM_OK) return s;
-  const int64_t np = layernorm_bwd_blocks(rows);
+  const int64_t np = layernorm_bwd_blocks(rows, d);
   s = st(sum_parts(part, np, d, 2 * static_cast<int64_t>(d), DT_F32, dgamma, false, S(stream)));
   if (s != ATOM_OK) return s;
   return st(sum_parts(part + d, np, d, 2 * static_cast<int64_t>(d), DT_F32, dbeta, false, S(stream)));

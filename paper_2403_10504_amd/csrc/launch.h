@@ -42,7 +42,7 @@ hipError_t layernorm_fwd(int dtype, const float* x, const void* gamma, const voi
 // dres (+)= LN backward of dy; also writes dres_lp (element-type copy of the
 // updated dres, may be null) and per-block partial column sums of dy*xhat and
 // dy into part[nblk][2][d] (nblk from layernorm_bwd_blocks).
-int64_t layernorm_bwd_blocks(int64_t rows);
+int64_t layernorm_bwd_blocks(int64_t rows, int d);
 hipError_t layernorm_bwd(int dtype, const void* dy, const float* x, const float* mean, const float* rstd,
                          const void* gamma, float* dres, void* dres_lp, bool accumulate, float* part, int64_t rows,
                          int d, hipStream_t s);

@@ -5,6 +5,7 @@
 
 #include <stdint.h>
 
+#include <algorithm>
 #include <string>
 #include <vector>
 
@@ -24,6 +25,15 @@ constexpr int64_t HEAD_CHUNK = 2048;
 constexpr uint64_t SPLITK_BYTES = 64ull << 20;
 // Steps one pipelined call may run (one loss slot each).
 constexpr int MAX_STEPS_PER_CALL = 64;
+// Host checkpoints: block inputs live in a device ring of this many entries
+// per micro-batch; the forward copies to the host every input the ring will
+// overwrite (indices 0..L-CKPT_RING) and the backward restores them.
+constexpr int CKPT_RING = 4;
+inline int ckpt_evicted(const atom_config& c) { return c.ckpt == ATOM_CKPT_HOST ? std::max(0, c.n_layer + 1 - CKPT_RING) : 0; }
+// Bytes of block inputs one step copies each way under host checkpoints.
+inline uint64_t ckpt_xfer_bytes(const atom_config& c) {
+  return static_cast<uint64_t>(ckpt_evicted(c)) * c.accum * static_cast<uint64_t>(c.batch) * c.seq_len * c.d_model * 4;
+}
 
 struct TensorDesc {
   std::string name;
@@ -42,7 +52,7 @@ struct ArenaLayout {
   // reserve regions
   uint64_t tok_in, tok_tgt, emb_perm, emb_seg, emb_uniq;  // slot 0; slot 1 at + tok_stride
   uint64_t tok_stride;
-  uint64_t ckpt, ckpt_bytes_each;  // (L+1) x accum x [N][d] fp32 block inputs
+  uint64_t ckpt, ckpt_bytes_each;  // (L+1) (host checkpoints: CKPT_RING) x accum x [N][d] fp32 block inputs
   uint64_t dres, dres_lp;          // accum x [N][d] fp32 / working dtype
   uint64_t loss_rows, loss_out;
   uint64_t splitk, splitk_bytes;   // fp32 workspace for GEMMs split over k

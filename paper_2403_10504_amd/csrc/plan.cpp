@@ -1,8 +1,7 @@
 // Static analysis of the swapped step: node layout, node costs, arena
 // layout and the partition search (Section III-D, Algorithm 1).
 //
-// Readings of the algorithm (the paper's listing is garbled in places; these
-// are the ones the design notes record):
+// Readings of the algorithm (the paper's listing is garbled in places):
 //  * Search space: with step size 1 the search visits every way to cut the
 //    topologically sorted chain into contiguous sub-models; that set is
 //    enumerated directly (all 2^(n-1) compositions) for n <= 20 nodes.  For
@@ -96,7 +95,7 @@ ArenaLayout arena_layout(const atom_config& c, uint64_t slot_bytes, int n_slots,
   a.tok_stride = off - tok0;
   take(a.tok_stride);
   a.ckpt_bytes_each = N * d * 4;
-  a.ckpt = take((c.ckpt == ATOM_CKPT_DEVICE ? (L + 1) * C : 4) * a.ckpt_bytes_each);
+  a.ckpt = take((c.ckpt == ATOM_CKPT_DEVICE ? L + 1 : CKPT_RING) * C * a.ckpt_bytes_each);
   a.dres = take(C * N * d * 4);
   a.dres_lp = c.dtype == ATOM_BF16 ? take(C * N * d * 2) : a.dres;
   a.loss_rows = take(C * N * 4);
@@ -104,8 +103,8 @@ ArenaLayout arena_layout(const atom_config& c, uint64_t slot_bytes, int n_slots,
   a.splitk_bytes = SPLITK_BYTES;
   a.splitk = take(a.splitk_bytes);
   // partial-sum scratch: column sums over ceil(N/64) row blocks, or LayerNorm
-  // partials (one per 16-row block, two rows of d each)
-  a.part_floats = std::max((N + 63) / 64 * std::max(3 * d, f), (N + 15) / 16 * 2 * d);
+  // partials (at most one per 8-row block, two rows of d each)
+  a.part_floats = std::max((N + 63) / 64 * std::max(3 * d, f), (N + 7) / 8 * 2 * d);
   // block workspace
   uint64_t w = 0;
   auto wtake = [&](uint64_t bytes) {
@@ -407,8 +406,8 @@ int atom_plan_search(const atom_config* cfg, uint64_t budget, uint64_t reserve, 
   out->reserve_bytes = reserve;
   out->slot_bytes = best.S;
   out->arena_bytes = best.arena;
-  out->h2d_bytes = best.h2d;
-  out->d2h_bytes = best.d2h;
+  out->h2d_bytes = best.h2d + ckpt_xfer_bytes(*cfg);
+  out->d2h_bytes = best.d2h + ckpt_xfer_bytes(*cfg);
   uint64_t W = 0, Smin = 0;
   for (int i = 0; i < n; ++i) {
     W += costs[i].weight_bytes;
@@ -419,7 +418,7 @@ int atom_plan_search(const atom_config* cfg, uint64_t budget, uint64_t reserve, 
   // backward (the budget minus the reserve, two gradient slots and the
   // weights of the group being executed).
   const uint64_t keep = budget > reserve + 3 * Smin ? budget - reserve - 3 * Smin : 0;
-  out->forced_h2d_bytes = W + (W > keep ? W - keep : 0);
+  out->forced_h2d_bytes = W + (W > keep ? W - keep : 0) + ckpt_xfer_bytes(*cfg);
   out->pred_fwd_s = best.t_fwd;
   out->pred_step_s = best.t_step;
   out->n_evaluated = evaluated;
@@ -469,9 +468,9 @@ int atom_plan_fixed(const atom_config* cfg, int32_t n_groups, const int32_t* las
   out->slot_bytes = S;
   out->arena_bytes = arena_layout(*cfg, S, n_slots, n_gslots).arena_bytes;
   out->budget_bytes = out->arena_bytes;
-  out->h2d_bytes = ev.h2d;
-  out->d2h_bytes = ev.d2h;
-  out->forced_h2d_bytes = ev.h2d;
+  out->h2d_bytes = ev.h2d + ckpt_xfer_bytes(*cfg);
+  out->d2h_bytes = ev.d2h + ckpt_xfer_bytes(*cfg);
+  out->forced_h2d_bytes = out->h2d_bytes;
   out->pred_fwd_s = ev.t_fwd;
   out->pred_step_s = ev.t_step;
   out->n_evaluated = 1;

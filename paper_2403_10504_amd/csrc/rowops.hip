@@ -123,8 +123,155 @@ __global__ void __launch_bounds__(256) ln_bwd_kernel(const T* __restrict__ dy, c
   for (int c = tid; c < 2 * d; c += 256) p[c] = colacc[c];
 }
 
+// Backward, one wavefront per row (d a multiple of 256, at most 64*4*LNW_MAXCH).
+// Lane l owns columns 4l + 256j (j < nch = d/256), read as 4-element vectors
+// (8 bytes bf16, 16 bytes fp32), so every load of a wave is one contiguous
+// 512- or 1024-byte run and row sums need only wavefront shuffles.  Each wave
+// takes rpw consecutive rows and keeps its column sums of dy*xhat and dy in
+// registers; the four waves' sums are added in LDS in wave order into one
+// partial per workgroup (part[block][2][d]).
+constexpr int LNW_MAXCH = 20;
+
+// Rows per wave: 4 when there are enough rows to give every compute unit a
+// workgroup, else 2.
+inline int lnw_rows_per_wave(int64_t rows) { return rows >= 4096 ? 4 : 2; }
+
+template <typename T> struct Vec4;
+template <> struct Vec4<bf16_t> {
+  uint2 v;
+  ATOM_DEV void load(const bf16_t* p) { v = *reinterpret_cast<const uint2*>(p); }
+  ATOM_DEV float get(int i) const {
+    const uint32_t w = i < 2 ? v.x : v.y;
+    return __uint_as_float((i & 1) ? (w & 0xffff0000u) : (w << 16));
+  }
+  ATOM_DEV static void store(bf16_t* p, const float* f) {
+    uint2 o;
+    o.x = static_cast<uint32_t>(f2bf(f[0])) | (static_cast<uint32_t>(f2bf(f[1])) << 16);
+    o.y = static_cast<uint32_t>(f2bf(f[2])) | (static_cast<uint32_t>(f2bf(f[3])) << 16);
+    *reinterpret_cast<uint2*>(p) = o;
+  }
+};
+template <> struct Vec4<float> {
+  float4 v;
+  ATOM_DEV void load(const float* p) { v = *reinterpret_cast<const float4*>(p); }
+  ATOM_DEV float get(int i) const { return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w; }
+  ATOM_DEV static void store(float* p, const float* f) {
+    *reinterpret_cast<float4*>(p) = make_float4(f[0], f[1], f[2], f[3]);
+  }
+};
+
+template <typename T, int MAXCH>
+__global__ void __launch_bounds__(256) ln_bwd_wave_kernel(const T* __restrict__ dy, const float* __restrict__ x,
+                                                          const float* __restrict__ mean,
+                                                          const float* __restrict__ rstd, const T* __restrict__ gamma,
+                                                          float* __restrict__ dres, T* __restrict__ dres_lp,
+                                                          int accumulate, float* __restrict__ part, int64_t rows,
+                                                          int d, int rpw) {
+  extern __shared__ float red[];  // [4][d]
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int nch = d >> 8;
+  float ca[MAXCH * 4], cb[MAXCH * 4];
+#pragma unroll
+  for (int i = 0; i < MAXCH * 4; ++i) {
+    ca[i] = 0.f;
+    cb[i] = 0.f;
+  }
+  const float inv_d = 1.f / static_cast<float>(d);
+  const int64_t row0 = (static_cast<int64_t>(blockIdx.x) * 4 + w) * rpw;
+  for (int rr = 0; rr < rpw; ++rr) {
+    const int64_t row = row0 + rr;
+    if (row >= rows) break;  // uniform over the wave
+    const float mu = mean[row], r = rstd[row];
+    float dyv[MAXCH * 4], xh[MAXCH * 4];
+    float sa = 0.f, sb = 0.f;
+#pragma unroll
+    for (int j = 0; j < MAXCH; ++j) {
+      if (j < nch) {
+        const int c = 4 * lane + 256 * j;
+        Vec4<T> vy, vg;
+        vy.load(dy + row * d + c);
+        vg.load(gamma + c);
+        const float4 xv = *reinterpret_cast<const float4*>(x + row * d + c);
+        const float xs[4] = {xv.x, xv.y, xv.z, xv.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float g = vy.get(i), h = (xs[i] - mu) * r;
+          dyv[4 * j + i] = g;
+          xh[4 * j + i] = h;
+          const float gp = g * vg.get(i);
+          sa += gp;
+          sb += gp * h;
+          ca[4 * j + i] += g * h;
+          cb[4 * j + i] += g;
+        }
+      }
+    }
+    const float a = wave_sum(sa) * inv_d, b = wave_sum(sb) * inv_d;
+#pragma unroll
+    for (int j = 0; j < MAXCH; ++j) {
+      if (j < nch) {
+        const int c = 4 * lane + 256 * j;
+        Vec4<T> vg;
+        vg.load(gamma + c);
+        float* dr = dres + row * d + c;
+        float o[4];
+        if (accumulate) {
+          const float4 prev = *reinterpret_cast<const float4*>(dr);
+          o[0] = prev.x;
+          o[1] = prev.y;
+          o[2] = prev.z;
+          o[3] = prev.w;
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float dx = r * (dyv[4 * j + i] * vg.get(i) - a - xh[4 * j + i] * b);
+          o[i] = accumulate ? o[i] + dx : dx;
+        }
+        *reinterpret_cast<float4*>(dr) = make_float4(o[0], o[1], o[2], o[3]);
+        if (dres_lp) Vec4<T>::store(dres_lp + row * d + c, o);
+      }
+    }
+  }
+  // workgroup partial: the four waves' column sums, added in wave order
+  float* p = part + static_cast<int64_t>(blockIdx.x) * 2 * d;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const float* src = q == 0 ? ca : cb;
+#pragma unroll
+    for (int j = 0; j < MAXCH; ++j)
+      if (j < nch)
+        *reinterpret_cast<float4*>(red + w * d + 4 * lane + 256 * j) =
+            make_float4(src[4 * j], src[4 * j + 1], src[4 * j + 2], src[4 * j + 3]);
+    __syncthreads();
+    for (int c = threadIdx.x; c < d; c += 256) p[q * d + c] = ((red[c] + red[d + c]) + red[2 * d + c]) + red[3 * d + c];
+    __syncthreads();
+  }
+}
+
 // ------------------------------------------------------------- column sums
 constexpr int CS_ROWS = 64;
+
+// Column sums over CS_ROWS-row blocks, four consecutive columns per thread
+// (vector loads); cols and ld multiples of 4.  Each column is summed over its
+// rows in order, as in colsum_partial_kernel.
+template <typename T>
+__global__ void __launch_bounds__(256) colsum_partial4_kernel(const T* __restrict__ x, int64_t rows, int cols,
+                                                              int64_t ld, float* __restrict__ part) {
+  const int c = (blockIdx.x * 256 + threadIdx.x) * 4;
+  if (c >= cols) return;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * CS_ROWS;
+  const int64_t r1 = min(rows, r0 + CS_ROWS);
+  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+  for (int64_t r = r0; r < r1; ++r) {
+    Vec4<T> v;
+    v.load(x + r * ld + c);
+    s0 += v.get(0);
+    s1 += v.get(1);
+    s2 += v.get(2);
+    s3 += v.get(3);
+  }
+  *reinterpret_cast<float4*>(part + static_cast<int64_t>(blockIdx.y) * cols + c) = make_float4(s0, s1, s2, s3);
+}
 
 template <typename T>
 __global__ void __launch_bounds__(256) colsum_partial_kernel(const T* __restrict__ x, int64_t rows, int cols,
@@ -138,15 +285,30 @@ __global__ void __launch_bounds__(256) colsum_partial_kernel(const T* __restrict
   part[static_cast<int64_t>(blockIdx.y) * cols + c] = s;
 }
 
+// out[c] (+)= sum over p of part[p * stride + c].  A workgroup owns 16
+// columns; its 16 slices each add parts slice, slice + 16, ... in order, and
+// the slice sums are added in slice order, so the result is independent of
+// scheduling.
+constexpr int SP_COLS = 16, SP_SLICES = 16;
+
 template <typename TO>
 __global__ void __launch_bounds__(256) sum_parts_kernel(const float* __restrict__ part, int64_t nparts, int cols,
                                                         int64_t stride, TO* __restrict__ out, int accumulate) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= cols) return;
+  __shared__ float sh[SP_SLICES][SP_COLS];
+  const int cl = threadIdx.x % SP_COLS, sl = threadIdx.x / SP_COLS;
+  const int c = blockIdx.x * SP_COLS + cl;
   float s = 0.f;
-  for (int64_t p = 0; p < nparts; ++p) s += part[p * stride + c];
-  if (accumulate) s += to_f<TO>(out[c]);
-  out[c] = from_f<TO>(s);
+  if (c < cols)
+    for (int64_t p = sl; p < nparts; p += SP_SLICES) s += part[p * stride + c];
+  sh[sl][cl] = s;
+  __syncthreads();
+  if (sl == 0 && c < cols) {
+    float t = sh[0][cl];
+#pragma unroll
+    for (int i = 1; i < SP_SLICES; ++i) t += sh[i][cl];
+    if (accumulate) t += to_f<TO>(out[c]);
+    out[c] = from_f<TO>(t);
+  }
 }
 
 // --------------------------------------------------------------- embedding
@@ -319,15 +481,32 @@ hipError_t ln_fwd_t(const float* x, const void* gamma, const void* beta, void* y
   return hipGetLastError();
 }
 
+bool lnw_usable(int d) { return d % 256 == 0 && d / 256 <= LNW_MAXCH; }
+
 template <typename T>
 hipError_t ln_bwd_t(const void* dy, const float* x, const float* mean, const float* rstd, const void* gamma,
                     float* dres, void* dres_lp, bool acc, float* part, int64_t rows, int d, hipStream_t s) {
   const int ne = (d + 255) / 256;
-  dim3 grid(static_cast<unsigned>((rows + LNB_ROWS - 1) / LNB_ROWS)), block(256);
   auto a0 = static_cast<const T*>(dy);
   auto g = static_cast<const T*>(gamma);
   auto lp = static_cast<T*>(dres_lp);
   const int ac = acc ? 1 : 0;
+  if (lnw_usable(d)) {
+    const int rpw = lnw_rows_per_wave(rows);
+    dim3 wgrid(static_cast<unsigned>((rows + 4 * rpw - 1) / (4 * rpw))), wblock(256);
+    const size_t lds = 4 * static_cast<size_t>(d) * sizeof(float);
+#define ATOM_LNW(CH)                                                                                            \
+  hipLaunchKernelGGL((ln_bwd_wave_kernel<T, CH>), wgrid, wblock, lds, s, a0, x, mean, rstd, g, dres, lp, ac, part, \
+                     rows, d, rpw)
+    if (ne <= 1) ATOM_LNW(1);
+    else if (ne <= 4) ATOM_LNW(4);
+    else if (ne <= 8) ATOM_LNW(8);
+    else if (ne <= 16) ATOM_LNW(16);
+    else ATOM_LNW(LNW_MAXCH);
+#undef ATOM_LNW
+    return hipGetLastError();
+  }
+  dim3 grid(static_cast<unsigned>((rows + LNB_ROWS - 1) / LNB_ROWS)), block(256);
 #define ATOM_LNB(E) \
   hipLaunchKernelGGL((ln_bwd_kernel<T, E>), grid, block, 2 * d * sizeof(float), s, a0, x, mean, rstd, g, dres, lp, \
                      ac, part, rows, d)
@@ -351,7 +530,13 @@ hipError_t layernorm_fwd(int dtype, const float* x, const void* gamma, const voi
                           : ln_fwd_t<float>(x, gamma, beta, y, mean, rstd, rows, d, s);
 }
 
-int64_t layernorm_bwd_blocks(int64_t rows) { return (rows + LNB_ROWS - 1) / LNB_ROWS; }
+int64_t layernorm_bwd_blocks(int64_t rows, int d) {
+  if (lnw_usable(d)) {
+    const int rpw = lnw_rows_per_wave(rows);
+    return (rows + 4 * rpw - 1) / (4 * rpw);
+  }
+  return (rows + LNB_ROWS - 1) / LNB_ROWS;
+}
 
 hipError_t layernorm_bwd(int dtype, const void* dy, const float* x, const float* mean, const float* rstd,
                          const void* gamma, float* dres, void* dres_lp, bool accumulate, float* part, int64_t rows,
@@ -367,6 +552,18 @@ int64_t colsum_blocks(int64_t rows) { return (rows + CS_ROWS - 1) / CS_ROWS; }
 hipError_t colsum_partial(int in_dtype, const void* x, int64_t rows, int cols, int64_t ld, float* part,
                           hipStream_t s) {
   if (rows <= 0 || cols <= 0) return hipErrorInvalidValue;
+  const bool vec = cols % 4 == 0 && ld % 4 == 0 &&
+                   reinterpret_cast<uintptr_t>(x) % (in_dtype == DT_BF16 ? 8 : 16) == 0;
+  if (vec) {
+    dim3 g4(static_cast<unsigned>((cols / 4 + 255) / 256), static_cast<unsigned>(colsum_blocks(rows))), b4(256);
+    if (in_dtype == DT_BF16)
+      hipLaunchKernelGGL(colsum_partial4_kernel<bf16_t>, g4, b4, 0, s, static_cast<const bf16_t*>(x), rows, cols,
+                         ld, part);
+    else
+      hipLaunchKernelGGL(colsum_partial4_kernel<float>, g4, b4, 0, s, static_cast<const float*>(x), rows, cols, ld,
+                         part);
+    return hipGetLastError();
+  }
   dim3 grid(static_cast<unsigned>((cols + 255) / 256), static_cast<unsigned>(colsum_blocks(rows))), block(256);
   if (in_dtype == DT_BF16)
     hipLaunchKernelGGL(colsum_partial_kernel<bf16_t>, grid, block, 0, s, static_cast<const bf16_t*>(x), rows, cols,
@@ -380,7 +577,7 @@ hipError_t colsum_partial(int in_dtype, const void* x, int64_t rows, int cols, i
 hipError_t sum_parts(const float* part, int64_t nparts, int cols, int64_t part_stride, int out_dtype, void* out,
                      bool accumulate, hipStream_t s) {
   if (cols <= 0) return hipErrorInvalidValue;
-  dim3 grid(static_cast<unsigned>((cols + 255) / 256)), block(256);
+  dim3 grid(static_cast<unsigned>((cols + SP_COLS - 1) / SP_COLS)), block(256);
   if (out_dtype == DT_BF16)
     hipLaunchKernelGGL(sum_parts_kernel<bf16_t>, grid, block, 0, s, part, nparts, cols, part_stride,
                        static_cast<bf16_t*>(out), accumulate ? 1 : 0);

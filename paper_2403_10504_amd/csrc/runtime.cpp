@@ -23,7 +23,9 @@
 // step still loads every weight and drains every gradient.
 //
 // Gradients of a group go to one of the plan's gradient slots (claimed
-// round-robin in backward order), are copied to pinned host memory (two buffers, by step parity) on the
+// round-robin in backward order), are copied to pinned host memory (one buffer
+// shared by the steps in flight: a group's copy waits until the group's
+// previous gradients have been accumulated) on the
 // system DMA engine, and a host thread adds them to the fp32 accumulators.
 //
 // Transfers.  Both directions run on the GPU's system DMA (SDMA) engines
@@ -131,8 +133,7 @@ struct Range {
 };
 
 // Group g of a step with parity p is the "instance" gi = p * G + g: the two
-// steps a pipelined call keeps in flight have separate residency, events and
-// host gradient buffers.
+// steps a pipelined call keeps in flight have separate residency and events.
 struct atom_ctx {
   atom_config cfg{};
   atom_plan plan{};
@@ -142,11 +143,10 @@ struct atom_ctx {
   int L = 0, G = 0, K = 0, C = 0, H = 0, dh = 0, dt = 0, e = 0, d = 0, f = 0, V = 0, B = 0, T = 0;
   int64_t N = 0, Vp = 0;
   int par = 0;       // parity of the step the compute stream is being given work for
-  int last_par = 0;  // parity of the last step whose gradients reached the host
 
   // host model (pinned), per-node ranges
   uint8_t* h_w = nullptr;             // weights, working dtype
-  uint8_t* h_g[2] = {nullptr, nullptr};  // gradients of a step (by parity), working dtype
+  uint8_t* h_g = nullptr;             // gradients of the last step, working dtype
   float* h_acc = nullptr;             // fp32 accumulators (element-indexed like h_w)
   uint64_t model_bytes = 0;
   std::vector<uint64_t> node_off, node_bytes;
@@ -173,6 +173,20 @@ struct atom_ctx {
   std::vector<uint64_t> gs_issued, gs_freed;  // per gradient slot: copies out issued / finished
   std::vector<int> gslot_of;                // per instance: gradient slot of its current claim
   int next_gslot = 0;                       // round-robin claim order
+
+  // Host checkpoints (ATOM_CKPT_HOST).  Block input idx (0..L) of micro-batch
+  // m lives in ring entry (idx % CKPT_RING) * C + m.  Inputs the ring
+  // overwrites in the forward are copied to pinned host memory on the D2H
+  // engine after the kernel that wrote them, and restored on the H2D engine
+  // once the last kernel that read the entry's later occupant has run.
+  bool ck_host = false;
+  uint8_t* h_ck = nullptr;                        // pinned [(L+1)][C][N][d] fp32
+  std::vector<int> ck_holder;                     // per ring entry: index it holds (-1: none)
+  std::vector<char> ck_wait;                      // per ring entry: a restore the compute stream has not waited for
+  std::vector<uint64_t> ck_out_req, ck_out_done;  // per (idx, m): copies to the host issued / finished
+  std::vector<uint64_t> ck_in_req, ck_in_done;    // per (idx, m): restores issued / finished
+  std::vector<hipEvent_t> ev_ckw, ev_cku;         // per ring entry: after its writer / its last reader
+  std::vector<char> cku_recorded;
 
   // per-step validation state, by parity
   bool tokens_ok[2] = {false, false};
@@ -242,9 +256,14 @@ inline int slot_of(atom_ctx* c, int par, int g) {
   return par == 0 ? r : c->K - 1 - r;
 }
 
+// Device entry of block input idx (the output of node idx) of a micro-batch.
+inline int ck_entry(atom_ctx* c, int idx, int micro) { return (c->ck_host ? idx % CKPT_RING : idx) * c->C + micro; }
+inline bool ck_evicted(atom_ctx* c, int idx) { return c->ck_host && idx + CKPT_RING <= c->L; }
+inline size_t ck_key(atom_ctx* c, int idx, int micro) { return static_cast<size_t>(idx) * c->C + micro; }
+
 float* ckpt_ptr(atom_ctx* c, int idx, int micro) {
-  return reinterpret_cast<float*>(A(c, c->lay.ckpt) +
-                                  (static_cast<uint64_t>(idx) * c->C + micro) * c->lay.ckpt_bytes_each);
+  return reinterpret_cast<float*>(A(c, c->lay.ckpt) + static_cast<uint64_t>(ck_entry(c, idx, micro)) *
+                                                          c->lay.ckpt_bytes_each);
 }
 
 // Device pointer of a weight tensor of `node` in its group's slot.
@@ -425,7 +444,7 @@ int ln_grad(atom_ctx* c, const void* dy, const float* x, const float* mu, const 
             float* dres, void* dres_lp, bool acc, float* part, const GradTarget& tg, const GradTarget& tb) {
   const int d = c->d;
   KCHK(c, layernorm_bwd(c->dt, dy, x, mu, rs, gamma, dres, dres_lp, acc, part, c->N, d, c->cs));
-  const int64_t np = layernorm_bwd_blocks(c->N);
+  const int64_t np = layernorm_bwd_blocks(c->N, d);
   KCHK(c, sum_parts(part, np, d, 2 * static_cast<int64_t>(d), tg.dtype, tg.p, tg.accumulate, c->cs));
   KCHK(c, sum_parts(part + d, np, d, 2 * static_cast<int64_t>(d), tb.dtype, tb.p, tb.accumulate, c->cs));
   return ATOM_OK;
@@ -582,7 +601,7 @@ void accum_range<uint16_t>(float* acc, const uint16_t* g, uint64_t n) {
 
 void accumulate_group(atom_ctx* c, int gi) {
   const int par = gi / c->G, g = gi % c->G;
-  const uint8_t* hg = c->h_g[par];
+  const uint8_t* hg = c->h_g;
   const auto& rs = c->group_ranges[g];
   uint64_t total = 0;
   for (auto& r : rs) total += r.n;
@@ -641,9 +660,9 @@ int wait_accum(atom_ctx* c) {
 
 // The host buffer of instance gi is rewritten by its next gradient copy only
 // after the previous one has been added to the accumulators.
-void wait_accum_instance(atom_ctx* c, int gi) {
+void wait_accum_group(atom_ctx* c, int g) {
   std::unique_lock<std::mutex> l(c->acc_m);
-  c->acc_done_cv.wait(l, [c, gi] { return c->acc_pending[gi] == 0; });
+  c->acc_done_cv.wait(l, [c, g] { return c->acc_pending[g] == 0 && c->acc_pending[c->G + g] == 0; });
 }
 
 bool group_bwd_complete(atom_ctx* c, int par, int g) {
@@ -776,6 +795,122 @@ int swap_in_impl(atom_ctx* c, int par, int g) {
   return ATOM_OK;
 }
 
+// ------------------------------------------------------ host checkpoints
+// Wait (on the host) until ring entry e's occupant needs nothing more from
+// the DMA engines: its copy to the host and any restore into it finished.
+void ckpt_settle(atom_ctx* c, int e, int micro) {
+  const int prev = c->ck_holder[e];
+  if (prev < 0 || !ck_evicted(c, prev)) return;
+  const size_t kp = ck_key(c, prev, micro);
+  std::unique_lock<std::mutex> l(c->xm);
+  c->xcv.wait(l, [c, kp] { return c->ck_out_done[kp] >= c->ck_out_req[kp] && c->ck_in_done[kp] >= c->ck_in_req[kp]; });
+}
+
+// Records that the compute stream has enqueued its last use (so far) of ring
+// entry e; a restore into e waits for it.
+int ckpt_used(atom_ctx* c, int e) {
+  HIPCHK(c, hipEventRecord(c->ev_cku[e], c->cs));
+  c->cku_recorded[e] = 1;
+  return ATOM_OK;
+}
+
+// Copies block input idx of a micro-batch to the host once the kernel that
+// wrote it has run (D2H engine).
+int ckpt_out(atom_ctx* c, int idx, int micro) {
+  const int e = ck_entry(c, idx, micro);
+  const size_t k = ck_key(c, idx, micro);
+  HIPCHK(c, hipEventRecord(c->ev_ckw[e], c->cs));
+  const uint64_t bytes = c->lay.ckpt_bytes_each;
+  uint8_t* dst = c->h_ck + k * bytes;
+  const float* src = ckpt_ptr(c, idx, micro);
+  hipEvent_t ev = c->ev_ckw[e];
+  uint64_t gen;
+  {
+    std::lock_guard<std::mutex> l(c->xm);
+    gen = ++c->ck_out_req[k];
+  }
+  // ev is recorded again only by the next writer of the entry, which first
+  // waits for this copy (ckpt_settle)
+  c->d2h_worker->submit([c, k, ev, dst, src, bytes, gen]() -> std::string {
+    std::string err;
+    hipError_t r;
+    while ((r = hipEventQuery(ev)) == hipErrorNotReady) usleep(POLL_US);
+    if (r != hipSuccess) err = std::string("waiting for a checkpoint: ") + hipGetErrorString(r);
+    if (err.empty()) err = c->dma.copy(dst, src, bytes);
+    {
+      std::lock_guard<std::mutex> l(c->xm);
+      c->ck_out_done[k] = gen;
+    }
+    c->xcv.notify_all();
+    return err;
+  });
+  c->stats.d2h_bytes += bytes;
+  return ATOM_OK;
+}
+
+// Restores block input idx of a micro-batch into its ring entry (H2D
+// engine) after the last use of the entry's current occupant and after the
+// copy of idx to the host.  No-op when the entry already holds idx.
+int ckpt_restore(atom_ctx* c, int idx, int micro) {
+  const int e = ck_entry(c, idx, micro);
+  if (c->ck_holder[e] == idx) return ATOM_OK;
+  if (!ck_evicted(c, idx))
+    return fail(c, ATOM_ESTATE, "block input " + std::to_string(idx) + " is not on the device");
+  const size_t k = ck_key(c, idx, micro);
+  hipEvent_t wait_ev = c->cku_recorded[e] ? c->ev_cku[e] : nullptr;
+  const uint64_t bytes = c->lay.ckpt_bytes_each;
+  const uint8_t* src = c->h_ck + k * bytes;
+  float* dst = ckpt_ptr(c, idx, micro);
+  uint64_t gen, out_gen;
+  {
+    std::lock_guard<std::mutex> l(c->xm);
+    if (c->ck_out_req[k] == 0) return fail(c, ATOM_ESTATE, "block input " + std::to_string(idx) + " never computed");
+    gen = ++c->ck_in_req[k];
+    out_gen = c->ck_out_req[k];
+  }
+  c->h2d_worker->submit([c, k, wait_ev, dst, src, bytes, gen, out_gen]() -> std::string {
+    {
+      std::unique_lock<std::mutex> l(c->xm);
+      c->xcv.wait(l, [c, k, out_gen] { return c->ck_out_done[k] >= out_gen; });
+    }
+    std::string err;
+    hipError_t r = hipSuccess;
+    if (wait_ev)
+      while ((r = hipEventQuery(wait_ev)) == hipErrorNotReady) usleep(POLL_US);
+    if (r != hipSuccess) err = std::string("waiting for a checkpoint entry: ") + hipGetErrorString(r);
+    if (err.empty()) err = c->dma_in.copy(dst, src, bytes);
+    {
+      std::lock_guard<std::mutex> l(c->xm);
+      c->ck_in_done[k] = gen;
+    }
+    c->xcv.notify_all();
+    return err;
+  });
+  c->ck_holder[e] = idx;
+  c->ck_wait[e] = 1;
+  c->cku_recorded[e] = 0;
+  c->stats.h2d_bytes += bytes;
+  return ATOM_OK;
+}
+
+// Makes block input idx readable by the next kernel on the compute stream
+// (restoring it if needed and waiting for the restore).
+int ckpt_ready(atom_ctx* c, int idx, int micro) {
+  const int e = ck_entry(c, idx, micro);
+  int st = ckpt_restore(c, idx, micro);
+  if (st != ATOM_OK) return st;
+  if (c->ck_wait[e]) {
+    const size_t k = ck_key(c, idx, micro);
+    {
+      std::unique_lock<std::mutex> l(c->xm);
+      c->xcv.wait(l, [c, k] { return c->ck_in_done[k] >= c->ck_in_req[k]; });
+    }
+    KCHK(c, dma_acquire(c->cs));
+    c->ck_wait[e] = 0;
+  }
+  return ATOM_OK;
+}
+
 int fwd_impl(atom_ctx* c, int node, int micro) {
   const int par = c->par;
   if (!c->tokens_ok[par]) return fail(c, ATOM_ESTATE, "tokens not set");
@@ -783,10 +918,25 @@ int fwd_impl(atom_ctx* c, int node, int micro) {
     return fail(c, ATOM_ESTATE, "input of node " + std::to_string(node) + " not computed");
   int st = prepare_group(c, node, node == c->L + 1);
   if (st != ATOM_OK) return st;
+  if (c->ck_host) {
+    if (node > 0 && (st = ckpt_ready(c, node - 1, micro)) != ATOM_OK) return st;
+    if (node <= c->L) {
+      // the node's output goes into a ring entry whose occupant must be settled
+      const int e = ck_entry(c, node, micro);
+      ckpt_settle(c, e, micro);
+      c->ck_holder[e] = node;
+      c->ck_wait[e] = 0;
+    }
+  }
   if (node == 0) st = embed_forward(c, micro);
   else if (node <= c->L) st = block_forward(c, node, micro, false);
   else st = head_forward_backward(c, node, micro);
   if (st != ATOM_OK) return st;
+  if (c->ck_host) {
+    if (node > 0 && (st = ckpt_used(c, ck_entry(c, node - 1, micro))) != ATOM_OK) return st;
+    if (node <= c->L && (st = ckpt_used(c, ck_entry(c, node, micro))) != ATOM_OK) return st;
+    if (ck_evicted(c, node) && (st = ckpt_out(c, node, micro)) != ATOM_OK) return st;
+  }
   c->fwd_done[par][static_cast<size_t>(node) * c->C + micro] = 1;
   return finish_group_use(c, node);
 }
@@ -800,8 +950,10 @@ int bwd_impl(atom_ctx* c, int node, int micro) {
   if (c->bwd_done[par][k]) return fail(c, ATOM_ESTATE, "backward already done");
   int st = prepare_group(c, node, true);
   if (st != ATOM_OK) return st;
+  if (c->ck_host && node > 0 && (st = ckpt_ready(c, node - 1, micro)) != ATOM_OK) return st;
   st = node == 0 ? embed_backward(c, micro) : block_backward(c, node, micro);
   if (st != ATOM_OK) return st;
+  if (c->ck_host && node > 0 && (st = ckpt_used(c, ck_entry(c, node - 1, micro))) != ATOM_OK) return st;
   c->bwd_done[par][k] = 1;
   return finish_group_use(c, node);
 }
@@ -829,10 +981,13 @@ int swap_out_impl(atom_ctx* c, int par, int g) {
     c->gs_issued[gs] += 1;
   }
   HIPCHK(c, hipEventRecord(c->ev_gready[gi], c->cs));
-  uint8_t* dst = c->h_g[par] + c->group_off[g];
+  uint8_t* dst = c->h_g + c->group_off[g];
   const uint64_t bytes = c->group_bytes[g];
   c->d2h_worker->submit([c, gi, gs, dst, gsl, bytes]() -> std::string {
-    wait_accum_instance(c, gi);  // the host buffer of this parity is free again
+    // the group's range of the host buffer has been added to the accumulators
+    // (copies run in submission order, so an earlier step's copy of the group
+    // has already queued its accumulation)
+    wait_accum_group(c, gi % c->G);
     std::string err;
     hipError_t e;
     while ((e = hipEventQuery(c->ev_gready[gi])) == hipErrorNotReady) usleep(POLL_US);
@@ -853,7 +1008,6 @@ int swap_out_impl(atom_ctx* c, int par, int g) {
     c->xcv.notify_all();
     return err;
   });
-  c->last_par = par;
   c->stats.d2h_bytes += bytes;
   c->stats.swap_outs += 1;
   return ATOM_OK;
@@ -905,7 +1059,11 @@ int run_steps(atom_ctx* c, const int32_t* tokens, int n, float* losses) {
     // forward (the head also runs its backward and starts the residual gradient)
     for (int j = 0; j < G; ++j) {
       for (int node = p.first[j]; node <= p.last[j]; ++node)
-        for (int m = 0; m < C; ++m) STEP(fwd_impl(c, node, m));
+        for (int m = 0; m < C; ++m) {
+          STEP(fwd_impl(c, node, m));
+          // host checkpoints: the head was the last reader of input L's entry
+          if (c->ck_host && node == c->L + 1 && c->L - CKPT_RING >= 0) STEP(ckpt_restore(c, c->L - CKPT_RING, m));
+        }
       if (j + K < G) STEP(swap_in_impl(c, par, j + K));
     }
     STEP(reduce_loss(c, s));
@@ -913,7 +1071,11 @@ int run_steps(atom_ctx* c, const int32_t* tokens, int n, float* losses) {
     // backward, with reloads; slots the last K groups free take the next step's first groups
     for (int j = G - 1; j >= 0; --j) {
       for (int node = std::min(p.last[j], c->L); node >= p.first[j]; --node)
-        for (int m = 0; m < C; ++m) STEP(bwd_impl(c, node, m));
+        for (int m = 0; m < C; ++m) {
+          STEP(bwd_impl(c, node, m));
+          // host checkpoints: this block was the last reader of input node-1's entry
+          if (c->ck_host && node - 1 - CKPT_RING >= 0) STEP(ckpt_restore(c, node - 1 - CKPT_RING, m));
+        }
       STEP(swap_out_impl(c, par, j));
       if (j - K >= 0) STEP(swap_in_impl(c, par, j - K));
       else if (more) STEP(swap_in_impl(c, nxt, K - 1 - j));
@@ -943,7 +1105,6 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
   g_create_error = "invalid argument";
   if (!cfg || !plan || !dev_arena || !compute_stream) return ATOM_EINVAL;
   if (!check_config(*cfg).empty()) return ATOM_EINVAL;
-  if (cfg->ckpt != ATOM_CKPT_DEVICE) return ATOM_EINVAL;  // host checkpoints: not supported by this build
   const int n = cfg->n_layer + 2;
   if (plan->n_nodes != n || plan->n_groups < 1 || plan->n_groups > n || plan->n_slots < 1 ||
       plan->n_slots > plan->n_groups || plan->accum != cfg->accum)
@@ -975,6 +1136,7 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
   c->N = static_cast<int64_t>(c->B) * c->T;
   c->dt = cfg->dtype == ATOM_BF16 ? DT_BF16 : DT_F32;
   c->e = elem_bytes(*cfg);
+  c->ck_host = cfg->ckpt == ATOM_CKPT_HOST;
 
   // host ranges per node and group
   c->tens.resize(n);
@@ -1027,8 +1189,7 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
     const char* what;
   };
   const PinnedBuf bufs[] = {{&c->h_w, c->model_bytes, "host weights"},
-                            {&c->h_g[0], c->model_bytes, "host gradients (even steps)"},
-                            {&c->h_g[1], c->model_bytes, "host gradients (odd steps)"},
+                            {&c->h_g, c->model_bytes, "host gradients"},
                             {reinterpret_cast<uint8_t**>(&c->h_tok[0]), static_cast<uint64_t>(tok_words) * 4,
                              "token staging (even steps)"},
                             {reinterpret_cast<uint8_t**>(&c->h_tok[1]), static_cast<uint64_t>(tok_words) * 4,
@@ -1039,6 +1200,17 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
       *b.p = nullptr;
       g_create_error = std::string("hipHostMalloc of ") + std::to_string(b.bytes) + " bytes for " + b.what +
                        " failed: " + hipGetErrorString(e);
+      atom_ctx_destroy(c);
+      return ATOM_ENOMEM_HOST;
+    }
+  }
+  if (c->ck_host) {
+    const uint64_t ck_bytes = static_cast<uint64_t>(std::max(1, ckpt_evicted(*cfg))) * c->C * c->lay.ckpt_bytes_each;
+    const hipError_t e = hipHostMalloc(reinterpret_cast<void**>(&c->h_ck), ck_bytes, hipHostMallocDefault);
+    if (e != hipSuccess) {
+      c->h_ck = nullptr;
+      g_create_error = "hipHostMalloc of " + std::to_string(ck_bytes) + " bytes for host checkpoints failed: " +
+                       hipGetErrorString(e);
       atom_ctx_destroy(c);
       return ATOM_ENOMEM_HOST;
     }
@@ -1062,8 +1234,7 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
       const int nt = c->pool->size();
       const uint64_t lo = nb * ti / nt, hi = nb * (ti + 1) / nt;
       memset(c->h_w + lo, 0, hi - lo);
-      memset(c->h_g[0] + lo, 0, hi - lo);
-      memset(c->h_g[1] + lo, 0, hi - lo);
+      memset(c->h_g + lo, 0, hi - lo);
       const uint64_t elo = n_elem * ti / nt, ehi = n_elem * (ti + 1) / nt;
       memset(c->h_acc + elo, 0, (ehi - elo) * 4);
     });
@@ -1079,19 +1250,30 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
   c->load_done.assign(GI2, 0);
   c->d2h_pending.assign(GI2, 0);
   c->gslot_of.assign(GI2, 0);
+  {
+    const size_t ring = static_cast<size_t>(CKPT_RING) * c->C, keys = static_cast<size_t>(c->L + 1) * c->C;
+    c->ck_holder.assign(ring, -1);
+    c->ck_wait.assign(ring, 0);
+    c->cku_recorded.assign(ring, 0);
+    c->ck_out_req.assign(keys, 0);
+    c->ck_out_done.assign(keys, 0);
+    c->ck_in_req.assign(keys, 0);
+    c->ck_in_done.assign(keys, 0);
+  }
   for (int par = 0; par < 2; ++par) {
     c->fwd_done[par].assign(static_cast<size_t>(n) * c->C, 0);
     c->bwd_done[par].assign(static_cast<size_t>(n) * c->C, 0);
     c->n_uniq[par].assign(c->C, 0);
   }
-  auto mk = [&](std::vector<hipEvent_t>& v, unsigned flags) {
-    v.assign(GI2, nullptr);
+  auto mk = [&](std::vector<hipEvent_t>& v, unsigned flags, size_t count) {
+    v.assign(count, nullptr);
     for (auto& e : v)
       if (hipEventCreateWithFlags(&e, flags) != hipSuccess) return false;
     return true;
   };
-  if (!mk(c->ev_lastuse, hipEventDisableTiming) ||
-      !mk(c->ev_gready, hipEventDisableTiming) ||
+  const size_t n_ring = c->ck_host ? static_cast<size_t>(CKPT_RING) * c->C : 0;
+  if (!mk(c->ev_lastuse, hipEventDisableTiming, GI2) || !mk(c->ev_gready, hipEventDisableTiming, GI2) ||
+      !mk(c->ev_ckw, hipEventDisableTiming, n_ring) || !mk(c->ev_cku, hipEventDisableTiming, n_ring) ||
       hipEventCreateWithFlags(&c->ev_tok[0], hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&c->ev_tok[1], hipEventDisableTiming) != hipSuccess) {
     g_create_error = "event creation failed";
@@ -1140,17 +1322,17 @@ void atom_ctx_destroy(atom_ctx* c) {
     c->acc_cv.notify_all();
     c->acc_thread.join();
   }
-  for (auto* v : {&c->ev_lastuse, &c->ev_gready, &c->probe_ev})
+  for (auto* v : {&c->ev_lastuse, &c->ev_gready, &c->probe_ev, &c->ev_ckw, &c->ev_cku})
     for (auto e : *v)
       if (e) (void)hipEventDestroy(e);
   for (auto e : c->ev_tok)
     if (e) (void)hipEventDestroy(e);
   delete c->pool;
   if (c->h_w) (void)hipHostFree(c->h_w);
-  for (auto p : c->h_g)
-    if (p) (void)hipHostFree(p);
+  if (c->h_g) (void)hipHostFree(c->h_g);
   for (auto p : c->h_tok)
     if (p) (void)hipHostFree(p);
+  if (c->h_ck) (void)hipHostFree(c->h_ck);
   free(c->h_acc);
   delete c;
 }
@@ -1160,7 +1342,7 @@ int atom_host_tensor(atom_ctx* c, int32_t node, int32_t which, void** ptr, uint6
   const uint64_t off = c->node_off[node];
   if (which == 0) *ptr = c->h_w + off;
   else if (which == 1) *ptr = c->h_acc + off / c->e;
-  else *ptr = c->h_g[c->last_par] + off;
+  else *ptr = c->h_g + off;
   if (bytes) *bytes = which == 1 ? c->node_bytes[node] / c->e * 4 : c->node_bytes[node];
   return ATOM_OK;
 }
@@ -1280,7 +1462,7 @@ int atom_link_bench(atom_ctx* c, uint64_t bytes, int32_t iters, double* h2d, dou
     std::thread t_in([&] {
       for (int i = 0; i < iters && up && err_in.empty(); ++i) err_in = c->dma_in.copy(dev0, c->h_w, n);
     });
-    for (int i = 0; i < iters && down && err.empty(); ++i) err = c->dma.copy(c->h_g[0], dev1, n);
+    for (int i = 0; i < iters && down && err.empty(); ++i) err = c->dma.copy(c->h_g, dev1, n);
     t_in.join();
     return std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
   };

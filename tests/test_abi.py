@@ -115,6 +115,26 @@ def test_6p7b_plan_keeps_all_weights_resident_under_24gb():
     assert p.h2d_bytes == p.d2h_bytes == p.forced_h2d_bytes
 
 
+def test_13b_host_checkpoints_plan():
+    """13B under 24 GB with block inputs on the host: the weights no longer fit
+    (26.2 GB), so groups reload in the backward; every block input the
+    four-entry device ring overwrites crosses the link once each way."""
+    cfg = CONFIGS["13b"]
+    assert cfg.ckpt_host
+    c = A.make_config(cfg)
+    p = A.atom_plan_partition(c, cfg.budget_bytes)
+    assert p.arena_bytes <= cfg.budget_bytes
+    assert p.n_slots < p.n_groups
+    ck = (cfg.n_layer + 1 - 4) * cfg.accum * cfg.batch * cfg.seq_len * cfg.d_model * 4
+    dev = A.make_config(cfg.with_(ckpt_host=False))
+    # same partition and slots with device checkpoints would need (L+1-4) more [N][d] fp32 entries
+    assert A.atom_reserve_bytes(dev) - A.atom_reserve_bytes(c) == ck
+    W = sum(A.atom_node_layout(c, i)[1] for i in range(cfg.n_nodes))
+    assert p.d2h_bytes == W + ck
+    assert p.h2d_bytes > W + ck  # reloads in the backward
+    assert p.forced_h2d_bytes >= W + ck
+
+
 def test_plan_fixed():
     c = A.make_config(TINY)
     n = TINY.n_layer + 2

@@ -135,7 +135,8 @@ def test_gemm_rejects_unsupported_shapes():
 
 # ----------------------------------------------------------------- LayerNorm
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-@pytest.mark.parametrize("rows,d", [(37, 256), (130, 768), (17, 320), (5, 4096), (3, 5120)])
+@pytest.mark.parametrize("rows,d", [(37, 256), (130, 768), (17, 320), (5, 4096), (3, 5120), (4100, 256),
+                                    (300, 2048), (1031, 5120)])
 def test_layernorm_fwd_bwd(dtype, rows, d):
     r = U.rng(rows + d)
     x = (r.standard_normal((rows, d)) * 2 + 0.5).astype(np.float32)
@@ -237,7 +238,7 @@ def test_cross_entropy_rows(dtype, rows, V, ld):
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_colsum(dtype):
     r = U.rng(3)
-    for rows, cols in ((1000, 300), (64, 2304), (7, 5)):
+    for rows, cols in ((1000, 300), (64, 2304), (7, 5), (4100, 64), (130, 12292), (33, 1030)):
         x = U.rep(r.standard_normal((rows, cols)), dtype)
         dx = U.dev(x, dtype)
         out = U.empty(cols, "f32")
