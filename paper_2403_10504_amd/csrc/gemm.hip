@@ -10,8 +10,10 @@
 //   data grad dx = dy W   : A = dy (KC),          B = W  (not KC)
 //   weight grad dW = dy^T x: A = dy (not KC),      B = x  (not KC)
 //
-// Tiling: a BM x BN output tile per workgroup of WM x WN waves (a large tile
-// for big problems, 128x128 otherwise), 128-byte k tile (64 bf16 or 32 fp32)
+// Tiling: a BM x BN output tile per workgroup of WM x WN waves (256x256 with
+// 16 waves of 64x64 for big problems: four waves per SIMD hide the global
+// and LDS latency better than eight waves of 64x128, measured +16 %;
+// 128x128 with 4 waves otherwise), 128-byte k tile (64 bf16 or 32 fp32)
 // double-buffered in LDS.  Every operand is staged in LDS with k contiguous
 // (rows padded to 144 bytes to spread ds_read_b128 over the banks); operands
 // that are not k-contiguous in memory are transposed while being written to
@@ -35,7 +37,7 @@ constexpr int ROW_BYTES = 128, PITCH_BYTES = 144;
 // Workgroup tile BM x BN computed by WM x WN waves, each owning a
 // (BM/WM) x (BN/WN) block of 16x16 MFMA tiles.
 #ifndef ATOM_GEMM_CFG
-#define ATOM_GEMM_CFG 256, 256, 4, 2
+#define ATOM_GEMM_CFG 256, 256, 4, 4
 #endif
 template <int BM_, int BN_, int WM_, int WN_>
 struct Cfg {
@@ -63,7 +65,50 @@ struct Loader {
   static constexpr int DW = R * ROW_BYTES / 4 / NT;   // dwords per thread
   static constexpr int UPK = R / TL::PAIR;            // !KC: dword units per k row
   static constexpr int UPT = 8 * UPK / NT;            // !KC: units per thread
+  static constexpr int NOFF = KC ? DW / 4 : UPT;
   uint32_t r[DW];
+  uint32_t off[NOFF];  // byte offsets of this thread's loads inside a full tile
+
+  // Offsets for load_fast (leading dimension ld, elements).
+  __device__ void init(int64_t ld, int tid) {
+    if constexpr (KC) {
+#pragma unroll
+      for (int i = 0; i < NOFF; ++i) {
+        const int c = tid + NT * i;
+        off[i] = static_cast<uint32_t>(((c >> 3) * ld + (c & 7) * TL::KV) * sizeof(T));
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < NOFF; ++i) {
+        const int u = tid + NT * i;
+        off[i] = static_cast<uint32_t>(((u / UPK) * TL::KV * ld + (u % UPK) * TL::PAIR) * sizeof(T));
+      }
+    }
+  }
+
+  // Unguarded load of a tile that lies wholly inside the operand (rows
+  // r0..r0+R-1 and k0..k0+BK-1): one uniform base pointer and the 32-bit
+  // per-thread offsets from init.
+  __device__ void load_fast(const T* __restrict__ X, int64_t ld, int r0, int k0) {
+    if constexpr (KC) {
+      const char* base = reinterpret_cast<const char*>(X + static_cast<int64_t>(r0) * ld + k0);
+#pragma unroll
+      for (int i = 0; i < NOFF; ++i) {
+        const uint4 v = *reinterpret_cast<const uint4*>(base + off[i]);
+        r[4 * i + 0] = v.x;
+        r[4 * i + 1] = v.y;
+        r[4 * i + 2] = v.z;
+        r[4 * i + 3] = v.w;
+      }
+    } else {
+      const char* base = reinterpret_cast<const char*>(X + static_cast<int64_t>(k0) * ld + r0);
+      const uint32_t step = static_cast<uint32_t>(ld * sizeof(T));
+#pragma unroll
+      for (int i = 0; i < NOFF; ++i)
+#pragma unroll
+        for (int j = 0; j < TL::KV; ++j) r[i * TL::KV + j] = *reinterpret_cast<const uint32_t*>(base + off[i] + j * step);
+    }
+  }
 
   // KC: rows are contiguous along k, R rows x 8 chunks of 16 bytes.
   // !KC: memory is [k][row]; a unit is KV consecutive k rows x PAIR rows.
@@ -255,9 +300,23 @@ __global__ void __launch_bounds__(CF::NT) gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  // operands that are not k-contiguous load tiles wholly inside the operand
+  // without bounds checks (measured: no gain for k-contiguous ones)
+  const bool kfull = g.K % TL::BK == 0;
+  const bool afast = !AKC && kfull && m0 + BM <= g.M, bfast = !BKC && kfull && n0 + BN <= g.N;
+  la.init(g.lda, tid);
+  lb.init(g.ldb, tid);
+  auto load_a = [&](int k0) {
+    if (afast) la.load_fast(A, g.lda, m0, k0);
+    else la.load(A, g.lda, g.M, g.K, m0, k0, tid);
+  };
+  auto load_b = [&](int k0) {
+    if (bfast) lb.load_fast(B, g.ldb, n0, k0);
+    else lb.load(B, g.ldb, g.N, g.K, n0, k0, tid);
+  };
   if (kt0 < kt1) {
-    la.load(A, g.lda, g.M, g.K, m0, kt0 * TL::BK, tid);
-    lb.load(B, g.ldb, g.N, g.K, n0, kt0 * TL::BK, tid);
+    load_a(kt0 * TL::BK);
+    load_b(kt0 * TL::BK);
     la.store(As[0], tid);
     lb.store(Bs[0], tid);
   }
@@ -267,8 +326,8 @@ __global__ void __launch_bounds__(CF::NT) gemm_kernel(GemmArgs g) {
     const int cur = (kt - kt0) & 1;
     const bool more = kt + 1 < kt1;
     if (more) {
-      la.load(A, g.lda, g.M, g.K, m0, (kt + 1) * TL::BK, tid);
-      lb.load(B, g.ldb, g.N, g.K, n0, (kt + 1) * TL::BK, tid);
+      load_a((kt + 1) * TL::BK);
+      load_b((kt + 1) * TL::BK);
     }
     const T* as = As[cur] + (wm * TM * 16 + lr) * TL::PITCH + lg * 8;
     const T* bs = Bs[cur] + (wn * TN * 16 + lr) * TL::PITCH + lg * 8;
