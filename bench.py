@@ -36,6 +36,26 @@ sys.path.insert(0, ROOT)
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 HBM_PEAK_GBS = 8000.0
 
+# HBM traffic of the weight-gradient GEMM per launch in the default workload
+# (6.7B, C = 1), from two rocprofv3 --pmc passes (FETCH_SIZE, then
+# WRITE_SIZE) over `bench.py --steps 2 --warmup 1 --no-cpu-baseline
+# --copy-calibration 2147483648`, each scaled by what the counter reads for
+# the plain copy kernel of known size (profiles/gemm_wgrad_6.7b_hbm_traffic.md).
+# Valid only for the kernel sources it was measured on.
+WGRAD_TRAFFIC = {"sources_sha256": "2cbb979ddf3d4612d6cb03e3638b83442f55eae064eeb36a0c1d56f6b4d52a99",
+                 "bytes_per_launch": 729856221}
+TRAFFIC_SOURCES = ("gemm.hip", "common.h", "launch.h")
+
+
+def kernel_sources_sha256():
+    import hashlib
+
+    h = hashlib.sha256()
+    for name in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, "paper_2403_10504_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
@@ -54,12 +74,12 @@ def step_flops(cfg):
 def cpu_baseline(cfg):
     """The fp64 oracle on a bounded sample of the workload, extrapolated to one step.
 
-    Sample: one decoder block forward + backward on one sequence of T' =
-    min(T, 512) tokens, with its causal attention (forward + backward) also
-    timed alone; the LM head + cross-entropy forward + backward on 512 tokens.
-    Weights are converted to fp64 before the clock starts.
-    Extrapolation: the block's non-attention time scales with tokens, its
-    attention time with T^2 per sequence; the head scales with tokens.
+    Sample: one decoder block forward + backward on one whole sequence of T
+    tokens (its causal attention forward + backward also timed alone) and the
+    LM head + cross-entropy forward + backward on batch x T tokens (about 10-15 s of
+    CPU work at the 6.7B width).  Weights are converted to fp64 before the
+    clock starts.  Extrapolation: x (accum * batch) sequences x layers for the
+    block, x tokens for the head.
     """
     import numpy as np
     from threadpoolctl import threadpool_info, threadpool_limits
@@ -69,8 +89,8 @@ def cpu_baseline(cfg):
 
     cores = len(os.sched_getaffinity(0))
     T, d, H, V = cfg.seq_len, cfg.d_model, cfg.n_head, cfg.vocab
-    Ts = min(T, 512)
-    n_head_tok = min(512, cfg.batch * T)
+    Ts = T
+    n_head_tok = cfg.batch * T
     with threadpool_limits(limits=cores):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
         rng = np.random.default_rng(0)
@@ -106,8 +126,8 @@ def cpu_baseline(cfg):
         "sample": (f"fp64 NumPy oracle: one decoder block forward+backward on a {Ts}-token sequence "
                    f"({t_block:.2f} s, of which causal attention {t_attn:.2f} s) and the LM head + "
                    f"cross-entropy forward+backward on {n_head_tok} tokens ({t_head:.2f} s); extrapolated to "
-                   f"{cfg.accum}x{cfg.batch} sequences of {T} tokens x {cfg.n_layer} blocks (attention x "
-                   f"(T/{Ts})^2, the rest x tokens)"),
+                   f"{cfg.accum}x{cfg.batch} sequences of {T} tokens x {cfg.n_layer} blocks and "
+                   f"{n_tok} head tokens"),
         "extrapolated_step_s": t_step,
     }
 
@@ -122,6 +142,8 @@ def main():
     ap.add_argument("--budget-gb", type=float, default=None, help="device budget (default: the config's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sequential", action="store_true", help="one atom_step call per step (no cross-step overlap)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="run one plain device copy of BYTES before the timed steps (calibrates HBM byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -175,6 +197,15 @@ def main():
         losses = run(args.warmup)
         log(f"warmup: losses {[round(l, 5) for l in losses]}")
 
+    if args.copy_calibration:
+        n = (args.copy_calibration + 15) // 16 * 16
+        src = torch.empty(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty(n, dtype=torch.uint8, device="cuda")
+        A.atom_k_copy(src.data_ptr(), dst.data_ptr(), n, torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        log(f"calibration copy of {n} bytes done")
+        del src, dst
+
     # dominant kernel: weight-gradient GEMM (A and B not k-contiguous)
     # (bf16 at C = 1 writes bf16 gradients; otherwise micro-batch 0 stores fp32)
     wgrad_epi = A.ATOM_EPI_STORE if (cfg.accum == 1 and cfg.dtype == "bf16") else A.ATOM_EPI_STORE_F32
@@ -184,7 +215,7 @@ def main():
     losses = run(args.steps)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
-    launches, probe_s, probe_flops = A.atom_probe_read(sess.ctx)
+    launches, probe_s, probe_flops, probe_bytes = A.atom_probe_read(sess.ctx)
     A.atom_probe_gemm(sess.ctx, 0, 0, -1)
     st = sess.stats()
     log(f"timed {args.steps} steps: {elapsed / args.steps * 1e3:.1f} ms/step, loss {losses[-1]:.5f}, "
@@ -197,6 +228,12 @@ def main():
     tokens_per_s = n_tok / (ms_per_step / 1e3)
     peak = MFMA_PEAK_TFLOPS[cfg.dtype]
     achieved = probe_flops / probe_s / 1e12 if probe_s > 0 else 0.0
+    alg_bytes = probe_bytes / max(launches, 1)
+    traffic = None
+    default_workload = args.config == "6.7b" and cfg.accum == 1 and not args.budget_gb
+    if default_workload and WGRAD_TRAFFIC["bytes_per_launch"] and \
+            WGRAD_TRAFFIC["sources_sha256"] == kernel_sources_sha256():
+        traffic = WGRAD_TRAFFIC["bytes_per_launch"]
     fl = step_flops(cfg)
     t_mfma = fl / (peak * 1e12)
     t_h2d_r0 = plan.forced_h2d_bytes / (h2d_gbs * 1e9)
@@ -237,7 +274,8 @@ def main():
             "peak": peak,
             "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4),
-            "traffic": None,
+            "traffic": traffic,
+            "alg_bytes_per_launch": round(alg_bytes),
             "launches": launches,
             "avg_launch_us": round(probe_s / max(launches, 1) * 1e6, 2),
         },

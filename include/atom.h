@@ -250,11 +250,13 @@ int atom_get_stats(atom_ctx* ctx, atom_stats* out);
 /* Kernel probe for measurement.  While enabled, every launch of the GEMM
  * instantiation (a_kcontig, b_kcontig, epilogue as in atom_kernels.h) that
  * the step makes is bracketed by timing events on the compute stream;
- * atom_probe_read returns the number of launches, their summed duration and
- * their summed algorithmic FLOPs (2*M*N*K) since the probe was enabled.
+ * atom_probe_read returns the number of launches, their summed duration,
+ * their summed algorithmic FLOPs (2*M*N*K) and their summed algorithmic HBM
+ * bytes (each operand read once, the output written once, plus the tensors
+ * the epilogue reads: residual, pre-activation) since the probe was enabled.
  * epi < 0 disables the probe.  At most 4096 launches are recorded per step. */
 int atom_probe_gemm(atom_ctx* ctx, int32_t a_kcontig, int32_t b_kcontig, int32_t epi);
-int atom_probe_read(atom_ctx* ctx, int64_t* launches, double* seconds, double* flops);
+int atom_probe_read(atom_ctx* ctx, int64_t* launches, double* seconds, double* flops, double* bytes);
 
 /* Host-link microbenchmark on the context's own pinned buffers and arena
  * (weight-slot region; call between steps): `bytes` per copy (clamped to the

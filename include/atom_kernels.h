@@ -93,6 +93,11 @@ int atom_k_xent(int dtype, const float* logits, int64_t ldz, const int32_t* tgt,
 int atom_k_embed_fwd(int dtype, const int32_t* tok, const void* wte, const void* wpe, float* x, int64_t n_tok,
                      int T, int V, int d, void* stream);
 
+/* Plain device copy of `bytes` (a multiple of 16; both pointers 16-byte
+ * aligned, not overlapping): reads and writes each byte once.  Measurement
+ * only: its known traffic calibrates the HBM byte counters. */
+int atom_k_copy(const void* src, void* dst, int64_t bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

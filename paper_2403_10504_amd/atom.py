@@ -95,7 +95,7 @@ _SIGS = {
     "atom_steps": (ctypes.c_int, [P, P, ctypes.c_int32, P]),
     "atom_get_stats": (ctypes.c_int, [P, P]),
     "atom_probe_gemm": (ctypes.c_int, [P, I32, I32, I32]),
-    "atom_probe_read": (ctypes.c_int, [P, P, P, P]),
+    "atom_probe_read": (ctypes.c_int, [P, P, P, P, P]),
     "atom_link_bench": (ctypes.c_int, [P, U64, I32, P, P, P]),
     "atom_last_error": (ctypes.c_char_p, [P]),
     "atom_k_gemm": (ctypes.c_int, [ctypes.c_int] * 7 + [P, I64, P, I64, P, I64, P, P, P, I64, P, U64, P]),
@@ -109,6 +109,7 @@ _SIGS = {
     "atom_k_colsum": (ctypes.c_int, [ctypes.c_int, P, I64, ctypes.c_int, P, P, P]),
     "atom_k_xent": (ctypes.c_int, [ctypes.c_int, P, I64, P, P, I64, P, I64, ctypes.c_int, ctypes.c_float, P]),
     "atom_k_embed_fwd": (ctypes.c_int, [ctypes.c_int, P, P, P, P, I64, ctypes.c_int, ctypes.c_int, ctypes.c_int, P]),
+    "atom_k_copy": (ctypes.c_int, [P, P, I64, P]),
 }
 EXPORTED = tuple(_SIGS)
 
@@ -320,8 +321,9 @@ def atom_probe_read(ctx):
     n = I64()
     sec = ctypes.c_double()
     fl = ctypes.c_double()
-    _check(lib().atom_probe_read(ctx, _ref(n), _ref(sec), _ref(fl)), ctx)
-    return n.value, sec.value, fl.value
+    by = ctypes.c_double()
+    _check(lib().atom_probe_read(ctx, _ref(n), _ref(sec), _ref(fl), _ref(by)), ctx)
+    return n.value, sec.value, fl.value, by.value
 
 
 def atom_link_bench(ctx, nbytes: int, iters: int):
@@ -377,3 +379,7 @@ def atom_k_xent(dtype, logits, ldz, tgt, dz, lddz, loss_rows, rows, V, scale, st
 
 def atom_k_embed_fwd(dtype, tok, wte, wpe, x, n_tok, T, V, d, stream=None):
     _kcall("atom_k_embed_fwd", dtype, tok, wte, wpe, x, n_tok, T, V, d, stream)
+
+
+def atom_k_copy(src, dst, nbytes, stream=None):
+    _kcall("atom_k_copy", src, dst, nbytes, stream)

@@ -97,4 +97,9 @@ int atom_k_embed_fwd(int dtype, const int32_t* tok, const void* wte, const void*
   return st(embed_fwd(dtype, tok, wte, wpe, x, n_tok, T, V, d, S(stream)));
 }
 
+int atom_k_copy(const void* src, void* dst, int64_t bytes, void* stream) {
+  if (!src || !dst || bytes < 0 || bytes % 16) return ATOM_EINVAL;
+  return st(copy_bytes(src, dst, bytes, S(stream)));
+}
+
 }  // extern "C"

@@ -78,6 +78,8 @@ hipError_t sum_fixed(const float* x, int64_t n, float* out, hipStream_t s);
 // fp32 -> element type conversion (n elements).
 hipError_t convert_f32(int dtype, const float* x, void* y, int64_t n, hipStream_t s);
 hipError_t fill_zero(void* p, int64_t bytes, hipStream_t s);
+// Streaming device copy of `bytes` (multiple of 16, 16-byte aligned).
+hipError_t copy_bytes(const void* src, void* dst, int64_t bytes, hipStream_t s);
 // Copy n 32-bit words on stream s by a kernel; src may be mapped pinned host
 // memory (small uploads that must not occupy a DMA engine).
 hipError_t copy_words(const uint32_t* src, uint32_t* dst, int64_t n, hipStream_t s);

@@ -442,6 +442,14 @@ __global__ void __launch_bounds__(256) fill_zero_kernel(uint4* __restrict__ p, i
   if (blockIdx.x == 0 && static_cast<int>(threadIdx.x) < ntail) tail[threadIdx.x] = 0;
 }
 
+// Streaming copy, 16 bytes per thread and iteration.
+__global__ void __launch_bounds__(256) copy16_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst,
+                                                     int64_t n16) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n16;
+       i += static_cast<int64_t>(gridDim.x) * 256)
+    dst[i] = src[i];
+}
+
 // Word copy whose source may be mapped pinned host memory (read over the host
 // link by the kernel itself).
 __global__ void __launch_bounds__(256) copy_words_kernel(const uint32_t* __restrict__ src,
@@ -665,6 +673,18 @@ hipError_t dma_acquire(hipStream_t s) {
 hipError_t copy_words(const uint32_t* src, uint32_t* dst, int64_t n, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(copy_words_kernel, dim3(grid_for(n)), dim3(256), 0, s, src, dst, n);
+  return hipGetLastError();
+}
+
+hipError_t copy_bytes(const void* src, void* dst, int64_t bytes, hipStream_t s) {
+  if (bytes <= 0) return hipSuccess;
+  if ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst) | static_cast<uintptr_t>(bytes)) & 15)
+    return hipErrorInvalidValue;
+  const int64_t n16 = bytes / 16;
+  const int64_t want = (n16 + 255) / 256;
+  const unsigned grid = static_cast<unsigned>(want < 8192 ? (want < 1 ? 1 : want) : 8192);
+  hipLaunchKernelGGL(copy16_kernel, dim3(grid), dim3(256), 0, s, static_cast<const uint4*>(src),
+                     static_cast<uint4*>(dst), n16);
   return hipGetLastError();
 }
 

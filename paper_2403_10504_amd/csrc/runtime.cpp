@@ -212,10 +212,10 @@ struct atom_ctx {
   // GEMM probe (measurement): events around launches of one instantiation
   int probe_akc = -1, probe_bkc = -1, probe_epi = -1;
   std::vector<hipEvent_t> probe_ev;  // 2 per launch
-  std::vector<double> probe_flop;    // per pending launch
+  std::vector<double> probe_flop, probe_byte;  // per pending launch
   int probe_pending = 0;
   int64_t probe_launches = 0;
-  double probe_seconds = 0, probe_flops = 0;
+  double probe_seconds = 0, probe_flops = 0, probe_bytes = 0;
 
   atom_stats stats{};
   std::string err;
@@ -356,6 +356,7 @@ int probe_collect(atom_ctx* c) {
     HIPCHK(c, hipEventElapsedTime(&ms, c->probe_ev[2 * i], c->probe_ev[2 * i + 1]));
     c->probe_seconds += ms * 1e-3;
     c->probe_flops += c->probe_flop[i];
+    c->probe_bytes += c->probe_byte[i];
     c->probe_launches += 1;
   }
   c->probe_pending = 0;
@@ -378,6 +379,15 @@ hipError_t run_gemm(atom_ctx* c, const GemmArgs& g, bool akc, bool bkc, int epi)
   e = hipEventRecord(c->probe_ev[2 * c->probe_pending + 1], c->cs);
   if (e != hipSuccess) return e;
   c->probe_flop[c->probe_pending] = 2.0 * g.M * g.N * static_cast<double>(g.K);
+  // algorithmic bytes: both operands read once, the output written once
+  // (fp32 or the element type), plus what the epilogue reads
+  const double ein = c->e;
+  const double eout = (epi == EPI_STORE_F32 || epi == EPI_ACC_F32 || epi == EPI_BIAS_RESID) ? 4.0 : ein;
+  double extra = 0.0;
+  if (epi == EPI_ACC_F32 || epi == EPI_BIAS_RESID) extra += 4.0 * g.M * g.N;
+  if (epi == EPI_BIAS_GELU || epi == EPI_GELU_BWD) extra += ein * g.M * g.N;
+  c->probe_byte[c->probe_pending] =
+      ein * (static_cast<double>(g.M) * g.K + static_cast<double>(g.K) * g.N) + eout * g.M * g.N + extra;
   c->probe_pending += 1;
   return hipSuccess;
 }
@@ -1282,6 +1292,7 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
   }
   c->probe_ev.assign(2 * PROBE_MAX, nullptr);
   c->probe_flop.assign(PROBE_MAX, 0.0);
+  c->probe_byte.assign(PROBE_MAX, 0.0);
   for (auto& e : c->probe_ev)
     if (hipEventCreate(&e) != hipSuccess) {
       atom_ctx_destroy(c);
@@ -1430,10 +1441,11 @@ int atom_probe_gemm(atom_ctx* c, int32_t akc, int32_t bkc, int32_t epi) {
   c->probe_launches = 0;
   c->probe_seconds = 0;
   c->probe_flops = 0;
+  c->probe_bytes = 0;
   return ATOM_OK;
 }
 
-int atom_probe_read(atom_ctx* c, int64_t* launches, double* seconds, double* flops) {
+int atom_probe_read(atom_ctx* c, int64_t* launches, double* seconds, double* flops, double* bytes) {
   if (!c) return ATOM_EINVAL;
   HIPCHK(c, hipStreamSynchronize(c->cs));
   int st = probe_collect(c);
@@ -1441,6 +1453,7 @@ int atom_probe_read(atom_ctx* c, int64_t* launches, double* seconds, double* flo
   if (launches) *launches = c->probe_launches;
   if (seconds) *seconds = c->probe_seconds;
   if (flops) *flops = c->probe_flops;
+  if (bytes) *bytes = c->probe_bytes;
   return ATOM_OK;
 }
 
