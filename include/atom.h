@@ -140,7 +140,7 @@ int atom_reserve_bytes(const atom_config* cfg, uint64_t* out);
 
 /* Planner core (Algorithm 1 with the constraints and selection rule of
  * Section III-D: co-resident executing and prefetched groups, overlap as a
- * reported soft constraint, smallest predicted step time then fewest groups
+ * reported soft constraint, smallest predicted step time then fewest bytes loaded then fewest groups
  * then smallest end-node list): searches contiguous
  * partitions of `n` nodes with the given costs, a device budget and
  * `reserve` bytes of non-slot memory.  Exhaustive for n <= 20 nodes; for

@@ -39,8 +39,11 @@ consecutive groups; backward: C*t_bwd(g_{j+1}) >= t_load(g_j) for every
 group that has to be reloaded.
 
 Selection.  Among feasible partitions: smallest predicted step time, then
-fewest groups (the smallest total cut size, since every cut is one [B,T,d]
-activation), then the lexicographically smallest list of group end nodes.
+fewest bytes loaded (the schedule model runs loads and stores at full rate
+each, so reloads that overlap the gradient stores look free although both
+directions share the host link), then fewest groups (the smallest total cut
+size, since every cut is one [B,T,d] activation), then the lexicographically
+smallest list of group end nodes.
 """
 from __future__ import annotations
 
@@ -162,7 +165,7 @@ def evaluate(groups, costs, budget, reserve, accum, dtype):
 
 
 def rank_key(plan):
-    return (plan["pred_step_s"], len(plan["groups"]), [b for _, b in plan["groups"]])
+    return (plan["pred_step_s"], plan["h2d_bytes"], len(plan["groups"]), [b for _, b in plan["groups"]])
 
 
 def best(candidates, costs, budget, reserve, accum, dtype):

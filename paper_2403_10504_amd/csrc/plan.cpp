@@ -18,9 +18,11 @@
 //    overlap_ok, not required, because on MI355X the host link cannot keep
 //    up with per-block compute at C = 1.
 //  * Objective: smallest predicted step time of the three-stream schedule,
-//    then fewest groups (the paper's minimum total cut size: every cut is one
-//    [B, T, d] activation), then the lexicographically smallest list of group
-//    end nodes.
+//    then fewest bytes loaded (the model runs loads and stores at full rate
+//    each, so reloads that overlap the gradient stores look free although
+//    both directions share the host link), then fewest groups (the paper's
+//    minimum total cut size: every cut is one [B, T, d] activation), then the
+//    lexicographically smallest list of group end nodes.
 #include <stdint.h>
 #include <string.h>
 
@@ -250,6 +252,7 @@ Eval evaluate(const std::vector<std::pair<int, int>>& g, const atom_node_cost* c
 bool better(const Eval& a, const std::vector<std::pair<int, int>>& ga, const Eval& b,
             const std::vector<std::pair<int, int>>& gb) {
   if (a.t_step != b.t_step) return a.t_step < b.t_step;
+  if (a.h2d != b.h2d) return a.h2d < b.h2d;
   if (ga.size() != gb.size()) return ga.size() < gb.size();
   for (size_t i = 0; i < ga.size(); ++i)
     if (ga[i].second != gb[i].second) return ga[i].second < gb[i].second;

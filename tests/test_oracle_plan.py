@@ -82,16 +82,25 @@ def test_brute_force_prefers_fine_groups_when_link_bound():
     assert not best["overlap_ok"]
 
 
-def test_brute_force_tie_break_fewest_groups():
+def test_brute_force_tie_breaks_bytes_then_groups():
     # no transfer cost: every partition has the same predicted time
     c = costs_uniform(5, tu=0.0, ts=0.0)
+    # everything stays resident in any partition (same bytes): fewest groups
     best = P.brute_force(c, budget=10 ** 9, reserve=0, accum=1, dtype=P.BF16)
     assert best["groups"] == [(0, 4)]
-    # a budget that fits at most 2 nodes per slot: fewest groups is 3, with
-    # group sizes (1,2,2), (2,1,2) or (2,2,1); their end lists are [0,2,4],
-    # [1,2,4] and [1,3,4], and the smallest is [0,2,4]
+    # 800 bytes beside the reserve: groups of two nodes get slots of 200 and
+    # gradient slots of 400, so two weight slots, and three groups reload one
+    # group in the backward; single nodes get six slots of 100 next to 200 of
+    # gradient slots, so nothing reloads: fewest bytes wins over fewest groups
     best = P.brute_force(c, budget=400 + 4 * 200, reserve=400, accum=1, dtype=P.BF16)
-    assert [b for _, b in best["groups"]] == [0, 2, 4]
+    assert best["groups"] == [(i, i) for i in range(5)]
+    assert best["h2d_bytes"] == 5 * 100
+    # among the three-group plans, the one reloading the smallest group wins
+    # ((1,2,2): 100 bytes; (2,1,2) and (2,2,1): 200), although [0,2,4] is also
+    # the smallest end list
+    three = P.best([[(0, 0), (1, 2), (3, 4)], [(0, 1), (2, 2), (3, 4)], [(0, 1), (2, 3), (4, 4)]], c,
+                   400 + 4 * 200, 400, 1, P.BF16)
+    assert [b for _, b in three["groups"]] == [0, 2, 4] and three["h2d_bytes"] == 600
 
 
 def test_brute_force_none_when_nothing_fits():
