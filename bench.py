@@ -268,8 +268,10 @@ def main():
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": f"gemm_kernel<{cfg.dtype}, A not k-contiguous, B not k-contiguous, epilogue {wgrad_epi}> "
-                      "(weight gradients)",
+            "kernel": (f"gemm_p3_kernel<A not k-contiguous, B not k-contiguous, epilogue {wgrad_epi}> "
+                       "(weight gradients; four-stage direct-to-LDS pipeline)" if cfg.dtype == "bf16" else
+                       f"gemm_kernel<f32, A not k-contiguous, B not k-contiguous, epilogue {wgrad_epi}> "
+                       "(weight gradients)"),
             "achieved": round(achieved, 2),
             "peak": peak,
             "unit": "TFLOP/s",

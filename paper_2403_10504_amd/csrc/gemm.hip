@@ -25,6 +25,7 @@
 // workgroups; the fp32 partials are summed in split order by a second kernel,
 // so the result does not depend on scheduling.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 #include "launch.h"
@@ -442,6 +443,241 @@ hipError_t launch_cfg(const GemmArgs& g, int epi, int splits, hipStream_t s) {
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------ pipelined
+// bf16 GEMM for large problems with a four-stage LDS pipeline fed by direct
+// global-to-LDS loads (global_load_lds_dwordx4: no staging registers, no LDS
+// store instructions).  256x256 output tile, 16 waves of 64x64, k tile of 32.
+// Iteration t waits for its own stage (the loads of the two later stages may
+// still be in flight), synchronises the workgroup, starts the loads of tile
+// t+3 into the stage iteration t-1 has just finished reading, then computes.
+// Each stage is a separate LDS array and the stage rotation is unrolled, so
+// the compiler sees which array every load and read touches and inserts no
+// waits of its own between them.
+//
+// LDS layouts (16-byte chunks are XOR-swizzled so that fragment reads are
+// free of bank conflicts; a direct load writes 1 KB per wave contiguously, so
+// the swizzle is applied to the global address each lane loads):
+//   k-contiguous operand  [256 rows][32 k]: row r, chunk c at slot c ^ ((r>>1)&3);
+//                         fragments by ds_read_b128.
+//   other operand         [32 k][256 rows]: k row k, chunk c (8 rows) at slot
+//                         c ^ 2(k&3); fragments by two ds_read_b64_tr_b16, each
+//                         transposing a 4 (k) x 16 (rows) block across 16 lanes.
+// Rows beyond the operand are clamped to its last valid row (or 8-row block),
+// so they read finite data that only reaches output rows or columns that are
+// never stored; k must be a multiple of 32.
+#ifndef ATOM_GEMM_PIPE
+#define ATOM_GEMM_PIPE 1
+#endif
+#ifndef P3_ROUNDS
+#define P3_ROUNDS 1
+#endif
+namespace p3 {
+constexpr int BM = 256, BN = 256, BK = 32, WM = 4, WN = 4, NT = 64 * WM * WN;
+constexpr int TM = BM / (16 * WM), TN = BN / (16 * WN);
+constexpr int OPB = BM * BK * 2;  // bytes of one operand tile in one stage
+
+typedef short v4s __attribute__((ext_vector_type(4)));
+#define ATOM_LDS(p) ((__attribute__((address_space(3))) void*)(p))
+#define ATOM_GLB(p) ((__attribute__((address_space(1))) void*)(p))
+
+// One 16-byte direct global-to-LDS load per lane: lane i of the wave writes
+// LDS bytes lds + 16 i.  Issued as inline assembly so that the compiler does
+// not track these LDS writes (its conservative tracking drains every load in
+// flight before LDS reads it cannot attribute to a stage); the kernel orders
+// them itself with wait_loads and the workgroup barrier.
+__device__ __forceinline__ void lds_dma16(const void* gptr, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(gptr), "s"(lds) : "memory");
+}
+
+// Workgroup barrier that is also a compiler barrier for memory accesses.
+// This wave's LDS reads must have completed (lgkmcnt) before it arrives, as
+// the loads issued right after the barrier overwrite the stage they read;
+// unlike __syncthreads it does not drain the direct loads still in flight.
+__device__ __forceinline__ void barrier_only() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Per-thread source of its one 16-byte chunk of an operand tile.
+template <bool KC>
+struct Src {
+  const bf16_t* p;  // address for k0 = 0
+  int64_t kstep;    // elements to advance per k tile
+  __device__ void init(const bf16_t* X, int64_t ld, int r0, int Rlim, int tid) {
+    if constexpr (KC) {
+      const int r = tid >> 2, slot = tid & 3;
+      const int c = slot ^ ((r >> 1) & 3);
+      const int rr = min(r0 + r, Rlim - 1);
+      p = X + static_cast<int64_t>(rr) * ld + c * 8;
+      kstep = BK;
+    } else {
+      const int k = tid >> 5, slot = tid & 31;
+      const int c = slot ^ (2 * (k & 3));
+      const int m = min(r0 + c * 8, Rlim - 8);
+      p = X + static_cast<int64_t>(k) * ld + m;
+      kstep = static_cast<int64_t>(BK) * ld;
+    }
+  }
+  __device__ __forceinline__ void load(uint8_t* stage, int kt, int w) const {
+    const uint32_t lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(ATOM_LDS(stage))) + w * 1024;
+    lds_dma16(p + kt * kstep, __builtin_amdgcn_readfirstlane(lds));
+  }
+};
+
+// Fragment (16 rows x 32 k) of tile rows row0..row0+15 from a stage.
+template <bool KC>
+__device__ __forceinline__ void frag(Frag<bf16_t>& f, const uint8_t* st, int row0, int lane) {
+  const int r = lane & 15, g = lane >> 4;
+  if constexpr (KC) {
+    const int row = row0 + r;
+    f.v = *reinterpret_cast<const uint4*>(st + row * 64 + 16 * (g ^ ((row >> 1) & 3)));
+  } else {
+    uint32_t w[4];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int k = 8 * g + 4 * h + (r >> 2);
+      const int m = row0 + 4 * (r & 3);
+      const int off = k * 512 + 16 * ((m >> 3) ^ (2 * (k & 3))) + 8 * (r & 1);
+      const v4s v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) v4s*)(const_cast<uint8_t*>(st) + off));
+      w[2 * h] = static_cast<uint32_t>(static_cast<uint16_t>(v[0])) | (static_cast<uint32_t>(static_cast<uint16_t>(v[1])) << 16);
+      w[2 * h + 1] = static_cast<uint32_t>(static_cast<uint16_t>(v[2])) | (static_cast<uint32_t>(static_cast<uint16_t>(v[3])) << 16);
+    }
+    f.v = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
+// Wait until at most n of this thread's loads are outstanding (n even, <= 4).
+__device__ __forceinline__ void wait_loads(int n) {
+  if (n >= 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+  else if (n >= 2) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
+  else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+}  // namespace p3
+
+template <bool AKC, bool BKC, int EPI>
+__global__ void __launch_bounds__(p3::NT) gemm_p3_kernel(GemmArgs g) {
+  using namespace p3;
+  __shared__ __attribute__((aligned(1024))) uint8_t sa0[OPB], sa1[OPB], sa2[OPB], sa3[OPB];
+  __shared__ __attribute__((aligned(1024))) uint8_t sb0[OPB], sb1[OPB], sb2[OPB], sb3[OPB];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int wm = w / WN, wn = w % WN;
+
+  const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
+  const int total = tiles_m * tiles_n;
+  int pid = blockIdx.x;
+  if ((total & 7) == 0) pid = (pid & 7) * (total >> 3) + (pid >> 3);
+  constexpr int GROUP = 8;
+  const int per_group = GROUP * tiles_n;
+  const int first_m = (pid / per_group) * GROUP;
+  const int gsize = min(tiles_m - first_m, GROUP);
+  const int pid_m = first_m + (pid % per_group) % gsize;
+  const int pid_n = (pid % per_group) / gsize;
+  const int m0 = pid_m * BM, n0 = pid_n * BN;
+
+  Src<AKC> sra;
+  Src<BKC> srb;
+  sra.init(static_cast<const bf16_t*>(g.A), g.lda, m0, g.M, tid);
+  srb.init(static_cast<const bf16_t*>(g.B), g.ldb, n0, g.N, tid);
+  const int nk = g.K / BK;
+
+  f32x4_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  auto stage_a = [&](int s) -> uint8_t* { return s == 0 ? sa0 : s == 1 ? sa1 : s == 2 ? sa2 : sa3; };
+  auto stage_b = [&](int s) -> uint8_t* { return s == 0 ? sb0 : s == 1 ? sb1 : s == 2 ? sb2 : sb3; };
+
+  // prologue: tiles 0, 1, 2
+#pragma unroll
+  for (int s = 0; s < 3; ++s)
+    if (s < nk) {
+      sra.load(stage_a(s), s, w);
+      srb.load(stage_b(s), s, w);
+    }
+
+  auto body = [&](auto S_, int t) {
+    constexpr int S = decltype(S_)::value;
+    // loads issued for tiles t+1 .. min(t+2, nk-1) may stay in flight
+    wait_loads(2 * (min(t + 2, nk - 1) - t));
+    barrier_only();
+    if (t + 3 < nk) {
+      sra.load(stage_a((S + 3) & 3), t + 3, w);
+      srb.load(stage_b((S + 3) & 3), t + 3, w);
+    }
+    const uint8_t* as = stage_a(S);
+    const uint8_t* bs = stage_b(S);
+    Frag<bf16_t> fa[TM], fb[TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i) frag<AKC>(fa[i], as, wm * TM * 16 + i * 16, lane);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) frag<BKC>(fb[j], bs, wn * TN * 16 + j * 16, lane);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) mfma16(acc[i][j], fb[j], fa[i]);
+  };
+  // four stages per loop iteration, so every stage index is a constant
+  for (int t = 0; t < nk; t += 4 * P3_ROUNDS) {
+#pragma unroll
+    for (int r = 0; r < P3_ROUNDS; ++r) {
+      const int tr = t + 4 * r;
+      if (tr < nk) body(std::integral_constant<int, 0>{}, tr);
+      if (tr + 1 < nk) body(std::integral_constant<int, 1>{}, tr + 1);
+      if (tr + 2 < nk) body(std::integral_constant<int, 2>{}, tr + 2);
+      if (tr + 3 < nk) body(std::integral_constant<int, 3>{}, tr + 3);
+    }
+  }
+
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // every direct load has landed
+  // acc[i][j][r] = C[m][nb + r]
+  const bool ld_vec = (g.ldc & 3) == 0;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int m = m0 + (wm * TM + i) * 16 + lr;
+    if (m >= g.M) continue;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int nb = n0 + (wn * TN + j) * 16 + lg * 4;
+      if (nb >= g.N) continue;
+      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      epilogue4<bf16_t, EPI>(g, m, nb, v, ld_vec);
+    }
+  }
+}
+
+
+// The pipelined kernel applies to bf16 problems with at least one 256x256
+// tile per CU, k a multiple of 32, and (for clamped edge rows) M and N
+// multiples of 8 with 16-byte aligned rows.
+bool p3_applies(const GemmArgs& g) {
+  if (!ATOM_GEMM_PIPE) return false;
+  const int tiles = ((g.M + p3::BM - 1) / p3::BM) * ((g.N + p3::BN - 1) / p3::BN);
+  return tiles >= 256 && g.K % p3::BK == 0 && g.K > 0 && g.M % 8 == 0 && g.N % 8 == 0 && g.lda % 8 == 0 &&
+         g.ldb % 8 == 0 && g.M >= 8 && g.N >= 8;
+}
+
+template <bool AKC, bool BKC>
+hipError_t launch_p3(const GemmArgs& g, int epi, hipStream_t s) {
+  const int tiles = ((g.M + p3::BM - 1) / p3::BM) * ((g.N + p3::BN - 1) / p3::BN);
+  dim3 grid(tiles), block(p3::NT);
+  switch (epi) {
+#define ATOM_CASE(E) \
+  case E: hipLaunchKernelGGL((gemm_p3_kernel<AKC, BKC, E>), grid, block, 0, s, g); break;
+    ATOM_CASE(EPI_STORE)
+    ATOM_CASE(EPI_STORE_F32)
+    ATOM_CASE(EPI_ACC_F32)
+    ATOM_CASE(EPI_BIAS)
+    ATOM_CASE(EPI_BIAS_GELU)
+    ATOM_CASE(EPI_BIAS_RESID)
+    ATOM_CASE(EPI_GELU_BWD)
+#undef ATOM_CASE
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 // Tile configuration and split count for a problem: the large tile when it
 // gives at least one workgroup per CU, else the 128x128 tile; a split over k
 // when even that leaves the CUs idle and k is long (weight gradients of
@@ -449,6 +685,9 @@ hipError_t launch_cfg(const GemmArgs& g, int epi, int splits, hipStream_t s) {
 template <typename T, bool AKC, bool BKC>
 hipError_t launch_t(const GemmArgs& g, int epi, hipStream_t s) {
   constexpr int CUS = 256;
+  if constexpr (sizeof(T) == 2) {
+    if (p3_applies(g)) return launch_p3<AKC, BKC>(g, epi, s);
+  }
   const int tiles_big = ((g.M + Big::BM - 1) / Big::BM) * ((g.N + Big::BN - 1) / Big::BN);
   if (tiles_big >= CUS) return launch_cfg<T, AKC, BKC, Big>(g, epi, 1, s);
   const int tiles = ((g.M + Small::BM - 1) / Small::BM) * ((g.N + Small::BN - 1) / Small::BN);

@@ -112,6 +112,44 @@ def test_gemm_large_tile_path(akc, bkc):
     assert err < 1e-4, err
 
 
+@pytest.mark.parametrize("akc,bkc", [(1, 1), (1, 0), (0, 0), (0, 1)])
+@pytest.mark.parametrize("epi", [A.ATOM_EPI_STORE, A.ATOM_EPI_STORE_F32, A.ATOM_EPI_BIAS_GELU, A.ATOM_EPI_BIAS_RESID])
+def test_gemm_pipelined_path(akc, bkc, epi):
+    """bf16 problems with >= 256 tiles of 256x256 and k a multiple of 32 take the
+    four-stage direct-to-LDS kernel; M and N end in partial tiles (ragged by 8
+    and 24 rows) whose loads are clamped to the last valid rows."""
+    M, N, K = 4104, 4120, 352
+    r = U.rng(akc + 2 * bkc + 4 * epi)
+    a_shape = (M, K) if akc else (K, M)
+    b_shape = (N, K) if bkc else (K, N)
+    Am = U.rep(r.standard_normal(a_shape), "bf16")
+    Bm = U.rep(r.standard_normal(b_shape), "bf16")
+    bias = U.rep(r.standard_normal(N), "bf16")
+    resid = r.standard_normal((M, N)).astype(np.float32)
+    dA, dB, dbias, dres = U.dev(Am, "bf16"), U.dev(Bm, "bf16"), U.dev(bias, "bf16"), U.dev_f32(resid)
+    out_f32 = epi in (A.ATOM_EPI_STORE_F32, A.ATOM_EPI_BIAS_RESID)
+    dC = U.empty((M, N), "f32" if out_f32 else "bf16")
+    daux = U.empty((M, N), "bf16")
+    A.atom_k_gemm(A.ATOM_BF16, akc, bkc, epi, M, N, K, U.ptr(dA), a_shape[1], U.ptr(dB), b_shape[1], U.ptr(dC), N,
+                  U.ptr(dbias), U.ptr(dres), U.ptr(daux), N, stream())
+    U.sync()
+    pick = np.sort(np.unique(np.concatenate([U.rng(7).choice(M, 40, replace=False), [M - 9, M - 1]])))
+    acc = (Am if akc else Am.T)[pick].astype(np.float64) @ (Bm.T if bkc else Bm).astype(np.float64)
+    got = U.host(dC)[pick]
+    if epi == A.ATOM_EPI_BIAS_GELU:
+        u = acc + bias
+        assert U.rel_err(U.host(daux)[pick], u) < 8e-3
+        ref = gpt.gelu(U.rep(u, "bf16").astype(np.float64))
+    elif epi == A.ATOM_EPI_BIAS_RESID:
+        ref = resid[pick] + acc + bias
+    else:
+        ref = acc
+    tol = 1e-4 if out_f32 else 8e-3
+    assert U.rel_err(got, ref) < tol
+    # the last columns (a partial tile) too
+    assert U.rel_err(got[:, -24:], ref[:, -24:]) < tol
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_gemm_split_k_is_exact_and_deterministic(dtype):
     M, N, K = 256, 392, 8192  # few output tiles, long k: splits over k
