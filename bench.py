@@ -142,6 +142,9 @@ def main():
     ap.add_argument("--budget-gb", type=float, default=None, help="device budget (default: the config's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sequential", action="store_true", help="one atom_step call per step (no cross-step overlap)")
+    ap.add_argument("--measured-plan", action="store_true",
+                    help="profile every node on the GPU (atom_profile_nodes) and plan the timed steps with those "
+                         "costs instead of the analytic ones")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="run one plain device copy of BYTES before the timed steps (calibrates HBM byte counters)")
     args = ap.parse_args()
@@ -174,6 +177,32 @@ def main():
     log(f"host model filled ({time.time() - t0:.1f} s)")
     n_batches = max(args.steps, args.warmup, 1)
     tokens = np.stack([synthetic.gen_tokens(cfg, seed=synthetic.TOKEN_SEED + i) for i in range(n_batches)])
+
+    plan_info = {"costs": "analytic", "pred_step_ms_analytic": round(plan.pred_step_s * 1e3, 1)}
+    if args.measured_plan:
+        c = A.make_config(cfg)
+        costs = A.atom_profile_nodes(sess.ctx, c, tokens[0])
+        blk = costs[1]
+        plan_info["node_costs_ms"] = {
+            "embed": [round(costs[0].t_load * 1e3, 3), round(costs[0].t_fwd * 1e3, 3), round(costs[0].t_bwd * 1e3, 3)],
+            "block": [round(blk.t_load * 1e3, 3), round(blk.t_fwd * 1e3, 3), round(blk.t_bwd * 1e3, 3)],
+            "head": [round(costs[-1].t_load * 1e3, 3), round(costs[-1].t_fwd * 1e3, 3), 0.0],
+            "order": "t_load, t_fwd, t_bwd per node (block: the first block)",
+        }
+        mplan = A.atom_plan_partition(c, budget, costs)
+        plan_info.update(costs="measured", pred_step_ms_measured=round(mplan.pred_step_s * 1e3, 1),
+                         analytic_groups=plan.n_groups, analytic_slots=plan.n_slots)
+        log(f"measured costs: block load {blk.t_load * 1e3:.2f} ms, fwd {blk.t_fwd * 1e3:.2f} ms, "
+            f"bwd {blk.t_bwd * 1e3:.2f} ms; plan {mplan.n_groups} groups, {mplan.n_slots} slots, "
+            f"predicted {mplan.pred_step_s * 1e3:.1f} ms")
+        if mplan.groups() != plan.groups() or mplan.n_slots != plan.n_slots:
+            sess.close()
+            del sess
+            sess = Session(cfg, plan=mplan)
+            sess.load_weights()
+        else:
+            sess.zero_grads()
+        plan = mplan
 
     link_bytes = min(1 << 30, plan.n_slots * plan.slot_bytes // 2)
     h2d_gbs, d2h_gbs, bidir_gbs = A.atom_link_bench(sess.ctx, link_bytes, 4)
@@ -297,7 +326,8 @@ def main():
             "host_accum_ms": round(st.host_accum_s * 1e3, 2),
         },
         "plan": {"groups": plan.n_groups, "slots": plan.n_slots, "slot_mb": round(plan.slot_bytes / 1e6, 1),
-                 "arena_gb": round(plan.arena_bytes / 1e9, 3), "pred_step_ms": round(plan.pred_step_s * 1e3, 1)},
+                 "arena_gb": round(plan.arena_bytes / 1e9, 3), "pred_step_ms": round(plan.pred_step_s * 1e3, 1),
+                 **plan_info},
         "loss": losses[-1],
     }
     sess.close()

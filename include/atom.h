@@ -238,6 +238,18 @@ int atom_step(atom_ctx* ctx, const int32_t* tokens, float* loss_out);
  * (ATOM_EINVAL; nothing is changed).  Synchronous. */
 int atom_steps(atom_ctx* ctx, const int32_t* tokens, int32_t n_steps, float* losses);
 
+/* Measured node costs for the planner (the per-layer profile of Section
+ * III-D: loading time t^u, forward time t^f, backward time t^b, plus the
+ * time to store a node's gradients): each node's weights copied alone to the
+ * device and its gradients back on the step's DMA engines (best of three),
+ * and the kernel time of each node's forward and backward (per micro-batch,
+ * HIP events on the compute stream) in a step of the context's plan on
+ * `tokens` (host int32 [accum][batch][seq_len + 1]) that follows one
+ * untimed step on the same tokens.  Both steps' gradients are added to the
+ * accumulators like atom_step's.  out: n = n_layer + 2
+ * entries; pass them to atom_plan_partition.  Synchronous. */
+int atom_profile_nodes(atom_ctx* ctx, const int32_t* tokens, atom_node_cost* out, int32_t n);
+
 /* Per-step counters of the last atom_step / atom_steps call (bytes and
  * swap counts summed over its steps; times per step). */
 typedef struct atom_stats {

@@ -97,6 +97,7 @@ _SIGS = {
     "atom_probe_gemm": (ctypes.c_int, [P, I32, I32, I32]),
     "atom_probe_read": (ctypes.c_int, [P, P, P, P, P]),
     "atom_link_bench": (ctypes.c_int, [P, U64, I32, P, P, P]),
+    "atom_profile_nodes": (ctypes.c_int, [P, P, P, I32]),
     "atom_last_error": (ctypes.c_char_p, [P]),
     "atom_k_gemm": (ctypes.c_int, [ctypes.c_int] * 7 + [P, I64, P, I64, P, I64, P, P, P, I64, P, U64, P]),
     "atom_k_layernorm_fwd": (ctypes.c_int, [ctypes.c_int, P, P, P, P, P, P, I64, ctypes.c_int, P]),
@@ -324,6 +325,15 @@ def atom_probe_read(ctx):
     by = ctypes.c_double()
     _check(lib().atom_probe_read(ctx, _ref(n), _ref(sec), _ref(fl), _ref(by)), ctx)
     return n.value, sec.value, fl.value, by.value
+
+
+def atom_profile_nodes(ctx, c: atom_config, tokens):
+    """Measured node costs (ctypes array of atom_node_cost) from one step on `tokens`."""
+    n = c.n_layer + 2
+    out = (atom_node_cost * n)()
+    t, p = _tokens_ptr(tokens)
+    _check(lib().atom_profile_nodes(ctx, p, out, n), ctx)
+    return out
 
 
 def atom_link_bench(ctx, nbytes: int, iters: int):

@@ -217,6 +217,11 @@ struct atom_ctx {
   int64_t probe_launches = 0;
   double probe_seconds = 0, probe_flops = 0, probe_bytes = 0;
 
+  // node profile (atom_profile_nodes): events around each node's forward
+  // and backward, per micro-batch
+  bool profiling = false;
+  std::vector<hipEvent_t> prof_ev;  // [node][micro][fwd, bwd][begin, end]
+
   atom_stats stats{};
   std::string err;
 };
@@ -938,10 +943,13 @@ int fwd_impl(atom_ctx* c, int node, int micro) {
       c->ck_wait[e] = 0;
     }
   }
+  const size_t pe = (static_cast<size_t>(node) * c->C + micro) * 4;
+  if (c->profiling) HIPCHK(c, hipEventRecord(c->prof_ev[pe], c->cs));
   if (node == 0) st = embed_forward(c, micro);
   else if (node <= c->L) st = block_forward(c, node, micro, false);
   else st = head_forward_backward(c, node, micro);
   if (st != ATOM_OK) return st;
+  if (c->profiling) HIPCHK(c, hipEventRecord(c->prof_ev[pe + 1], c->cs));
   if (c->ck_host) {
     if (node > 0 && (st = ckpt_used(c, ck_entry(c, node - 1, micro))) != ATOM_OK) return st;
     if (node <= c->L && (st = ckpt_used(c, ck_entry(c, node, micro))) != ATOM_OK) return st;
@@ -961,8 +969,11 @@ int bwd_impl(atom_ctx* c, int node, int micro) {
   int st = prepare_group(c, node, true);
   if (st != ATOM_OK) return st;
   if (c->ck_host && node > 0 && (st = ckpt_ready(c, node - 1, micro)) != ATOM_OK) return st;
+  const size_t pe = (static_cast<size_t>(node) * c->C + micro) * 4 + 2;
+  if (c->profiling) HIPCHK(c, hipEventRecord(c->prof_ev[pe], c->cs));
   st = node == 0 ? embed_backward(c, micro) : block_backward(c, node, micro);
   if (st != ATOM_OK) return st;
+  if (c->profiling) HIPCHK(c, hipEventRecord(c->prof_ev[pe + 1], c->cs));
   if (c->ck_host && node > 0 && (st = ckpt_used(c, ck_entry(c, node - 1, micro))) != ATOM_OK) return st;
   c->bwd_done[par][k] = 1;
   return finish_group_use(c, node);
@@ -1333,7 +1344,7 @@ void atom_ctx_destroy(atom_ctx* c) {
     c->acc_cv.notify_all();
     c->acc_thread.join();
   }
-  for (auto* v : {&c->ev_lastuse, &c->ev_gready, &c->probe_ev, &c->ev_ckw, &c->ev_cku})
+  for (auto* v : {&c->ev_lastuse, &c->ev_gready, &c->probe_ev, &c->ev_ckw, &c->ev_cku, &c->prof_ev})
     for (auto e : *v)
       if (e) (void)hipEventDestroy(e);
   for (auto e : c->ev_tok)
@@ -1490,6 +1501,65 @@ int atom_link_bench(atom_ctx* c, uint64_t bytes, int32_t iters, double* h2d, dou
   if (h2d) *h2d = gb / tu;
   if (d2h) *d2h = gb / td;
   if (bidir) *bidir = 2.0 * gb / tb;
+  return ATOM_OK;
+}
+
+int atom_profile_nodes(atom_ctx* c, const int32_t* tokens, atom_node_cost* out, int32_t n) {
+  if (!c || !tokens || !out || n != c->L + 2) return fail(c, ATOM_EINVAL, "bad argument");
+  int st = sync_all(c);
+  if (st != ATOM_OK) return st;
+  // copy times of each node alone on the step's DMA engines (best of three)
+  uint8_t* dev = A(c, c->lay.wslots);
+  for (int i = 0; i < n; ++i) {
+    double best_in = 1e30, best_out = 1e30;
+    for (int rep = 0; rep < 3; ++rep) {
+      auto t0 = std::chrono::steady_clock::now();
+      std::string e = c->dma_in.copy(dev, c->h_w + c->node_off[i], c->node_bytes[i]);
+      auto t1 = std::chrono::steady_clock::now();
+      if (e.empty()) e = c->dma.copy(c->h_g + c->node_off[i], dev, c->node_bytes[i]);
+      auto t2 = std::chrono::steady_clock::now();
+      if (!e.empty()) return fail(c, ATOM_EHIP, e);
+      best_in = std::min(best_in, std::chrono::duration<double>(t1 - t0).count());
+      best_out = std::min(best_out, std::chrono::duration<double>(t2 - t1).count());
+    }
+    out[i].weight_bytes = c->node_bytes[i];
+    out[i].t_load = best_in;
+    out[i].t_store = best_out;
+  }
+  std::fill(c->slot_owner.begin(), c->slot_owner.end(), -1);
+  drop_residency(c);
+  // kernel times of each node in one step of the context's plan
+  const size_t ne = static_cast<size_t>(n) * c->C * 4;
+  if (c->prof_ev.size() != ne) {
+    for (auto e : c->prof_ev)
+      if (e) (void)hipEventDestroy(e);
+    c->prof_ev.assign(ne, nullptr);
+    for (auto& e : c->prof_ev) HIPCHK(c, hipEventCreate(&e));
+  }
+  // one step to warm up (the first launch of a kernel loads its code), then
+  // the timed one
+  st = run_steps(c, tokens, 1, nullptr);
+  if (st != ATOM_OK) return st;
+  c->profiling = true;
+  c->stats = atom_stats{};
+  st = run_steps(c, tokens, 1, nullptr);
+  c->profiling = false;
+  if (st != ATOM_OK) return st;
+  for (int i = 0; i < n; ++i) {
+    double f = 0, b = 0;
+    for (int m = 0; m < c->C; ++m) {
+      const size_t pe = (static_cast<size_t>(i) * c->C + m) * 4;
+      float ms = 0.f;
+      HIPCHK(c, hipEventElapsedTime(&ms, c->prof_ev[pe], c->prof_ev[pe + 1]));
+      f += ms * 1e-3;
+      if (i <= c->L) {
+        HIPCHK(c, hipEventElapsedTime(&ms, c->prof_ev[pe + 2], c->prof_ev[pe + 3]));
+        b += ms * 1e-3;
+      }
+    }
+    out[i].t_fwd = f / c->C;
+    out[i].t_bwd = b / c->C;
+  }
   return ATOM_OK;
 }
 

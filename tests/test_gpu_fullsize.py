@@ -1,4 +1,4 @@
-"""Whole-step parity at the full widths of the GPT-3 6.7B and 13B steps.
+"""Whole-step parity at the full widths of the GPT-3 Small, XL, 6.7B and 13B steps.
 
 One decoder block (n_layer = 1) with every other size of the configuration
 (d_model, heads, MLP width, vocabulary 50257, batch x 2048 tokens): the
@@ -24,7 +24,7 @@ pytestmark = pytest.mark.gpu
 TOL = 2e-2
 
 
-@pytest.mark.parametrize("name", ["6.7b", "13b"])
+@pytest.mark.parametrize("name", ["small", "xl", "6.7b", "13b"])
 def test_full_width_block_matches_oracle(name):
     cfg = synthetic.CONFIGS[name].with_(n_layer=1)
     t0 = time.time()

@@ -205,3 +205,30 @@ def test_arena_is_the_device_budget():
         s.step(synthetic.gen_tokens(cfg))
         t.cuda.synchronize()
         assert t.cuda.max_memory_allocated() - base <= held + (4 << 20)
+
+
+def test_measured_costs_plan_gives_same_step():
+    """Node costs measured on the GPU (the per-layer profile the planner
+    consumes) are positive, loading time grows with bytes, and a plan made from
+    them runs the step bitwise like the analytic plan (a plan moves data, it
+    changes no arithmetic)."""
+    cfg = TINY.with_(n_layer=4, dtype="bf16")
+    tok = synthetic.gen_tokens(cfg)
+    c = A.make_config(cfg)
+    with Session(cfg, plan=swapped_plan(cfg)) as s:
+        s.load_weights()
+        costs = A.atom_profile_nodes(s.ctx, c, tok)
+    n = cfg.n_nodes
+    assert len(costs) == n
+    for i, x in enumerate(costs):
+        assert x.weight_bytes > 0 and x.t_load > 0 and x.t_store > 0 and x.t_fwd > 0
+        assert (x.t_bwd > 0) == (i <= cfg.n_layer)
+    budget = A.atom_reserve_bytes(c) + 8 * costs[1].weight_bytes
+    measured = A.atom_plan_partition(c, budget, costs)
+    analytic = A.atom_plan_partition(c, budget)
+    l1, g1, _, _ = run_step(cfg, plan=measured, tokens=tok)
+    l2, g2, _, _ = run_step(cfg, plan=analytic, tokens=tok)
+    assert l1 == l2
+    for node in range(n):
+        for name in g1[node]:
+            assert np.array_equal(g1[node][name], g2[node][name]), (node, name)
