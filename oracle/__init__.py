@@ -9,6 +9,7 @@ seeded inputs and holds none of the method's arithmetic.
 
 * oracle.gpt   - fp64 GPT forward and backward (Section III-B model, Table II
                  shapes), the result every swap schedule must reproduce.
+* oracle.adamw - AdamW, the host optimizer step after a global batch.
 * oracle.plan  - brute-force enumeration of contiguous partitions of the layer
                  chain under the memory and overlap constraints of Algorithm 1
                  (Section III-D), with the selection rule.
