@@ -142,6 +142,9 @@ def main():
     ap.add_argument("--budget-gb", type=float, default=None, help="device budget (default: the config's)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sequential", action="store_true", help="one atom_step call per step (no cross-step overlap)")
+    ap.add_argument("--optimizer", action="store_true",
+                    help="after the timed global batch, run the host AdamW step once (timed on its own, "
+                         "not part of the step throughput, as in the paper)")
     ap.add_argument("--measured-plan", action="store_true",
                     help="profile every node on the GPU (atom_profile_nodes) and plan the timed steps with those "
                          "costs instead of the analytic ones")
@@ -330,6 +333,18 @@ def main():
                  **plan_info},
         "loss": losses[-1],
     }
+    if args.optimizer:
+        t0 = time.perf_counter()
+        A.atom_optimizer_init(sess.ctx)
+        t_init = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        A.atom_optimizer_step(sess.ctx, 1e-4, 1.0 / args.steps, 1)
+        t_opt = time.perf_counter() - t0
+        n_par = synthetic.param_count(cfg)
+        result["optimizer"] = {"kind": "host AdamW (fp32 master, moments), once per global batch",
+                               "init_s": round(t_init, 3), "step_s": round(t_opt, 3),
+                               "params": n_par, "host_gbs": round(n_par * 34 / t_opt / 1e9, 1)}
+        log(f"host AdamW over {n_par / 1e9:.2f} B parameters: {t_opt:.2f} s (init {t_init:.2f} s)")
     sess.close()
     if not args.no_cpu_baseline:
         log("timing the oracle on the host (cpu_baseline)")

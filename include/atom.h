@@ -238,6 +238,25 @@ int atom_step(atom_ctx* ctx, const int32_t* tokens, float* loss_out);
  * (ATOM_EINVAL; nothing is changed).  Synchronous. */
 int atom_steps(atom_ctx* ctx, const int32_t* tokens, int32_t n_steps, float* losses);
 
+/* Host optimizer (Section V-B: AdamW on the host CPUs once a global batch
+ * is complete, learning rate 1e-4 after a linear warm-up, betas 0.9 and
+ * 0.999).  atom_optimizer_init allocates fp32 master weights (copied from
+ * the host model) and the two moments (zero), 12 bytes per parameter of
+ * pageable memory.  atom_optimizer_step waits for all work, then for every
+ * parameter: g = grad_scale * accumulator (e.g. 1 / steps of the global
+ * batch), m = beta1 m + (1 - beta1) g, v = beta2 v + (1 - beta2) g^2,
+ * p = p (1 - lr wd) - lr (m / (1 - beta1^step)) / (sqrt(v / (1 - beta2^step))
+ * + eps), with weight decay only on the linear layers' weight matrices
+ * (w_qkv, w_o, w_fc, w_pr, w_head); it writes the working-dtype weights
+ * (bf16 rounded to nearest even) into the host model and zeroes the
+ * accumulators.  fp32 arithmetic on the host thread pool.  step >= 1 counts
+ * optimizer steps.  ATOM_ESTATE before atom_optimizer_init. */
+typedef struct atom_adamw {
+  float lr, beta1, beta2, eps, weight_decay;
+} atom_adamw;
+int atom_optimizer_init(atom_ctx* ctx);
+int atom_optimizer_step(atom_ctx* ctx, const atom_adamw* hp, float grad_scale, int32_t step);
+
 /* Measured node costs for the planner (the per-layer profile of Section
  * III-D: loading time t^u, forward time t^f, backward time t^b, plus the
  * time to store a node's gradients): each node's weights copied alone to the

@@ -98,6 +98,8 @@ _SIGS = {
     "atom_probe_read": (ctypes.c_int, [P, P, P, P, P]),
     "atom_link_bench": (ctypes.c_int, [P, U64, I32, P, P, P]),
     "atom_profile_nodes": (ctypes.c_int, [P, P, P, I32]),
+    "atom_optimizer_init": (ctypes.c_int, [P]),
+    "atom_optimizer_step": (ctypes.c_int, [P, P, ctypes.c_float, I32]),
     "atom_last_error": (ctypes.c_char_p, [P]),
     "atom_k_gemm": (ctypes.c_int, [ctypes.c_int] * 7 + [P, I64, P, I64, P, I64, P, P, P, I64, P, U64, P]),
     "atom_k_layernorm_fwd": (ctypes.c_int, [ctypes.c_int, P, P, P, P, P, P, I64, ctypes.c_int, P]),
@@ -334,6 +336,19 @@ def atom_profile_nodes(ctx, c: atom_config, tokens):
     t, p = _tokens_ptr(tokens)
     _check(lib().atom_profile_nodes(ctx, p, out, n), ctx)
     return out
+
+
+class atom_adamw(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_float) for n in ("lr", "beta1", "beta2", "eps", "weight_decay")]
+
+
+def atom_optimizer_init(ctx):
+    _check(lib().atom_optimizer_init(ctx), ctx)
+
+
+def atom_optimizer_step(ctx, lr, grad_scale, step, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0):
+    hp = atom_adamw(lr, beta1, beta2, eps, weight_decay)
+    _check(lib().atom_optimizer_step(ctx, _ref(hp), grad_scale, step), ctx)
 
 
 def atom_link_bench(ctx, nbytes: int, iters: int):

@@ -49,6 +49,7 @@
 
 #include <algorithm>
 #include <chrono>
+#include <cmath>
 #include <condition_variable>
 #include <deque>
 #include <functional>
@@ -216,6 +217,12 @@ struct atom_ctx {
   int probe_pending = 0;
   int64_t probe_launches = 0;
   double probe_seconds = 0, probe_flops = 0, probe_bytes = 0;
+
+  // host optimizer (atom_optimizer_init / atom_optimizer_step): fp32 master
+  // weights and the two AdamW moments, element-indexed like h_w (pageable)
+  float* h_master = nullptr;
+  float* h_m = nullptr;
+  float* h_v = nullptr;
 
   // node profile (atom_profile_nodes): events around each node's forward
   // and backward, per micro-batch
@@ -1356,6 +1363,9 @@ void atom_ctx_destroy(atom_ctx* c) {
     if (p) (void)hipHostFree(p);
   if (c->h_ck) (void)hipHostFree(c->h_ck);
   free(c->h_acc);
+  free(c->h_master);
+  free(c->h_m);
+  free(c->h_v);
   delete c;
 }
 
@@ -1501,6 +1511,97 @@ int atom_link_bench(atom_ctx* c, uint64_t bytes, int32_t iters, double* h2d, dou
   if (h2d) *h2d = gb / tu;
   if (d2h) *d2h = gb / td;
   if (bidir) *bidir = 2.0 * gb / tb;
+  return ATOM_OK;
+}
+
+int atom_optimizer_init(atom_ctx* c) {
+  if (!c) return ATOM_EINVAL;
+  int st = wait_accum(c);
+  if (st != ATOM_OK) return st;
+  const uint64_t n = c->model_bytes / c->e;
+  float** bufs[] = {&c->h_master, &c->h_m, &c->h_v};
+  for (float** b : bufs)
+    if (!*b && posix_memalign(reinterpret_cast<void**>(b), 4096, n * 4) != 0) {
+      *b = nullptr;
+      return fail(c, ATOM_ENOMEM_HOST, "allocation of the optimizer state failed");
+    }
+  c->pool->run([&](int ti) {
+    const int nt = c->pool->size();
+    const uint64_t lo = n * ti / nt, hi = n * (ti + 1) / nt;
+    for (uint64_t i = lo; i < hi; ++i) {
+      if (c->dt == DT_BF16) {
+        const uint32_t u = static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(c->h_w)[i]) << 16;
+        memcpy(&c->h_master[i], &u, 4);
+      } else {
+        c->h_master[i] = reinterpret_cast<const float*>(c->h_w)[i];
+      }
+    }
+    memset(c->h_m + lo, 0, (hi - lo) * 4);
+    memset(c->h_v + lo, 0, (hi - lo) * 4);
+  });
+  return ATOM_OK;
+}
+
+namespace {
+// fp32 -> bf16 bits, round to nearest even (finite inputs).
+inline uint16_t host_bf16(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  return static_cast<uint16_t>((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+}  // namespace
+
+int atom_optimizer_step(atom_ctx* c, const atom_adamw* hp, float grad_scale, int32_t step) {
+  if (!c || !hp || step < 1) return fail(c, ATOM_EINVAL, "bad optimizer arguments");
+  if (!c->h_master) return fail(c, ATOM_ESTATE, "atom_optimizer_init was not called");
+  int st = sync_all(c);
+  if (st != ATOM_OK) return st;
+  // per-tensor element ranges with their decay flag
+  struct Seg {
+    uint64_t off, n;
+    bool decay;
+  };
+  std::vector<Seg> segs;
+  uint64_t total = 0;
+  for (int node = 0; node <= c->L + 1; ++node)
+    for (const auto& t : c->tens[node]) {
+      const bool decay = t.name == "w_qkv" || t.name == "w_o" || t.name == "w_fc" || t.name == "w_pr" ||
+                         t.name == "w_head";
+      segs.push_back({(c->node_off[node] + t.offset) / c->e, t.bytes / c->e, decay});
+      total += t.bytes / c->e;
+    }
+  const float lr = hp->lr, b1 = hp->beta1, b2 = hp->beta2, eps = hp->eps, wd = hp->weight_decay;
+  // 1 - beta and the bias corrections in double: in fp32 they would lose
+  // most of their digits to cancellation (1 - 0.999^2 keeps about three)
+  const double b1d = b1, b2d = b2;
+  const float c1 = static_cast<float>(1.0 - b1d), c2 = static_cast<float>(1.0 - b2d);
+  const float bc1 = static_cast<float>(1.0 - std::pow(b1d, step));
+  const float bc2 = static_cast<float>(1.0 - std::pow(b2d, step));
+  const bool bf = c->dt == DT_BF16;
+  c->pool->run([&](int ti) {
+    const int nt = c->pool->size();
+    const uint64_t lo = total * ti / nt, hi = total * (ti + 1) / nt;
+    uint64_t pos = 0;
+    for (const Seg& sg : segs) {
+      const uint64_t a = std::max(lo, pos), b = std::min(hi, pos + sg.n);
+      if (a < b) {
+        const float keep = sg.decay ? 1.f - lr * wd : 1.f;
+        for (uint64_t k = sg.off + (a - pos), e = sg.off + (b - pos); k < e; ++k) {
+          const float g = c->h_acc[k] * grad_scale;
+          const float m = b1 * c->h_m[k] + c1 * g;
+          const float v = b2 * c->h_v[k] + c2 * g * g;
+          c->h_m[k] = m;
+          c->h_v[k] = v;
+          const float p = c->h_master[k] * keep - lr * (m / bc1) / (std::sqrt(v / bc2) + eps);
+          c->h_master[k] = p;
+          if (bf) reinterpret_cast<uint16_t*>(c->h_w)[k] = host_bf16(p);
+          else reinterpret_cast<float*>(c->h_w)[k] = p;
+          c->h_acc[k] = 0.f;
+        }
+      }
+      pos += sg.n;
+    }
+  });
   return ATOM_OK;
 }
 

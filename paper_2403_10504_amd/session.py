@@ -74,6 +74,10 @@ class Session:
                 else:
                     v[...] = val.reshape(v.shape)
 
+    def weights(self):
+        """The host model as float32 arrays (list over nodes of {name: array})."""
+        return self.grads(A.WEIGHTS)
+
     def grads(self, which: int = A.GRAD_ACC):
         """Gradients as float32 arrays: accumulators (default) or the last step's."""
         import synthetic
@@ -83,7 +87,7 @@ class Session:
             p = {}
             for name, rows, cols, _, _ in self.layout[node]:
                 v = np.array(self.host_view(node, name, which))
-                if which == A.GRAD_LAST and self.elem == np.uint16:
+                if which != A.GRAD_ACC and self.elem == np.uint16:
                     v = synthetic.bf16_bits_to_f32(v)
                 if name == "w_head":
                     v = v[: self.cfg.vocab]
