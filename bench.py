@@ -42,8 +42,8 @@ HBM_PEAK_GBS = 8000.0
 # --copy-calibration 2147483648`, each scaled by what the counter reads for
 # the plain copy kernel of known size (profiles/gemm_wgrad_6.7b_hbm_traffic.md).
 # Valid only for the kernel sources it was measured on.
-WGRAD_TRAFFIC = {"sources_sha256": "6612382d7d756080aa1d069d2f582b4c5866db5a969373588bf979ec5aff679b",
-                 "bytes_per_launch": 733620730}
+WGRAD_TRAFFIC = {"sources_sha256": "d54ccc3969434e3b117227ca5a9c9a38f5d4c9f3c0f26b6736b43e518413d347",
+                 "bytes_per_launch": 733172971}
 TRAFFIC_SOURCES = ("gemm.hip", "common.h", "launch.h")
 
 

@@ -460,8 +460,9 @@ hipError_t launch_cfg(const GemmArgs& g, int epi, int splits, hipStream_t s) {
 //   k-contiguous operand  [256 rows][32 k]: row r, chunk c at slot c ^ ((r>>1)&3);
 //                         fragments by ds_read_b128.
 //   other operand         [32 k][256 rows]: k row k, chunk c (8 rows) at slot
-//                         c ^ 2(k&3); fragments by two ds_read_b64_tr_b16, each
-//                         transposing a 4 (k) x 16 (rows) block across 16 lanes.
+//                         c ^ tr_swz(k); fragments by two ds_read_b64_tr_b16,
+//                         each transposing a 4 (k) x 16 (rows) block across 16
+//                         lanes.
 // Rows beyond the operand are clamped to its last valid row (or 8-row block),
 // so they read finite data that only reaches output rows or columns that are
 // never stored; k must be a multiple of 32.
@@ -495,6 +496,13 @@ __device__ __forceinline__ void lds_dma16(const void* gptr, uint32_t lds) {
 // unlike __syncthreads it does not drain the direct loads still in flight.
 __device__ __forceinline__ void barrier_only() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
+// Swizzle of the transposed-read layout: a ds_read_b64_tr_b16 serves 32
+// lanes per LDS cycle, i.e. the k rows K0..K0+3 and K0+8..K0+11 of two
+// 16-lane groups; 2 (k & 3) + 8 ((k >> 3) & 1) puts their 16 chunks on
+// distinct banks (measured: no conflicts, against two conflict cycles per
+// read with 2 (k & 3) alone).
+__device__ __forceinline__ int tr_swz(int k) { return 2 * (k & 3) + 8 * ((k >> 3) & 1); }
+
 // Per-thread source of its one 16-byte chunk of an operand tile.
 template <bool KC>
 struct Src {
@@ -509,7 +517,7 @@ struct Src {
       kstep = BK;
     } else {
       const int k = tid >> 5, slot = tid & 31;
-      const int c = slot ^ (2 * (k & 3));
+      const int c = slot ^ tr_swz(k);
       const int m = min(r0 + c * 8, Rlim - 8);
       p = X + static_cast<int64_t>(k) * ld + m;
       kstep = static_cast<int64_t>(BK) * ld;
@@ -521,22 +529,39 @@ struct Src {
   }
 };
 
-// Fragment (16 rows x 32 k) of tile rows row0..row0+15 from a stage.
+// Byte offsets inside a stage of this lane's fragment reads of tile rows
+// row0..row0+15 (one for k-contiguous operands, two transposed reads
+// otherwise); loop-invariant, computed once.
 template <bool KC>
-__device__ __forceinline__ void frag(Frag<bf16_t>& f, const uint8_t* st, int row0, int lane) {
-  const int r = lane & 15, g = lane >> 4;
+struct FragOff {
+  uint32_t o[KC ? 1 : 2];
+  __device__ void init(int row0, int lane) {
+    const int r = lane & 15, g = lane >> 4;
+    if constexpr (KC) {
+      const int row = row0 + r;
+      o[0] = row * 64 + 16 * (g ^ ((row >> 1) & 3));
+    } else {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int k = 8 * g + 4 * h + (r >> 2);
+        const int m = row0 + 4 * (r & 3);
+        o[h] = k * 512 + 16 * ((m >> 3) ^ tr_swz(k)) + 8 * (r & 1);
+      }
+    }
+  }
+};
+
+// Fragment (16 rows x 32 k) of one 16-row tile from a stage.
+template <bool KC>
+__device__ __forceinline__ void frag(Frag<bf16_t>& f, const uint8_t* st, const FragOff<KC>& fo) {
   if constexpr (KC) {
-    const int row = row0 + r;
-    f.v = *reinterpret_cast<const uint4*>(st + row * 64 + 16 * (g ^ ((row >> 1) & 3)));
+    f.v = *reinterpret_cast<const uint4*>(st + fo.o[0]);
   } else {
     uint32_t w[4];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const int k = 8 * g + 4 * h + (r >> 2);
-      const int m = row0 + 4 * (r & 3);
-      const int off = k * 512 + 16 * ((m >> 3) ^ (2 * (k & 3))) + 8 * (r & 1);
       const v4s v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (__attribute__((address_space(3))) v4s*)(const_cast<uint8_t*>(st) + off));
+          (__attribute__((address_space(3))) v4s*)(const_cast<uint8_t*>(st) + fo.o[h]));
       w[2 * h] = static_cast<uint32_t>(static_cast<uint16_t>(v[0])) | (static_cast<uint32_t>(static_cast<uint16_t>(v[1])) << 16);
       w[2 * h + 1] = static_cast<uint32_t>(static_cast<uint16_t>(v[2])) | (static_cast<uint32_t>(static_cast<uint16_t>(v[3])) << 16);
     }
@@ -586,6 +611,13 @@ __global__ void __launch_bounds__(p3::NT) gemm_p3_kernel(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  FragOff<AKC> foa[TM];
+  FragOff<BKC> fob[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) foa[i].init(wm * TM * 16 + i * 16, lane);
+#pragma unroll
+  for (int j = 0; j < TN; ++j) fob[j].init(wn * TN * 16 + j * 16, lane);
+
   auto stage_a = [&](int s) -> uint8_t* { return s == 0 ? sa0 : s == 1 ? sa1 : s == 2 ? sa2 : sa3; };
   auto stage_b = [&](int s) -> uint8_t* { return s == 0 ? sb0 : s == 1 ? sb1 : s == 2 ? sb2 : sb3; };
 
@@ -610,9 +642,9 @@ __global__ void __launch_bounds__(p3::NT) gemm_p3_kernel(GemmArgs g) {
     const uint8_t* bs = stage_b(S);
     Frag<bf16_t> fa[TM], fb[TN];
 #pragma unroll
-    for (int i = 0; i < TM; ++i) frag<AKC>(fa[i], as, wm * TM * 16 + i * 16, lane);
+    for (int i = 0; i < TM; ++i) frag<AKC>(fa[i], as, foa[i]);
 #pragma unroll
-    for (int j = 0; j < TN; ++j) frag<BKC>(fb[j], bs, wn * TN * 16 + j * 16, lane);
+    for (int j = 0; j < TN; ++j) frag<BKC>(fb[j], bs, fob[j]);
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
