@@ -42,9 +42,20 @@ HBM_PEAK_GBS = 8000.0
 # --copy-calibration 2147483648`, each scaled by what the counter reads for
 # the plain copy kernel of known size (profiles/gemm_wgrad_6.7b_hbm_traffic.md).
 # Valid only for the kernel sources it was measured on.
-WGRAD_TRAFFIC = {"sources_sha256": "d54ccc3969434e3b117227ca5a9c9a38f5d4c9f3c0f26b6736b43e518413d347",
-                 "bytes_per_launch": 733172971}
+WGRAD_TRAFFIC = {"sources_sha256": "9b4e31dd5e96e94bafdffd92060dcaaaa19ca035baf37b8934801b3049cf1a8b",
+                 "bytes_per_launch": 743549643}
 TRAFFIC_SOURCES = ("gemm.hip", "common.h", "launch.h")
+
+
+def wgrad_kernel_name(cfg, epi):
+    """The kernel the weight-gradient GEMMs (k = tokens of a micro-batch) launch."""
+    if cfg.dtype != "bf16":
+        return f"gemm_kernel<f32, A not k-contiguous, B not k-contiguous, epilogue {epi}> (weight gradients)"
+    if (cfg.batch * cfg.seq_len) % 128 == 0:
+        return (f"gemm_p4_kernel<A not k-contiguous, B not k-contiguous, epilogue {epi}> (weight gradients; "
+                "four waves of 128x128 with double-buffered fragments, four-stage direct-to-LDS pipeline)")
+    return (f"gemm_p3_kernel<A not k-contiguous, B not k-contiguous, epilogue {epi}> (weight gradients; "
+            "sixteen waves, four-stage direct-to-LDS pipeline)")
 
 
 def kernel_sources_sha256():
@@ -300,10 +311,7 @@ def main():
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": (f"gemm_p3_kernel<A not k-contiguous, B not k-contiguous, epilogue {wgrad_epi}> "
-                       "(weight gradients; four-stage direct-to-LDS pipeline)" if cfg.dtype == "bf16" else
-                       f"gemm_kernel<f32, A not k-contiguous, B not k-contiguous, epilogue {wgrad_epi}> "
-                       "(weight gradients)"),
+            "kernel": wgrad_kernel_name(cfg, wgrad_epi),
             "achieved": round(achieved, 2),
             "peak": peak,
             "unit": "TFLOP/s",

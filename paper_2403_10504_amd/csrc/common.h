@@ -108,12 +108,19 @@ ATOM_DEV float wave_max(float v) {
 }
 
 // GELU, tanh form, and its derivative.
-ATOM_DEV float gelu_f(float u) {
-  const float c = 0.7978845608028654f, a = 0.044715f;
-  return 0.5f * u * (1.f + tanhf(c * (u + a * u * u * u)));
+// GELU, tanh form, through 0.5 (1 + tanh y) = s = 1 / (1 + exp(-2y)) with
+// y = c (u + a u^3): one hardware exp2 and one reciprocal (each within a few
+// units in the last place) instead of a library tanh.  s saturates cleanly:
+// exp2 overflows to inf for y << 0 (s = 0), and goes to 0 for y >> 0 (s = 1).
+ATOM_DEV float gelu_s(float u) {
+  const float c = 0.7978845608028654f, a = 0.044715f, m2log2e = -2.8853900817779268f;  // -2 log2(e)
+  const float y = c * (u + a * u * u * u);
+  return __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(m2log2e * y));
 }
+ATOM_DEV float gelu_f(float u) { return u * gelu_s(u); }
+// d/du [u s] = s + u * 2 s (1 - s) * c (1 + 3 a u^2), since 1 - tanh^2 = 4 s (1 - s).
 ATOM_DEV float gelu_grad_f(float u) {
   const float c = 0.7978845608028654f, a = 0.044715f;
-  float t = tanhf(c * (u + a * u * u * u));
-  return 0.5f * (1.f + t) + 0.5f * u * (1.f - t * t) * c * (1.f + 3.f * a * u * u);
+  const float s = gelu_s(u);
+  return s + 2.f * u * s * (1.f - s) * c * (1.f + 3.f * a * u * u);
 }

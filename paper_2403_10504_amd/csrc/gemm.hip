@@ -487,7 +487,7 @@ typedef short v4s __attribute__((ext_vector_type(4)));
 // flight before LDS reads it cannot attribute to a stage); the kernel orders
 // them itself with wait_loads and the workgroup barrier.
 __device__ __forceinline__ void lds_dma16(const void* gptr, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(gptr), "s"(lds) : "memory");
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(gptr), "s"(lds) : "memory", "m0");
 }
 
 // Workgroup barrier that is also a compiler barrier for memory accesses.
@@ -680,6 +680,165 @@ __global__ void __launch_bounds__(p3::NT) gemm_p3_kernel(GemmArgs g) {
 }
 
 
+// Four-wave variant of the pipelined kernel: the same 256x256 tile, k tile
+// and LDS layouts, but four waves of 128x128 (one per SIMD, accumulators in
+// AGPRs) whose fragment registers are double-buffered, so that the LDS reads
+// of tile t+1 are issued between the MFMAs of tile t instead of after a
+// barrier that every wave of the CU has to reach first.  A stage is free once
+// the barrier that follows the reads of its tile has passed; the loads of
+// tile t+4 go into the stage of tile t, so four tiles are in flight.
+#ifndef ATOM_GEMM_P4
+#define ATOM_GEMM_P4 1
+#endif
+namespace p4 {
+constexpr int BM = 256, BN = 256, BK = 32, WM = 2, WN = 2, NT = 64 * WM * WN;
+constexpr int TM = BM / (16 * WM), TN = BN / (16 * WN);
+constexpr int OPB = BM * BK * 2;
+constexpr int LPT = OPB / (NT * 16);  // direct loads per thread per operand and tile
+
+// Barrier after this wave's LDS reads have completed; the wait is the
+// builtin so that the compiler knows those fragment registers are ready.
+__device__ __forceinline__ void barrier_after_reads() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0), vmcnt and expcnt unconstrained
+  asm volatile("s_barrier" ::: "memory");
+}
+
+// acc += a b with the accumulator pinned to its AGPRs.  The 256 accumulator
+// registers of a wave fill the AGPR file; left to itself the register
+// allocator splits them between AGPRs and VGPRs and copies them around every
+// MFMA.  Issued in program order (volatile); the kernel supplies the wait
+// states between the accumulators' other writes and reads and these MFMAs.
+__device__ __forceinline__ void mfma_agpr(f32x4_t& acc, const Frag<bf16_t>& a, const Frag<bf16_t>& b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0"
+               : "+a"(acc)
+               : "v"(__builtin_bit_cast(bf16x8_t, a.v)), "v"(__builtin_bit_cast(bf16x8_t, b.v)));
+}
+}  // namespace p4
+
+template <bool AKC, bool BKC, int EPI>
+__global__ void __launch_bounds__(p4::NT) __attribute__((amdgpu_waves_per_eu(1, 1))) gemm_p4_kernel(GemmArgs g) {
+  using namespace p4;
+  using p3::Src;
+  using p3::FragOff;
+  __shared__ __attribute__((aligned(1024))) uint8_t sa0[OPB], sa1[OPB], sa2[OPB], sa3[OPB];
+  __shared__ __attribute__((aligned(1024))) uint8_t sb0[OPB], sb1[OPB], sb2[OPB], sb3[OPB];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int wm = w / WN, wn = w % WN;
+
+  const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
+  const int total = tiles_m * tiles_n;
+  int pid = blockIdx.x;
+  if ((total & 7) == 0) pid = (pid & 7) * (total >> 3) + (pid >> 3);
+  constexpr int GROUP = 8;
+  const int per_group = GROUP * tiles_n;
+  const int first_m = (pid / per_group) * GROUP;
+  const int gsize = min(tiles_m - first_m, GROUP);
+  const int pid_m = first_m + (pid % per_group) % gsize;
+  const int pid_n = (pid % per_group) / gsize;
+  const int m0 = pid_m * BM, n0 = pid_n * BN;
+
+  // load q of a thread is the 16-byte chunk q * NT + tid of the tile
+  Src<AKC> sra[LPT];
+  Src<BKC> srb[LPT];
+#pragma unroll
+  for (int q = 0; q < LPT; ++q) {
+    sra[q].init(static_cast<const bf16_t*>(g.A), g.lda, m0, g.M, q * NT + tid);
+    srb[q].init(static_cast<const bf16_t*>(g.B), g.ldb, n0, g.N, q * NT + tid);
+  }
+  const int nk = g.K / BK;
+
+  f32x4_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      asm volatile("" : "+a"(acc[i][j]));
+    }
+  // wait states between the zeroing writes and the first MFMA reading them
+  asm volatile("s_nop 7\n\ts_nop 7");
+
+  FragOff<AKC> foa[TM];
+  FragOff<BKC> fob[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) foa[i].init(wm * TM * 16 + i * 16, lane);
+#pragma unroll
+  for (int j = 0; j < TN; ++j) fob[j].init(wn * TN * 16 + j * 16, lane);
+
+  auto stage_a = [&](int s) -> uint8_t* { return s == 0 ? sa0 : s == 1 ? sa1 : s == 2 ? sa2 : sa3; };
+  auto stage_b = [&](int s) -> uint8_t* { return s == 0 ? sb0 : s == 1 ? sb1 : s == 2 ? sb2 : sb3; };
+  auto load_tile = [&](int s, int kt) {
+#pragma unroll
+    for (int q = 0; q < LPT; ++q) sra[q].load(stage_a(s), kt, q * (NT / 64) + w);
+#pragma unroll
+    for (int q = 0; q < LPT; ++q) srb[q].load(stage_b(s), kt, q * (NT / 64) + w);
+  };
+
+  Frag<bf16_t> fa0[TM], fb0[TN], fa1[TM], fb1[TN];
+  // prologue: tiles 0..3 in flight, fragments of tile 0 in set 0.  Loads
+  // past the last tile repeat it (into stages nobody reads again), so every
+  // iteration has the same loads outstanding; they land before the exit.
+#pragma unroll
+  for (int s = 0; s < 4; ++s) load_tile(s, min(s, nk - 1));
+  asm volatile("s_waitcnt vmcnt(24)" ::: "memory");
+  barrier_after_reads();
+#pragma unroll
+  for (int i = 0; i < TM; ++i) p3::frag<AKC>(fa0[i], stage_a(0), foa[i]);
+#pragma unroll
+  for (int j = 0; j < TN; ++j) p3::frag<BKC>(fb0[j], stage_b(0), fob[j]);
+
+  auto body = [&](auto S_, int t, Frag<bf16_t>(&ca)[TM], Frag<bf16_t>(&cb)[TN], Frag<bf16_t>(&na)[TM],
+                  Frag<bf16_t>(&nb)[TN]) {
+    constexpr int S = decltype(S_)::value;
+    // tile t+1 has landed for every wave, and every wave has read tile t
+    asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+    barrier_after_reads();
+    const int kt = min(t + 4, nk - 1);
+    // per row i: the fragments i of tile t+1 (after the last tile they come
+    // from a stale stage and are never used), one direct load of tile t+4,
+    // then the MFMAs of row i of this tile, which hide the reads' latency
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      p3::frag<AKC>(na[i], stage_a((S + 1) & 3), foa[i]);
+      p3::frag<BKC>(nb[i], stage_b((S + 1) & 3), fob[i]);
+      if (i < LPT) sra[i].load(stage_a(S), kt, i * (NT / 64) + w);
+      else if (i < 2 * LPT) srb[i - LPT].load(stage_b(S), kt, (i - LPT) * (NT / 64) + w);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) mfma_agpr(acc[i][j], cb[j], ca[i]);
+    }
+  };
+  // nk is a multiple of 4: no tile is conditional inside the loop
+  for (int t = 0; t < nk; t += 4) {
+    body(std::integral_constant<int, 0>{}, t, fa0, fb0, fa1, fb1);
+    body(std::integral_constant<int, 1>{}, t + 1, fa1, fb1, fa0, fb0);
+    body(std::integral_constant<int, 2>{}, t + 2, fa0, fb0, fa1, fb1);
+    body(std::integral_constant<int, 3>{}, t + 3, fa1, fb1, fa0, fb0);
+  }
+
+  // every direct load has landed; wait states between the last MFMAs and
+  // the reads of their accumulators
+  asm volatile("s_waitcnt vmcnt(0)\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) asm volatile("" : "+a"(acc[i][j]));
+  const bool ld_vec = (g.ldc & 3) == 0;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int m = m0 + (wm * TM + i) * 16 + lr;
+    if (m >= g.M) continue;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int nb = n0 + (wn * TN + j) * 16 + lg * 4;
+      if (nb >= g.N) continue;
+      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      epilogue4<bf16_t, EPI>(g, m, nb, v, ld_vec);
+    }
+  }
+}
+
+
 // The pipelined kernel applies to bf16 problems with at least one 256x256
 // tile per CU, k a multiple of 32, and (for clamped edge rows) M and N
 // multiples of 8 with 16-byte aligned rows.
@@ -690,21 +849,36 @@ bool p3_applies(const GemmArgs& g) {
          g.ldb % 8 == 0 && g.M >= 8 && g.N >= 8;
 }
 
+// The four-wave kernel takes the plain epilogues (stores, accumulation, bias)
+// when k is a multiple of four k tiles; with one wave per SIMD, the epilogues
+// that read or write a second [M][N] tensor ran faster on sixteen waves.
+bool p4_applies(const GemmArgs& g, int epi) {
+  return ATOM_GEMM_P4 && g.K % (4 * p4::BK) == 0 &&
+         (epi == EPI_STORE || epi == EPI_STORE_F32 || epi == EPI_ACC_F32 || epi == EPI_BIAS);
+}
+
 template <bool AKC, bool BKC>
 hipError_t launch_p3(const GemmArgs& g, int epi, hipStream_t s) {
   const int tiles = ((g.M + p3::BM - 1) / p3::BM) * ((g.N + p3::BN - 1) / p3::BN);
-  dim3 grid(tiles), block(p3::NT);
+  const bool four = p4_applies(g, epi);
+  const dim3 grid(tiles);
   switch (epi) {
-#define ATOM_CASE(E) \
-  case E: hipLaunchKernelGGL((gemm_p3_kernel<AKC, BKC, E>), grid, block, 0, s, g); break;
-    ATOM_CASE(EPI_STORE)
-    ATOM_CASE(EPI_STORE_F32)
-    ATOM_CASE(EPI_ACC_F32)
-    ATOM_CASE(EPI_BIAS)
-    ATOM_CASE(EPI_BIAS_GELU)
-    ATOM_CASE(EPI_BIAS_RESID)
-    ATOM_CASE(EPI_GELU_BWD)
-#undef ATOM_CASE
+#define ATOM_CASE4(E)                                                                             \
+  case E:                                                                                         \
+    if (four) hipLaunchKernelGGL((gemm_p4_kernel<AKC, BKC, E>), grid, dim3(p4::NT), 0, s, g);      \
+    else hipLaunchKernelGGL((gemm_p3_kernel<AKC, BKC, E>), grid, dim3(p3::NT), 0, s, g);           \
+    break;
+#define ATOM_CASE3(E) \
+  case E: hipLaunchKernelGGL((gemm_p3_kernel<AKC, BKC, E>), grid, dim3(p3::NT), 0, s, g); break;
+    ATOM_CASE4(EPI_STORE)
+    ATOM_CASE4(EPI_STORE_F32)
+    ATOM_CASE4(EPI_ACC_F32)
+    ATOM_CASE4(EPI_BIAS)
+    ATOM_CASE3(EPI_BIAS_GELU)
+    ATOM_CASE3(EPI_BIAS_RESID)
+    ATOM_CASE3(EPI_GELU_BWD)
+#undef ATOM_CASE4
+#undef ATOM_CASE3
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -112,24 +112,33 @@ def test_gemm_large_tile_path(akc, bkc):
     assert err < 1e-4, err
 
 
+ALL_EPI = [A.ATOM_EPI_STORE, A.ATOM_EPI_STORE_F32, A.ATOM_EPI_ACC_F32, A.ATOM_EPI_BIAS, A.ATOM_EPI_BIAS_GELU,
+           A.ATOM_EPI_BIAS_RESID, A.ATOM_EPI_GELU_BWD]
+
+
+@pytest.mark.parametrize("K", [352, 384, 128])
 @pytest.mark.parametrize("akc,bkc", [(1, 1), (1, 0), (0, 0), (0, 1)])
-@pytest.mark.parametrize("epi", [A.ATOM_EPI_STORE, A.ATOM_EPI_STORE_F32, A.ATOM_EPI_BIAS_GELU, A.ATOM_EPI_BIAS_RESID])
-def test_gemm_pipelined_path(akc, bkc, epi):
+@pytest.mark.parametrize("epi", ALL_EPI)
+def test_gemm_pipelined_path(akc, bkc, epi, K):
     """bf16 problems with >= 256 tiles of 256x256 and k a multiple of 32 take the
-    four-stage direct-to-LDS kernel; M and N end in partial tiles (ragged by 8
-    and 24 rows) whose loads are clamped to the last valid rows."""
-    M, N, K = 4104, 4120, 352
-    r = U.rng(akc + 2 * bkc + 4 * epi)
+    four-stage direct-to-LDS kernels: sixteen waves for k = 352, and for k a
+    multiple of 128 (384: three loop trips; 128: the prologue's tiles only) the
+    four-wave kernel with the plain epilogues.  M and N end in partial tiles
+    (ragged by 8 and 24 rows) whose loads are clamped to the last valid rows."""
+    M, N = 4104, 4120
+    r = U.rng(akc + 2 * bkc + 4 * epi + K)
     a_shape = (M, K) if akc else (K, M)
     b_shape = (N, K) if bkc else (K, N)
     Am = U.rep(r.standard_normal(a_shape), "bf16")
     Bm = U.rep(r.standard_normal(b_shape), "bf16")
     bias = U.rep(r.standard_normal(N), "bf16")
     resid = r.standard_normal((M, N)).astype(np.float32)
+    aux = U.rep(r.standard_normal((M, N)), "bf16")
+    cinit = r.standard_normal((M, N)).astype(np.float32)
     dA, dB, dbias, dres = U.dev(Am, "bf16"), U.dev(Bm, "bf16"), U.dev(bias, "bf16"), U.dev_f32(resid)
-    out_f32 = epi in (A.ATOM_EPI_STORE_F32, A.ATOM_EPI_BIAS_RESID)
-    dC = U.empty((M, N), "f32" if out_f32 else "bf16")
-    daux = U.empty((M, N), "bf16")
+    out_f32 = epi in (A.ATOM_EPI_STORE_F32, A.ATOM_EPI_ACC_F32, A.ATOM_EPI_BIAS_RESID)
+    dC = U.dev_f32(cinit) if epi == A.ATOM_EPI_ACC_F32 else U.empty((M, N), "f32" if out_f32 else "bf16")
+    daux = U.dev(aux, "bf16") if epi == A.ATOM_EPI_GELU_BWD else U.empty((M, N), "bf16")
     A.atom_k_gemm(A.ATOM_BF16, akc, bkc, epi, M, N, K, U.ptr(dA), a_shape[1], U.ptr(dB), b_shape[1], U.ptr(dC), N,
                   U.ptr(dbias), U.ptr(dres), U.ptr(daux), N, stream())
     U.sync()
@@ -142,6 +151,12 @@ def test_gemm_pipelined_path(akc, bkc, epi):
         ref = gpt.gelu(U.rep(u, "bf16").astype(np.float64))
     elif epi == A.ATOM_EPI_BIAS_RESID:
         ref = resid[pick] + acc + bias
+    elif epi == A.ATOM_EPI_ACC_F32:
+        ref = cinit[pick] + acc
+    elif epi == A.ATOM_EPI_BIAS:
+        ref = acc + bias
+    elif epi == A.ATOM_EPI_GELU_BWD:
+        ref = acc * gpt.gelu_grad(aux[pick].astype(np.float64))
     else:
         ref = acc
     tol = 1e-4 if out_f32 else 8e-3

@@ -6,8 +6,10 @@ refreshes the working copy.  The oracle applies AdamW in fp64 to the same
 accumulated gradients (read back from the host, so the comparison measures the
 optimizer alone).  Tolerance: fp32 rounding of an update of size about lr,
 relative to the weights (max-norm), 1e-6; the bf16 copy equals the master
-rounded to nearest even.  A second global batch checks the moments carry
-over and the accumulators were zeroed.
+rounded to nearest even, within one bf16 ulp near rounding ties and a few
+fp32 ulp of the largest weight for weights the update drives through zero.
+A second global batch checks the moments carry over and the accumulators
+were zeroed.
 """
 import numpy as np
 import pytest
@@ -53,7 +55,11 @@ def test_adamw_after_global_batch_matches_oracle(dtype):
                     else:
                         want = U.rep(ref.astype(np.float32), "bf16")
                         # the master is fp32: its bf16 rounding may differ from the fp64
-                        # oracle's by one bf16 ulp where the value sits near a rounding tie
-                        d = np.abs(got[i][k].astype(np.float64) - want) / np.maximum(np.abs(want), 1e-30)
-                        assert np.max(d) <= 2.0 ** -7, (b, i, k)
+                        # oracle's by one bf16 ulp where the value sits near a rounding tie,
+                        # and a weight that the update drives through zero keeps the fp32
+                        # master's absolute rounding error (a few ulp of the largest weight)
+                        d = np.abs(got[i][k].astype(np.float64) - want)
+                        bound = 2.0 ** -7 * np.abs(want) + 4 * 2.0 ** -24 * np.max(np.abs(ref))
+                        w = np.unravel_index(np.argmax(d - bound), d.shape)
+                        assert np.all(d <= bound), (b, i, k, w, got[i][k][w], want[w], ref[w])
                         assert np.mean(got[i][k] == want) > 0.99, (b, i, k)
