@@ -720,8 +720,8 @@ __global__ void __launch_bounds__(p4::NT) __attribute__((amdgpu_waves_per_eu(1, 
   using namespace p4;
   using p3::Src;
   using p3::FragOff;
-  __shared__ __attribute__((aligned(1024))) uint8_t sa0[OPB], sa1[OPB], sa2[OPB], sa3[OPB];
-  __shared__ __attribute__((aligned(1024))) uint8_t sb0[OPB], sb1[OPB], sb2[OPB], sb3[OPB];
+  // stages 0..3 of A, then of B; after the loop, the epilogue's staging
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[8 * OPB];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int wm = w / WN, wn = w % WN;
@@ -766,8 +766,8 @@ __global__ void __launch_bounds__(p4::NT) __attribute__((amdgpu_waves_per_eu(1, 
 #pragma unroll
   for (int j = 0; j < TN; ++j) fob[j].init(wn * TN * 16 + j * 16, lane);
 
-  auto stage_a = [&](int s) -> uint8_t* { return s == 0 ? sa0 : s == 1 ? sa1 : s == 2 ? sa2 : sa3; };
-  auto stage_b = [&](int s) -> uint8_t* { return s == 0 ? sb0 : s == 1 ? sb1 : s == 2 ? sb2 : sb3; };
+  auto stage_a = [&](int s) -> uint8_t* { return lds + s * OPB; };
+  auto stage_b = [&](int s) -> uint8_t* { return lds + (4 + s) * OPB; };
   auto load_tile = [&](int s, int kt) {
 #pragma unroll
     for (int q = 0; q < LPT; ++q) sra[q].load(stage_a(s), kt, q * (NT / 64) + w);
@@ -823,17 +823,34 @@ __global__ void __launch_bounds__(p4::NT) __attribute__((amdgpu_waves_per_eu(1, 
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) asm volatile("" : "+a"(acc[i][j]));
+  // Epilogue through LDS, 32 rows of the wave's 128x128 block at a time: the
+  // accumulators go to a wave-private [32][128] fp32 staging area, and each
+  // lane takes back 4 consecutive columns of one row, so a wave's stores (and
+  // the epilogue's reads of bias, residual or saved pre-activations) cover
+  // two whole 128-column rows instead of 32-byte pieces of 16 rows.
+  barrier_after_reads();  // every wave is done with the stages
+  constexpr int PITCH = 132;  // floats per staged row; rows 16 bytes of banks apart
+  float* stg = reinterpret_cast<float*>(lds) + w * (32 * PITCH);
   const bool ld_vec = (g.ldc & 3) == 0;
+  const int row0 = m0 + wm * TM * 16, col0 = n0 + wn * TN * 16;
 #pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int m = m0 + (wm * TM + i) * 16 + lr;
-    if (m >= g.M) continue;
+  for (int h = 0; h < TM / 2; ++h) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int nb = n0 + (wn * TN + j) * 16 + lg * 4;
-      if (nb >= g.N) continue;
-      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-      epilogue4<bf16_t, EPI>(g, m, nb, v, ld_vec);
+    for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const f32x4_t& a = acc[2 * h + ii][j];
+        *reinterpret_cast<float4*>(stg + (ii * 16 + lr) * PITCH + j * 16 + lg * 4) = make_float4(a[0], a[1], a[2], a[3]);
+      }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int rr = 2 * q + (lane >> 5), cc = 4 * (lane & 31);
+      const float4 x = *reinterpret_cast<const float4*>(stg + rr * PITCH + cc);
+      const int m = row0 + h * 32 + rr, nb = col0 + cc;
+      if (m < g.M && nb < g.N) {
+        float v[4] = {x.x, x.y, x.z, x.w};
+        epilogue4<bf16_t, EPI>(g, m, nb, v, ld_vec);
+      }
     }
   }
 }
@@ -849,12 +866,11 @@ bool p3_applies(const GemmArgs& g) {
          g.ldb % 8 == 0 && g.M >= 8 && g.N >= 8;
 }
 
-// The four-wave kernel takes the plain epilogues (stores, accumulation, bias)
-// when k is a multiple of four k tiles; with one wave per SIMD, the epilogues
-// that read or write a second [M][N] tensor ran faster on sixteen waves.
+// The four-wave kernel takes every epilogue but bias + fp32 residual and
+// GELU' (2 % and 8 % faster on sixteen waves, measured in the 6.7B step) when
+// k is a multiple of four k tiles.
 bool p4_applies(const GemmArgs& g, int epi) {
-  return ATOM_GEMM_P4 && g.K % (4 * p4::BK) == 0 &&
-         (epi == EPI_STORE || epi == EPI_STORE_F32 || epi == EPI_ACC_F32 || epi == EPI_BIAS);
+  return ATOM_GEMM_P4 && g.K % (4 * p4::BK) == 0 && epi != EPI_BIAS_RESID && epi != EPI_GELU_BWD;
 }
 
 template <bool AKC, bool BKC>
@@ -874,7 +890,7 @@ hipError_t launch_p3(const GemmArgs& g, int epi, hipStream_t s) {
     ATOM_CASE4(EPI_STORE_F32)
     ATOM_CASE4(EPI_ACC_F32)
     ATOM_CASE4(EPI_BIAS)
-    ATOM_CASE3(EPI_BIAS_GELU)
+    ATOM_CASE4(EPI_BIAS_GELU)
     ATOM_CASE3(EPI_BIAS_RESID)
     ATOM_CASE3(EPI_GELU_BWD)
 #undef ATOM_CASE4

@@ -123,7 +123,7 @@ def test_gemm_pipelined_path(akc, bkc, epi, K):
     """bf16 problems with >= 256 tiles of 256x256 and k a multiple of 32 take the
     four-stage direct-to-LDS kernels: sixteen waves for k = 352, and for k a
     multiple of 128 (384: three loop trips; 128: the prologue's tiles only) the
-    four-wave kernel with the plain epilogues.  M and N end in partial tiles
+    four-wave kernel for every epilogue but bias + residual and GELU'.  M and N end in partial tiles
     (ragged by 8 and 24 rows) whose loads are clamped to the last valid rows."""
     M, N = 4104, 4120
     r = U.rng(akc + 2 * bkc + 4 * epi + K)
