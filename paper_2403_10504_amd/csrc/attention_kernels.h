@@ -1,5 +1,8 @@
 // Causal self-attention kernel templates; instantiated by attention.hip
-// (bf16) and attention_f32.hip (fp32 validation mode).
+// (bf16: the direct-load kernels attn_fwd_dl, attn_bwd_dkdv_dl,
+// attn_bwd_dq_dl) and attention_f32.hip (fp32 validation mode: the
+// register-staged kernels below, which stage tiles through registers into
+// padded LDS and transpose V, Q, dO or K while storing).
 //
 // Fused causal self-attention on CDNA4 matrix cores (tiled, online softmax;
 // the [T, T] score matrix never leaves registers).
@@ -167,8 +170,8 @@ template <typename T>
 __device__ __forceinline__ void store_row4(T* p, const float* v) {
   if constexpr (sizeof(T) == 2) {
     uint2 w;
-    w.x = static_cast<uint32_t>(f2bf(v[0])) | (static_cast<uint32_t>(f2bf(v[1])) << 16);
-    w.y = static_cast<uint32_t>(f2bf(v[2])) | (static_cast<uint32_t>(f2bf(v[3])) << 16);
+    w.x = pack_bf16(v[0], v[1]);
+    w.y = pack_bf16(v[2], v[3]);
     *reinterpret_cast<uint2*>(p) = w;
   } else {
     *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
@@ -338,6 +341,203 @@ __global__ void __launch_bounds__(256, ATOM_ATTN_FWD_OCC) attn_fwd_kernel(const 
       for (int c = 0; c < L::NCT; ++c) {
         float v[4] = {acc_o[g][c][0] * inv, acc_o[g][c][1] * inv, acc_o[g][c][2] * inv, acc_o[g][c][3] * inv};
         store_row4<T>(orow + c * 16 + 4 * lg, v);
+      }
+      if (lg == 0) lse[(static_cast<int64_t>(b) * H + h) * Tn + qi] = (m_i[g] + log2f(l_tot)) * LN2;
+    }
+  }
+}
+
+// ------------------------------------------- forward, bf16, direct loads
+// The K and V tiles of a key tile go straight from global memory to LDS
+// (global_load_lds_dwordx4, no staging registers, no LDS stores), two stages
+// deep: the loads of tile t+1 are issued after the barrier that opens tile t,
+// into the stage tile t-1 used.  V stays in its natural [key][dh] layout and
+// the A operand of O^T += V^T P^T is read with ds_read_b64_tr_b16.  Each
+// fragment read is issued one step ahead of the MFMAs that use it.
+//
+// Stage layout: K [64][DH] then V [64][DH], rows of DH*2 bytes in 16-byte
+// chunks; chunk c of row r sits at slot c ^ kswz(r) (K) or c ^ vswz(r) (V):
+//   K: a ds_read_b128 serves 16 lanes per LDS cycle, 16 consecutive rows at
+//      one chunk;
+//   V: a ds_read_b64_tr_b16 serves 32 lanes, 8 consecutive rows at one
+//      aligned chunk pair (vswz is even, so pairs stay pairs).
+// Keys past the end read the last row (finite data; their scores are masked
+// to -inf, so they weigh zero).
+template <int DH>
+struct FwdDL {
+  static constexpr int CPR = DH / 8;             // chunks per row
+  static constexpr int TILE = BT * DH * 2;       // bytes of a K or V tile
+  static constexpr int STAGE = 2 * TILE;
+  static constexpr int LPT = TILE / (256 * 16);  // direct loads per thread per tile and operand
+  static_assert(DH == 64 || DH == 128, "head size");
+  __device__ static int kswz(int r) { return DH == 128 ? (r & 15) : ((r >> 1) & 7); }
+  __device__ static int vswz(int r) { return DH == 128 ? 2 * (r & 7) : 2 * ((r >> 1) & 3); }
+};
+
+template <int DH, int G>
+__global__ void __launch_bounds__(256, 2) attn_fwd_dl_kernel(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ o,
+                                                             float* __restrict__ lse, int B, int Tn, int H) {
+  using F = FwdDL<DH>;
+  constexpr int NS = DH / 32, NCT = DH / 16, BQ = 4 * 16 * G, RB = DH * 2;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * F::STAGE];
+
+  // the wave index through readfirstlane, so that everything derived from
+  // it (the wave's queries, the diagonal test) is known to be wave-uniform
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lr = lane & 15, lg = lane >> 4;
+  const int bh = blockIdx.y, b = bh / H, h = bh % H;
+  const int d = H * DH;
+  const int64_t ld = 3 * static_cast<int64_t>(d);
+  const bf16_t* qb = qkv + static_cast<int64_t>(b) * Tn * ld + h * DH;
+  const bf16_t* kb = qb + d;
+  const bf16_t* vb = qb + 2 * d;
+  const int q0 = blockIdx.x * BQ;
+  const int qw = q0 + w * 16 * G;
+  const float sc = LOG2E / sqrtf(static_cast<float>(DH));
+
+  Frag<bf16_t> qf[G][NS];
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int s = 0; s < NS; ++s) frag_global(qf[g][s], qb, ld, qw + g * 16 + lr, Tn, 32 * s + 8 * lg);
+
+  f32x4_t acc_o[G][NCT];
+  float m_i[G], l_i[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    m_i[g] = -1e30f;
+    l_i[g] = 0.f;
+#pragma unroll
+    for (int c = 0; c < NCT; ++c) acc_o[g][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // load q of a thread: chunk q*256 + tid of the tile (row, slot)
+  auto load_tile = [&](int st, int j0) {
+    const uint32_t kl = lds_offset(lds + st * F::STAGE), vl = kl + F::TILE;
+#pragma unroll
+    for (int q = 0; q < F::LPT; ++q) {
+      const int id = q * 256 + tid, row = id / F::CPR, slot = id % F::CPR;
+      const int64_t gr = static_cast<int64_t>(min(j0 + row, Tn - 1)) * ld;
+      const uint32_t lo = __builtin_amdgcn_readfirstlane((q * 256 + w * 64) * 16);
+      lds_dma16(kb + gr + (slot ^ F::kswz(row)) * 8, kl + lo);
+      lds_dma16(vb + gr + (slot ^ F::vswz(row)) * 8, vl + lo);
+    }
+  };
+  // fragment addresses inside a stage
+  auto kfrag = [&](Frag<bf16_t>& f, const uint8_t* ks, int jt, int s) {
+    const int row = jt * 16 + lr;
+    f.v = *reinterpret_cast<const uint4*>(ks + row * RB + ((4 * s + lg) ^ F::kswz(row)) * 16);
+  };
+  auto vfrag = [&](Frag<bf16_t>& f, const uint8_t* vs, int s2, int c) {
+    // keys 32 s2 + 4 lg + 0..3 (elements 0..3) and 32 s2 + 16 + 4 lg + 0..3
+    // (elements 4..7), the order of the P fragment built from two 16-key tiles
+    const int chunk = 2 * c + ((lr & 3) >> 1);
+    const int r0 = 32 * s2 + 4 * lg + (lr >> 2), r1 = r0 + 16;
+    const uint2 lo = ds_read_tr8(vs + r0 * RB + (chunk ^ F::vswz(r0)) * 16 + 8 * (lr & 1));
+    const uint2 hi = ds_read_tr8(vs + r1 * RB + (chunk ^ F::vswz(r1)) * 16 + 8 * (lr & 1));
+    f.v = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  };
+
+  const int n_kt = min((Tn + BT - 1) / BT, (min(q0 + BQ, Tn) - 1) / BT + 1);
+  load_tile(0, 0);
+  for (int kt = 0; kt < n_kt; ++kt) {
+    const int j0 = kt * BT, cur = kt & 1;
+    // tile kt has landed for every wave, and every wave is done with tile kt-1
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    asm volatile("s_barrier" ::: "memory");
+    if (kt + 1 < n_kt) load_tile(cur ^ 1, j0 + BT);
+    const uint8_t* ks = lds + cur * F::STAGE;
+    const uint8_t* vs = ks + F::TILE;
+    if (j0 <= qw + 16 * G - 1) {
+      float p[G][4][4];
+      float mloc[G];
+#pragma unroll
+      for (int g = 0; g < G; ++g) mloc[g] = -INFINITY;
+      Frag<bf16_t> kf[2][NS];
+#pragma unroll
+      for (int s = 0; s < NS; ++s) kfrag(kf[0][s], ks, 0, s);
+      const bool edge = j0 + BT > qw || j0 + BT > Tn;  // tile touches the diagonal or the end
+#pragma unroll
+      for (int jt = 0; jt < 4; ++jt) {
+        if (jt + 1 < 4) {
+#pragma unroll
+          for (int s = 0; s < NS; ++s) kfrag(kf[(jt + 1) & 1][s], ks, jt + 1, s);
+        }
+        f32x4_t a[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) a[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+#pragma unroll
+          for (int g = 0; g < G; ++g) mfma16(a[g], kf[jt & 1][s], qf[g][s]);
+        // raw scores, masked by selects (not per-element control flow); the
+        // scale goes into the max once and into the exponent's FMA
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const int qi = qw + g * 16 + lr;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int j = j0 + jt * 16 + 4 * lg + r;
+            float x = a[g][r];
+            if (edge) x = ((j <= qi) & (j < Tn)) ? x : -INFINITY;
+            p[g][jt][r] = x;
+            mloc[g] = fmaxf(mloc[g], x);
+          }
+        }
+      }
+      Frag<bf16_t> vf[2];
+      vfrag(vf[0], vs, 0, 0);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float mx = fmaxf(mloc[g], __shfl_xor(mloc[g], 16, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * sc;
+        if (__builtin_amdgcn_ballot_w64(mx > m_i[g] + RESCALE_LOG2) != 0) {
+          const float m_new = fmaxf(m_i[g], mx);
+          const float alpha = ex2(m_i[g] - m_new);
+          l_i[g] *= alpha;
+          m_i[g] = m_new;
+#pragma unroll
+          for (int c = 0; c < NCT; ++c) acc_o[g][c] *= alpha;
+        }
+        float lsum = 0.f;
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            p[g][jt][r] = ex2(__builtin_fmaf(p[g][jt][r], sc, -m_i[g]));
+            lsum += p[g][jt][r];
+          }
+        l_i[g] += lsum;
+      }
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        Frag<bf16_t> pf[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) frag_from_pair(pf[g], p[g], s2);
+#pragma unroll
+        for (int c = 0; c < NCT; ++c) {
+          const int n = s2 * NCT + c;
+          if (n + 1 < 2 * NCT) vfrag(vf[(n + 1) & 1], vs, (n + 1) / NCT, (n + 1) % NCT);
+#pragma unroll
+          for (int g = 0; g < G; ++g) mfma16(acc_o[g][c], vf[n & 1], pf[g]);
+        }
+      }
+    }
+  }
+
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const int qi = qw + g * 16 + lr;
+    float l_tot = l_i[g] + __shfl_xor(l_i[g], 16, 64);
+    l_tot += __shfl_xor(l_tot, 32, 64);
+    if (qi < Tn) {
+      const float inv = 1.f / l_tot;
+      bf16_t* orow = o + (static_cast<int64_t>(b) * Tn + qi) * d + h * DH;
+#pragma unroll
+      for (int c = 0; c < NCT; ++c) {
+        float v[4] = {acc_o[g][c][0] * inv, acc_o[g][c][1] * inv, acc_o[g][c][2] * inv, acc_o[g][c][3] * inv};
+        store_row4<bf16_t>(orow + c * 16 + 4 * lg, v);
       }
       if (lg == 0) lse[(static_cast<int64_t>(b) * H + h) * Tn + qi] = (m_i[g] + log2f(l_tot)) * LN2;
     }
@@ -661,29 +861,352 @@ __global__ void __launch_bounds__(64 * NW, ATOM_ATTN_DQ_OCC) attn_bwd_dq_kernel(
   }
 }
 
-// Query groups per wave (forward and dQ) and waves per dK/dV workgroup.
-// dQ: eight waves of 16 queries (two waves per SIMD within the register
-// file) beat four waves of 32 queries (one wave per SIMD): 1.14x.
-#ifndef ATOM_ATTN_DQ_G
-#define ATOM_ATTN_DQ_G 1
-#endif
-#ifndef ATOM_ATTN_DQ_W
-#define ATOM_ATTN_DQ_W 8
-#endif
+// ----------------------------------------- backward: dK, dV, bf16, direct loads
+// Q and dO tiles (natural layout) by direct loads, two stages; both are read
+// as row fragments (S = Q K^T, dP = dO V^T) and transposed in pair order
+// (dK^T += Q^T dS, dV^T += dO^T P), so both use the two-way swizzle dsw.
+// The rows' LSE and D go through registers into small per-stage arrays.
+template <int DH>
+__device__ __forceinline__ int dsw(int r);
+
+template <int DH, int W>
+__global__ void __launch_bounds__(64 * W) attn_bwd_dkdv_dl_kernel(const bf16_t* __restrict__ qkv,
+                                                                  const bf16_t* __restrict__ dout,
+                                                                  const float* __restrict__ lse,
+                                                                  const float* __restrict__ delta,
+                                                                  bf16_t* __restrict__ dqkv, int B, int Tn, int H) {
+  using F = FwdDL<DH>;
+  constexpr int NS = DH / 32, NCT = DH / 16, NT = 64 * W, RB = DH * 2, BKEYS = 16 * W;
+  constexpr int LPT = F::TILE / (NT * 16);
+  static_assert(LPT >= 1 && F::TILE % (NT * 16) == 0, "tile split");
+  constexpr int STAGE = 2 * F::TILE + 2 * BT * 4;  // Q, dO, LSE (log2 units), D
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lr = lane & 15, lg = lane >> 4;
+  const int bh = blockIdx.y, b = bh / H, h = bh % H;
+  const int d = H * DH;
+  const int64_t ld = 3 * static_cast<int64_t>(d);
+  const bf16_t* qb = qkv + static_cast<int64_t>(b) * Tn * ld + h * DH;
+  const bf16_t* kb = qb + d;
+  const bf16_t* vb = qb + 2 * d;
+  const bf16_t* ob = dout + static_cast<int64_t>(b) * Tn * d + h * DH;  // dO, row stride d
+  const float* lse_b = lse + (static_cast<int64_t>(b) * H + h) * Tn;
+  const float* del_b = delta + (static_cast<int64_t>(b) * H + h) * Tn;
+  const int k0 = blockIdx.x * BKEYS;
+  const int kw = k0 + w * 16;  // this wave's first key
+  const int kj = kw + lr;      // this lane's key
+  const float sc = LOG2E / sqrtf(static_cast<float>(DH));
+
+  Frag<bf16_t> kf[NS], vf[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    frag_global(kf[s], kb, ld, kj, Tn, 32 * s + 8 * lg);
+    frag_global(vf[s], vb, ld, kj, Tn, 32 * s + 8 * lg);
+  }
+  f32x4_t acc_dk[NCT], acc_dv[NCT];
+#pragma unroll
+  for (int c = 0; c < NCT; ++c) {
+    acc_dk[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    acc_dv[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  }
+
+  auto load_tile = [&](int st, int i0) {
+    const uint32_t ql = lds_offset(lds + st * STAGE), ol = ql + F::TILE;
+#pragma unroll
+    for (int q = 0; q < LPT; ++q) {
+      const int id = q * NT + tid, row = id / F::CPR, slot = id % F::CPR;
+      const int r = min(i0 + row, Tn - 1);
+      const uint32_t lo = __builtin_amdgcn_readfirstlane((q * NT + w * 64) * 16);
+      lds_dma16(qb + static_cast<int64_t>(r) * ld + (slot ^ dsw<DH>(row)) * 8, ql + lo);
+      lds_dma16(ob + static_cast<int64_t>(r) * d + (slot ^ dsw<DH>(row)) * 8, ol + lo);
+    }
+  };
+  // LSE and D of a tile's rows: read into registers, stored to LDS after the
+  // tile's compute (rows past the end get LSE = +inf, so their P is 0)
+  float pre_lse = 0.f, pre_del = 0.f;
+  auto read_rows = [&](int i0) {
+    if (tid < BT) {
+      const int i = i0 + tid;
+      pre_lse = i < Tn ? lse_b[i] * LOG2E : INFINITY;
+      pre_del = i < Tn ? del_b[i] : 0.f;
+    }
+  };
+  auto store_rows = [&](int st) {
+    if (tid < BT) {
+      float* rows = reinterpret_cast<float*>(lds + st * STAGE + 2 * F::TILE);
+      rows[tid] = pre_lse;
+      rows[BT + tid] = pre_del;
+    }
+  };
+  auto rowfrag = [&](Frag<bf16_t>& f, const uint8_t* st, int it, int s) {
+    const int row = it * 16 + lr, chunk = 4 * s + lg;
+    f.v = *reinterpret_cast<const uint4*>(st + row * RB + (chunk ^ dsw<DH>(row)) * 16);
+  };
+  auto trfrag = [&](Frag<bf16_t>& f, const uint8_t* st, int s2, int c) {
+    const int chunk = 2 * c + ((lr & 3) >> 1);
+    const int r0 = 32 * s2 + 4 * lg + (lr >> 2), r1 = r0 + 16;
+    const uint2 lo = ds_read_tr8(st + r0 * RB + (chunk ^ dsw<DH>(r0)) * 16 + 8 * (lr & 1));
+    const uint2 hi = ds_read_tr8(st + r1 * RB + (chunk ^ dsw<DH>(r1)) * 16 + 8 * (lr & 1));
+    f.v = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  };
+
+  const int qt0 = k0 / BT, n_qt = (Tn + BT - 1) / BT;
+  const bool tail_keys = kw + 16 > Tn;  // some of this wave's keys are past the end
+  if (qt0 < n_qt) {
+    load_tile(0, qt0 * BT);
+    read_rows(qt0 * BT);
+    store_rows(0);
+  }
+  for (int qt = qt0; qt < n_qt; ++qt) {
+    const int i0 = qt * BT, cur = (qt - qt0) & 1;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    asm volatile("s_barrier" ::: "memory");
+    const bool more = qt + 1 < n_qt;
+    if (more) {
+      load_tile(cur ^ 1, i0 + BT);
+      read_rows(i0 + BT);
+    }
+    if (i0 + BT - 1 >= kw && kw < Tn) {  // some query of the tile sees some key of this wave
+      const uint8_t* qs = lds + cur * STAGE;
+      const uint8_t* os = qs + F::TILE;
+      const float* lse_s = reinterpret_cast<const float*>(qs + 2 * F::TILE);
+      const float* del_s = lse_s + BT;
+      const bool mask = i0 < kw + 15 || tail_keys;  // diagonal tile or keys past the end
+      float p[4][4], ds[4][4];
+      Frag<bf16_t> qf[2][NS], of[2][NS];
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        rowfrag(qf[0][s], qs, 0, s);
+        rowfrag(of[0][s], os, 0, s);
+      }
+#pragma unroll
+      for (int it = 0; it < 4; ++it) {
+        if (it + 1 < 4) {
+#pragma unroll
+          for (int s = 0; s < NS; ++s) {
+            rowfrag(qf[(it + 1) & 1][s], qs, it + 1, s);
+            rowfrag(of[(it + 1) & 1][s], os, it + 1, s);
+          }
+        }
+        f32x4_t sa = f32x4_t{0.f, 0.f, 0.f, 0.f}, dp = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+          mfma16(sa, qf[it & 1][s], kf[s]);  // S[i][j]: lane holds key kj, queries 4lg + r
+          mfma16(dp, of[it & 1][s], vf[s]);  // dP[i][j]
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int il = it * 16 + 4 * lg + r;
+          float pv = ex2(__builtin_fmaf(sa[r], sc, -lse_s[il]));
+          if (mask) pv = ((kj <= i0 + il) & (kj < Tn)) ? pv : 0.f;
+          p[it][r] = pv;
+          ds[it][r] = pv * (dp[r] - del_s[il]);
+        }
+      }
+      Frag<bf16_t> ot2[2], qt2[2];
+      trfrag(ot2[0], os, 0, 0);
+      trfrag(qt2[0], qs, 0, 0);
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        Frag<bf16_t> pf, dsf;
+        frag_from_pair(pf, p, s2);
+        frag_from_pair(dsf, ds, s2);
+#pragma unroll
+        for (int c = 0; c < NCT; ++c) {
+          const int n = s2 * NCT + c;
+          if (n + 1 < 2 * NCT) {
+            trfrag(ot2[(n + 1) & 1], os, (n + 1) / NCT, (n + 1) % NCT);
+            trfrag(qt2[(n + 1) & 1], qs, (n + 1) / NCT, (n + 1) % NCT);
+          }
+          mfma16(acc_dv[c], ot2[n & 1], pf);   // dV^T[c][j]
+          mfma16(acc_dk[c], qt2[n & 1], dsf);  // dK^T[c][j]
+        }
+      }
+    }
+    if (more) store_rows(cur ^ 1);
+  }
+
+  if (kj < Tn) {
+    const float scale = 1.f / sqrtf(static_cast<float>(DH));
+    bf16_t* row = dqkv + (static_cast<int64_t>(b) * Tn + kj) * ld + h * DH;
+#pragma unroll
+    for (int c = 0; c < NCT; ++c) {
+      float vk[4] = {acc_dk[c][0] * scale, acc_dk[c][1] * scale, acc_dk[c][2] * scale, acc_dk[c][3] * scale};
+      float vv[4] = {acc_dv[c][0], acc_dv[c][1], acc_dv[c][2], acc_dv[c][3]};
+      store_row4<bf16_t>(row + d + c * 16 + 4 * lg, vk);
+      store_row4<bf16_t>(row + 2 * d + c * 16 + 4 * lg, vv);
+    }
+  }
+}
+
+// -------------------------------------------- backward: dQ, bf16, direct loads
+// K and V tiles by direct loads, two stages (as in the forward).  K is read
+// both ways, as row fragments for S^T = K Q^T and transposed (pair order)
+// for dQ^T += K^T dS^T, so its slots use one swizzle that serves both access
+// patterns: dsw(r) = 2 (r & 7) + ((r >> 3) & 1) for 16-chunk rows (16
+// consecutive rows at one chunk, and 8 consecutive rows at one chunk pair,
+// all land on distinct banks), 2 ((r >> 1) & 3) + ((r >> 3) & 1) for 8-chunk
+// rows.
+template <int DH>
+__device__ __forceinline__ int dsw(int r) {
+  return DH == 128 ? 2 * (r & 7) + ((r >> 3) & 1) : 2 * ((r >> 1) & 3) + ((r >> 3) & 1);
+}
+
+template <int DH, int NW>
+__global__ void __launch_bounds__(64 * NW) attn_bwd_dq_dl_kernel(const bf16_t* __restrict__ qkv,
+                                                                const bf16_t* __restrict__ dout,
+                                                                const float* __restrict__ lse,
+                                                                const float* __restrict__ delta,
+                                                                bf16_t* __restrict__ dqkv, int B, int Tn, int H) {
+  using F = FwdDL<DH>;
+  constexpr int NS = DH / 32, NCT = DH / 16, BQ = NW * 16, NT = 64 * NW, RB = DH * 2;
+  constexpr int LPT = F::TILE / (NT * 16);  // direct loads per thread per tile and operand
+  static_assert(LPT >= 1 && F::TILE % (NT * 16) == 0, "tile split");
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * F::STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lr = lane & 15, lg = lane >> 4;
+  const int bh = blockIdx.y, b = bh / H, h = bh % H;
+  const int d = H * DH;
+  const int64_t ld = 3 * static_cast<int64_t>(d);
+  const bf16_t* qb = qkv + static_cast<int64_t>(b) * Tn * ld + h * DH;
+  const bf16_t* kb = qb + d;
+  const bf16_t* vb = qb + 2 * d;
+  const bf16_t* ob = dout + static_cast<int64_t>(b) * Tn * d + h * DH;
+  const int q0 = blockIdx.x * BQ;
+  const int qw = q0 + w * 16;
+  const int qi = qw + lr;
+  const float sc = LOG2E / sqrtf(static_cast<float>(DH));
+
+  Frag<bf16_t> qf[NS], of[NS];
+  const float lse_i = qi < Tn ? lse[(static_cast<int64_t>(b) * H + h) * Tn + qi] * LOG2E : INFINITY;
+  const float del_i = qi < Tn ? delta[(static_cast<int64_t>(b) * H + h) * Tn + qi] : 0.f;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    frag_global(qf[s], qb, ld, qi, Tn, 32 * s + 8 * lg);
+    frag_global(of[s], ob, d, qi, Tn, 32 * s + 8 * lg);
+  }
+  f32x4_t acc_dq[NCT];
+#pragma unroll
+  for (int c = 0; c < NCT; ++c) acc_dq[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  auto load_tile = [&](int st, int j0) {
+    const uint32_t kl = lds_offset(lds + st * F::STAGE), vl = kl + F::TILE;
+#pragma unroll
+    for (int q = 0; q < LPT; ++q) {
+      const int id = q * NT + tid, row = id / F::CPR, slot = id % F::CPR;
+      const int64_t gr = static_cast<int64_t>(min(j0 + row, Tn - 1)) * ld;
+      const uint32_t lo = __builtin_amdgcn_readfirstlane((q * NT + w * 64) * 16);
+      lds_dma16(kb + gr + (slot ^ dsw<DH>(row)) * 8, kl + lo);
+      lds_dma16(vb + gr + (slot ^ F::kswz(row)) * 8, vl + lo);
+    }
+  };
+  auto rowfrag = [&](Frag<bf16_t>& f, const uint8_t* st, int jt, int s, bool dual) {
+    const int row = jt * 16 + lr, chunk = 4 * s + lg;
+    f.v = *reinterpret_cast<const uint4*>(st + row * RB + (chunk ^ (dual ? dsw<DH>(row) : F::kswz(row))) * 16);
+  };
+  auto trfrag = [&](Frag<bf16_t>& f, const uint8_t* st, int s2, int c) {
+    const int chunk = 2 * c + ((lr & 3) >> 1);
+    const int r0 = 32 * s2 + 4 * lg + (lr >> 2), r1 = r0 + 16;
+    const uint2 lo = ds_read_tr8(st + r0 * RB + (chunk ^ dsw<DH>(r0)) * 16 + 8 * (lr & 1));
+    const uint2 hi = ds_read_tr8(st + r1 * RB + (chunk ^ dsw<DH>(r1)) * 16 + 8 * (lr & 1));
+    f.v = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  };
+
+  const int n_kt = min((Tn + BT - 1) / BT, (min(q0 + BQ, Tn) - 1) / BT + 1);
+  load_tile(0, 0);
+  for (int kt = 0; kt < n_kt; ++kt) {
+    const int j0 = kt * BT, cur = kt & 1;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    asm volatile("s_barrier" ::: "memory");
+    if (kt + 1 < n_kt) load_tile(cur ^ 1, j0 + BT);
+    if (j0 <= qw + 15) {
+      const uint8_t* ks = lds + cur * F::STAGE;
+      const uint8_t* vs = ks + F::TILE;
+      const bool edge = j0 + BT > qw || j0 + BT > Tn;
+      float ds[4][4];
+      Frag<bf16_t> kf[2][NS], vf[2][NS];
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        rowfrag(kf[0][s], ks, 0, s, true);
+        rowfrag(vf[0][s], vs, 0, s, false);
+      }
+#pragma unroll
+      for (int jt = 0; jt < 4; ++jt) {
+        if (jt + 1 < 4) {
+#pragma unroll
+          for (int s = 0; s < NS; ++s) {
+            rowfrag(kf[(jt + 1) & 1][s], ks, jt + 1, s, true);
+            rowfrag(vf[(jt + 1) & 1][s], vs, jt + 1, s, false);
+          }
+        }
+        f32x4_t sa = f32x4_t{0.f, 0.f, 0.f, 0.f}, dp = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+          mfma16(sa, kf[jt & 1][s], qf[s]);  // S^T[j][i]: lane holds one query, keys 4lg + r
+          mfma16(dp, vf[jt & 1][s], of[s]);  // dP^T[j][i]
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int j = j0 + jt * 16 + 4 * lg + r;
+          float pv = ex2(__builtin_fmaf(sa[r], sc, -lse_i));
+          if (edge) pv = ((j <= qi) & (j < Tn)) ? pv : 0.f;
+          ds[jt][r] = pv * (dp[r] - del_i);
+        }
+      }
+      Frag<bf16_t> kt2[2];
+      trfrag(kt2[0], ks, 0, 0);
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        Frag<bf16_t> dsf;
+        frag_from_pair(dsf, ds, s2);
+#pragma unroll
+        for (int c = 0; c < NCT; ++c) {
+          const int n = s2 * NCT + c;
+          if (n + 1 < 2 * NCT) trfrag(kt2[(n + 1) & 1], ks, (n + 1) / NCT, (n + 1) % NCT);
+          mfma16(acc_dq[c], kt2[n & 1], dsf);  // dQ^T[c][i]
+        }
+      }
+    }
+  }
+
+  if (qi < Tn) {
+    const float scale = 1.f / sqrtf(static_cast<float>(DH));
+    bf16_t* row = dqkv + (static_cast<int64_t>(b) * Tn + qi) * ld + h * DH;
+#pragma unroll
+    for (int c = 0; c < NCT; ++c) {
+      float v[4] = {acc_dq[c][0] * scale, acc_dq[c][1] * scale, acc_dq[c][2] * scale, acc_dq[c][3] * scale};
+      store_row4<bf16_t>(row + c * 16 + 4 * lg, v);
+    }
+  }
+}
+
+// Query groups per wave in the forward (G), waves per dK/dV workgroup (W),
+// and query groups (GQ) and waves (WQ) of the dQ kernel; bf16 takes the
+// direct-load kernels, fp32 the register-staged ones.  dQ: eight waves of 16
+// queries (two waves per SIMD within the register file) beat four waves of 32
+// queries (one wave per SIMD): 1.14x.
 template <typename T, int DH>
 struct ACfg {
   static constexpr int G = sizeof(T) == 2 ? 2 : 1;
   static constexpr int W = sizeof(T) == 2 ? 8 : 4;
-  static constexpr int GQ = sizeof(T) == 2 ? ATOM_ATTN_DQ_G : 1;  // dQ: query groups per wave
-  static constexpr int WQ = sizeof(T) == 2 ? ATOM_ATTN_DQ_W : 4;  // dQ: waves per workgroup
+  static constexpr int GQ = 1;
+  static constexpr int WQ = sizeof(T) == 2 ? 8 : 4;
 };
 
 template <typename T, int DH>
 hipError_t fwd_t(const void* qkv, void* o, float* lse, int B, int Tn, int H, hipStream_t s) {
   constexpr int G = ACfg<T, DH>::G;
   dim3 grid((Tn + 64 * G - 1) / (64 * G), B * H), block(256);
-  hipLaunchKernelGGL((attn_fwd_kernel<T, DH, G>), grid, block, 0, s, static_cast<const T*>(qkv), static_cast<T*>(o),
-                     lse, B, Tn, H);
+  if constexpr (sizeof(T) == 2)
+    hipLaunchKernelGGL((attn_fwd_dl_kernel<DH, G>), grid, block, 0, s, static_cast<const bf16_t*>(qkv),
+                       static_cast<bf16_t*>(o), lse, B, Tn, H);
+  else
+    hipLaunchKernelGGL((attn_fwd_kernel<T, DH, G>), grid, block, 0, s, static_cast<const T*>(qkv), static_cast<T*>(o),
+                       lse, B, Tn, H);
   return hipGetLastError();
 }
 
@@ -696,15 +1219,24 @@ hipError_t bwd_t(const void* qkv, const void* o, const void* dout, const float* 
                      static_cast<const T*>(o), static_cast<const T*>(dout), delta, n_rows, Tn, H, DH);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<T, DH, W>), dim3((Tn + 16 * W - 1) / (16 * W), B * H), dim3(64 * W), 0,
-                     s, static_cast<const T*>(qkv), static_cast<const T*>(dout), lse, delta, static_cast<T*>(dqkv), B,
-                     Tn, H);
+  if constexpr (sizeof(T) == 2)
+    hipLaunchKernelGGL((attn_bwd_dkdv_dl_kernel<DH, W>), dim3((Tn + 16 * W - 1) / (16 * W), B * H), dim3(64 * W), 0,
+                       s, static_cast<const bf16_t*>(qkv), static_cast<const bf16_t*>(dout), lse, delta,
+                       static_cast<bf16_t*>(dqkv), B, Tn, H);
+  else
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<T, DH, W>), dim3((Tn + 16 * W - 1) / (16 * W), B * H), dim3(64 * W), 0,
+                       s, static_cast<const T*>(qkv), static_cast<const T*>(dout), lse, delta, static_cast<T*>(dqkv),
+                       B, Tn, H);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   constexpr int GQ = ACfg<T, DH>::GQ, WQ = ACfg<T, DH>::WQ;
-  hipLaunchKernelGGL((attn_bwd_dq_kernel<T, DH, GQ, WQ>), dim3((Tn + 16 * WQ * GQ - 1) / (16 * WQ * GQ), B * H),
-                     dim3(64 * WQ), 0, s,
-                     static_cast<const T*>(qkv), static_cast<const T*>(dout), lse, delta, static_cast<T*>(dqkv), B,
-                     Tn, H);
+  if constexpr (sizeof(T) == 2)
+    hipLaunchKernelGGL((attn_bwd_dq_dl_kernel<DH, WQ>), dim3((Tn + 16 * WQ - 1) / (16 * WQ), B * H), dim3(64 * WQ), 0,
+                       s, static_cast<const bf16_t*>(qkv), static_cast<const bf16_t*>(dout), lse, delta,
+                       static_cast<bf16_t*>(dqkv), B, Tn, H);
+  else
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<T, DH, GQ, WQ>), dim3((Tn + 16 * WQ * GQ - 1) / (16 * WQ * GQ), B * H),
+                       dim3(64 * WQ), 0, s, static_cast<const T*>(qkv), static_cast<const T*>(dout), lse, delta,
+                       static_cast<T*>(dqkv), B, Tn, H);
   return hipGetLastError();
 }
 

@@ -30,6 +30,15 @@ ATOM_DEV float bf2f(bf16_t h) { return __uint_as_float(static_cast<uint32_t>(h) 
 // conversion (pairs of calls fuse into one v_cvt_pk_bf16_f32).
 ATOM_DEV bf16_t f2bf(float f) { return __builtin_bit_cast(bf16_t, static_cast<__bf16>(f)); }
 
+// Two fp32 -> one dword of two bf16 (a low, b high), round to nearest even:
+// one v_cvt_pk_bf16_f32 (converting separately and packing with shifts cost
+// three instructions per pair).
+ATOM_DEV uint32_t pack_bf16(float a, float b) {
+  typedef float f2v __attribute__((ext_vector_type(2)));
+  typedef __bf16 b2v __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2v{a, b}), b2v));
+}
+
 template <typename T> ATOM_DEV float to_f(T v);
 template <> ATOM_DEV float to_f<float>(float v) { return v; }
 template <> ATOM_DEV float to_f<bf16_t>(bf16_t v) { return bf2f(v); }
@@ -71,12 +80,36 @@ ATOM_DEV void frag_from_f32(Frag<bf16_t>& f, const float* x) {
   uint32_t w[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
-    w[i] = static_cast<uint32_t>(f2bf(x[2 * i])) | (static_cast<uint32_t>(f2bf(x[2 * i + 1])) << 16);
+    w[i] = pack_bf16(x[2 * i], x[2 * i + 1]);
   f.v = make_uint4(w[0], w[1], w[2], w[3]);
 }
 ATOM_DEV void frag_from_f32(Frag<float>& f, const float* x) {
   f.lo = make_float4(x[0], x[1], x[2], x[3]);
   f.hi = make_float4(x[4], x[5], x[6], x[7]);
+}
+
+// LDS byte address of a __shared__ object.
+ATOM_DEV uint32_t lds_offset(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void*)(p)));
+}
+
+// One 16-byte direct global-to-LDS load per lane: lane i of the wave writes
+// LDS bytes lds + 16 i (lds wave-uniform).  Issued as inline assembly so
+// that the compiler does not track these LDS writes (its conservative
+// tracking drains every load in flight before LDS reads it cannot attribute
+// to a stage); kernels order them with explicit vmcnt waits and barriers.
+ATOM_DEV void lds_dma16(const void* gptr, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(gptr), "s"(lds) : "memory", "m0");
+}
+
+// ds_read_b64_tr_b16: each lane of a 16-lane group names 8 bytes (4 bf16 of
+// one row r = lane >> 2 of a 4-row block, columns 4 (lane & 3) .. +3); lane l
+// receives column l of the block's 4 rows, in row order.
+ATOM_DEV uint2 ds_read_tr8(const void* p) {
+  typedef short v4s __attribute__((ext_vector_type(4)));
+  const v4s v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(const_cast<void*>(p)));
+  return make_uint2(static_cast<uint32_t>(static_cast<uint16_t>(v[0])) | (static_cast<uint32_t>(static_cast<uint16_t>(v[1])) << 16),
+                    static_cast<uint32_t>(static_cast<uint16_t>(v[2])) | (static_cast<uint32_t>(static_cast<uint16_t>(v[3])) << 16));
 }
 
 // acc += A_frag x B_frag over one 32-wide k slice (16x16 output tile).

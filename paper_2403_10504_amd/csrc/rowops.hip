@@ -146,8 +146,8 @@ template <> struct Vec4<bf16_t> {
   }
   ATOM_DEV static void store(bf16_t* p, const float* f) {
     uint2 o;
-    o.x = static_cast<uint32_t>(f2bf(f[0])) | (static_cast<uint32_t>(f2bf(f[1])) << 16);
-    o.y = static_cast<uint32_t>(f2bf(f[2])) | (static_cast<uint32_t>(f2bf(f[3])) << 16);
+    o.x = pack_bf16(f[0], f[1]);
+    o.y = pack_bf16(f[2], f[3]);
     *reinterpret_cast<uint2*>(p) = o;
   }
 };
