@@ -347,6 +347,25 @@ __global__ void __launch_bounds__(256, ATOM_ATTN_FWD_OCC) attn_fwd_kernel(const 
   }
 }
 
+// Work item of a workgroup in a [n_x blocks][B*H heads] grid.  The hardware
+// hands consecutive linear ids to the 8 XCDs in turn, so with the plain ids an
+// XCD would see only blocks x = k and k+8 of every head: under the causal
+// mask the last XCD did 2.4x the work of the first, and every XCD read every
+// head's K and V.  Each XCD instead takes a contiguous range of (head, block)
+// pairs: whole heads, all their blocks (equal work, one head's tiles in one
+// L2).  heavy_last: block x does work growing with x, so x runs from the
+// heaviest down and the light blocks fill in behind.
+struct BlockId {
+  int x, bh;
+};
+__device__ __forceinline__ BlockId attn_block(bool heavy_last) {
+  const int n_x = gridDim.x, total = gridDim.x * gridDim.y;
+  const int lin = blockIdx.y * n_x + blockIdx.x;
+  const int v = (total & 7) == 0 ? (lin & 7) * (total >> 3) + (lin >> 3) : lin;
+  const int x = v % n_x;
+  return BlockId{heavy_last ? n_x - 1 - x : x, v / n_x};
+}
+
 // ------------------------------------------- forward, bf16, direct loads
 // The K and V tiles of a key tile go straight from global memory to LDS
 // (global_load_lds_dwordx4, no staging registers, no LDS stores), two stages
@@ -385,13 +404,14 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_dl_kernel(const bf16_t* __res
   // it (the wave's queries, the diagonal test) is known to be wave-uniform
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 15, lg = lane >> 4;
-  const int bh = blockIdx.y, b = bh / H, h = bh % H;
+  const BlockId blk = attn_block(true);
+  const int bh = blk.bh, b = bh / H, h = bh % H;
   const int d = H * DH;
   const int64_t ld = 3 * static_cast<int64_t>(d);
   const bf16_t* qb = qkv + static_cast<int64_t>(b) * Tn * ld + h * DH;
   const bf16_t* kb = qb + d;
   const bf16_t* vb = qb + 2 * d;
-  const int q0 = blockIdx.x * BQ;
+  const int q0 = blk.x * BQ;
   const int qw = q0 + w * 16 * G;
   const float sc = LOG2E / sqrtf(static_cast<float>(DH));
 
@@ -884,7 +904,8 @@ __global__ void __launch_bounds__(64 * W) attn_bwd_dkdv_dl_kernel(const bf16_t* 
 
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 15, lg = lane >> 4;
-  const int bh = blockIdx.y, b = bh / H, h = bh % H;
+  const BlockId blk = attn_block(false);  // key block x sees the queries from x on
+  const int bh = blk.bh, b = bh / H, h = bh % H;
   const int d = H * DH;
   const int64_t ld = 3 * static_cast<int64_t>(d);
   const bf16_t* qb = qkv + static_cast<int64_t>(b) * Tn * ld + h * DH;
@@ -893,7 +914,7 @@ __global__ void __launch_bounds__(64 * W) attn_bwd_dkdv_dl_kernel(const bf16_t* 
   const bf16_t* ob = dout + static_cast<int64_t>(b) * Tn * d + h * DH;  // dO, row stride d
   const float* lse_b = lse + (static_cast<int64_t>(b) * H + h) * Tn;
   const float* del_b = delta + (static_cast<int64_t>(b) * H + h) * Tn;
-  const int k0 = blockIdx.x * BKEYS;
+  const int k0 = blk.x * BKEYS;
   const int kw = k0 + w * 16;  // this wave's first key
   const int kj = kw + lr;      // this lane's key
   const float sc = LOG2E / sqrtf(static_cast<float>(DH));
@@ -1068,14 +1089,15 @@ __global__ void __launch_bounds__(64 * NW) attn_bwd_dq_dl_kernel(const bf16_t* _
 
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 15, lg = lane >> 4;
-  const int bh = blockIdx.y, b = bh / H, h = bh % H;
+  const BlockId blk = attn_block(true);
+  const int bh = blk.bh, b = bh / H, h = bh % H;
   const int d = H * DH;
   const int64_t ld = 3 * static_cast<int64_t>(d);
   const bf16_t* qb = qkv + static_cast<int64_t>(b) * Tn * ld + h * DH;
   const bf16_t* kb = qb + d;
   const bf16_t* vb = qb + 2 * d;
   const bf16_t* ob = dout + static_cast<int64_t>(b) * Tn * d + h * DH;
-  const int q0 = blockIdx.x * BQ;
+  const int q0 = blk.x * BQ;
   const int qw = q0 + w * 16;
   const int qi = qw + lr;
   const float sc = LOG2E / sqrtf(static_cast<float>(DH));
