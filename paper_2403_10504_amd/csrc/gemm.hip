@@ -255,6 +255,17 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& g, int m, int nb, floa
   }
 }
 
+// Epilogues that read an element operand (C itself, the fp32 residual or the
+// saved pre-activation) and epilogues that add the bias.
+template <int EPI>
+constexpr bool epi_reads_elem() {
+  return EPI == EPI_ACC_F32 || EPI == EPI_BIAS_RESID || EPI == EPI_GELU_BWD;
+}
+template <int EPI>
+constexpr bool epi_has_bias() {
+  return EPI == EPI_BIAS || EPI == EPI_BIAS_GELU || EPI == EPI_BIAS_RESID;
+}
+
 // One output tile per workgroup (blockIdx.x), one k range per split
 // (blockIdx.y).  With splits > 1 the raw fp32 sums go to the workspace
 // ws[split][M][N] and splitk_reduce applies the epilogue.
@@ -727,6 +738,18 @@ __global__ void __launch_bounds__(p4::NT) __attribute__((amdgpu_waves_per_eu(1, 
     srb[q].init(static_cast<const bf16_t*>(g.B), g.ldb, n0, g.N, q * NT + tid);
   }
   const int nk = g.K / BK;
+  // Each XCD starts its k loop at its own eighth of k (the tile's sum is
+  // rotated, the same for every launch of the shape).  Workgroups walk k in
+  // step, so without it the whole GPU reads the same column range of every
+  // row at once; when both operands are k-contiguous, rows of a long k are
+  // 32 KB apart and those addresses share their low bits, which crowds a few
+  // memory channels (4096x4096x16384: 500 -> 418 us).  The workgroups of one
+  // XCD share operand tiles through its L2, so they keep one offset.
+  const int koff = ((total & 7) == 0) ? ((blockIdx.x & 7) * (nk >> 3)) & ~3 : 0;
+  auto rot = [&](int kt) {
+    const int r = kt + koff;
+    return r >= nk ? r - nk : r;
+  };
 
   f32x4_t acc[TM][TN];
 #pragma unroll
@@ -760,7 +783,7 @@ __global__ void __launch_bounds__(p4::NT) __attribute__((amdgpu_waves_per_eu(1, 
   // past the last tile repeat it (into stages nobody reads again), so every
   // iteration has the same loads outstanding; they land before the exit.
 #pragma unroll
-  for (int s = 0; s < 4; ++s) load_tile(s, min(s, nk - 1));
+  for (int s = 0; s < 4; ++s) load_tile(s, rot(min(s, nk - 1)));
   asm volatile("s_waitcnt vmcnt(24)" ::: "memory");
   barrier_after_reads();
 #pragma unroll
@@ -774,7 +797,7 @@ __global__ void __launch_bounds__(p4::NT) __attribute__((amdgpu_waves_per_eu(1, 
     // tile t+1 has landed for every wave, and every wave has read tile t
     asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
     barrier_after_reads();
-    const int kt = min(t + 4, nk - 1);
+    const int kt = rot(min(t + 4, nk - 1));
     // per row i: the fragments i of tile t+1 (after the last tile they come
     // from a stale stage and are never used), then the MFMAs of row i of this
     // tile, which hide the reads' latency, with one direct load of tile t+4
@@ -815,28 +838,109 @@ __global__ void __launch_bounds__(p4::NT) __attribute__((amdgpu_waves_per_eu(1, 
   barrier_after_reads();  // every wave is done with the stages
   constexpr int PITCH = 132;  // floats per staged row; rows 16 bytes of banks apart
   float* stg = reinterpret_cast<float*>(lds) + w * (32 * PITCH);
-  const bool ld_vec = (g.ldc & 3) == 0;
   const int row0 = m0 + wm * TM * 16, col0 = n0 + wn * TN * 16;
+  // N, ldc and ldaux are multiples of 4 (p4_applies): a lane's four columns
+  // are all inside the matrix or all past it, and every access is one
+  // 4-vector.  They are the same columns in every row the lane stores, so the
+  // bias is loaded once and the row pointers advance by a fixed stride.
+  const int cc = 4 * (lane & 31), nb = col0 + cc, rsub = lane >> 5;
+  const bool col_ok = nb < g.N;
+  float bv[4] = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (epi_has_bias<EPI>())
+    if (col_ok) {
+      const uint2 w2 = *reinterpret_cast<const uint2*>(static_cast<const bf16_t*>(g.bias) + nb);
+      bv[0] = bf2f(w2.x & 0xffff); bv[1] = bf2f(w2.x >> 16); bv[2] = bf2f(w2.y & 0xffff); bv[3] = bf2f(w2.y >> 16);
+    }
+  constexpr bool F32_OUT = EPI == EPI_STORE_F32 || EPI == EPI_ACC_F32 || EPI == EPI_BIAS_RESID;
+  // The element operands (C itself, the fp32 residual or the saved bf16
+  // pre-activation) are requested ahead of their use: every CU reaches its
+  // epilogue at about the same time, so a load issued just before its use
+  // waits out a GPU-wide burst.  bf16 operands go out two blocks of 32 rows
+  // ahead (two registers per row), fp32 ones one block ahead.
+  // Interior blocks take a branch-free copy of the epilogue: with per-row
+  // bounds tests the compiler waits for every load in flight at each test,
+  // which defeats the loads issued ahead.
+  auto epilogue = [&](auto GUARD_) {
+    constexpr bool GUARD = decltype(GUARD_)::value;
+    constexpr bool ELEM = epi_reads_elem<EPI>();
+    constexpr int AHEAD = EPI == EPI_GELU_BWD ? 2 : 1;
+    using Raw = typename std::conditional<EPI == EPI_GELU_BWD, uint2, float4>::type;
+    Raw xr[TM / 2][16];
+    auto load_block = [&](int h) {
+      const int mq = row0 + h * 32 + rsub;
 #pragma unroll
-  for (int h = 0; h < TM / 2; ++h) {
-#pragma unroll
-    for (int ii = 0; ii < 2; ++ii)
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const f32x4_t& a = acc[2 * h + ii][j];
-        *reinterpret_cast<float4*>(stg + (ii * 16 + lr) * PITCH + j * 16 + lg * 4) = make_float4(a[0], a[1], a[2], a[3]);
+      for (int q = 0; q < 16; ++q) {
+        if (!GUARD || (mq + 2 * q < g.M && col_ok)) {
+          if constexpr (EPI == EPI_GELU_BWD)
+            xr[h][q] = *reinterpret_cast<const uint2*>(static_cast<const bf16_t*>(g.aux) +
+                                                       static_cast<int64_t>(mq + 2 * q) * g.ldaux + nb);
+          else
+            xr[h][q] = *reinterpret_cast<const float4*>((EPI == EPI_ACC_F32 ? static_cast<const float*>(g.C) : g.resid) +
+                                                        static_cast<int64_t>(mq + 2 * q) * g.ldc + nb);
+        }
       }
+    };
+    if constexpr (ELEM) {
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const int rr = 2 * q + (lane >> 5), cc = 4 * (lane & 31);
-      const float4 x = *reinterpret_cast<const float4*>(stg + rr * PITCH + cc);
-      const int m = row0 + h * 32 + rr, nb = col0 + cc;
-      if (m < g.M && nb < g.N) {
-        float v[4] = {x.x, x.y, x.z, x.w};
-        epilogue4<bf16_t, EPI>(g, m, nb, v, ld_vec);
+      for (int h = 0; h <= AHEAD; ++h) load_block(h);
+    }
+#pragma unroll
+    for (int h = 0; h < TM / 2; ++h) {
+      if constexpr (ELEM)
+        if (h > 0 && h + AHEAD < TM / 2) load_block(h + AHEAD);
+      const int mq = row0 + h * 32 + rsub;  // row of q = 0; row q is mq + 2q
+      const int64_t cq = static_cast<int64_t>(mq) * g.ldc + nb, aq = static_cast<int64_t>(mq) * g.ldaux + nb;
+#pragma unroll
+      for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const f32x4_t& a = acc[2 * h + ii][j];
+          *reinterpret_cast<float4*>(stg + (ii * 16 + lr) * PITCH + j * 16 + lg * 4) = make_float4(a[0], a[1], a[2], a[3]);
+        }
+      float4 sv[16];
+#pragma unroll
+      for (int q = 0; q < 16; ++q) sv[q] = *reinterpret_cast<const float4*>(stg + (2 * q + rsub) * PITCH + cc);
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        if (GUARD && !(mq + 2 * q < g.M && col_ok)) continue;
+        float v[4] = {sv[q].x, sv[q].y, sv[q].z, sv[q].w};
+        const int64_t off = cq + 2 * q * g.ldc;
+        float xe[4] = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (EPI == EPI_GELU_BWD) {
+          xe[0] = bf2f(xr[h][q].x & 0xffff); xe[1] = bf2f(xr[h][q].x >> 16);
+          xe[2] = bf2f(xr[h][q].y & 0xffff); xe[3] = bf2f(xr[h][q].y >> 16);
+        } else if constexpr (ELEM) {
+          xe[0] = xr[h][q].x; xe[1] = xr[h][q].y; xe[2] = xr[h][q].z; xe[3] = xr[h][q].w;
+        }
+        // the arithmetic of epilogue4, in the same order
+        if constexpr (EPI == EPI_ACC_F32) {
+          for (int r = 0; r < 4; ++r) v[r] += xe[r];
+        } else if constexpr (EPI == EPI_BIAS) {
+          for (int r = 0; r < 4; ++r) v[r] += bv[r];
+        } else if constexpr (EPI == EPI_BIAS_GELU) {
+          float gv[4];
+          for (int r = 0; r < 4; ++r) {
+            const float u = to_f<bf16_t>(from_f<bf16_t>(v[r] + bv[r]));
+            v[r] = u;
+            gv[r] = gelu_f(u);
+          }
+          *reinterpret_cast<uint2*>(static_cast<bf16_t*>(g.aux) + aq + 2 * q * g.ldaux) =
+              make_uint2(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]));
+          for (int r = 0; r < 4; ++r) v[r] = gv[r];
+        } else if constexpr (EPI == EPI_BIAS_RESID) {
+          for (int r = 0; r < 4; ++r) v[r] = xe[r] + (v[r] + bv[r]);
+        } else if constexpr (EPI == EPI_GELU_BWD) {
+          for (int r = 0; r < 4; ++r) v[r] *= gelu_grad_f(xe[r]);
+        }
+        if constexpr (F32_OUT)
+          *reinterpret_cast<float4*>(static_cast<float*>(g.C) + off) = make_float4(v[0], v[1], v[2], v[3]);
+        else
+          *reinterpret_cast<uint2*>(static_cast<bf16_t*>(g.C) + off) = make_uint2(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]));
       }
     }
-  }
+  };
+  if (row0 + TM * 16 <= g.M && col0 + TN * 16 <= g.N) epilogue(std::false_type{});
+  else epilogue(std::true_type{});
 }
 
 
@@ -850,11 +954,12 @@ bool p3_applies(const GemmArgs& g) {
          g.ldb % 8 == 0 && g.M >= 8 && g.N >= 8;
 }
 
-// The four-wave kernel takes every epilogue but bias + fp32 residual and
-// GELU' (2 % and 8 % faster on sixteen waves, measured in the 6.7B step) when
-// k is a multiple of four k tiles.
+// The four-wave kernel takes every epilogue when k is a multiple of four k
+// tiles and the output rows (and the saved pre-activation's) are 16-byte
+// aligned.
 bool p4_applies(const GemmArgs& g, int epi) {
-  return ATOM_GEMM_P4 && g.K % (4 * p4::BK) == 0 && epi != EPI_BIAS_RESID && epi != EPI_GELU_BWD;
+  const bool aux = epi == EPI_BIAS_GELU || epi == EPI_GELU_BWD;
+  return ATOM_GEMM_P4 && g.K % (4 * p4::BK) == 0 && g.ldc % 4 == 0 && (!aux || g.ldaux % 4 == 0);
 }
 
 template <bool AKC, bool BKC>
@@ -875,8 +980,8 @@ hipError_t launch_p3(const GemmArgs& g, int epi, hipStream_t s) {
     ATOM_CASE4(EPI_ACC_F32)
     ATOM_CASE4(EPI_BIAS)
     ATOM_CASE4(EPI_BIAS_GELU)
-    ATOM_CASE3(EPI_BIAS_RESID)
-    ATOM_CASE3(EPI_GELU_BWD)
+    ATOM_CASE4(EPI_BIAS_RESID)
+    ATOM_CASE4(EPI_GELU_BWD)
 #undef ATOM_CASE4
 #undef ATOM_CASE3
     default: return hipErrorInvalidValue;

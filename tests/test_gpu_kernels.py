@@ -123,10 +123,24 @@ def test_gemm_pipelined_path(akc, bkc, epi, K):
     """bf16 problems with >= 256 tiles of 256x256 and k a multiple of 32 take the
     four-stage direct-to-LDS kernels: sixteen waves for k = 352, and for k a
     multiple of 128 (384: three loop trips; 128: the prologue's tiles only) the
-    four-wave kernel for every epilogue but bias + residual and GELU'.  M and N end in partial tiles
-    (ragged by 8 and 24 rows) whose loads are clamped to the last valid rows."""
-    M, N = 4104, 4120
-    r = U.rng(akc + 2 * bkc + 4 * epi + K)
+    four-wave kernel for every epilogue.  M and N end in partial tiles (ragged
+    by 8 and 24 rows) whose loads are clamped to the last valid rows and whose
+    epilogue takes the bounds-tested copy."""
+    check_pipelined(akc, bkc, epi, 4104, 4120, K, seed=akc + 2 * bkc + 4 * epi + K)
+
+
+@pytest.mark.parametrize("akc,bkc", [(1, 1), (1, 0), (0, 0)])
+@pytest.mark.parametrize("epi", [A.ATOM_EPI_STORE, A.ATOM_EPI_BIAS_GELU, A.ATOM_EPI_BIAS_RESID, A.ATOM_EPI_GELU_BWD])
+def test_gemm_pipelined_rotated_k(akc, bkc, epi):
+    """A whole number of 256x256 tiles per XCD (4096 x 4096: 256 tiles) makes
+    the four-wave kernel start each XCD's k loop at its own eighth of k
+    (k = 1152: 36 tiles of 32, offsets 0, 4, ..., 28) and takes the
+    branch-free epilogue in every tile."""
+    check_pipelined(akc, bkc, epi, 4096, 4096, 1152, seed=100 + akc + 2 * bkc + 4 * epi)
+
+
+def check_pipelined(akc, bkc, epi, M, N, K, seed):
+    r = U.rng(seed)
     a_shape = (M, K) if akc else (K, M)
     b_shape = (N, K) if bkc else (K, N)
     Am = U.rep(r.standard_normal(a_shape), "bf16")
