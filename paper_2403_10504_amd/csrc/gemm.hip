@@ -737,18 +737,21 @@ __global__ void __launch_bounds__(p4::NT) __attribute__((amdgpu_waves_per_eu(1, 
     sra[q].init(static_cast<const bf16_t*>(g.A), g.lda, m0, g.M, q * NT + tid);
     srb[q].init(static_cast<const bf16_t*>(g.B), g.ldb, n0, g.N, q * NT + tid);
   }
-  const int nk = g.K / BK;
-  // Each XCD starts its k loop at its own eighth of k (the tile's sum is
-  // rotated, the same for every launch of the shape).  Workgroups walk k in
-  // step, so without it the whole GPU reads the same column range of every
-  // row at once; when both operands are k-contiguous, rows of a long k are
-  // 32 KB apart and those addresses share their low bits, which crowds a few
-  // memory channels (4096x4096x16384: 500 -> 418 us).  The workgroups of one
-  // XCD share operand tiles through its L2, so they keep one offset.
+  // k range of this workgroup: split blockIdx.y of gridDim.y equal ranges
+  // (the launcher makes each a multiple of four k tiles)
+  const int nk = g.K / BK / static_cast<int>(gridDim.y);
+  const int kbase = static_cast<int>(blockIdx.y) * nk;
+  // Each XCD starts its k loop at its own eighth of the range (the tile's
+  // sum is rotated, the same for every launch of the shape).  Workgroups
+  // walk k in step, so without it the whole GPU reads the same column range
+  // of every row at once; when both operands are k-contiguous, rows of a long
+  // k are 32 KB apart and those addresses share their low bits, which crowds
+  // a few memory channels (4096x4096x16384: 500 -> 418 us).  The workgroups
+  // of one XCD share operand tiles through its L2, so they keep one offset.
   const int koff = ((total & 7) == 0) ? ((blockIdx.x & 7) * (nk >> 3)) & ~3 : 0;
   auto rot = [&](int kt) {
     const int r = kt + koff;
-    return r >= nk ? r - nk : r;
+    return kbase + (r >= nk ? r - nk : r);
   };
 
   f32x4_t acc[TM][TN];
@@ -851,7 +854,6 @@ __global__ void __launch_bounds__(p4::NT) __attribute__((amdgpu_waves_per_eu(1, 
       const uint2 w2 = *reinterpret_cast<const uint2*>(static_cast<const bf16_t*>(g.bias) + nb);
       bv[0] = bf2f(w2.x & 0xffff); bv[1] = bf2f(w2.x >> 16); bv[2] = bf2f(w2.y & 0xffff); bv[3] = bf2f(w2.y >> 16);
     }
-  constexpr bool F32_OUT = EPI == EPI_STORE_F32 || EPI == EPI_ACC_F32 || EPI == EPI_BIAS_RESID;
   // The element operands (C itself, the fp32 residual or the saved bf16
   // pre-activation) are requested ahead of their use: every CU reaches its
   // epilogue at about the same time, so a load issued just before its use
@@ -860,23 +862,25 @@ __global__ void __launch_bounds__(p4::NT) __attribute__((amdgpu_waves_per_eu(1, 
   // Interior blocks take a branch-free copy of the epilogue: with per-row
   // bounds tests the compiler waits for every load in flight at each test,
   // which defeats the loads issued ahead.
-  auto epilogue = [&](auto GUARD_) {
+  auto epilogue = [&](auto GUARD_, auto EPI_, const GemmArgs& ga) {
     constexpr bool GUARD = decltype(GUARD_)::value;
-    constexpr bool ELEM = epi_reads_elem<EPI>();
-    constexpr int AHEAD = EPI == EPI_GELU_BWD ? 2 : 1;
-    using Raw = typename std::conditional<EPI == EPI_GELU_BWD, uint2, float4>::type;
+    constexpr int E = decltype(EPI_)::value;
+    constexpr bool F32_OUT = E == EPI_STORE_F32 || E == EPI_ACC_F32 || E == EPI_BIAS_RESID;
+    constexpr bool ELEM = epi_reads_elem<E>();
+    constexpr int AHEAD = E == EPI_GELU_BWD ? 2 : 1;
+    using Raw = typename std::conditional<E == EPI_GELU_BWD, uint2, float4>::type;
     Raw xr[TM / 2][16];
     auto load_block = [&](int h) {
       const int mq = row0 + h * 32 + rsub;
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
-        if (!GUARD || (mq + 2 * q < g.M && col_ok)) {
-          if constexpr (EPI == EPI_GELU_BWD)
-            xr[h][q] = *reinterpret_cast<const uint2*>(static_cast<const bf16_t*>(g.aux) +
-                                                       static_cast<int64_t>(mq + 2 * q) * g.ldaux + nb);
+        if (!GUARD || (mq + 2 * q < ga.M && col_ok)) {
+          if constexpr (E == EPI_GELU_BWD)
+            xr[h][q] = *reinterpret_cast<const uint2*>(static_cast<const bf16_t*>(ga.aux) +
+                                                       static_cast<int64_t>(mq + 2 * q) * ga.ldaux + nb);
           else
-            xr[h][q] = *reinterpret_cast<const float4*>((EPI == EPI_ACC_F32 ? static_cast<const float*>(g.C) : g.resid) +
-                                                        static_cast<int64_t>(mq + 2 * q) * g.ldc + nb);
+            xr[h][q] = *reinterpret_cast<const float4*>((E == EPI_ACC_F32 ? static_cast<const float*>(ga.C) : ga.resid) +
+                                                        static_cast<int64_t>(mq + 2 * q) * ga.ldc + nb);
         }
       }
     };
@@ -889,7 +893,7 @@ __global__ void __launch_bounds__(p4::NT) __attribute__((amdgpu_waves_per_eu(1, 
       if constexpr (ELEM)
         if (h > 0 && h + AHEAD < TM / 2) load_block(h + AHEAD);
       const int mq = row0 + h * 32 + rsub;  // row of q = 0; row q is mq + 2q
-      const int64_t cq = static_cast<int64_t>(mq) * g.ldc + nb, aq = static_cast<int64_t>(mq) * g.ldaux + nb;
+      const int64_t cq = static_cast<int64_t>(mq) * ga.ldc + nb, aq = static_cast<int64_t>(mq) * ga.ldaux + nb;
 #pragma unroll
       for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
@@ -902,57 +906,72 @@ __global__ void __launch_bounds__(p4::NT) __attribute__((amdgpu_waves_per_eu(1, 
       for (int q = 0; q < 16; ++q) sv[q] = *reinterpret_cast<const float4*>(stg + (2 * q + rsub) * PITCH + cc);
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
-        if (GUARD && !(mq + 2 * q < g.M && col_ok)) continue;
+        if (GUARD && !(mq + 2 * q < ga.M && col_ok)) continue;
         float v[4] = {sv[q].x, sv[q].y, sv[q].z, sv[q].w};
-        const int64_t off = cq + 2 * q * g.ldc;
+        const int64_t off = cq + 2 * q * ga.ldc;
         float xe[4] = {0.f, 0.f, 0.f, 0.f};
-        if constexpr (EPI == EPI_GELU_BWD) {
+        if constexpr (E == EPI_GELU_BWD) {
           xe[0] = bf2f(xr[h][q].x & 0xffff); xe[1] = bf2f(xr[h][q].x >> 16);
           xe[2] = bf2f(xr[h][q].y & 0xffff); xe[3] = bf2f(xr[h][q].y >> 16);
         } else if constexpr (ELEM) {
           xe[0] = xr[h][q].x; xe[1] = xr[h][q].y; xe[2] = xr[h][q].z; xe[3] = xr[h][q].w;
         }
         // the arithmetic of epilogue4, in the same order
-        if constexpr (EPI == EPI_ACC_F32) {
+        if constexpr (E == EPI_ACC_F32) {
           for (int r = 0; r < 4; ++r) v[r] += xe[r];
-        } else if constexpr (EPI == EPI_BIAS) {
+        } else if constexpr (E == EPI_BIAS) {
           for (int r = 0; r < 4; ++r) v[r] += bv[r];
-        } else if constexpr (EPI == EPI_BIAS_GELU) {
+        } else if constexpr (E == EPI_BIAS_GELU) {
           float gv[4];
           for (int r = 0; r < 4; ++r) {
             const float u = to_f<bf16_t>(from_f<bf16_t>(v[r] + bv[r]));
             v[r] = u;
             gv[r] = gelu_f(u);
           }
-          *reinterpret_cast<uint2*>(static_cast<bf16_t*>(g.aux) + aq + 2 * q * g.ldaux) =
+          *reinterpret_cast<uint2*>(static_cast<bf16_t*>(ga.aux) + aq + 2 * q * ga.ldaux) =
               make_uint2(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]));
           for (int r = 0; r < 4; ++r) v[r] = gv[r];
-        } else if constexpr (EPI == EPI_BIAS_RESID) {
+        } else if constexpr (E == EPI_BIAS_RESID) {
           for (int r = 0; r < 4; ++r) v[r] = xe[r] + (v[r] + bv[r]);
-        } else if constexpr (EPI == EPI_GELU_BWD) {
+        } else if constexpr (E == EPI_GELU_BWD) {
           for (int r = 0; r < 4; ++r) v[r] *= gelu_grad_f(xe[r]);
         }
         if constexpr (F32_OUT)
-          *reinterpret_cast<float4*>(static_cast<float*>(g.C) + off) = make_float4(v[0], v[1], v[2], v[3]);
+          *reinterpret_cast<float4*>(static_cast<float*>(ga.C) + off) = make_float4(v[0], v[1], v[2], v[3]);
         else
-          *reinterpret_cast<uint2*>(static_cast<bf16_t*>(g.C) + off) = make_uint2(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]));
+          *reinterpret_cast<uint2*>(static_cast<bf16_t*>(ga.C) + off) = make_uint2(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]));
       }
     }
   };
-  if (row0 + TM * 16 <= g.M && col0 + TN * 16 <= g.N) epilogue(std::false_type{});
-  else epilogue(std::true_type{});
+  const bool interior = row0 + TM * 16 <= g.M && col0 + TN * 16 <= g.N;
+  if constexpr (EPI == EPI_STORE || EPI == EPI_STORE_F32 || EPI == EPI_ACC_F32) {
+    if (gridDim.y > 1) {
+      // a split over k: the raw fp32 sums go to ws[split][M][N], and
+      // splitk_reduce adds the splits in order and applies the epilogue
+      GemmArgs gw = g;
+      gw.C = g.ws + static_cast<int64_t>(blockIdx.y) * g.M * g.N;
+      gw.ldc = g.N;
+      if (interior) epilogue(std::false_type{}, std::integral_constant<int, EPI_STORE_F32>{}, gw);
+      else epilogue(std::true_type{}, std::integral_constant<int, EPI_STORE_F32>{}, gw);
+      return;
+    }
+  }
+  if (interior) epilogue(std::false_type{}, std::integral_constant<int, EPI>{}, g);
+  else epilogue(std::true_type{}, std::integral_constant<int, EPI>{}, g);
 }
 
 
-// The pipelined kernel applies to bf16 problems with at least one 256x256
-// tile per CU, k a multiple of 32, and (for clamped edge rows) M and N
-// multiples of 8 with 16-byte aligned rows.
-bool p3_applies(const GemmArgs& g) {
-  if (!ATOM_GEMM_PIPE) return false;
-  const int tiles = ((g.M + p3::BM - 1) / p3::BM) * ((g.N + p3::BN - 1) / p3::BN);
-  return tiles >= 256 && g.K % p3::BK == 0 && g.K > 0 && g.M % 8 == 0 && g.N % 8 == 0 && g.lda % 8 == 0 &&
+// The pipelined kernels apply to bf16 problems with k a multiple of 32 and
+// (for clamped edge rows) M and N multiples of 8 with 16-byte aligned rows;
+// launch_p3 takes those with at least one 256x256 tile per CU.
+bool pipe_shape_ok(const GemmArgs& g) {
+  return ATOM_GEMM_PIPE && g.K % p3::BK == 0 && g.K > 0 && g.M % 8 == 0 && g.N % 8 == 0 && g.lda % 8 == 0 &&
          g.ldb % 8 == 0 && g.M >= 8 && g.N >= 8;
 }
+
+int pipe_tiles(const GemmArgs& g) { return ((g.M + p3::BM - 1) / p3::BM) * ((g.N + p3::BN - 1) / p3::BN); }
+
+bool p3_applies(const GemmArgs& g) { return pipe_shape_ok(g) && pipe_tiles(g) >= 256; }
 
 // The four-wave kernel takes every epilogue when k is a multiple of four k
 // tiles and the output rows (and the saved pre-activation's) are 16-byte
@@ -989,6 +1008,53 @@ hipError_t launch_p3(const GemmArgs& g, int epi, hipStream_t s) {
   return hipGetLastError();
 }
 
+// The four-wave kernel on fewer 256x256 tiles than CUs (weight gradients of
+// the narrower layers): the split count over k, 1 from 192 tiles on, else the
+// smallest power of two that brings the workgroups to 192 or more, provided
+// the epilogue can follow the sum of the splits, k divides into ranges of
+// whole four-tile steps and the workspace holds the partial sums; 0 where
+// the kernel does not apply.
+int p4_splits(const GemmArgs& g, int epi, int tiles) {
+  if (!pipe_shape_ok(g) || !p4_applies(g, epi)) return 0;
+  if (tiles >= 192) return 1;
+  if (!(epi == EPI_STORE || epi == EPI_STORE_F32 || epi == EPI_ACC_F32) || !g.ws) return 0;
+  for (int sp = 2; sp <= 16; sp *= 2) {
+    if (g.K % (4 * p4::BK * sp) != 0) return 0;
+    if (static_cast<uint64_t>(sp) * g.M * g.N * 4 > g.ws_bytes) return 0;
+    if (tiles * sp >= 192) return sp;
+  }
+  return 0;
+}
+
+template <bool AKC, bool BKC>
+hipError_t launch_p4_split(const GemmArgs& g, int epi, int tiles, int splits, hipStream_t s) {
+  const dim3 grid(tiles, splits);
+  switch (epi) {
+#define ATOM_CASE(E) \
+  case E: hipLaunchKernelGGL((gemm_p4_kernel<AKC, BKC, E>), grid, dim3(p4::NT), 0, s, g); break;
+    ATOM_CASE(EPI_STORE)
+    ATOM_CASE(EPI_STORE_F32)
+    ATOM_CASE(EPI_ACC_F32)
+    ATOM_CASE(EPI_BIAS)
+    ATOM_CASE(EPI_BIAS_GELU)
+    ATOM_CASE(EPI_BIAS_RESID)
+    ATOM_CASE(EPI_GELU_BWD)
+#undef ATOM_CASE
+    default: return hipErrorInvalidValue;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || splits == 1) return e;
+  const int64_t MN = static_cast<int64_t>(g.M) * g.N;
+  dim3 rgrid(static_cast<unsigned>((MN / 4 + 255) / 256 + 1)), rblock(256);
+  switch (epi) {
+    case EPI_STORE: hipLaunchKernelGGL((splitk_reduce<bf16_t, EPI_STORE>), rgrid, rblock, 0, s, g, splits); break;
+    case EPI_STORE_F32: hipLaunchKernelGGL((splitk_reduce<bf16_t, EPI_STORE_F32>), rgrid, rblock, 0, s, g, splits); break;
+    case EPI_ACC_F32: hipLaunchKernelGGL((splitk_reduce<bf16_t, EPI_ACC_F32>), rgrid, rblock, 0, s, g, splits); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 // Tile configuration and split count for a problem: the large tile when it
 // gives at least one workgroup per CU, else the 128x128 tile; a split over k
 // when even that leaves the CUs idle and k is long (weight gradients of
@@ -998,6 +1064,8 @@ hipError_t launch_t(const GemmArgs& g, int epi, hipStream_t s) {
   constexpr int CUS = 256;
   if constexpr (sizeof(T) == 2) {
     if (p3_applies(g)) return launch_p3<AKC, BKC>(g, epi, s);
+    const int tiles = pipe_tiles(g), splits = p4_splits(g, epi, tiles);
+    if (splits > 0) return launch_p4_split<AKC, BKC>(g, epi, tiles, splits, s);
   }
   const int tiles_big = ((g.M + Big::BM - 1) / Big::BM) * ((g.N + Big::BN - 1) / Big::BN);
   if (tiles_big >= CUS) return launch_cfg<T, AKC, BKC, Big>(g, epi, 1, s);

@@ -139,7 +139,30 @@ def test_gemm_pipelined_rotated_k(akc, bkc, epi):
     check_pipelined(akc, bkc, epi, 4096, 4096, 1152, seed=100 + akc + 2 * bkc + 4 * epi)
 
 
-def check_pipelined(akc, bkc, epi, M, N, K, seed):
+@pytest.mark.parametrize("akc,bkc", [(1, 1), (1, 0), (0, 0)])
+@pytest.mark.parametrize("M,N,K,epi", [
+    (3072, 4096, 1024, A.ATOM_EPI_BIAS_GELU),  # 192 tiles: four waves, no split
+    (3072, 4096, 1024, A.ATOM_EPI_GELU_BWD),
+    (2048, 2048, 4096, A.ATOM_EPI_STORE),  # 64 tiles: four splits of k
+    (1544, 1032, 2048, A.ATOM_EPI_ACC_F32),  # 35 ragged tiles: eight splits
+    (1544, 1032, 2048, A.ATOM_EPI_STORE_F32),
+])
+def test_gemm_four_wave_few_tiles(akc, bkc, M, N, K, epi):
+    """Fewer 256x256 tiles than CUs: the four-wave kernel takes problems from
+    192 tiles on as they are, and fewer tiles over 2-16 ranges of k whose fp32
+    partial sums splitk_reduce adds in order, when the workspace holds them."""
+    seed = 200 + akc + 2 * bkc + 4 * epi + M
+    check_pipelined(akc, bkc, epi, M, N, K, seed=seed, ws_bytes=64 << 20)
+    if epi == A.ATOM_EPI_STORE_F32:
+        # the split sum is deterministic and differs from the unsplit order
+        c1 = check_pipelined(akc, bkc, epi, M, N, K, seed=seed, ws_bytes=64 << 20)
+        c2 = check_pipelined(akc, bkc, epi, M, N, K, seed=seed, ws_bytes=64 << 20)
+        c0 = check_pipelined(akc, bkc, epi, M, N, K, seed=seed, ws_bytes=0)
+        assert np.array_equal(c1, c2)
+        assert not np.array_equal(c0, c1)
+
+
+def check_pipelined(akc, bkc, epi, M, N, K, seed, ws_bytes=0):
     r = U.rng(seed)
     a_shape = (M, K) if akc else (K, M)
     b_shape = (N, K) if bkc else (K, N)
@@ -153,8 +176,10 @@ def check_pipelined(akc, bkc, epi, M, N, K, seed):
     out_f32 = epi in (A.ATOM_EPI_STORE_F32, A.ATOM_EPI_ACC_F32, A.ATOM_EPI_BIAS_RESID)
     dC = U.dev_f32(cinit) if epi == A.ATOM_EPI_ACC_F32 else U.empty((M, N), "f32" if out_f32 else "bf16")
     daux = U.dev(aux, "bf16") if epi == A.ATOM_EPI_GELU_BWD else U.empty((M, N), "bf16")
+    dws = U.empty((ws_bytes // 4,), "f32") if ws_bytes else None
     A.atom_k_gemm(A.ATOM_BF16, akc, bkc, epi, M, N, K, U.ptr(dA), a_shape[1], U.ptr(dB), b_shape[1], U.ptr(dC), N,
-                  U.ptr(dbias), U.ptr(dres), U.ptr(daux), N, stream())
+                  U.ptr(dbias), U.ptr(dres), U.ptr(daux), N, stream(), ws=U.ptr(dws) if ws_bytes else None,
+                  ws_bytes=ws_bytes)
     U.sync()
     pick = np.sort(np.unique(np.concatenate([U.rng(7).choice(M, 40, replace=False), [M - 9, M - 1]])))
     acc = (Am if akc else Am.T)[pick].astype(np.float64) @ (Bm.T if bkc else Bm).astype(np.float64)
@@ -177,6 +202,7 @@ def check_pipelined(akc, bkc, epi, M, N, K, seed):
     assert U.rel_err(got, ref) < tol
     # the last columns (a partial tile) too
     assert U.rel_err(got[:, -24:], ref[:, -24:]) < tol
+    return got
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
