@@ -1010,20 +1010,20 @@ hipError_t launch_p3(const GemmArgs& g, int epi, hipStream_t s) {
 
 // The four-wave kernel on fewer 256x256 tiles than CUs (weight gradients of
 // the narrower layers): the split count over k, 1 from 192 tiles on, else the
-// smallest power of two that brings the workgroups to 192 or more, provided
-// the epilogue can follow the sum of the splits, k divides into ranges of
-// whole four-tile steps and the workspace holds the partial sums; 0 where
-// the kernel does not apply.
+// smallest power of two that brings the workgroups to 192 or more, or the
+// largest one the workspace holds if that leaves at least 96; splits need an
+// epilogue that can follow their sum and k ranges of whole four-tile steps.
+// 0 where the kernel does not apply.
 int p4_splits(const GemmArgs& g, int epi, int tiles) {
   if (!pipe_shape_ok(g) || !p4_applies(g, epi)) return 0;
   if (tiles >= 192) return 1;
   if (!(epi == EPI_STORE || epi == EPI_STORE_F32 || epi == EPI_ACC_F32) || !g.ws) return 0;
-  for (int sp = 2; sp <= 16; sp *= 2) {
-    if (g.K % (4 * p4::BK * sp) != 0) return 0;
-    if (static_cast<uint64_t>(sp) * g.M * g.N * 4 > g.ws_bytes) return 0;
-    if (tiles * sp >= 192) return sp;
+  int best = 0;
+  for (int sp = 2; sp <= 16 && tiles * best < 192; sp *= 2) {
+    if (g.K % (4 * p4::BK * sp) != 0 || static_cast<uint64_t>(sp) * g.M * g.N * 4 > g.ws_bytes) break;
+    best = sp;
   }
-  return 0;
+  return tiles * best >= 96 ? best : 0;
 }
 
 template <bool AKC, bool BKC>

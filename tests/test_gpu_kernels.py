@@ -146,11 +146,13 @@ def test_gemm_pipelined_rotated_k(akc, bkc, epi):
     (2048, 2048, 4096, A.ATOM_EPI_STORE),  # 64 tiles: four splits of k
     (1544, 1032, 2048, A.ATOM_EPI_ACC_F32),  # 35 ragged tiles: eight splits
     (1544, 1032, 2048, A.ATOM_EPI_STORE_F32),
+    (3072, 768, 16384, A.ATOM_EPI_STORE),  # 36 tiles: eight splits would overflow 64 MB, so four
 ])
 def test_gemm_four_wave_few_tiles(akc, bkc, M, N, K, epi):
     """Fewer 256x256 tiles than CUs: the four-wave kernel takes problems from
     192 tiles on as they are, and fewer tiles over 2-16 ranges of k whose fp32
-    partial sums splitk_reduce adds in order, when the workspace holds them."""
+    partial sums splitk_reduce adds in order (as many splits as bring the
+    workgroups to 192, or as the workspace holds if that leaves 96)."""
     seed = 200 + akc + 2 * bkc + 4 * epi + M
     check_pipelined(akc, bkc, epi, M, N, K, seed=seed, ws_bytes=64 << 20)
     if epi == A.ATOM_EPI_STORE_F32:
