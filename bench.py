@@ -163,6 +163,10 @@ def main():
     ap.add_argument("--measured-plan", action="store_true",
                     help="profile every node on the GPU (atom_profile_nodes) and plan the timed steps with those "
                          "costs instead of the analytic ones")
+    ap.add_argument("--retain", action="store_true",
+                    help="keep every group's weights on the device across the steps of the call when each group "
+                         "has a slot of its own (atom_set_retention: loaded once per global batch, gradients "
+                         "still copied out every step); not the default, which loads every weight every step")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="run one plain device copy of BYTES before the timed steps (calibrates HBM byte counters)")
     args = ap.parse_args()
@@ -246,6 +250,8 @@ def main():
             log(f"steps {i0}..{i0 + len(out) - 1}: {sess.stats().step_s * 1e3:.1f} ms/step")
         return out
 
+    if args.retain:
+        sess.set_retention(True)
     if args.warmup:
         losses = run(args.warmup)
         log(f"warmup: losses {[round(l, 5) for l in losses]}")
@@ -317,7 +323,8 @@ def main():
                             f"{args.steps} steps of one global batch in one pipelined call; ")
                          + (f"device budget {budget / 1e9:.0f} GB" if budget < (1 << 49) else "whole model resident")
                          + ("; paper schedule (one node per group, two weight slots)" if args.schedule == "paper"
-                            else "")),
+                            else "")
+                         + ("; weights retained across the steps of the call" if args.retain else "")),
             "global_batch": cfg.accum * cfg.batch,
             "seq_len": cfg.seq_len,
             "accum": cfg.accum,
@@ -356,6 +363,17 @@ def main():
                  **plan_info},
         "loss": losses[-1],
     }
+    if args.retain:
+        # loads amortised over the call; the gradients still leave every step
+        h2d_step = st.h2d_bytes / args.steps
+        t_link = max(h2d_step / (h2d_gbs * 1e9), plan.d2h_bytes / (d2h_gbs * 1e9))
+        result["retention"] = {
+            "h2d_bytes_per_step": round(h2d_step),
+            "d2h_bytes_per_step": round(st.d2h_bytes / args.steps),
+            "t_link_s": t_link,
+            "bound": "mfma" if t_mfma >= t_link else "link",
+            "frac": round(max(t_mfma, t_link) / (ms_per_step / 1e3), 4),
+        }
     if args.optimizer:
         t0 = time.perf_counter()
         A.atom_optimizer_init(sess.ctx)

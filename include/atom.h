@@ -238,6 +238,19 @@ int atom_step(atom_ctx* ctx, const int32_t* tokens, float* loss_out);
  * (ATOM_EINVAL; nothing is changed).  Synchronous. */
 int atom_steps(atom_ctx* ctx, const int32_t* tokens, int32_t n_steps, float* losses);
 
+/* Weight retention across the steps of one atom_steps call (default off).
+ * The host model does not change inside a global batch, and the paper keeps
+ * the sub-models that fit on the device from one iteration to the next (the
+ * embedding's, Section III-C; the last forward sub-model into the backward,
+ * Section IV).  With retention on and a plan that gives every group a weight
+ * slot of its own (n_slots >= n_groups), atom_steps loads each group once per
+ * call instead of once per step; gradients still leave the GPU every step and
+ * reach the host accumulators.  Results are bitwise those with retention off
+ * (same kernels, same order, same weights).  No effect when n_slots <
+ * n_groups, and none on calls other than atom_steps (atom_step is one step).
+ * The next call loads every group again.  ATOM_EINVAL for a NULL ctx. */
+int atom_set_retention(atom_ctx* ctx, int32_t on);
+
 /* Host optimizer (Section V-B: AdamW on the host CPUs once a global batch
  * is complete, learning rate 1e-4 after a linear warm-up, betas 0.9 and
  * 0.999).  atom_optimizer_init allocates fp32 master weights (copied from

@@ -93,6 +93,7 @@ _SIGS = {
     "atom_sync": (ctypes.c_int, [P, P]),
     "atom_step": (ctypes.c_int, [P, P, P]),
     "atom_steps": (ctypes.c_int, [P, P, ctypes.c_int32, P]),
+    "atom_set_retention": (ctypes.c_int, [P, ctypes.c_int32]),
     "atom_get_stats": (ctypes.c_int, [P, P]),
     "atom_probe_gemm": (ctypes.c_int, [P, I32, I32, I32]),
     "atom_probe_read": (ctypes.c_int, [P, P, P, P, P]),
@@ -297,6 +298,10 @@ def atom_step(ctx, tokens) -> float:
     v = ctypes.c_float()
     _check(lib().atom_step(ctx, p, _ref(v)), ctx)
     return v.value
+
+
+def atom_set_retention(ctx, on: bool):
+    _check(lib().atom_set_retention(ctx, int(bool(on))), ctx)
 
 
 def atom_steps(ctx, tokens) -> np.ndarray:

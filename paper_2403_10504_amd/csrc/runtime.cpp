@@ -181,6 +181,9 @@ struct atom_ctx {
   // engine after the kernel that wrote them, and restored on the H2D engine
   // once the last kernel that read the entry's later occupant has run.
   bool ck_host = false;
+  // weights retained across the steps of one atom_steps call (every group
+  // in a slot of its own); retain_active while such a call runs
+  bool retain = false, retain_active = false;
   uint8_t* h_ck = nullptr;                        // pinned [(L+1)][C][N][d] fp32
   std::vector<int> ck_holder;                     // per ring entry: index it holds (-1: none)
   std::vector<char> ck_wait;                      // per ring entry: a restore the compute stream has not waited for
@@ -265,7 +268,7 @@ inline int GI(atom_ctx* c, int par, int g) { return par * c->G + g; }
 // Weight slot of group g in a step of parity par (see the file comment).
 inline int slot_of(atom_ctx* c, int par, int g) {
   const int r = g % c->K;
-  return par == 0 ? r : c->K - 1 - r;
+  return par == 0 || c->retain_active ? r : c->K - 1 - r;
 }
 
 // Device entry of block input idx (the output of node idx) of a micro-batch.
@@ -710,6 +713,23 @@ void drop_residency(atom_ctx* c) {
   std::fill(c->need_wait.begin(), c->need_wait.end(), 0);
 }
 
+// Retained weights: group g's slot, loaded in an earlier step of the same
+// call, serves the step of parity par without a copy.  Every group runs in
+// every step, so the compute stream has already waited for that load (and
+// acquired the DMA-written data); kernels on it run in order, so the step of
+// parity par reads the slot only after the previous step is done with it.
+int hand_over(atom_ctx* c, int par, int g) {
+  const int gi = GI(c, par, g), pi = GI(c, par ^ 1, g);
+  if (!c->resident[pi] || c->need_wait[pi])
+    return fail(c, ATOM_ESTATE, "group " + std::to_string(g) + " was not used before its hand-over");
+  c->resident[pi] = 0;
+  c->resident[gi] = 1;
+  c->need_wait[gi] = 0;
+  c->lastuse_recorded[gi] = 0;
+  c->slot_owner[slot_of(c, par, g)] = gi;
+  return ATOM_OK;
+}
+
 // Token preprocessing on the host and an asynchronous upload on the compute
 // stream into token slot par.  Ids are validated before anything is copied.
 int upload_tokens(atom_ctx* c, int par, const int32_t* tokens) {
@@ -1071,10 +1091,17 @@ int run_steps(atom_ctx* c, const int32_t* tokens, int n, float* losses) {
   if (st != ATOM_OK) return st;
   drop_residency(c);
   std::fill(c->slot_owner.begin(), c->slot_owner.end(), -1);
+  // with retention and a slot per group, each group is loaded once per call
+  const bool keep = c->retain && G <= K;
+  c->retain_active = keep;
 #define STEP(expr)                  \
   do {                              \
     if ((st = (expr)) != ATOM_OK) { \
       sync_all(c);                  \
+      if (keep) {                   \
+        c->retain_active = false;   \
+        drop_residency(c);          \
+      }                             \
       return st;                    \
     }                               \
   } while (0)
@@ -1084,6 +1111,8 @@ int run_steps(atom_ctx* c, const int32_t* tokens, int n, float* losses) {
     const int par = s & 1, nxt = par ^ 1;
     const bool more = s + 1 < n;
     c->par = par;
+    if (keep && s > 0)
+      for (int g = 0; g < G; ++g) STEP(hand_over(c, par, g));
     // forward (the head also runs its backward and starts the residual gradient)
     for (int j = 0; j < G; ++j) {
       for (int node = p.first[j]; node <= p.last[j]; ++node)
@@ -1106,11 +1135,17 @@ int run_steps(atom_ctx* c, const int32_t* tokens, int n, float* losses) {
         }
       STEP(swap_out_impl(c, par, j));
       if (j - K >= 0) STEP(swap_in_impl(c, par, j - K));
-      else if (more) STEP(swap_in_impl(c, nxt, K - 1 - j));
+      else if (more && !keep) STEP(swap_in_impl(c, nxt, K - 1 - j));
     }
   }
 #undef STEP
   c->par = 0;
+  if (keep) {
+    // the next call loads everything again (the host model may change
+    // between calls), in the usual slot order
+    c->retain_active = false;
+    drop_residency(c);
+  }
   st = sync_all(c);
   if (st != ATOM_OK) return st;
   if (losses) {
@@ -1442,6 +1477,12 @@ int atom_steps(atom_ctx* c, const int32_t* tokens, int32_t n, float* losses) {
   c->stats.step_s = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count() / n;
   c->stats.host_accum_s = c->acc_seconds / n;
   return st;
+}
+
+int atom_set_retention(atom_ctx* c, int32_t on) {
+  if (!c) return ATOM_EINVAL;
+  c->retain = on != 0;
+  return ATOM_OK;
 }
 
 int atom_step(atom_ctx* c, const int32_t* tokens, float* loss_out) {

@@ -103,6 +103,10 @@ class Session:
         """Pipelined steps of one global batch; tokens [n][C][B][T+1]."""
         return A.atom_steps(self.ctx, tokens)
 
+    def set_retention(self, on: bool):
+        """Load each group once per steps() call when every group has a slot."""
+        A.atom_set_retention(self.ctx, on)
+
     def zero_grads(self):
         A.atom_zero_grads(self.ctx)
 

@@ -141,3 +141,74 @@ def test_gradient_slot_count_does_not_change_results():
         plan_for(cfg, last, 2, 1)
     with pytest.raises(A.AtomError):
         plan_for(cfg, last, 2, A.ATOM_MAX_GSLOTS + 1)
+
+
+def pipelined_retained(cfg, plan, tok, on=True):
+    with Session(cfg, plan=plan) as s:
+        s.load_weights()
+        s.set_retention(on)
+        losses = s.steps(tok)
+        st = s.stats()
+        # a second call loads everything again, and gives the same results
+        s.zero_grads()
+        again = s.steps(tok)
+        st2 = s.stats()
+        return losses, s.grads(A.GRAD_ACC), s.grads(A.GRAD_LAST), st, again, st2
+
+
+RETAIN_CASES = {
+    # one node per group, a slot each
+    "f32_singletons_all_slots": (TINY.with_(n_layer=3), lambda n: list(range(n)), 5),
+    # bf16 pairs, G = K = 3
+    "bf16_pairs_all_slots": (TINY.with_(dtype="bf16", n_layer=4), lambda n: [1, 3, 5], 3),
+    # bf16, two micro-batches per step (fp32 accumulation slot), G = K = 5
+    "bf16_accum2_all_slots": (TINY.with_(dtype="bf16", accum=2, n_layer=3), lambda n: list(range(n)), 5),
+    # fewer slots than groups: retention has no effect
+    "f32_singletons_k2": (TINY.with_(n_layer=3), lambda n: list(range(n)), 2),
+}
+
+
+@pytest.mark.parametrize("case", sorted(RETAIN_CASES))
+def test_retained_weights_equal_reloaded_weights(case):
+    cfg, last_fn, k = RETAIN_CASES[case]
+    n = cfg.n_nodes
+    last = last_fn(n)
+    if last[-1] != n - 1:
+        last = last + [n - 1]
+    plan = plan_for(cfg, last, k)
+    tok = tokens_for(cfg, 3)
+    l_ref, acc_ref, last_ref, st_ref = pipelined(cfg, plan, tok)
+    l_ret, acc_ret, last_ret, st_ret, again, st2 = pipelined_retained(cfg, plan, tok)
+    print(case, l_ref, l_ret, st_ref.h2d_bytes, st_ret.h2d_bytes, flush=True)
+    assert np.array_equal(l_ref, l_ret)
+    assert np.array_equal(l_ref, again)
+    assert_same(acc_ref, acc_ret)
+    assert_same(last_ref, last_ret)
+    assert st_ret.d2h_bytes == st_ref.d2h_bytes  # gradients still leave every step
+    assert st_ret.swap_outs == st_ref.swap_outs
+    assert st2.h2d_bytes == st_ret.h2d_bytes
+    if plan.n_slots >= plan.n_groups:
+        # each group loaded once per call instead of once per step
+        assert st_ret.h2d_bytes * 3 == st_ref.h2d_bytes
+        assert st_ret.swap_ins == plan.n_groups
+    else:
+        assert st_ret.h2d_bytes == st_ref.h2d_bytes
+
+
+def test_single_step_after_retained_call():
+    cfg = TINY.with_(n_layer=3)
+    plan = plan_for(cfg, list(range(cfg.n_nodes)), cfg.n_nodes)
+    tok = tokens_for(cfg, 3)
+    with Session(cfg, plan=plan) as s:
+        s.load_weights()
+        s.set_retention(True)
+        s.steps(tok[:2])
+        s.zero_grads()
+        l_after = s.step(tok[2])
+        g_after = s.grads(A.GRAD_ACC)
+    with Session(cfg, plan=plan) as s:
+        s.load_weights()
+        l_fresh = s.step(tok[2])
+        g_fresh = s.grads(A.GRAD_ACC)
+    assert l_after == l_fresh
+    assert_same(g_after, g_fresh)
