@@ -42,8 +42,8 @@ HBM_PEAK_GBS = 8000.0
 # --copy-calibration 2147483648`, each scaled by what the counter reads for
 # the plain copy kernel of known size (profiles/gemm_wgrad_6.7b_hbm_traffic.md).
 # Valid only for the kernel sources it was measured on.
-WGRAD_TRAFFIC = {"sources_sha256": "6e9bf278b4129018a04e2c5ea6aa5b6f14cd6f10040684980afd2456bcf1ebe5",
-                 "bytes_per_launch": 725677999}
+WGRAD_TRAFFIC = {"sources_sha256": "6b95969b8bedcd64d1c806cac43b3496df7bd74a1c7e50cdf07fa046c845cf33",
+                 "bytes_per_launch": 725704458}
 TRAFFIC_SOURCES = ("gemm.hip", "common.h", "launch.h")
 
 
