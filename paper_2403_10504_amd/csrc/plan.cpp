@@ -104,9 +104,9 @@ ArenaLayout arena_layout(const atom_config& c, uint64_t slot_bytes, int n_slots,
   a.loss_out = take(MAX_STEPS_PER_CALL * 4);
   a.splitk_bytes = SPLITK_BYTES;
   a.splitk = take(a.splitk_bytes);
-  // partial-sum scratch: column sums over ceil(N/64) row blocks, or LayerNorm
+  // partial-sum scratch: column sums over ceil(N/16) row blocks, or LayerNorm
   // partials (at most one per 8-row block, two rows of d each)
-  a.part_floats = std::max((N + 63) / 64 * std::max(3 * d, f), (N + 7) / 8 * 2 * d);
+  a.part_floats = std::max((N + 15) / 16 * std::max(3 * d, f), (N + 7) / 8 * 2 * d);
   // block workspace
   uint64_t w = 0;
   auto wtake = [&](uint64_t bytes) {

@@ -249,7 +249,10 @@ __global__ void __launch_bounds__(256) ln_bwd_wave_kernel(const T* __restrict__ 
 }
 
 // ------------------------------------------------------------- column sums
-constexpr int CS_ROWS = 64;
+// Rows per partial sum: 16, so that a [4096][4096] input gives 1024
+// workgroups (four per CU) whose loads are all issued before the first add
+// (64 rows per block left one workgroup per CU and 2 TB/s).
+constexpr int CS_ROWS = 16;
 
 // Column sums over CS_ROWS-row blocks, four consecutive columns per thread
 // (vector loads); cols and ld multiples of 4.  Each column is summed over its
@@ -262,13 +265,26 @@ __global__ void __launch_bounds__(256) colsum_partial4_kernel(const T* __restric
   const int64_t r0 = static_cast<int64_t>(blockIdx.y) * CS_ROWS;
   const int64_t r1 = min(rows, r0 + CS_ROWS);
   float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
-  for (int64_t r = r0; r < r1; ++r) {
-    Vec4<T> v;
-    v.load(x + r * ld + c);
-    s0 += v.get(0);
-    s1 += v.get(1);
-    s2 += v.get(2);
-    s3 += v.get(3);
+  if (r1 - r0 == CS_ROWS) {
+    Vec4<T> v[CS_ROWS];
+#pragma unroll
+    for (int i = 0; i < CS_ROWS; ++i) v[i].load(x + (r0 + i) * ld + c);
+#pragma unroll
+    for (int i = 0; i < CS_ROWS; ++i) {
+      s0 += v[i].get(0);
+      s1 += v[i].get(1);
+      s2 += v[i].get(2);
+      s3 += v[i].get(3);
+    }
+  } else {
+    for (int64_t r = r0; r < r1; ++r) {
+      Vec4<T> v;
+      v.load(x + r * ld + c);
+      s0 += v.get(0);
+      s1 += v.get(1);
+      s2 += v.get(2);
+      s3 += v.get(3);
+    }
   }
   *reinterpret_cast<float4*>(part + static_cast<int64_t>(blockIdx.y) * cols + c) = make_float4(s0, s1, s2, s3);
 }

@@ -246,4 +246,4 @@ def test_kernel_entry_points_validate_before_launch():
         A.atom_k_attn_fwd(A.ATOM_BF16, 4096, 4096, 4096, 1, 16, 1, 96)
     assert e.value.status == A.ATOM_EINVAL
     assert A.atom_k_layernorm_bwd_part_floats(100, 64) == 7 * 2 * 64
-    assert A.atom_k_colsum_part_floats(130, 10) == 3 * 10
+    assert A.atom_k_colsum_part_floats(130, 10) == 9 * 10  # blocks of 16 rows
