@@ -431,16 +431,34 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_dl_kernel(const bf16_t* __res
     for (int c = 0; c < NCT; ++c) acc_o[g][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
 
-  // load q of a thread: chunk q*256 + tid of the tile (row, slot)
+  // load q of a thread: chunk q*256 + tid of the tile (row, slot).  Its
+  // sources for key tile 0 are computed once; a whole tile adds the tile's
+  // row offset (a wave-uniform product), only the last, partial tile clamps
+  // its rows to the last key.
+  const bf16_t* ksrc[F::LPT];
+  const bf16_t* vsrc[F::LPT];
+#pragma unroll
+  for (int q = 0; q < F::LPT; ++q) {
+    const int id = q * 256 + tid, row = id / F::CPR, slot = id % F::CPR;
+    ksrc[q] = kb + static_cast<int64_t>(row) * ld + (slot ^ F::kswz(row)) * 8;
+    vsrc[q] = vb + static_cast<int64_t>(row) * ld + (slot ^ F::vswz(row)) * 8;
+  }
   auto load_tile = [&](int st, int j0) {
     const uint32_t kl = lds_offset(lds + st * F::STAGE), vl = kl + F::TILE;
+    const bool whole = j0 + BT <= Tn;
 #pragma unroll
     for (int q = 0; q < F::LPT; ++q) {
-      const int id = q * 256 + tid, row = id / F::CPR, slot = id % F::CPR;
-      const int64_t gr = static_cast<int64_t>(min(j0 + row, Tn - 1)) * ld;
       const uint32_t lo = __builtin_amdgcn_readfirstlane((q * 256 + w * 64) * 16);
-      lds_dma16(kb + gr + (slot ^ F::kswz(row)) * 8, kl + lo);
-      lds_dma16(vb + gr + (slot ^ F::vswz(row)) * 8, vl + lo);
+      if (whole) {
+        const int64_t off = static_cast<int64_t>(j0) * ld;
+        lds_dma16(ksrc[q] + off, kl + lo);
+        lds_dma16(vsrc[q] + off, vl + lo);
+      } else {
+        const int id = q * 256 + tid, row = id / F::CPR, slot = id % F::CPR;
+        const int64_t gr = static_cast<int64_t>(min(j0 + row, Tn - 1)) * ld;
+        lds_dma16(kb + gr + (slot ^ F::kswz(row)) * 8, kl + lo);
+        lds_dma16(vb + gr + (slot ^ F::vswz(row)) * 8, vl + lo);
+      }
     }
   };
   // fragment addresses inside a stage
