@@ -314,8 +314,18 @@ __global__ void __launch_bounds__(256) sum_parts_kernel(const float* __restrict_
   const int cl = threadIdx.x % SP_COLS, sl = threadIdx.x / SP_COLS;
   const int c = blockIdx.x * SP_COLS + cl;
   float s = 0.f;
-  if (c < cols)
-    for (int64_t p = sl; p < nparts; p += SP_SLICES) s += part[p * stride + c];
+  if (c < cols) {
+    // eight parts requested at a time, added in the same order as one by one
+    int64_t p = sl;
+    for (; p + 7 * SP_SLICES < nparts; p += 8 * SP_SLICES) {
+      float v[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = part[(p + i * SP_SLICES) * stride + c];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s += v[i];
+    }
+    for (; p < nparts; p += SP_SLICES) s += part[p * stride + c];
+  }
   sh[sl][cl] = s;
   __syncthreads();
   if (sl == 0 && c < cols) {
