@@ -301,6 +301,8 @@ def main():
     t_h2d_r0 = forced_h2d / (h2d_gbs * 1e9)
     t_h2d_r1 = plan.h2d_bytes / (h2d_gbs * 1e9)
     r0 = max(t_mfma, t_h2d_r0)
+    t_link_floor = max(plan.h2d_bytes / (h2d_gbs * 1e9), plan.d2h_bytes / (d2h_gbs * 1e9),
+                       (plan.h2d_bytes + plan.d2h_bytes) / (bidir_gbs * 1e9))
 
     result = {
         "metric": "training tokens/sec on 1 MI355X (swapped); % of max(MFMA, H2D) roofline",
@@ -356,6 +358,10 @@ def main():
             "bound": "mfma" if t_mfma >= t_h2d_r0 else "h2d",
             "frac_r0": round(r0 / (ms_per_step / 1e3), 4),
             "frac_r1": round(max(t_mfma, t_h2d_r1) / (ms_per_step / 1e3), 4),
+            # the host link with both directions counted: weights in, gradients
+            # out, each alone and both at once (pipelined steps overlap them)
+            "t_link_floor_s": t_link_floor,
+            "frac_link_floor": round(t_link_floor / (ms_per_step / 1e3), 4),
             "host_accum_ms": round(st.host_accum_s * 1e3, 2),
         },
         "plan": {"groups": plan.n_groups, "slots": plan.n_slots, "slot_mb": round(plan.slot_bytes / 1e6, 1),
