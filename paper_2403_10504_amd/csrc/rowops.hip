@@ -13,9 +13,8 @@ namespace {
 constexpr float LN_EPS = 1e-5f;
 
 // ---------------------------------------------------------------- LayerNorm
-// One 256-thread workgroup per row; thread t owns columns t, t+256, ...
-// (at most MAXE of them).  Reductions: wavefront shuffles, then the four
-// wave sums in order, so results do not depend on scheduling.
+// Workgroup reductions: wavefront shuffles, then the four wave sums in order,
+// so results do not depend on scheduling.
 __device__ __forceinline__ float block_sum4(float v, float* sh) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   v = wave_sum(v);
@@ -24,44 +23,6 @@ __device__ __forceinline__ float block_sum4(float v, float* sh) {
   const float r = (sh[0] + sh[1]) + (sh[2] + sh[3]);
   __syncthreads();
   return r;
-}
-
-template <typename T, int MAXE>
-__global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ x, const T* __restrict__ gamma,
-                                                     const T* __restrict__ beta, T* __restrict__ y,
-                                                     float* __restrict__ mean, float* __restrict__ rstd, int d) {
-  __shared__ float sh[4];
-  const int tid = threadIdx.x;
-  const int64_t row = blockIdx.x;
-  const float* xr = x + row * d;
-  float v[MAXE];
-  float s = 0.f;
-#pragma unroll
-  for (int i = 0; i < MAXE; ++i) {
-    const int c = tid + 256 * i;
-    v[i] = c < d ? xr[c] : 0.f;
-    s += v[i];
-  }
-  const float mu = block_sum4(s, sh) / static_cast<float>(d);
-  float q = 0.f;
-#pragma unroll
-  for (int i = 0; i < MAXE; ++i)
-    if (tid + 256 * i < d) {
-      const float t = v[i] - mu;
-      q += t * t;
-    }
-  const float var = block_sum4(q, sh) / static_cast<float>(d);
-  const float r = 1.f / sqrtf(var + LN_EPS);
-  T* yr = y + row * d;
-#pragma unroll
-  for (int i = 0; i < MAXE; ++i) {
-    const int c = tid + 256 * i;
-    if (c < d) yr[c] = from_f<T>((v[i] - mu) * r * to_f<T>(gamma[c]) + to_f<T>(beta[c]));
-  }
-  if (tid == 0) {
-    mean[row] = mu;
-    rstd[row] = r;
-  }
 }
 
 // Backward: LNB_ROWS consecutive rows per workgroup; per-thread partial
@@ -159,6 +120,61 @@ template <> struct Vec4<float> {
     *reinterpret_cast<float4*>(p) = make_float4(f[0], f[1], f[2], f[3]);
   }
 };
+
+// Forward, one workgroup per row: four consecutive columns per thread and
+// pass (16-byte loads of x, 8-byte bf16 stores), NV passes cover d.
+template <typename T, int NV>
+__global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ x, const T* __restrict__ gamma,
+                                                     const T* __restrict__ beta, T* __restrict__ y,
+                                                     float* __restrict__ mean, float* __restrict__ rstd, int d) {
+  __shared__ float sh[4];
+  const int tid = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const float* xr = x + row * d;
+  float v[NV][4];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = 4 * tid + 1024 * i;
+    const float4 t = c < d ? *reinterpret_cast<const float4*>(xr + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+    v[i][0] = t.x;
+    v[i][1] = t.y;
+    v[i][2] = t.z;
+    v[i][3] = t.w;
+    s += (t.x + t.y) + (t.z + t.w);
+  }
+  const float mu = block_sum4(s, sh) / static_cast<float>(d);
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i)
+    if (4 * tid + 1024 * i < d) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float t = v[i][e] - mu;
+        q += t * t;
+      }
+    }
+  const float var = block_sum4(q, sh) / static_cast<float>(d);
+  const float r = 1.f / sqrtf(var + LN_EPS);
+  T* yr = y + row * d;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = 4 * tid + 1024 * i;
+    if (c < d) {
+      Vec4<T> g, b;
+      g.load(gamma + c);
+      b.load(beta + c);
+      float o[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = (v[i][e] - mu) * r * g.get(e) + b.get(e);
+      Vec4<T>::store(yr + c, o);
+    }
+  }
+  if (tid == 0) {
+    mean[row] = mu;
+    rstd[row] = r;
+  }
+}
 
 template <typename T, int MAXCH>
 __global__ void __launch_bounds__(256) ln_bwd_wave_kernel(const T* __restrict__ dy, const float* __restrict__ x,
@@ -505,12 +521,10 @@ hipError_t ln_fwd_t(const float* x, const void* gamma, const void* beta, void* y
   auto b = static_cast<const T*>(beta);
   auto yy = static_cast<T*>(y);
 #define ATOM_LNF(E) hipLaunchKernelGGL((ln_fwd_kernel<T, E>), grid, block, 0, s, x, g, b, yy, mean, rstd, d)
-  if (ne <= 1) ATOM_LNF(1);
-  else if (ne <= 2) ATOM_LNF(2);
-  else if (ne <= 4) ATOM_LNF(4);
-  else if (ne <= 8) ATOM_LNF(8);
-  else if (ne <= 16) ATOM_LNF(16);
-  else ATOM_LNF(32);
+  if (ne <= 4) ATOM_LNF(1);
+  else if (ne <= 8) ATOM_LNF(2);
+  else if (ne <= 16) ATOM_LNF(4);
+  else ATOM_LNF(8);
 #undef ATOM_LNF
   return hipGetLastError();
 }
