@@ -602,6 +602,37 @@ __global__ void __launch_bounds__(256) attn_delta_kernel(const T* __restrict__ o
   }
 }
 
+// bf16: eight consecutive elements per thread (16-byte loads), DH/8 threads
+// per (row, head) summed by shuffles in a fixed order.  Head h of row r sits
+// at (r*H + h)*DH, so the pairs are contiguous and a workgroup reads one
+// contiguous range of O and of dO.
+template <int DH>
+__global__ void __launch_bounds__(256) attn_delta_bf16_kernel(const bf16_t* __restrict__ o,
+                                                              const bf16_t* __restrict__ dout,
+                                                              float* __restrict__ delta, int64_t n_pairs, int Tn,
+                                                              int H) {
+  constexpr int G = DH / 8;
+  const int64_t gid = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t idx = gid / G;
+  const int sub = static_cast<int>(gid % G);
+  float s = 0.f;
+  if (idx < n_pairs) {
+    const uint4 a = *reinterpret_cast<const uint4*>(o + idx * DH + 8 * sub);
+    const uint4 b = *reinterpret_cast<const uint4*>(dout + idx * DH + 8 * sub);
+    const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, bw[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      s += bf2f(aw[k] & 0xffff) * bf2f(bw[k] & 0xffff) + bf2f(aw[k] >> 16) * bf2f(bw[k] >> 16);
+  }
+#pragma unroll
+  for (int off = G / 2; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+  if (idx < n_pairs && sub == 0) {
+    const int64_t row = idx / H, bb = row / Tn, t = row % Tn;
+    const int h = static_cast<int>(idx % H);
+    delta[(bb * H + h) * Tn + t] = s;
+  }
+}
+
 // ------------------------------------------------------ backward: dK, dV
 template <typename T, int DH, int W>
 __global__ void __launch_bounds__(64 * W) attn_bwd_dkdv_kernel(const T* __restrict__ qkv,
@@ -1255,8 +1286,13 @@ hipError_t bwd_t(const void* qkv, const void* o, const void* dout, const float* 
                  int Tn, int H, hipStream_t s) {
   constexpr int W = ACfg<T, DH>::W;
   const int64_t n_rows = static_cast<int64_t>(B) * Tn;
-  hipLaunchKernelGGL(attn_delta_kernel<T>, dim3(static_cast<unsigned>((n_rows * H + 3) / 4)), dim3(256), 0, s,
-                     static_cast<const T*>(o), static_cast<const T*>(dout), delta, n_rows, Tn, H, DH);
+  if constexpr (sizeof(T) == 2)
+    hipLaunchKernelGGL(attn_delta_bf16_kernel<DH>, dim3(static_cast<unsigned>((n_rows * H * (DH / 8) + 255) / 256)),
+                       dim3(256), 0, s, static_cast<const bf16_t*>(o), static_cast<const bf16_t*>(dout), delta,
+                       n_rows * H, Tn, H);
+  else
+    hipLaunchKernelGGL(attn_delta_kernel<T>, dim3(static_cast<unsigned>((n_rows * H + 3) / 4)), dim3(256), 0, s,
+                       static_cast<const T*>(o), static_cast<const T*>(dout), delta, n_rows, Tn, H, DH);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if constexpr (sizeof(T) == 2)
