@@ -231,6 +231,13 @@ def test_ctx_create_rejects_bad_arguments_without_gpu():
     assert e.value.status == A.ATOM_EBUDGET
 
 
+def test_context_calls_reject_a_null_context_without_gpu():
+    for call in (lambda: A.atom_set_retention(None, True), lambda: A.atom_optimizer_init(None)):
+        with pytest.raises(A.AtomError) as e:
+            call()
+        assert e.value.status == A.ATOM_EINVAL
+
+
 def test_kernel_entry_points_validate_before_launch():
     # dtype and null-pointer checks return EINVAL without touching a device
     with pytest.raises(A.AtomError) as e:
