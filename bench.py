@@ -72,6 +72,33 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def host_digests(sess, which):
+    """SHA-256 of each node's host buffer `which` (raw bytes), hashed in parallel."""
+    import ctypes
+    import hashlib
+    from concurrent.futures import ThreadPoolExecutor
+
+    from paper_2403_10504_amd import atom as A
+
+    def one(node):
+        ptr, nbytes = A.atom_host_tensor(sess.ctx, node, which)
+        return hashlib.sha256((ctypes.c_char * nbytes).from_address(ptr)).hexdigest()
+
+    with ThreadPoolExecutor(8) as ex:
+        return list(ex.map(one, range(sess.n_nodes)))
+
+
+def blas_info():
+    """The BLAS numpy uses here: library, version, threading layer and thread count."""
+    from threadpoolctl import threadpool_info
+
+    out = []
+    for i in threadpool_info():
+        if i.get("user_api") == "blas":
+            out.append({k: i.get(k) for k in ("internal_api", "version", "threading_layer", "num_threads")})
+    return out
+
+
 def step_flops(cfg):
     """Algorithmic FLOPs of one training step (forward + backward, no recompute):
     6 per parameter per token for the linear layers (blocks and LM head) plus
@@ -104,6 +131,7 @@ def cpu_baseline(cfg):
     n_head_tok = cfg.batch * T
     with threadpool_limits(limits=cores):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        blas = blas_info()
         rng = np.random.default_rng(0)
         # weights handed over in fp64 so the timed region holds only the step's arithmetic
         p = {name: synthetic.gen_param(cfg, 1, name).astype(np.float64) for name, _, _ in synthetic.param_specs(cfg, 1)}
@@ -133,6 +161,8 @@ def cpu_baseline(cfg):
         "value": n_tok / t_step,
         "unit": "tokens/s",
         "cores": threads,
+        "affinity_cores": cores,
+        "blas": blas,
         "kind": "oracle",
         "sample": (f"fp64 NumPy oracle: one decoder block forward+backward on a {Ts}-token sequence "
                    f"({t_block:.2f} s, of which causal attention {t_attn:.2f} s) and the LM head + "
@@ -167,6 +197,9 @@ def main():
                     help="keep every group's weights on the device across the steps of the call when each group "
                          "has a slot of its own (atom_set_retention: loaded once per global batch, gradients "
                          "still copied out every step); not the default, which loads every weight every step")
+    ap.add_argument("--seq-steps", type=int, default=3,
+                    help="after the timed steps, time this many single-step calls (the survey-literal step: no "
+                         "cross-step overlap) and report their median beside the headline")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="run one plain device copy of BYTES before the timed steps (calibrates HBM byte counters)")
     args = ap.parse_args()
@@ -282,6 +315,37 @@ def main():
     if not all(math.isfinite(l) for l in losses):
         raise RuntimeError(f"non-finite loss: {losses}")
 
+    # Parity of the timed path: the last timed step's gradients and loss
+    # against one atom_step (no cross-step pipelining, nothing resident at its
+    # start) on the same tokens, bitwise.
+    t0 = time.perf_counter()
+    dig_timed = host_digests(sess, A.GRAD_LAST)
+    loss_seq = sess.step(tokens[args.steps - 1])
+    dig_seq = host_digests(sess, A.GRAD_LAST)
+    grad_check = {"kind": "last timed step vs one atom_step on the same tokens, bitwise",
+                  "loss_equal": bool(loss_seq == losses[-1]),
+                  "grads_equal": dig_timed == dig_seq,
+                  "nodes_differing": [i for i, (a, b) in enumerate(zip(dig_timed, dig_seq)) if a != b],
+                  "check_s": round(time.perf_counter() - t0, 2)}
+    log(f"parity check of the timed path: {grad_check}")
+    if not (grad_check["loss_equal"] and grad_check["grads_equal"]):
+        raise RuntimeError(f"the timed path differs from a single atom_step: {grad_check}")
+
+    # The survey-literal reading of a step: each step on its own (no weights
+    # resident at its start, the next step's loads not overlapping this step's
+    # gradient drain).  Timed over a few steps beside the pipelined headline.
+    seq_ms = None
+    if not args.sequential and args.seq_steps > 0:
+        times = []
+        for i in range(args.seq_steps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            sess.step(tokens[i % len(tokens)])
+            torch.cuda.synchronize()
+            times.append(time.perf_counter() - t0)
+        seq_ms = sorted(times)[len(times) // 2] * 1e3
+        log(f"sequential steps: {[round(t * 1e3, 1) for t in times]} ms (median {seq_ms:.1f})")
+
     ms_per_step = elapsed / args.steps * 1e3
     n_tok = cfg.accum * cfg.batch * cfg.seq_len
     tokens_per_s = n_tok / (ms_per_step / 1e3)
@@ -327,7 +391,9 @@ def main():
                          + ("; paper schedule (one node per group, two weight slots)" if args.schedule == "paper"
                             else "")
                          + ("; weights retained across the steps of the call" if args.retain else "")),
-            "global_batch": cfg.accum * cfg.batch,
+            "global_batch": args.steps * cfg.accum * cfg.batch,
+            "global_batch_unit": "sequences (timed steps x accum x batch)",
+            "micro_batch": cfg.batch,
             "seq_len": cfg.seq_len,
             "accum": cfg.accum,
             "device_budget_gb": round(budget / 1e9, 2) if budget < (1 << 49) else None,
@@ -364,6 +430,15 @@ def main():
             "frac_link_floor": round(t_link_floor / (ms_per_step / 1e3), 4),
             "host_accum_ms": round(st.host_accum_s * 1e3, 2),
         },
+        "sequential_step": None if seq_ms is None else {
+            "steps": args.seq_steps,
+            "ms_per_step": round(seq_ms, 3),
+            "tokens_per_s": round(n_tok / (seq_ms / 1e3), 1),
+            "frac_r0": round(r0 / (seq_ms / 1e3), 4),
+            "note": "each step alone: no weights resident at its start, the next step's loads do not overlap "
+                    "its gradient drain",
+        },
+        "grad_check": grad_check,
         "plan": {"groups": plan.n_groups, "slots": plan.n_slots, "slot_mb": round(plan.slot_bytes / 1e6, 1),
                  "arena_gb": round(plan.arena_bytes / 1e9, 3), "pred_step_ms": round(plan.pred_step_s * 1e3, 1),
                  **plan_info},

@@ -25,7 +25,11 @@
  * atom_plan.arena_bytes, e.g. a torch uint8 tensor) and the compute
  * stream; both must outlive the context.  The library never allocates
  * device memory.  Weight and gradient copies run on the GPU's system DMA
- * engines (one fixed engine per direction), issued by library threads.
+ * engines (one fixed engine per direction), issued by library threads.  The
+ * context therefore takes no copy streams: a copy queued on a HIP stream
+ * would run on HIP's own engine selection (device-to-host copies as a blit
+ * kernel that competes with the training kernels for compute units), so
+ * only the compute stream comes from the caller.
  * The library owns the pinned host model (weights in the working dtype), the
  * host gradient buffer (the last step's gradients in the working dtype) and
  * the fp32 gradient accumulators.  Pinned host memory: the weights, one
@@ -196,23 +200,32 @@ int atom_set_tokens(atom_ctx* ctx, const int32_t* tokens);
 
 /* --- the per-group calls atom_step composes (all asynchronous) --- */
 
-/* Swap group `group`'s weights into its slot on the H2D stream, after the
- * slot's previous occupant has finished its last compute.  ATOM_ESTATE if
- * the group is already resident. */
+/* Swap-in (Section IV: a second stream prefetches the next sub-model as soon
+ * as the current one starts; Section III-D: a sub-model is a contiguous group
+ * of nodes).  Copies group `group`'s weights from the pinned host model into
+ * its weight slot on the host-to-device system DMA engine; the copy is issued
+ * by a library worker thread once the slot's previous occupant has finished
+ * its last kernel (an event on the compute stream).  The first kernel of the
+ * group waits for the copy.  ATOM_ESTATE if the group is already resident. */
 int atom_swap_in(atom_ctx* ctx, int32_t group);
-/* Forward of one node for micro-batch `micro` on the compute stream.  Node 0
- * embeds the tokens; a block node writes its output checkpoint; node L+1
+/* Forward of one node (Section III-B: the GPT-3 layers; Section III-C:
+ * micro-batch `micro` of the C accumulated ones) on the compute stream.  Node
+ * 0 embeds the tokens; a block node writes its output checkpoint; node L+1
  * runs the final LayerNorm, the LM head, the cross-entropy and the head's
  * backward (it starts the gradient of the residual stream).  ATOM_ESTATE if
  * the node's group is not swapped in, or its input is not ready. */
 int atom_block_fwd(atom_ctx* ctx, int32_t node, int32_t micro);
-/* Backward of one node for micro-batch `micro`: a block restores its input
- * checkpoint, recomputes its forward and writes its gradients into the
- * group's gradient slot; node 0 runs the embedding backward.  Node L+1 has no
- * separate backward (ATOM_EINVAL). */
+/* Backward of one node for micro-batch `micro` (Section III-B; the last
+ * forward sub-model is reused by the backward, Section IV): a block restores
+ * its input checkpoint, recomputes its forward and writes its gradients into
+ * the group's gradient slot; node 0 runs the embedding backward.  Node L+1
+ * has no separate backward (ATOM_EINVAL). */
 int atom_block_bwd(atom_ctx* ctx, int32_t node, int32_t micro);
-/* Copy group `group`'s gradients to the host on the D2H stream, then (on a
- * host thread) add them to the fp32 accumulators.  Releases the group's
+/* Swap-out of a completed sub-model (Section IV).  Copies group `group`'s
+ * gradients to the pinned host gradient buffer on the device-to-host system
+ * DMA engine (issued by a library worker thread after the group's last
+ * backward kernel), then a host thread adds them to the fp32 accumulators
+ * (the gradient of the global batch, Section III-E).  Releases the group's
  * weight slot. */
 int atom_swap_out(atom_ctx* ctx, int32_t group);
 /* Wait for every stream and host accumulation; *loss_out (may be NULL)
@@ -282,6 +295,12 @@ int atom_optimizer_step(atom_ctx* ctx, const atom_adamw* hp, float grad_scale, i
  * entries; pass them to atom_plan_partition.  Synchronous. */
 int atom_profile_nodes(atom_ctx* ctx, const int32_t* tokens, atom_node_cost* out, int32_t n);
 
+/* The configuration and plan a context was created with (either pointer may
+ * be NULL).  Bindings use it to check host token arrays against
+ * [accum][batch][seq_len + 1] before a call reads them.  ATOM_EINVAL for a
+ * NULL ctx. */
+int atom_ctx_config(const atom_ctx* ctx, atom_config* cfg, atom_plan* plan);
+
 /* Per-step counters of the last atom_step / atom_steps call (bytes and
  * swap counts summed over its steps; times per step). */
 typedef struct atom_stats {
@@ -298,7 +317,9 @@ int atom_get_stats(atom_ctx* ctx, atom_stats* out);
  * their summed algorithmic FLOPs (2*M*N*K) and their summed algorithmic HBM
  * bytes (each operand read once, the output written once, plus the tensors
  * the epilogue reads: residual, pre-activation) since the probe was enabled.
- * epi < 0 disables the probe.  At most 4096 launches are recorded per step. */
+ * The LM head's weight gradient runs over the padded vocabulary but is
+ * counted at V rows.  epi < 0 disables the probe.  At most 4096 launches are
+ * recorded per step call (atom_step or atom_steps); later ones go untimed. */
 int atom_probe_gemm(atom_ctx* ctx, int32_t a_kcontig, int32_t b_kcontig, int32_t epi);
 int atom_probe_read(atom_ctx* ctx, int64_t* launches, double* seconds, double* flops, double* bytes);
 

@@ -95,6 +95,7 @@ _SIGS = {
     "atom_steps": (ctypes.c_int, [P, P, ctypes.c_int32, P]),
     "atom_set_retention": (ctypes.c_int, [P, ctypes.c_int32]),
     "atom_get_stats": (ctypes.c_int, [P, P]),
+    "atom_ctx_config": (ctypes.c_int, [P, P, P]),
     "atom_probe_gemm": (ctypes.c_int, [P, I32, I32, I32]),
     "atom_probe_read": (ctypes.c_int, [P, P, P, P, P]),
     "atom_link_bench": (ctypes.c_int, [P, U64, I32, P, P, P]),
@@ -261,13 +262,28 @@ def atom_zero_grads(ctx):
     _check(lib().atom_zero_grads(ctx), ctx)
 
 
-def _tokens_ptr(tokens):
+def atom_ctx_config(ctx):
+    """(atom_config, atom_plan) the context was created with."""
+    c, p = atom_config(), atom_plan()
+    _check(lib().atom_ctx_config(ctx, _ref(c), _ref(p)), ctx)
+    return c, p
+
+
+def _tokens_ptr(ctx, tokens, steps=False):
+    """int32 copy of `tokens` and its pointer, after checking the shape the C
+    side will read: [accum][batch][seq_len + 1], with a leading step count
+    for atom_steps."""
     t = np.ascontiguousarray(tokens, dtype=np.int32)
+    c, _ = atom_ctx_config(ctx)
+    want = (c.accum, c.batch, c.seq_len + 1)
+    if (t.shape[1:] if steps else t.shape) != want or (steps and (t.ndim != 4 or t.shape[0] < 1)):
+        lead = "[n_steps]" if steps else ""
+        raise ValueError(f"tokens must be {lead}[accum][batch][seq_len + 1] = {lead}{list(want)}, got {list(t.shape)}")
     return t, t.ctypes.data_as(P)
 
 
 def atom_set_tokens(ctx, tokens):
-    t, p = _tokens_ptr(tokens)
+    t, p = _tokens_ptr(ctx, tokens)
     _check(lib().atom_set_tokens(ctx, p), ctx)
 
 
@@ -294,7 +310,7 @@ def atom_sync(ctx) -> float:
 
 
 def atom_step(ctx, tokens) -> float:
-    t, p = _tokens_ptr(tokens)
+    t, p = _tokens_ptr(ctx, tokens)
     v = ctypes.c_float()
     _check(lib().atom_step(ctx, p, _ref(v)), ctx)
     return v.value
@@ -306,9 +322,7 @@ def atom_set_retention(ctx, on: bool):
 
 def atom_steps(ctx, tokens) -> np.ndarray:
     """tokens: int32 [n_steps][accum][batch][seq_len + 1]; returns the losses."""
-    t, p = _tokens_ptr(tokens)
-    if t.ndim != 4:
-        raise ValueError("tokens must be [n_steps][accum][batch][seq_len + 1]")
+    t, p = _tokens_ptr(ctx, tokens, steps=True)
     n = t.shape[0]
     out = np.zeros(n, dtype=np.float32)
     _check(lib().atom_steps(ctx, p, n, out.ctypes.data_as(P)), ctx)
@@ -338,7 +352,7 @@ def atom_profile_nodes(ctx, c: atom_config, tokens):
     """Measured node costs (ctypes array of atom_node_cost) from one step on `tokens`."""
     n = c.n_layer + 2
     out = (atom_node_cost * n)()
-    t, p = _tokens_ptr(tokens)
+    t, p = _tokens_ptr(ctx, tokens)
     _check(lib().atom_profile_nodes(ctx, p, out, n), ctx)
     return out
 

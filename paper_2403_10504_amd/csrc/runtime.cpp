@@ -1,6 +1,7 @@
 // Runtime of the swapped GPT step: the context, the pinned host model, the
-// swap engine (weights in on the H2D stream, gradients out on the D2H stream,
-// events between them and the compute stream), the composition of each
+// swap engine (weights in on one system DMA engine, gradients out on another,
+// each fed by its own worker thread that waits on compute-stream events), the
+// composition of each
 // node's forward and backward from the kernels, host-side gradient
 // accumulation, and the schedule of whole steps.
 //
@@ -82,6 +83,10 @@ class HostPool {
   }
   int size() const { return n_; }
   // Runs fn(i) for i in [0, n) on all threads; returns when all are done.
+  // Not reentrant (one job at a time): during steps only the accumulation
+  // thread calls it; the context's other users (zeroing, optimizer) first
+  // drain every copy and the accumulation queue (sync_all), so no two
+  // callers overlap.
   void run(const std::function<void(int)>& fn) {
     {
       std::lock_guard<std::mutex> l(m_);
@@ -379,7 +384,10 @@ int probe_collect(atom_ctx* c) {
 }
 
 // Every GEMM of the step goes through here so the probe can time it.
-hipError_t run_gemm(atom_ctx* c, const GemmArgs& g, bool akc, bool bkc, int epi) {
+// alg_m (if >= 0) is the algorithmic row count the probe counts instead of
+// g.M: the LM head's weight gradient runs over the padded vocabulary Vp but
+// computes V useful rows.
+hipError_t run_gemm(atom_ctx* c, const GemmArgs& g, bool akc, bool bkc, int epi, int alg_m = -1) {
   const bool probe = c->probe_epi == epi && c->probe_akc == static_cast<int>(akc) &&
                      c->probe_bkc == static_cast<int>(bkc) && c->probe_pending < PROBE_MAX;
   if (probe) {
@@ -393,16 +401,16 @@ hipError_t run_gemm(atom_ctx* c, const GemmArgs& g, bool akc, bool bkc, int epi)
   if (e != hipSuccess || !probe) return e;
   e = hipEventRecord(c->probe_ev[2 * c->probe_pending + 1], c->cs);
   if (e != hipSuccess) return e;
-  c->probe_flop[c->probe_pending] = 2.0 * g.M * g.N * static_cast<double>(g.K);
+  const double M = alg_m >= 0 ? alg_m : g.M;
+  c->probe_flop[c->probe_pending] = 2.0 * M * g.N * static_cast<double>(g.K);
   // algorithmic bytes: both operands read once, the output written once
   // (fp32 or the element type), plus what the epilogue reads
   const double ein = c->e;
   const double eout = (epi == EPI_STORE_F32 || epi == EPI_ACC_F32 || epi == EPI_BIAS_RESID) ? 4.0 : ein;
   double extra = 0.0;
-  if (epi == EPI_ACC_F32 || epi == EPI_BIAS_RESID) extra += 4.0 * g.M * g.N;
-  if (epi == EPI_BIAS_GELU || epi == EPI_GELU_BWD) extra += ein * g.M * g.N;
-  c->probe_byte[c->probe_pending] =
-      ein * (static_cast<double>(g.M) * g.K + static_cast<double>(g.K) * g.N) + eout * g.M * g.N + extra;
+  if (epi == EPI_ACC_F32 || epi == EPI_BIAS_RESID) extra += 4.0 * M * g.N;
+  if (epi == EPI_BIAS_GELU || epi == EPI_GELU_BWD) extra += ein * M * g.N;
+  c->probe_byte[c->probe_pending] = ein * (M * g.K + static_cast<double>(g.K) * g.N) + eout * M * g.N + extra;
   c->probe_pending += 1;
   return hipSuccess;
 }
@@ -580,7 +588,7 @@ int head_forward_backward(atom_ctx* c, int node, int micro) {
                    EPI_STORE));
   GradTarget t = gptr(c, node, T_WHEAD, micro);
   KCHK(c, run_gemm(c, gargs(dz, Vp, yhat, d, t.p, d, static_cast<int>(Vp), d, static_cast<int>(N)), false, false,
-                   wgrad_epi(t)));
+                   wgrad_epi(t), c->V));
   return ln_grad(c, dyhat, x, fmu, frs, wptr(c, node, T_LNFG), dres, dres_lp_out, false, part,
                  gptr(c, node, T_LNFG, micro), gptr(c, node, T_LNFB, micro));
 }
@@ -1416,7 +1424,9 @@ int atom_host_tensor(atom_ctx* c, int32_t node, int32_t which, void** ptr, uint6
 
 int atom_zero_grads(atom_ctx* c) {
   if (!c) return ATOM_EINVAL;
-  int s = wait_accum(c);
+  // gradient copies still in flight (e.g. from a manual atom_swap_out) end
+  // in an accumulation: wait for all of them, not only the queued ones
+  int s = sync_all(c);
   if (s != ATOM_OK) return s;
   memset(c->h_acc, 0, c->model_bytes / c->e * 4);
   return ATOM_OK;
@@ -1557,7 +1567,7 @@ int atom_link_bench(atom_ctx* c, uint64_t bytes, int32_t iters, double* h2d, dou
 
 int atom_optimizer_init(atom_ctx* c) {
   if (!c) return ATOM_EINVAL;
-  int st = wait_accum(c);
+  int st = sync_all(c);
   if (st != ATOM_OK) return st;
   const uint64_t n = c->model_bytes / c->e;
   float** bufs[] = {&c->h_master, &c->h_m, &c->h_v};
@@ -1702,6 +1712,13 @@ int atom_profile_nodes(atom_ctx* c, const int32_t* tokens, atom_node_cost* out, 
     out[i].t_fwd = f / c->C;
     out[i].t_bwd = b / c->C;
   }
+  return ATOM_OK;
+}
+
+int atom_ctx_config(const atom_ctx* c, atom_config* cfg, atom_plan* plan) {
+  if (!c) return ATOM_EINVAL;
+  if (cfg) *cfg = c->cfg;
+  if (plan) *plan = c->plan;
   return ATOM_OK;
 }
 

@@ -69,3 +69,21 @@ def dt_code(dtype):
 
 def sync():
     torch().cuda.synchronize()
+
+
+def host_digests(sess, which):
+    """SHA-256 of the raw bytes of each node's host buffer `which` (list over nodes).
+
+    Nodes are hashed in parallel (hashlib releases the GIL on large buffers)."""
+    import ctypes
+    import hashlib
+    from concurrent.futures import ThreadPoolExecutor
+
+    from paper_2403_10504_amd import atom as A
+
+    def one(node):
+        ptr, nbytes = A.atom_host_tensor(sess.ctx, node, which)
+        return hashlib.sha256((ctypes.c_char * nbytes).from_address(ptr)).hexdigest()
+
+    with ThreadPoolExecutor(8) as ex:
+        return list(ex.map(one, range(sess.n_nodes)))

@@ -111,8 +111,15 @@ def test_steps_rejects_bad_count_and_bad_ids():
     with Session(cfg) as s:
         s.load_weights()
         tok = tokens_for(cfg, 2)
-        with pytest.raises(A.AtomError):
+        with pytest.raises(ValueError):
             A.atom_steps(s.ctx, tok[:0])
+        # shapes the C side would read out of bounds are refused by the binding
+        with pytest.raises(ValueError):
+            s.steps(tok[:, :, :, :-1])
+        with pytest.raises(ValueError):
+            s.step(tok[0, 0])
+        with pytest.raises(ValueError):
+            A.atom_step(s.ctx, tok)
         bad = tok.copy()
         bad[1, 0, 0, 0] = cfg.vocab
         with pytest.raises(A.AtomError):
