@@ -99,6 +99,37 @@ def blas_info():
     return out
 
 
+RULES = {0: "paper: minimum cut among partitions meeting memory and overlap",
+         1: "fallback: no partition meets overlap; fastest memory-feasible", 2: "fixed partition"}
+
+
+def link_fit(sess, plan):
+    """Copy time against size on the step's DMA engines (Section III-B: loading
+    time grows linearly with a layer's size): t = a + bytes / r fitted by least
+    squares for each direction, with R^2."""
+    import numpy as np
+
+    from paper_2403_10504_amd import atom as A
+
+    cap = plan.n_slots * plan.slot_bytes // 2
+    sizes = [s for s in (4 << 20, 16 << 20, 64 << 20, 256 << 20, 1 << 30) if s <= cap]
+    rows = []
+    for size in sizes:
+        iters = max(2, (1 << 30) // size)
+        h, d, _ = A.atom_link_bench(sess.ctx, size, iters)
+        rows.append((size, size / (h * 1e9), size / (d * 1e9)))
+    out = {"sizes_mb": [round(r[0] / 2 ** 20, 1) for r in rows]}
+    x = np.array([r[0] for r in rows], np.float64)
+    for k, name in ((1, "h2d"), (2, "d2h")):
+        t = np.array([r[k] for r in rows])
+        b, a = np.polyfit(x, t, 1)
+        pred = a + b * x
+        r2 = 1.0 - float(np.sum((t - pred) ** 2)) / float(np.sum((t - t.mean()) ** 2))
+        out[name] = {"t_ms": [round(v * 1e3, 3) for v in t], "a_ms": round(a * 1e3, 4), "r_gbs": round(1 / b / 1e9, 2),
+                     "r2": round(r2, 6)}
+    return out
+
+
 def step_flops(cfg):
     """Algorithmic FLOPs of one training step (forward + backward, no recompute):
     6 per parameter per token for the linear layers (blocks and LM head) plus
@@ -200,6 +231,8 @@ def main():
     ap.add_argument("--seq-steps", type=int, default=3,
                     help="after the timed steps, time this many single-step calls (the survey-literal step: no "
                          "cross-step overlap) and report their median beside the headline")
+    ap.add_argument("--link-fit", action="store_true",
+                    help="fit copy time against size (t = a + bytes / r, R^2) on the step's DMA engines")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="run one plain device copy of BYTES before the timed steps (calibrates HBM byte counters)")
     args = ap.parse_args()
@@ -238,36 +271,43 @@ def main():
     n_batches = max(args.steps, args.warmup, 1)
     tokens = np.stack([synthetic.gen_tokens(cfg, seed=synthetic.TOKEN_SEED + i) for i in range(n_batches)])
 
-    plan_info = {"schedule": args.schedule, "costs": "analytic",
-                 "pred_step_ms_analytic": round(plan.pred_step_s * 1e3, 1)}
+    c = A.make_config(cfg)
+    link_bytes = min(1 << 30, plan.n_slots * plan.slot_bytes // 2)
+    h2d_gbs, d2h_gbs, bidir_gbs = A.atom_link_bench(sess.ctx, link_bytes, 4)
+    duplex = min(1.0, bidir_gbs / (h2d_gbs + d2h_gbs))
+    log(f"host link: H2D {h2d_gbs:.1f} GB/s, D2H {d2h_gbs:.1f} GB/s, both {bidir_gbs:.1f} GB/s "
+        f"(each direction at {duplex:.3f} of its rate alone while both run)")
+    fit = link_fit(sess, plan) if args.link_fit else None
+
+    # measured node costs (t^u, t^f, t^b, m_i of Section III-D) predict the
+    # timed call through the planner's schedule model
+    t0 = time.time()
+    costs = A.atom_profile_nodes(sess.ctx, c, tokens[0])
+    blk = costs[1]
+    log(f"node profile ({time.time() - t0:.1f} s): block load {blk.t_load * 1e3:.2f} ms, fwd {blk.t_fwd * 1e3:.2f} "
+        f"ms, bwd {blk.t_bwd * 1e3:.2f} ms, working memory {blk.mem_bytes / 1e6:.1f} MB")
+    plan_info = {"schedule": args.schedule, "costs": "analytic", "rule": RULES.get(plan.rule, plan.rule),
+                 "overlap_ok": bool(plan.overlap_ok), "cut_mb": round(plan.cut_bytes / 1e6, 1),
+                 "pred_step_ms_analytic": round(plan.pred_step_s * 1e3, 1),
+                 "pred_first_step_ms_analytic": round(plan.pred_first_step_s * 1e3, 1)}
+    plan_info["node_costs"] = {
+        name: {"t_load_ms": round(x.t_load * 1e3, 3), "t_store_ms": round(x.t_store * 1e3, 3),
+               "t_fwd_ms": round(x.t_fwd * 1e3, 3), "t_bwd_ms": round(x.t_bwd * 1e3, 3),
+               "mem_mb": round(x.mem_bytes / 1e6, 1), "weight_mb": round(x.weight_bytes / 1e6, 1)}
+        for name, x in (("embed", costs[0]), ("block", blk), ("head", costs[-1]))}
     if args.measured_plan:
-        c = A.make_config(cfg)
-        costs = A.atom_profile_nodes(sess.ctx, c, tokens[0])
-        blk = costs[1]
-        plan_info["node_costs_ms"] = {
-            "embed": [round(costs[0].t_load * 1e3, 3), round(costs[0].t_fwd * 1e3, 3), round(costs[0].t_bwd * 1e3, 3)],
-            "block": [round(blk.t_load * 1e3, 3), round(blk.t_fwd * 1e3, 3), round(blk.t_bwd * 1e3, 3)],
-            "head": [round(costs[-1].t_load * 1e3, 3), round(costs[-1].t_fwd * 1e3, 3), 0.0],
-            "order": "t_load, t_fwd, t_bwd per node (block: the first block)",
-        }
-        mplan = A.atom_plan_partition(c, budget, costs)
-        plan_info.update(costs="measured", pred_step_ms_measured=round(mplan.pred_step_s * 1e3, 1),
+        mplan = A.atom_plan_partition(c, budget, costs, duplex=duplex)
+        plan_info.update(costs="measured", rule=RULES.get(mplan.rule, mplan.rule),
                          analytic_groups=plan.n_groups, analytic_slots=plan.n_slots)
-        log(f"measured costs: block load {blk.t_load * 1e3:.2f} ms, fwd {blk.t_fwd * 1e3:.2f} ms, "
-            f"bwd {blk.t_bwd * 1e3:.2f} ms; plan {mplan.n_groups} groups, {mplan.n_slots} slots, "
-            f"predicted {mplan.pred_step_s * 1e3:.1f} ms")
-        if mplan.groups() != plan.groups() or mplan.n_slots != plan.n_slots:
+        log(f"measured-cost plan: {mplan.n_groups} groups, {mplan.n_slots} slots, "
+            f"predicted {mplan.pred_step_s * 1e3:.1f} ms per pipelined step")
+        if mplan.groups() != plan.groups() or mplan.n_slots != plan.n_slots or mplan.n_gslots != plan.n_gslots:
             sess.close()
             del sess
             sess = Session(cfg, plan=mplan)
             sess.load_weights()
-        else:
-            sess.zero_grads()
         plan = mplan
-
-    link_bytes = min(1 << 30, plan.n_slots * plan.slot_bytes // 2)
-    h2d_gbs, d2h_gbs, bidir_gbs = A.atom_link_bench(sess.ctx, link_bytes, 4)
-    log(f"host link: H2D {h2d_gbs:.1f} GB/s, D2H {d2h_gbs:.1f} GB/s, both {bidir_gbs:.1f} GB/s")
+    sess.zero_grads()
 
     def run(n):
         """n steps (tokens[i] for step i); returns the losses."""
@@ -314,6 +354,15 @@ def main():
         f"host accumulate {st.host_accum_s * 1e3:.1f} ms")
     if not all(math.isfinite(l) for l in losses):
         raise RuntimeError(f"non-finite loss: {losses}")
+
+    # the schedule model's prediction of this call and of one step alone
+    # (measured node costs, measured link sharing)
+    ends, _ = A.atom_plan_predict(c, plan, costs, duplex, min(args.steps, A.MAX_STEPS_PER_CALL))
+    pred_call = ends[-1] / len(ends)
+    pred_one = A.atom_plan_predict(c, plan, costs, duplex, 1)[0][0]
+    steady = ((ends[-1] - ends[-3]) / 2.0) if len(ends) >= 3 else None
+    log(f"predicted {pred_call * 1e3:.1f} ms per step of the call (steady {steady and steady * 1e3:.1f}), "
+        f"{pred_one * 1e3:.1f} ms for one step alone")
 
     # Parity of the timed path: the last timed step's gradients and loss
     # against one atom_step (no cross-step pipelining, nothing resident at its
@@ -439,6 +488,19 @@ def main():
                     "its gradient drain",
         },
         "grad_check": grad_check,
+        "prediction": {
+            "model": "event model of the schedule (compute stream, two DMA engines sharing the host link)",
+            "costs": "measured node costs (atom_profile_nodes) and the measured link sharing",
+            "duplex": round(duplex, 4),
+            "pred_ms_per_step": round(pred_call * 1e3, 1),
+            "measured_ms_per_step": round(elapsed / args.steps * 1e3, 1),
+            "err": round(pred_call / (elapsed / args.steps) - 1.0, 4),
+            "pred_steady_ms": None if steady is None else round(steady * 1e3, 1),
+            "pred_one_step_ms": round(pred_one * 1e3, 1),
+            "measured_one_step_ms": None if seq_ms is None else round(seq_ms, 1),
+            "err_one_step": None if seq_ms is None else round(pred_one / (seq_ms / 1e3) - 1.0, 4),
+        },
+        "link_fit": fit,
         "plan": {"groups": plan.n_groups, "slots": plan.n_slots, "slot_mb": round(plan.slot_bytes / 1e6, 1),
                  "arena_gb": round(plan.arena_bytes / 1e9, 3), "pred_step_ms": round(plan.pred_step_s * 1e3, 1),
                  **plan_info},

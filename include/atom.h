@@ -83,31 +83,63 @@ typedef struct atom_config {
                   * plan's h2d/d2h/forced byte counts include these copies. */
 } atom_config;
 
-/* Cost of one node of the augmented graph (Section III-D: the node's
- * loading time t^u, forward time t^f, backward time t^b; memory is its
- * weight bytes, which sets the slot it needs).  Times in seconds; t_fwd and
- * t_bwd are per micro-batch, t_bwd includes the forward recompute; t_store
- * is the time to copy the node's gradients back to the host. */
+/* Cost of one node of the augmented graph (Section III-D, problem
+ * definition: the node's maximum working memory m_i, forward time t^f,
+ * backward time t^b and loading time t^u).  weight_bytes is what a swap moves
+ * for the node (its weights; this sets the slot a group needs).  mem_bytes is
+ * m_i besides the weights: the device workspace the node's kernels use while
+ * it runs (activations, partial sums; every node recomputes its activations
+ * from its input checkpoint in the backward, so none of it outlives the node).
+ * cut_bytes is the size of the node's output tensor for one micro-batch, the
+ * tensor that crosses the cut when a group ends at this node (the fp32
+ * [batch][seq_len][d_model] residual stream; Table II lists it per model).
+ * Times in seconds; t_fwd and t_bwd are per micro-batch, t_bwd includes the
+ * forward recompute; t_store is the time to copy the node's gradients back to
+ * the host. */
 typedef struct atom_node_cost {
-  uint64_t weight_bytes;
+  uint64_t weight_bytes, mem_bytes, cut_bytes;
   double t_fwd, t_bwd, t_load, t_store;
 } atom_node_cost;
 
+/* Planner options.  strict = 1 keeps the paper's search result literally:
+ * only partitions that meet both the memory and the overlap constraint
+ * qualify, and ATOM_ENOPLAN is returned when none does.  strict = 0 falls
+ * back to the fastest memory-feasible partition when no partition meets the
+ * overlap constraint (atom_plan.rule = ATOM_RULE_TIME).  duplex is the rate
+ * of each copy direction while both directions run, relative to its rate
+ * alone (both share the host link; 0 selects ATOM_DEFAULT_DUPLEX). */
+#define ATOM_DEFAULT_DUPLEX 0.85
+typedef struct atom_plan_opts {
+  int32_t strict;
+  double duplex;
+} atom_plan_opts;
+
+/* How a plan was selected. */
+enum { ATOM_RULE_PAPER = 0, ATOM_RULE_TIME = 1, ATOM_RULE_FIXED = 2 };
+
 /* A partition of the chain into contiguous groups and its static layout.
- * Group g holds nodes first[g]..last[g] and uses weight slot g % n_slots;
+ * Group g holds nodes first[g]..last[g] and uses weight slot g % n_slots in
+ * even steps (n_slots-1-(g % n_slots) in odd steps of a pipelined call);
  * the last n_slots groups stay resident from the forward into the backward.
  * Gradients of a group go to one of n_gslots gradient slots (2 to 16, used
- * round-robin in backward order); a copy out to the host must finish before
+ * round-robin in claim order); a copy out to the host must finish before
  * its slot is reused, so more slots let the copies lag further behind the
  * backward.  arena_bytes = reserve_bytes + (n_slots + n_gslots) * slot_bytes
- * (+ 2 * slot_bytes fp32 accumulation slot for bf16 with accum > 1). */
+ * (+ 2 * slot_bytes fp32 accumulation slot for bf16 with accum > 1), where
+ * reserve_bytes holds the largest m_i.  cut_bytes is the total size of the
+ * tensors on the cut edges (Section III-D's selection criterion).
+ * Predicted times come from an event model of the schedule (the compute
+ * stream and the two copy engines, which share the host link at `duplex`):
+ * pred_first_step_s is one step alone (atom_step), pred_step_s a step of a
+ * pipelined call in steady state (atom_steps), pred_fwd_s the forward part of
+ * the first. */
 #define ATOM_MAX_GSLOTS 16
 typedef struct atom_plan {
-  int32_t n_nodes, n_groups, n_slots, overlap_ok, exhaustive, accum, n_gslots;
+  int32_t n_nodes, n_groups, n_slots, overlap_ok, exhaustive, accum, n_gslots, rule;
   int32_t first[ATOM_MAX_NODES], last[ATOM_MAX_NODES];
-  uint64_t budget_bytes, reserve_bytes, slot_bytes, arena_bytes;
-  uint64_t h2d_bytes, d2h_bytes, forced_h2d_bytes;
-  double pred_fwd_s, pred_step_s;
+  uint64_t budget_bytes, reserve_bytes, slot_bytes, arena_bytes, work_bytes;
+  uint64_t h2d_bytes, d2h_bytes, forced_h2d_bytes, cut_bytes;
+  double pred_fwd_s, pred_first_step_s, pred_step_s, duplex;
   int64_t n_evaluated;
 } atom_plan;
 
@@ -134,43 +166,64 @@ int atom_node_layout(const atom_config* cfg, int32_t node, atom_tensor_desc* out
 /* Analytic node costs for cfg (n = n_layer + 2 entries): FLOP counts at an
  * assumed MFMA rate and bytes at an assumed host-link rate (the values are
  * half the dense MFMA peak, i.e. 1.25 PFLOP/s bf16 or 78.65 TFLOP/s fp32, 50 GB/s
- * host link each way, 4 TB/s HBM for the embedding); callers may substitute
- * measured costs. */
+ * host link each way, 4 TB/s HBM for the embedding); mem_bytes is the
+ * workspace the arena carves for the node (blocks: the block workspace;
+ * head: the head workspace; embedding: none); callers may substitute
+ * measured costs (atom_profile_nodes). */
 int atom_node_costs(const atom_config* cfg, atom_node_cost* out, int32_t n);
 
 /* Device bytes the step needs besides weight and gradient slots
  * (checkpoints, activations, workspace, tokens). */
 int atom_reserve_bytes(const atom_config* cfg, uint64_t* out);
 
-/* Planner core (Algorithm 1 with the constraints and selection rule of
- * Section III-D: co-resident executing and prefetched groups, overlap as a
- * reported soft constraint, smallest predicted step time then fewest bytes loaded then fewest groups
- * then smallest end-node list): searches contiguous
- * partitions of `n` nodes with the given costs, a device budget and
- * `reserve` bytes of non-slot memory.  Exhaustive for n <= 20 nodes; for
- * longer chains it searches the structured family that identical decoder
- * blocks allow.  The memory model counts two gradient slots (n_gslots = 2).
- * Returns ATOM_ENOPLAN when no partition fits. */
-int atom_plan_search(const atom_config* cfg, uint64_t budget_bytes, uint64_t reserve_bytes,
-                     const atom_node_cost* costs, int32_t n, atom_plan* out);
+/* Planner core (Algorithm 1, Section III-D).  Searches the contiguous
+ * partitions of the n = cfg->n_layer + 2 nodes (node 0 the embedding, node
+ * n-1 the head) under
+ *   memory (hard): base_bytes + max_i mem_bytes + K * S + 2 S (+ 2 S fp32
+ *     accumulation slot for bf16 with accum > 1) <= budget, with S the
+ *     largest group's weight bytes and K = min(G, what fits) >= min(G, 2)
+ *     weight slots, so the executing and the prefetched group are
+ *     co-resident; budget left over becomes gradient slots (up to 16);
+ *   overlap: accum * t^f(g_j) >= t^u(g_{j+1}) for consecutive groups, and
+ *     accum * t^b(g_{j+1}) >= t^u(g_j) for every group loaded again in the
+ *     backward (j < G - K);
+ * and selects, among partitions meeting both, the one with the smallest
+ * total cut size, then the smallest predicted step time, then the smallest
+ * list of group end nodes (ATOM_RULE_PAPER).  When none meets the overlap
+ * constraint: ATOM_ENOPLAN if opts->strict, else the memory-feasible one with
+ * the smallest predicted step time, then fewest bytes loaded, then smallest
+ * cut, then end list (ATOM_RULE_TIME).  Exhaustive for n <= 16 nodes; longer
+ * chains search the structured family identical decoder blocks allow (the
+ * embedding alone or with the first block, the head alone or with the last,
+ * the remaining blocks in runs of s).  opts may be NULL (non-strict, default
+ * duplex).  ATOM_ENOPLAN when no partition fits the budget. */
+int atom_plan_search(const atom_config* cfg, uint64_t budget_bytes, uint64_t base_bytes,
+                     const atom_node_cost* costs, int32_t n, const atom_plan_opts* opts, atom_plan* out);
 
 /* atom_plan_partition: the static analysis of Section III-D for cfg under
- * a device budget.  costs == NULL uses atom_node_costs; the reserve comes
- * from atom_reserve_bytes.  Budget the search leaves unused becomes extra
- * gradient slots (up to ATOM_MAX_GSLOTS), which changes no transfer and no
- * result, only how far gradient copies may lag the backward.  Errors:
- * ATOM_EINVAL, ATOM_ENOPLAN. */
+ * a device budget.  costs == NULL uses atom_node_costs.  The arena carves
+ * each node's workspace at its analytic size, so a node's m_i counts as at
+ * least that.  opts may be NULL.  Errors: ATOM_EINVAL, ATOM_ENOPLAN. */
 int atom_plan_partition(const atom_config* cfg, uint64_t device_budget_bytes, const atom_node_cost* costs,
-                        int32_t n_costs, atom_plan* out);
+                        int32_t n_costs, const atom_plan_opts* opts, atom_plan* out);
 
 /* A plan for a given partition: group g ends at node last[g] (strictly
  * increasing, last[n_groups-1] = n_layer + 1), with n_slots weight slots
  * (1 <= n_slots <= n_groups, at least min(n_groups, 2)) and n_gslots
  * gradient slots (2..ATOM_MAX_GSLOTS).  Fills the slot
  * size, arena size and transfer bytes from the layout; predicted times use
- * the analytic costs.  ATOM_EINVAL for a malformed partition. */
+ * the analytic costs and the default duplex.  ATOM_EINVAL for a malformed
+ * partition. */
 int atom_plan_fixed(const atom_config* cfg, int32_t n_groups, const int32_t* last, int32_t n_slots,
                     int32_t n_gslots, atom_plan* out);
+
+/* Predicted end time of every step of one call of n_steps (1..64) steps of
+ * `plan` (n_steps = 1: atom_step; more: atom_steps) under node costs `costs`
+ * (NULL = analytic) and link sharing `duplex` (0 = default), from the event
+ * model atom_plan documents: ends[s] for s < n_steps; *fwd_s (may be NULL)
+ * the end of step 0's forward.  ATOM_EINVAL for a bad plan or count. */
+int atom_plan_predict(const atom_config* cfg, const atom_plan* plan, const atom_node_cost* costs, int32_t n_costs,
+                      double duplex, int32_t n_steps, double* ends, double* fwd_s);
 
 /* Create a context: validates cfg against plan, carves the arena, allocates
  * the pinned host model (zero weights; fill them through atom_host_tensor)
@@ -284,15 +337,20 @@ int atom_optimizer_init(atom_ctx* ctx);
 int atom_optimizer_step(atom_ctx* ctx, const atom_adamw* hp, float grad_scale, int32_t step);
 
 /* Measured node costs for the planner (the per-layer profile of Section
- * III-D: loading time t^u, forward time t^f, backward time t^b, plus the
- * time to store a node's gradients): each node's weights copied alone to the
- * device and its gradients back on the step's DMA engines (best of three),
- * and the kernel time of each node's forward and backward (per micro-batch,
- * HIP events on the compute stream) in a step of the context's plan on
- * `tokens` (host int32 [accum][batch][seq_len + 1]) that follows one
- * untimed step on the same tokens.  Both steps' gradients are added to the
- * accumulators like atom_step's.  out: n = n_layer + 2
- * entries; pass them to atom_plan_partition.  Synchronous. */
+ * III-D: loading time t^u, forward time t^f, backward time t^b and working
+ * memory m_i, plus the time to store a node's gradients): each node's weights
+ * copied alone to the device and its gradients back on the step's DMA engines
+ * (best of three); the kernel time of each node's forward and backward (per
+ * micro-batch, HIP events on the compute stream) in a step of the context's
+ * plan on `tokens` (host int32 [accum][batch][seq_len + 1]) that follows one
+ * untimed step on the same tokens; and mem_bytes, how far into the device
+ * workspace the node's kernels wrote (the workspace is filled with a marker
+ * word before each node runs and scanned after it; no workspace data outlives
+ * a node, so the results are those of an ordinary step).  cut_bytes is the
+ * node's output tensor (fp32 [batch][seq_len][d_model]; 4 for the head).
+ * Both steps' gradients are added to the accumulators like atom_step's.
+ * out: n = n_layer + 2 entries; pass them to atom_plan_partition or
+ * atom_plan_predict.  Synchronous. */
 int atom_profile_nodes(atom_ctx* ctx, const int32_t* tokens, atom_node_cost* out, int32_t n);
 
 /* The configuration and plan a context was created with (either pointer may

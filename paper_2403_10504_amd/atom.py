@@ -33,21 +33,35 @@ class atom_config(ctypes.Structure):
                 ("n_layer", "d_model", "n_head", "d_mlp", "vocab", "seq_len", "batch", "accum", "dtype", "ckpt")]
 
 
+ATOM_RULE_PAPER, ATOM_RULE_TIME, ATOM_RULE_FIXED = 0, 1, 2
+ATOM_DEFAULT_DUPLEX = 0.85
+COST_FIELDS = ("weight_bytes", "mem_bytes", "cut_bytes", "t_fwd", "t_bwd", "t_load", "t_store")
+
+
 class atom_node_cost(ctypes.Structure):
-    _fields_ = [("weight_bytes", ctypes.c_uint64), ("t_fwd", ctypes.c_double), ("t_bwd", ctypes.c_double),
+    _fields_ = [("weight_bytes", ctypes.c_uint64), ("mem_bytes", ctypes.c_uint64), ("cut_bytes", ctypes.c_uint64),
+                ("t_fwd", ctypes.c_double), ("t_bwd", ctypes.c_double),
                 ("t_load", ctypes.c_double), ("t_store", ctypes.c_double)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k in COST_FIELDS}
+
+
+class atom_plan_opts(ctypes.Structure):
+    _fields_ = [("strict", ctypes.c_int32), ("duplex", ctypes.c_double)]
 
 
 class atom_plan(ctypes.Structure):
     _fields_ = [("n_nodes", ctypes.c_int32), ("n_groups", ctypes.c_int32), ("n_slots", ctypes.c_int32),
                 ("overlap_ok", ctypes.c_int32), ("exhaustive", ctypes.c_int32), ("accum", ctypes.c_int32),
-                ("n_gslots", ctypes.c_int32),
+                ("n_gslots", ctypes.c_int32), ("rule", ctypes.c_int32),
                 ("first", ctypes.c_int32 * ATOM_MAX_NODES), ("last", ctypes.c_int32 * ATOM_MAX_NODES),
                 ("budget_bytes", ctypes.c_uint64), ("reserve_bytes", ctypes.c_uint64),
-                ("slot_bytes", ctypes.c_uint64), ("arena_bytes", ctypes.c_uint64),
+                ("slot_bytes", ctypes.c_uint64), ("arena_bytes", ctypes.c_uint64), ("work_bytes", ctypes.c_uint64),
                 ("h2d_bytes", ctypes.c_uint64), ("d2h_bytes", ctypes.c_uint64),
-                ("forced_h2d_bytes", ctypes.c_uint64), ("pred_fwd_s", ctypes.c_double),
-                ("pred_step_s", ctypes.c_double), ("n_evaluated", ctypes.c_int64)]
+                ("forced_h2d_bytes", ctypes.c_uint64), ("cut_bytes", ctypes.c_uint64),
+                ("pred_fwd_s", ctypes.c_double), ("pred_first_step_s", ctypes.c_double),
+                ("pred_step_s", ctypes.c_double), ("duplex", ctypes.c_double), ("n_evaluated", ctypes.c_int64)]
 
     def groups(self):
         return [(self.first[g], self.last[g]) for g in range(self.n_groups)]
@@ -78,8 +92,9 @@ _SIGS = {
     "atom_node_layout": (ctypes.c_int, [P, I32, P, I32, P, P]),
     "atom_node_costs": (ctypes.c_int, [P, P, I32]),
     "atom_reserve_bytes": (ctypes.c_int, [P, P]),
-    "atom_plan_search": (ctypes.c_int, [P, U64, U64, P, I32, P]),
-    "atom_plan_partition": (ctypes.c_int, [P, U64, P, I32, P]),
+    "atom_plan_search": (ctypes.c_int, [P, U64, U64, P, I32, P, P]),
+    "atom_plan_partition": (ctypes.c_int, [P, U64, P, I32, P, P]),
+    "atom_plan_predict": (ctypes.c_int, [P, P, P, I32, ctypes.c_double, I32, P, P]),
     "atom_plan_fixed": (ctypes.c_int, [P, I32, P, I32, I32, P]),
     "atom_ctx_create": (ctypes.c_int, [P, P, P, U64, P, P]),
     "atom_ctx_destroy": (None, [P]),
@@ -207,28 +222,49 @@ def atom_reserve_bytes(c: atom_config) -> int:
 
 
 def costs_array(costs):
-    """atom_node_cost array from a list of dicts (weight_bytes, t_fwd, t_bwd, t_load, t_store)."""
+    """atom_node_cost array from a list of dicts (COST_FIELDS; mem_bytes and cut_bytes default to 0)."""
+    if isinstance(costs, ctypes.Array):
+        return costs
     arr = (atom_node_cost * len(costs))()
     for i, x in enumerate(costs):
-        arr[i] = atom_node_cost(int(x["weight_bytes"]), x["t_fwd"], x["t_bwd"], x["t_load"], x["t_store"])
+        arr[i] = atom_node_cost(int(x["weight_bytes"]), int(x.get("mem_bytes", 0)), int(x.get("cut_bytes", 0)),
+                                x["t_fwd"], x["t_bwd"], x["t_load"], x["t_store"])
     return arr
 
 
-def atom_plan_search(c: atom_config, budget: int, reserve: int, costs) -> atom_plan:
+def _opts(strict=False, duplex=0.0):
+    return atom_plan_opts(int(bool(strict)), float(duplex))
+
+
+def atom_plan_search(c: atom_config, budget: int, base: int, costs, strict=False, duplex=0.0) -> atom_plan:
     p = atom_plan()
-    arr = costs if isinstance(costs, ctypes.Array) else costs_array(costs)
-    _check(lib().atom_plan_search(_ref(c), budget, reserve, arr, len(arr), _ref(p)))
+    arr = costs_array(costs)
+    o = _opts(strict, duplex)
+    _check(lib().atom_plan_search(_ref(c), budget, base, arr, len(arr), _ref(o), _ref(p)))
     return p
 
 
-def atom_plan_partition(c: atom_config, budget: int, costs=None) -> atom_plan:
+def atom_plan_partition(c: atom_config, budget: int, costs=None, strict=False, duplex=0.0) -> atom_plan:
     p = atom_plan()
+    o = _opts(strict, duplex)
     if costs is None:
-        _check(lib().atom_plan_partition(_ref(c), budget, None, 0, _ref(p)))
+        _check(lib().atom_plan_partition(_ref(c), budget, None, 0, _ref(o), _ref(p)))
     else:
-        arr = costs if isinstance(costs, ctypes.Array) else costs_array(costs)
-        _check(lib().atom_plan_partition(_ref(c), budget, arr, len(arr), _ref(p)))
+        arr = costs_array(costs)
+        _check(lib().atom_plan_partition(_ref(c), budget, arr, len(arr), _ref(o), _ref(p)))
     return p
+
+
+def atom_plan_predict(c: atom_config, plan: atom_plan, costs=None, duplex=0.0, n_steps=1):
+    """(step end times of one call of n_steps steps, forward end of step 0)."""
+    ends = (ctypes.c_double * n_steps)()
+    fwd = ctypes.c_double()
+    if costs is None:
+        _check(lib().atom_plan_predict(_ref(c), _ref(plan), None, 0, float(duplex), n_steps, ends, _ref(fwd)))
+    else:
+        arr = costs_array(costs)
+        _check(lib().atom_plan_predict(_ref(c), _ref(plan), arr, len(arr), float(duplex), n_steps, ends, _ref(fwd)))
+    return list(ends), fwd.value
 
 
 def atom_plan_fixed(c: atom_config, last_nodes, n_slots: int, n_gslots: int = 2) -> atom_plan:

@@ -78,6 +78,11 @@ hipError_t sum_fixed(const float* x, int64_t n, float* out, hipStream_t s);
 // fp32 -> element type conversion (n elements).
 hipError_t convert_f32(int dtype, const float* x, void* y, int64_t n, hipStream_t s);
 hipError_t fill_zero(void* p, int64_t bytes, hipStream_t s);
+// Working-memory probe: fill `bytes` (a multiple of 16, 16-byte aligned) with
+// a 32-bit word; high_water raises *out (a device counter) to 1 + the index of
+// the last 16-byte unit that no longer holds it.
+hipError_t fill_word(void* p, int64_t bytes, uint32_t word, hipStream_t s);
+hipError_t high_water(const void* p, int64_t bytes, uint32_t word, unsigned long long* out, hipStream_t s);
 // Streaming device copy of `bytes` (multiple of 16, 16-byte aligned).
 hipError_t copy_bytes(const void* src, void* dst, int64_t bytes, hipStream_t s);
 // Copy n 32-bit words on stream s by a kernel; src may be mapped pinned host

@@ -55,6 +55,7 @@ struct ArenaLayout {
   uint64_t ckpt, ckpt_bytes_each;  // (L+1) (host checkpoints: CKPT_RING) x accum x [N][d] fp32 block inputs
   uint64_t dres, dres_lp;          // accum x [N][d] fp32 / working dtype
   uint64_t loss_rows, loss_out;
+  uint64_t hwm;                    // 8-byte counters of the working-memory probe (atom_profile_nodes)
   uint64_t splitk, splitk_bytes;   // fp32 workspace for GEMMs split over k
   uint64_t ws;                     // start of the union workspace
   // block workspace (offsets inside ws)
@@ -62,6 +63,7 @@ struct ArenaLayout {
   // head workspace (offsets inside ws)
   uint64_t yhat, fmu, frs, logits, dz, dyhat, hpart;
   uint64_t ws_bytes, part_floats;
+  uint64_t block_ws, head_ws;      // workspace a block / the head uses (ws_bytes is the larger)
   uint64_t reserve_bytes;
   // slots (valid once a plan is known)
   uint64_t wslots, gslots, accslot;

@@ -484,6 +484,32 @@ __global__ void __launch_bounds__(256) fill_zero_kernel(uint4* __restrict__ p, i
   if (blockIdx.x == 0 && static_cast<int>(threadIdx.x) < ntail) tail[threadIdx.x] = 0;
 }
 
+__global__ void __launch_bounds__(256) fill_word_kernel(uint4* __restrict__ p, int64_t n16, uint32_t w) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n16;
+       i += static_cast<int64_t>(gridDim.x) * 256)
+    p[i] = make_uint4(w, w, w, w);
+}
+
+// *out = max(*out, 1 + index of the last 16-byte unit of p[0..n16) that
+// holds a word other than w); *out is left alone if every unit still holds w.
+__global__ void __launch_bounds__(256) high_water_kernel(const uint4* __restrict__ p, int64_t n16, uint32_t w,
+                                                         unsigned long long* __restrict__ out) {
+  unsigned long long hi = 0;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n16;
+       i += static_cast<int64_t>(gridDim.x) * 256) {
+    const uint4 v = p[i];
+    if (v.x != w || v.y != w || v.z != w || v.w != w) hi = static_cast<unsigned long long>(i) + 1;
+  }
+  __shared__ unsigned long long red[256];
+  red[threadIdx.x] = hi;
+  __syncthreads();
+  for (int k = 128; k > 0; k >>= 1) {
+    if (static_cast<int>(threadIdx.x) < k) red[threadIdx.x] = red[threadIdx.x + k] > red[threadIdx.x] ? red[threadIdx.x + k] : red[threadIdx.x];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0 && red[0] > 0) atomicMax(out, red[0]);
+}
+
 // Streaming copy, 16 bytes per thread and iteration.
 __global__ void __launch_bounds__(256) copy16_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst,
                                                      int64_t n16) {
@@ -725,6 +751,24 @@ hipError_t copy_bytes(const void* src, void* dst, int64_t bytes, hipStream_t s) 
   const unsigned grid = static_cast<unsigned>(want < 8192 ? (want < 1 ? 1 : want) : 8192);
   hipLaunchKernelGGL(copy16_kernel, dim3(grid), dim3(256), 0, s, static_cast<const uint4*>(src),
                      static_cast<uint4*>(dst), n16);
+  return hipGetLastError();
+}
+
+hipError_t fill_word(void* p, int64_t bytes, uint32_t word, hipStream_t s) {
+  if (bytes <= 0) return hipSuccess;
+  if ((reinterpret_cast<uintptr_t>(p) | static_cast<uintptr_t>(bytes)) & 15) return hipErrorInvalidValue;
+  const int64_t n16 = bytes / 16;
+  hipLaunchKernelGGL(fill_word_kernel, dim3(grid_for(n16)), dim3(256), 0, s, static_cast<uint4*>(p), n16, word);
+  return hipGetLastError();
+}
+
+hipError_t high_water(const void* p, int64_t bytes, uint32_t word, unsigned long long* out, hipStream_t s) {
+  if (bytes <= 0) return hipSuccess;
+  if ((reinterpret_cast<uintptr_t>(p) | static_cast<uintptr_t>(bytes)) & 15) return hipErrorInvalidValue;
+  const int64_t n16 = bytes / 16;
+  const int64_t want = (n16 + 255) / 256;
+  const unsigned grid = static_cast<unsigned>(want < 4096 ? (want < 1 ? 1 : want) : 4096);
+  hipLaunchKernelGGL(high_water_kernel, dim3(grid), dim3(256), 0, s, static_cast<const uint4*>(p), n16, word, out);
   return hipGetLastError();
 }
 

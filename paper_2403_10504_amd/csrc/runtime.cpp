@@ -961,6 +961,16 @@ int ckpt_ready(atom_ctx* c, int idx, int micro) {
   return ATOM_OK;
 }
 
+// Working-memory probe (atom_profile_nodes): the union workspace is filled
+// with this word before each node runs, and a counter per node and direction
+// records how far into the workspace the node's kernels wrote.  No data in
+// the workspace outlives the node that wrote it, so the fill changes nothing.
+constexpr uint32_t HWM_WORD = 0xFFC0FFEEu;  // a NaN in fp32, two NaNs in bf16
+
+unsigned long long* hwm_counter(atom_ctx* c, int node, int dir) {
+  return reinterpret_cast<unsigned long long*>(A(c, c->lay.hwm)) + 2 * node + dir;
+}
+
 int fwd_impl(atom_ctx* c, int node, int micro) {
   const int par = c->par;
   if (!c->tokens_ok[par]) return fail(c, ATOM_ESTATE, "tokens not set");
@@ -979,12 +989,18 @@ int fwd_impl(atom_ctx* c, int node, int micro) {
     }
   }
   const size_t pe = (static_cast<size_t>(node) * c->C + micro) * 4;
-  if (c->profiling) HIPCHK(c, hipEventRecord(c->prof_ev[pe], c->cs));
+  if (c->profiling) {
+    KCHK(c, fill_word(WS(c, 0), static_cast<int64_t>(c->lay.ws_bytes), HWM_WORD, c->cs));
+    HIPCHK(c, hipEventRecord(c->prof_ev[pe], c->cs));
+  }
   if (node == 0) st = embed_forward(c, micro);
   else if (node <= c->L) st = block_forward(c, node, micro, false);
   else st = head_forward_backward(c, node, micro);
   if (st != ATOM_OK) return st;
-  if (c->profiling) HIPCHK(c, hipEventRecord(c->prof_ev[pe + 1], c->cs));
+  if (c->profiling) {
+    HIPCHK(c, hipEventRecord(c->prof_ev[pe + 1], c->cs));
+    KCHK(c, high_water(WS(c, 0), static_cast<int64_t>(c->lay.ws_bytes), HWM_WORD, hwm_counter(c, node, 0), c->cs));
+  }
   if (c->ck_host) {
     if (node > 0 && (st = ckpt_used(c, ck_entry(c, node - 1, micro))) != ATOM_OK) return st;
     if (node <= c->L && (st = ckpt_used(c, ck_entry(c, node, micro))) != ATOM_OK) return st;
@@ -1005,10 +1021,16 @@ int bwd_impl(atom_ctx* c, int node, int micro) {
   if (st != ATOM_OK) return st;
   if (c->ck_host && node > 0 && (st = ckpt_ready(c, node - 1, micro)) != ATOM_OK) return st;
   const size_t pe = (static_cast<size_t>(node) * c->C + micro) * 4 + 2;
-  if (c->profiling) HIPCHK(c, hipEventRecord(c->prof_ev[pe], c->cs));
+  if (c->profiling) {
+    KCHK(c, fill_word(WS(c, 0), static_cast<int64_t>(c->lay.ws_bytes), HWM_WORD, c->cs));
+    HIPCHK(c, hipEventRecord(c->prof_ev[pe], c->cs));
+  }
   st = node == 0 ? embed_backward(c, micro) : block_backward(c, node, micro);
   if (st != ATOM_OK) return st;
-  if (c->profiling) HIPCHK(c, hipEventRecord(c->prof_ev[pe + 1], c->cs));
+  if (c->profiling) {
+    HIPCHK(c, hipEventRecord(c->prof_ev[pe + 1], c->cs));
+    KCHK(c, high_water(WS(c, 0), static_cast<int64_t>(c->lay.ws_bytes), HWM_WORD, hwm_counter(c, node, 1), c->cs));
+  }
   if (c->ck_host && node > 0 && (st = ckpt_used(c, ck_entry(c, node - 1, micro))) != ATOM_OK) return st;
   c->bwd_done[par][k] = 1;
   return finish_group_use(c, node);
@@ -1692,11 +1714,15 @@ int atom_profile_nodes(atom_ctx* c, const int32_t* tokens, atom_node_cost* out, 
   // the timed one
   st = run_steps(c, tokens, 1, nullptr);
   if (st != ATOM_OK) return st;
+  KCHK(c, fill_zero(A(c, c->lay.hwm), static_cast<int64_t>(n) * 2 * 8, c->cs));
   c->profiling = true;
   c->stats = atom_stats{};
   st = run_steps(c, tokens, 1, nullptr);
   c->profiling = false;
   if (st != ATOM_OK) return st;
+  std::vector<unsigned long long> hwm(static_cast<size_t>(n) * 2);
+  HIPCHK(c, hipMemcpy(hwm.data(), A(c, c->lay.hwm), hwm.size() * 8, hipMemcpyDeviceToHost));
+  const uint64_t cut = static_cast<uint64_t>(c->N) * c->d * 4;
   for (int i = 0; i < n; ++i) {
     double f = 0, b = 0;
     for (int m = 0; m < c->C; ++m) {
@@ -1711,6 +1737,8 @@ int atom_profile_nodes(atom_ctx* c, const int32_t* tokens, atom_node_cost* out, 
     }
     out[i].t_fwd = f / c->C;
     out[i].t_bwd = b / c->C;
+    out[i].mem_bytes = 16 * std::max(hwm[2 * i], hwm[2 * i + 1]);
+    out[i].cut_bytes = i <= c->L ? cut : 4;
   }
   return ATOM_OK;
 }

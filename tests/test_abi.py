@@ -29,7 +29,7 @@ def header_functions():
 def test_library_exports_every_declared_function():
     lib = A.lib()
     declared = header_functions()
-    assert len(declared) >= 30
+    assert len(declared) >= 32
     for name in declared:
         assert hasattr(lib, name), name
     assert set(declared) == set(A.EXPORTED)
@@ -90,15 +90,13 @@ def test_reserve_and_partition_fit_budget():
         # leftover budget becomes gradient slots, up to the limit
         assert 2 <= p.n_gslots <= A.ATOM_MAX_GSLOTS
         assert p.n_gslots == A.ATOM_MAX_GSLOTS or budget - p.arena_bytes < p.slot_bytes
-        # the search itself (Algorithm 1's memory model) counts two gradient slots
-        q = A.atom_plan_search(c, budget, r, A.atom_node_costs(c))
-        assert q.n_gslots == 2 and q.groups() == groups_of(p) and q.n_slots == p.n_slots
+        # the reserve holds the largest working memory of a node (m_i)
+        costs = A.atom_node_costs(c)
+        assert p.work_bytes == max(x.mem_bytes for x in costs) > 0
+        q = A.atom_plan_search(c, budget, r - p.work_bytes, costs)
+        assert q.groups() == p.groups() and q.n_slots == p.n_slots and q.n_gslots == p.n_gslots
         groups = p.groups()
         assert groups[0][0] == 0 and groups[-1][1] == cfg.n_layer + 1
-
-
-def groups_of(p):
-    return p.groups()
 
 
 def test_budget_too_small_is_enoplan():
@@ -152,64 +150,122 @@ def random_costs(rng, n, tiers=True):
     out = []
     for i in range(n):
         w = int(rng.integers(1, 6)) * 256 if tiers else int(rng.integers(1, 10 ** 6))
-        out.append(dict(weight_bytes=w, t_fwd=float(rng.choice([0.5, 1.0, 1.5, 2.0])),
-                        t_bwd=float(rng.choice([1.0, 2.0, 3.0])), t_load=float(rng.choice([0.25, 1.0, 2.0, 4.0])),
-                        t_store=float(rng.choice([0.5, 1.0, 3.0]))))
+        out.append(dict(weight_bytes=w, mem_bytes=int(rng.integers(0, 4)) * 128, cut_bytes=int(rng.choice([64, 64, 96])),
+                        t_fwd=float(rng.choice([0.5, 1.0, 1.5, 2.0])), t_bwd=float(rng.choice([1.0, 2.0, 3.0])),
+                        t_load=float(rng.choice([0.25, 1.0, 2.0, 4.0])), t_store=float(rng.choice([0.5, 1.0, 3.0]))))
+    out[-1]["t_bwd"] = 0.0  # the head's backward runs inside its forward
     return out
 
 
-def _compare(c, costs, budget, reserve, accum, dtype, want):
+def ck_times(cfg, costs):
+    """Host-checkpoint copy times the C planner derives: one node's block input
+    (all micro-batches) at the costs' average link rates."""
+    if not cfg.ckpt_host:
+        return {}
+    ckb = float(cfg.accum * cfg.batch * cfg.seq_len * cfg.d_model * 4)
+    w = sum(x["weight_bytes"] for x in costs)
+    tl = sum(x["t_load"] for x in costs)
+    ts = sum(x["t_store"] for x in costs)
+    return dict(n_layer=cfg.n_layer, ck_host=True, t_ck_in=ckb * (tl / w), t_ck_out=ckb * (ts / w))
+
+
+def _compare(c, cfg, costs, budget, base, want, strict=False, duplex=A.ATOM_DEFAULT_DUPLEX):
     try:
-        got = A.atom_plan_search(c, budget, reserve, costs)
+        got = A.atom_plan_search(c, budget, base, costs, strict=strict, duplex=duplex)
     except A.AtomError as e:
         assert e.status == A.ATOM_ENOPLAN and want is None
-        return
+        return None
     assert want is not None
     assert got.groups() == want["groups"]
-    assert got.n_slots == want["n_slots"]
+    assert (got.n_slots, got.n_gslots) == (want["n_slots"], want["n_gslots"])
     assert got.slot_bytes == want["slot_bytes"]
     assert got.arena_bytes == want["arena_bytes"]
-    assert got.pred_step_s == want["pred_step_s"]  # bit-identical: same sums and maxima
+    assert got.cut_bytes == want["cut_bytes"]
+    assert got.rule == (A.ATOM_RULE_PAPER if want["rule"] == "paper" else A.ATOM_RULE_TIME)
+    # bit-identical: the same sums, maxima and event arithmetic
+    assert got.pred_step_s == want["pred_step_s"]
+    assert got.pred_first_step_s == want["pred_first_step_s"]
     assert got.pred_fwd_s == want["pred_fwd_s"]
     assert bool(got.overlap_ok) == want["overlap_ok"]
-    assert (got.h2d_bytes, got.d2h_bytes) == (want["h2d_bytes"], want["d2h_bytes"])
+    ck = cfg.accum * cfg.batch * cfg.seq_len * cfg.d_model * 4 * max(0, cfg.n_layer + 1 - 4) if cfg.ckpt_host else 0
+    assert (got.h2d_bytes, got.d2h_bytes) == (want["h2d_bytes"] + ck, want["d2h_bytes"] + ck)
+    return got
 
 
-@pytest.mark.parametrize("seed", range(40))
+@pytest.mark.parametrize("seed", range(64))
 def test_planner_matches_brute_force(seed):
     rng = np.random.default_rng(seed)
-    n = int(rng.integers(1, 12))
+    n = int(rng.integers(3, 11))
     costs = random_costs(rng, n)
     accum = int(rng.choice([1, 2, 4]))
     dtype = int(rng.choice([OP.F32, OP.BF16]))
-    reserve = int(rng.integers(0, 4096))
+    ck_host = n >= 6 and bool(rng.integers(0, 2))
+    strict = bool(rng.integers(0, 2))
+    duplex = float(rng.choice([0.5, 0.85, 1.0]))
+    base = int(rng.integers(0, 4096))
     total = sum(c["weight_bytes"] for c in costs)
-    budget = reserve + int(rng.integers(2 * 256, 6 * total + 1024))
-    c = A.make_config(TINY.with_(accum=accum, dtype="bf16" if dtype == OP.BF16 else "f32"))
-    want = OP.brute_force(costs, budget, reserve, accum, dtype)
-    _compare(c, costs, budget, reserve, accum, dtype, want)
+    budget = base + 384 + int(rng.integers(total // 2 + 256, 5 * total // 2 + 1024))
+    cfg = TINY.with_(n_layer=n - 2, accum=accum, dtype="bf16" if dtype == OP.BF16 else "f32", ckpt_host=ck_host)
+    c = A.make_config(cfg)
+    want = OP.brute_force(costs, budget, base, accum, dtype, strict=strict, duplex=duplex, **ck_times(cfg, costs))
+    _compare(c, cfg, costs, budget, base, want, strict, duplex)
+
+
+def test_planner_rules_through_the_abi():
+    # the oracle's hand cases, through the C planner
+    cfg = TINY.with_(n_layer=2)
+    c = A.make_config(cfg)
+    def uni(tf, tb, tu, ts, cut=7):
+        out = [dict(weight_bytes=100, mem_bytes=0, cut_bytes=cut, t_fwd=tf, t_bwd=tb, t_load=tu, t_store=ts)
+               for _ in range(4)]
+        out[3]["t_bwd"] = 0.0
+        return out
+    # minimum cut among overlapping partitions beats the faster one
+    got = A.atom_plan_search(c, 4 * 200, 0, uni(2.0, 4.0, 1.0, 1.0))
+    assert got.groups() == [(0, 1), (2, 3)] and got.rule == A.ATOM_RULE_PAPER and got.overlap_ok
+    # nothing overlaps: strict mode has no plan, the fallback is the fastest
+    slow = uni(0.1, 0.2, 5.0, 5.0)
+    with pytest.raises(A.AtomError) as e:
+        A.atom_plan_search(c, 600, 0, slow, strict=True)
+    assert e.value.status == A.ATOM_ENOPLAN
+    got = A.atom_plan_search(c, 600, 0, slow)
+    assert got.rule == A.ATOM_RULE_TIME and not got.overlap_ok
 
 
 @pytest.mark.parametrize("seed", range(6))
 def test_planner_structured_search_for_long_chains(seed):
     rng = np.random.default_rng(100 + seed)
-    L = int(rng.integers(19, 30))
-    blk = dict(weight_bytes=4096, t_fwd=1.0, t_bwd=3.0, t_load=float(rng.choice([0.5, 2.0, 8.0])), t_store=2.0)
-    emb = dict(weight_bytes=int(rng.choice([2048, 8192])), t_fwd=0.1, t_bwd=0.1, t_load=1.0, t_store=1.0)
-    head = dict(weight_bytes=int(rng.choice([4096, 12288])), t_fwd=2.0, t_bwd=0.0, t_load=3.0, t_store=3.0)
+    L = int(rng.integers(15, 30))
+    blk = dict(weight_bytes=4096, mem_bytes=1024, cut_bytes=64, t_fwd=1.0, t_bwd=3.0,
+               t_load=float(rng.choice([0.5, 2.0, 8.0])), t_store=2.0)
+    emb = dict(weight_bytes=int(rng.choice([2048, 8192])), mem_bytes=0, cut_bytes=64, t_fwd=0.1, t_bwd=0.1,
+               t_load=1.0, t_store=1.0)
+    head = dict(weight_bytes=int(rng.choice([4096, 12288])), mem_bytes=2048, cut_bytes=4, t_fwd=2.0, t_bwd=0.0,
+                t_load=3.0, t_store=3.0)
     costs = [emb] + [dict(blk) for _ in range(L)] + [head]
-    reserve = 10000
-    budget = reserve + int(rng.integers(6, 3 * L)) * 4096
-    c = A.make_config(TINY.with_(n_layer=L))
-    want = OP.best(OP.structured_candidates(L), costs, budget, reserve, 1, OP.F32)
-    got = A.atom_plan_search(c, budget, reserve, costs) if want else None
-    if want is None:
-        with pytest.raises(A.AtomError):
-            A.atom_plan_search(c, budget, reserve, costs)
-        return
-    assert not got.exhaustive
-    assert got.groups() == want["groups"]
-    assert got.pred_step_s == want["pred_step_s"]
+    base = 10000
+    budget = base + 2048 + int(rng.integers(6, 3 * L)) * 4096
+    cfg = TINY.with_(n_layer=L)
+    c = A.make_config(cfg)
+    want = OP.best(OP.structured_candidates(L), costs, budget, base, 1, OP.F32, duplex=A.ATOM_DEFAULT_DUPLEX)
+    got = _compare(c, cfg, costs, budget, base, want)
+    if got is not None:
+        assert got.exhaustive == (L + 2 <= 16)
+
+
+def test_plan_predict_matches_the_oracle_schedule():
+    cfg = CONFIGS["13b"].with_(n_layer=6)
+    c = A.make_config(cfg)
+    plan = A.atom_plan_fixed(c, list(range(cfg.n_nodes)), 6, 3)
+    costs = [x.as_dict() for x in A.atom_node_costs(c)]
+    for n_steps, duplex in ((1, 0.85), (5, 0.5), (3, 1.0)):
+        ends, fwd = A.atom_plan_predict(c, plan, costs, duplex, n_steps)
+        t_fwd, want = OP.simulate(plan.groups(), costs, 1, 6, 3, n_steps, duplex, **ck_times(cfg, costs))
+        assert ends == want and fwd == t_fwd
+    # the plan's own predictions are the default-duplex ones
+    ends, _ = A.atom_plan_predict(c, plan, None, 0.0, OP.PIPE_STEPS)
+    assert plan.pred_step_s == (ends[-1] - ends[-3]) / 2.0
+    assert plan.pred_first_step_s == A.atom_plan_predict(c, plan, None, 0.0, 1)[0][0]
 
 
 def test_ctx_create_rejects_bad_arguments_without_gpu():

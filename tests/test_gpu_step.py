@@ -218,11 +218,28 @@ def test_measured_costs_plan_gives_same_step():
     with Session(cfg, plan=swapped_plan(cfg)) as s:
         s.load_weights()
         costs = A.atom_profile_nodes(s.ctx, c, tok)
+        profiled = s.grads(A.GRAD_LAST)
     n = cfg.n_nodes
     assert len(costs) == n
+    analytic_costs = A.atom_node_costs(c)
+    N = cfg.batch * cfg.seq_len
     for i, x in enumerate(costs):
         assert x.weight_bytes > 0 and x.t_load > 0 and x.t_store > 0 and x.t_fwd > 0
         assert (x.t_bwd > 0) == (i <= cfg.n_layer)
+        # working memory: how far the node's kernels wrote into the workspace,
+        # within what the arena carves for it (the embedding uses none)
+        assert x.mem_bytes <= analytic_costs[i].mem_bytes, (i, x.mem_bytes, analytic_costs[i].mem_bytes)
+        if i == 0:
+            assert x.mem_bytes == 0
+        else:
+            assert x.mem_bytes >= analytic_costs[i].mem_bytes // 2, (i, x.mem_bytes)
+        assert x.cut_bytes == (N * cfg.d_model * 4 if i <= cfg.n_layer else 4)
+    # the profiled step (workspace filled with a marker before every node)
+    # computed exactly what an ordinary step computes
+    _, last, _, _ = run_step(cfg, plan=swapped_plan(cfg), tokens=tok)
+    for node in range(n):
+        for name in last[node]:
+            assert np.array_equal(profiled[node][name], last[node][name]), (node, name)
     budget = A.atom_reserve_bytes(c) + 8 * costs[1].weight_bytes
     measured = A.atom_plan_partition(c, budget, costs)
     analytic = A.atom_plan_partition(c, budget)

@@ -1,8 +1,7 @@
-"""Pins of the planner oracle: enumeration, schedule closed forms, paper sizes."""
-import math
+"""Pins of the planner oracle: enumeration, schedule closed forms, the
+selection rule of Section III-D, paper sizes."""
 import os
 
-import numpy as np
 import pytest
 
 from oracle import plan as P
@@ -11,8 +10,9 @@ from synthetic import CONFIGS, Config, param_count
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
-def costs_uniform(n, w=100, tf=1.0, tb=2.0, tu=3.0, ts=3.0):
-    return [dict(weight_bytes=w, t_fwd=tf, t_bwd=tb, t_load=tu, t_store=ts) for _ in range(n)]
+def costs_uniform(n, w=100, tf=1.0, tb=2.0, tu=3.0, ts=3.0, mem=0, cut=10):
+    return [dict(weight_bytes=w, mem_bytes=mem, cut_bytes=cut, t_fwd=tf, t_bwd=tb, t_load=tu, t_store=ts)
+            for _ in range(n)]
 
 
 def test_compositions_are_all_distinct_contiguous_partitions():
@@ -27,85 +27,204 @@ def test_compositions_are_all_distinct_contiguous_partitions():
             assert all(a <= b for a, b in p)
 
 
-def test_single_group_schedule_is_serial():
+# ------------------------------------------------------------------ schedule
+def test_single_group_step_is_serial():
+    # one group of three nodes (embedding, block, head): load all, forward of
+    # two micro-batches, backward (the head has none), store all
     c = costs_uniform(3)
-    t_fwd, t_step = P.simulate([(0, 2)], c, accum=2, K=1)
-    # load all, compute forward of 2 micro-batches, backward, store all
+    c[2]["t_bwd"] = 0.0
+    t_fwd, ends = P.simulate([(0, 2)], c, accum=2, K=1, R=2)
     assert t_fwd == 9.0 + 2 * 3.0
-    assert t_step == 9.0 + 6.0 + 12.0 + 9.0
+    assert ends == [9.0 + 6.0 + 2 * 4.0 + 9.0]
 
 
-def test_link_bound_resident_schedule_is_sum_of_transfers():
+def test_link_bound_resident_step_is_sum_of_transfers():
+    # no compute, every group in its own slot: loads back to back, then the
+    # stores back to back (the backward needs the loss, so nothing overlaps)
     c = costs_uniform(5, tf=0.0, tb=0.0, tu=1.5, ts=2.5)
     groups = [(i, i) for i in range(5)]
-    t_fwd, t_step = P.simulate(groups, c, accum=1, K=5)
-    assert t_fwd == 7.5 and t_step == 7.5 + 12.5
+    t_fwd, ends = P.simulate(groups, c, accum=1, K=5, R=2, duplex=0.5)
+    assert t_fwd == 7.5 and ends == [7.5 + 12.5]
 
 
-def test_compute_bound_schedule_exposes_only_first_load_and_last_store():
+def test_compute_bound_exposes_first_load_and_last_store():
     c = costs_uniform(4, tf=10.0, tb=20.0, tu=1.0, ts=1.0)
+    c[3]["t_bwd"] = 0.0
     groups = [(i, i) for i in range(4)]
-    t_fwd, t_step = P.simulate(groups, c, accum=1, K=4)
+    t_fwd, ends = P.simulate(groups, c, accum=1, K=4, R=2)
     assert t_fwd == 1.0 + 40.0
-    assert t_step == 1.0 + 40.0 + 80.0 + 1.0
+    assert ends == [1.0 + 40.0 + 60.0 + 1.0]
+    # pipelined: the next step's loads hide under this step's backward
+    _, ends = P.simulate(groups, c, accum=1, K=4, R=2, n_steps=4)
+    assert [b - a for a, b in zip(ends, ends[1:])] == [100.0, 100.0, 100.0]
 
 
-def test_two_slots_force_reloads_in_backward():
+@pytest.mark.parametrize("duplex,want", [(1.0, [5.0, 8.0]), (0.5, [7.0, 10.0])])
+def test_shared_link_between_steps(duplex, want):
+    # one group, no compute: step 0's gradient copy (3 s alone) and step 1's
+    # load (2 s alone) start together after step 0's backward.  Full duplex:
+    # they run side by side.  duplex 0.5: both at half rate until the load
+    # ends at 2 + 2/0.5 = 6 with 1 s of the copy left, which ends at 7; step
+    # 1's copy then runs alone from 7 to 10.
+    c = [dict(weight_bytes=1, mem_bytes=0, cut_bytes=1, t_fwd=0.0, t_bwd=0.0, t_load=t, t_store=s)
+         for t, s in ((0.5, 1.0), (1.0, 1.0), (0.5, 1.0))]
+    _, ends = P.simulate([(0, 2)], c, accum=1, K=1, R=2, n_steps=2, duplex=duplex)
+    assert ends == want
+
+
+def test_gradient_slots_throttle_the_backward():
+    # five one-node groups, all resident, slow copies out: with R gradient
+    # slots, the backward of the group R claims later waits for the copy out
+    # of the slot it reuses.  Claims: head (group 4) at its forward, then
+    # groups 3, 2, 1, 0 in the backward.
+    c = costs_uniform(5, tf=0.0, tb=1.0, tu=0.0, ts=10.0)
+    c[4]["t_bwd"] = 0.0
+    groups = [(i, i) for i in range(5)]
+    # R = 16: copies queue on the engine; backward runs 4 x 1 s unhindered;
+    # the five copies of 10 s run back to back from t = 0 (the head's copy
+    # waits only for the head's forward)
+    _, ends = P.simulate(groups, c, accum=1, K=5, R=16)
+    assert ends == [50.0]
+    # R = 2: group 2's backward (third claim) waits for the head's copy
+    # (0..10), group 1's for group 3's copy (10..20), group 0's for group 2's
+    # (20..30); the last copy, group 0's, runs 40..50: the same end, but the
+    # backward now ends at 31
+    jobs = P.build_jobs(groups, c, 1, 5, 2, 1)
+    end = P.run_jobs(jobs, 1.0)
+    bwd_end = max(e for e, j in zip(end, jobs) if j[4] == "bwd")
+    assert bwd_end == 31.0
+    assert P.step_ends(jobs, end, 1) == [50.0]
+
+
+def test_reload_waits_for_the_slot_it_reuses():
+    # four one-node groups in two slots: groups 0 and 1 are loaded again in
+    # the backward, each after the backward of the group two later
+    c = costs_uniform(4, tf=1.0, tb=1.0, tu=2.0, ts=0.0)
+    c[3]["t_bwd"] = 0.0
+    jobs = P.build_jobs([(i, i) for i in range(4)], c, 1, 2, 2, 1)
+    kinds = [(j[0], j[4]) for j in jobs]
+    assert kinds.count(("I", "reload")) == 2
+    end = P.run_jobs(jobs, 1.0)
+    # forward: load0 0-2, fwd0 2-3, load1 2-4 (queued), fwd1 4-5, load2 after
+    # fwd0 and load1: 4-6, fwd2 6-7, load3 6-8, fwd3 (head) 8-9.  Backward:
+    # the head has no backward, so its group's last compute is its forward
+    # (9) and reload1 (into its slot) runs 9-11; bwd2 9-10 (resident);
+    # reload0 after bwd2 and behind reload1: 11-13; bwd1 11-12; bwd0 13-14
+    assert P.step_ends(jobs, end, 1) == [14.0]
+    reloads = [e for e, j in zip(end, jobs) if j[4] == "reload"]
+    assert reloads == [11.0, 13.0]
+
+
+def test_host_checkpoint_ring():
+    # five blocks, one group, no weights to move and no compute: only the
+    # block inputs 0 and 1 leave the four-entry ring (1 s each way).  ckout0
+    # 0-1 (after fwd0), ckout1 1-2; fwd4 waits ckout0, fwd5 waits ckout1 (2);
+    # the head's restore of input 1 runs 2-3, bwd5's restore of input 0 3-4;
+    # bwd2 waits input 1 (3), bwd1 waits input 0 (4)
+    c = [dict(weight_bytes=1, mem_bytes=0, cut_bytes=1, t_fwd=0.0, t_bwd=0.0, t_load=0.0, t_store=0.0)
+         for _ in range(7)]
+    t_fwd, ends = P.simulate([(0, 6)], c, accum=1, K=1, R=2, n_layer=5, ck_host=True, t_ck_out=1.0, t_ck_in=1.0)
+    assert t_fwd == 2.0 and ends == [4.0]
+    jobs = P.build_jobs([(0, 6)], c, 1, 1, 2, 1, n_layer=5, ck_host=True, t_ck_out=1.0, t_ck_in=1.0)
+    assert sum(j[4] == "ckout" for j in jobs) == 2 and sum(j[4] == "restore" for j in jobs) == 2
+
+
+# ------------------------------------------------------------------ memory
+def test_memory_slots_and_working_memory():
     c = costs_uniform(4, w=10)
     groups = [(i, i) for i in range(4)]
-    ok, K, S, arena = P.memory(groups, c, budget=1000 + 4 * 10, reserve=1000, accum=1, dtype=P.BF16)
-    assert ok and K == 2 and S == 10 and arena == 1040
-    h2d, d2h = P.transfer_bytes(groups, c, K)
-    assert h2d == 40 + 20 and d2h == 40
+    # base 1000, two gradient slots of 10: two weight slots fit in 40
+    ok, K, R, S, arena = P.memory(groups, c, budget=1000 + 4 * 10, base=1000, accum=1, dtype=P.BF16)
+    assert ok and (K, R, S, arena) == (2, 2, 10, 1040)
+    assert P.transfer_bytes(groups, c, K) == (40 + 20, 40)
+    # the largest working memory m_i joins the reserve (max, not sum)
+    c[2]["mem_bytes"] = 500
+    c[1]["mem_bytes"] = 300
+    assert not P.memory(groups, c, budget=1000 + 4 * 10, base=1000, accum=1, dtype=P.BF16)[0]
+    ok, K, R, S, arena = P.memory(groups, c, budget=1500 + 4 * 10, base=1000, accum=1, dtype=P.BF16)
+    assert ok and K == 2 and arena == 1540
+    # budget left after the weight slots becomes gradient slots, up to 16
+    ok, K, R, S, arena = P.memory(groups, c, budget=1500 + 4 * 10 + 2 * 10 + 7 * 10, base=1000, accum=1,
+                                  dtype=P.BF16)
+    assert (K, R) == (4, 9) and arena == 1500 + 4 * 10 + 9 * 10
+    ok, K, R, S, arena = P.memory(groups, c, budget=10 ** 9, base=1000, accum=1, dtype=P.BF16)
+    assert (K, R) == (4, 16)
 
 
 def test_memory_rejects_budget_below_two_slots():
     c = costs_uniform(4, w=10)
     groups = [(i, i) for i in range(4)]
-    assert not P.memory(groups, c, budget=1000 + 3 * 10, reserve=1000, accum=1, dtype=P.BF16)[0]
+    assert not P.memory(groups, c, budget=1000 + 3 * 10, base=1000, accum=1, dtype=P.BF16)[0]
     # a single group needs one weight slot only
-    assert P.memory([(0, 3)], c, budget=1000 + 3 * 40, reserve=1000, accum=1, dtype=P.BF16)[0]
+    assert P.memory([(0, 3)], c, budget=1000 + 3 * 40, base=1000, accum=1, dtype=P.BF16)[0]
     # bf16 with accumulation adds an fp32 slot of 2S
-    assert not P.memory(groups, c, budget=1000 + 5 * 10, reserve=1000, accum=2, dtype=P.BF16)[0]
-    assert P.memory(groups, c, budget=1000 + 6 * 10, reserve=1000, accum=2, dtype=P.BF16)[0]
-    assert P.memory(groups, c, budget=1000 + 4 * 10, reserve=1000, accum=2, dtype=P.F32)[0]
+    assert not P.memory(groups, c, budget=1000 + 5 * 10, base=1000, accum=2, dtype=P.BF16)[0]
+    assert P.memory(groups, c, budget=1000 + 6 * 10, base=1000, accum=2, dtype=P.BF16)[0]
+    assert P.memory(groups, c, budget=1000 + 4 * 10, base=1000, accum=2, dtype=P.F32)[0]
 
 
-def test_brute_force_prefers_fine_groups_when_link_bound():
-    c = costs_uniform(6, tf=0.1, tb=0.2, tu=1.0, ts=1.0)
-    best = P.brute_force(c, budget=10 ** 9, reserve=0, accum=1, dtype=P.BF16)
-    # link-bound: all loads, then the last group's forward and backward, then
-    # all stores; a small last group minimises the exposed compute, and the
-    # fewest-groups tie-break then merges everything before it
-    assert best["pred_step_s"] == pytest.approx(6.0 + 0.1 + 0.2 + 6.0, abs=1e-12)
-    assert best["groups"] == [(0, 4), (5, 5)]
-    assert not best["overlap_ok"]
+# ------------------------------------------------------------------ overlap
+def test_overlap_constraint():
+    c = costs_uniform(4, tf=1.0, tb=2.0, tu=3.0)
+    g = [(i, i) for i in range(4)]
+    assert not P.overlap_ok(g, c, accum=1, K=4)  # forward 1 < load 3
+    assert P.overlap_ok(g, c, accum=3, K=4)  # C = 3: 3 >= 3 (the paper's remedy)
+    # backward: a reloaded group j needs C t^b(g_{j+1}) >= t^u(g_j)
+    c2 = costs_uniform(4, tf=3.0, tb=1.0, tu=2.0)
+    assert P.overlap_ok(g, c2, accum=1, K=4)  # nothing reloaded
+    assert not P.overlap_ok(g, c2, accum=1, K=2)  # groups 0, 1 reloaded: 1 < 2
+    assert P.overlap_ok(g, c2, accum=2, K=2)
+    # a single group has no neighbour: the constraint holds vacuously
+    assert P.overlap_ok([(0, 3)], c, accum=1, K=1)
 
 
-def test_brute_force_tie_breaks_bytes_then_groups():
-    # no transfer cost: every partition has the same predicted time
-    c = costs_uniform(5, tu=0.0, ts=0.0)
-    # everything stays resident in any partition (same bytes): fewest groups
-    best = P.brute_force(c, budget=10 ** 9, reserve=0, accum=1, dtype=P.BF16)
-    assert best["groups"] == [(0, 4)]
-    # 800 bytes beside the reserve: groups of two nodes get slots of 200 and
-    # gradient slots of 400, so two weight slots, and three groups reload one
-    # group in the backward; single nodes get six slots of 100 next to 200 of
-    # gradient slots, so nothing reloads: fewest bytes wins over fewest groups
-    best = P.brute_force(c, budget=400 + 4 * 200, reserve=400, accum=1, dtype=P.BF16)
-    assert best["groups"] == [(i, i) for i in range(5)]
-    assert best["h2d_bytes"] == 5 * 100
-    # among the three-group plans, the one reloading the smallest group wins
-    # ((1,2,2): 100 bytes; (2,1,2) and (2,2,1): 200), although [0,2,4] is also
-    # the smallest end list
-    three = P.best([[(0, 0), (1, 2), (3, 4)], [(0, 1), (2, 2), (3, 4)], [(0, 1), (2, 3), (4, 4)]], c,
-                   400 + 4 * 200, 400, 1, P.BF16)
-    assert [b for _, b in three["groups"]] == [0, 2, 4] and three["h2d_bytes"] == 600
+# ------------------------------------------------------------------ selection
+def test_minimum_cut_beats_a_faster_partition():
+    # everything overlaps; the whole model in one group has no cut at all and
+    # wins, although loading it whole exposes 4 s of transfers at each end
+    c = costs_uniform(4, tf=2.0, tb=4.0, tu=1.0, ts=1.0, cut=7)
+    c[3]["t_bwd"] = 0.0
+    best = P.brute_force(c, budget=10 ** 6, base=0, accum=1, dtype=P.BF16)
+    assert best["groups"] == [(0, 3)] and best["rule"] == "paper" and best["cut_bytes"] == 0
+    singles = P.evaluate([(i, i) for i in range(4)], c, 10 ** 6, 0, 1, P.BF16)
+    assert singles["overlap_ok"] and singles["pred_first_step_s"] < best["pred_first_step_s"]
+    # with a budget that cannot hold the whole model in one slot, the fewest
+    # cuts among overlapping partitions win: two groups of two nodes
+    # (S = 200: 3 S + 2 S gradient slots... K = 2, no reload)
+    best = P.brute_force(c, budget=4 * 200, base=0, accum=1, dtype=P.BF16)
+    assert best["rule"] == "paper" and len(best["groups"]) == 2 and best["cut_bytes"] == 7
+    assert best["groups"] == [(0, 1), (2, 3)]
+
+
+def test_cut_sizes_decide_between_equal_group_counts():
+    # cuts differ per edge: the partition with the cheaper edge wins
+    c = costs_uniform(4, tf=2.0, tb=4.0, tu=1.0, ts=1.0)
+    for i, cb in enumerate((50, 5, 50, 0)):
+        c[i]["cut_bytes"] = cb
+    best = P.best([[(0, 0), (1, 3)], [(0, 1), (2, 3)], [(0, 2), (3, 3)]], c, 4 * 300, 0, 1, P.BF16)
+    assert best["groups"] == [(0, 1), (2, 3)] and best["cut_bytes"] == 5
+
+
+def test_no_overlapping_partition_strict_and_fallback():
+    # loads dwarf compute and the budget forbids one group: nothing overlaps
+    c = costs_uniform(4, tf=0.1, tb=0.2, tu=5.0, ts=5.0)
+    c[3]["t_bwd"] = 0.0
+    budget = 4 * 100 + 2 * 100  # singletons: four slots and two gradient slots
+    assert P.brute_force(c, budget, 0, 1, P.BF16, strict=True) is None
+    best = P.brute_force(c, budget, 0, 1, P.BF16)
+    assert best["rule"] == "time" and not best["overlap_ok"]
+    # the fallback is the fastest memory-feasible partition
+    for g in P.compositions(4):
+        p = P.evaluate(g, c, budget, 0, 1, P.BF16)
+        assert p is None or p["pred_step_s"] >= best["pred_step_s"]
+    # and C large enough restores the paper's rule
+    best = P.brute_force(c, budget, 0, 100, P.F32)
+    assert best["rule"] == "paper" and best["overlap_ok"]
 
 
 def test_brute_force_none_when_nothing_fits():
     c = costs_uniform(3, w=100)
-    assert P.brute_force(c, budget=350, reserve=0, accum=1, dtype=P.BF16) is None
+    assert P.brute_force(c, budget=350, base=0, accum=1, dtype=P.BF16) is None
 
 
 def test_structured_candidates_are_valid_partitions():
@@ -120,6 +239,7 @@ def test_structured_candidates_are_valid_partitions():
         assert [(i, i) for i in range(n)] in cands
 
 
+# ------------------------------------------------------------------ paper sizes
 def _read_golden(name):
     rows = []
     with open(os.path.join(GOLDEN, name)) as f:
