@@ -73,6 +73,18 @@ int atom_k_attn_fwd(int dtype, const void* qkv, void* o, float* lse, int B, int 
 int atom_k_attn_bwd(int dtype, const void* qkv, const void* o, const void* dout, const float* lse, float* delta,
                     void* dqkv, int B, int T, int H, int dh, void* stream);
 
+/* atom_k_attn_bwd for callers that cannot allocate (code under HIP graph
+ * capture, serving loops, harnesses that forbid hipMalloc): the same kernels,
+ * with the D scratch in a library-owned device array of
+ * ATOM_ATTN_NOALLOC_MAX_ROWS floats (4 MiB per GPU, held until the process
+ * ends) instead of a `delta` argument.  Allocates nothing.  B * H * T above
+ * the limit: ATOM_EINVAL.  Every call on one GPU uses the same array, so
+ * calls that overlap on one GPU (different streams, or threads) race; calls
+ * in order on one stream do not.  Nothing in the array must start at zero. */
+#define ATOM_ATTN_NOALLOC_MAX_ROWS (1 << 20)
+int atom_k_attn_bwd_noalloc(int dtype, const void* qkv, const void* o, const void* dout, const float* lse,
+                            void* dqkv, int B, int T, int H, int dh, void* stream);
+
 /* Scratch floats atom_k_colsum needs in `part`. */
 int64_t atom_k_colsum_part_floats(int64_t rows, int cols);
 

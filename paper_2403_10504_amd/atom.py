@@ -125,6 +125,7 @@ _SIGS = {
                                             ctypes.c_int, P]),
     "atom_k_attn_fwd": (ctypes.c_int, [ctypes.c_int, P, P, P] + [ctypes.c_int] * 4 + [P]),
     "atom_k_attn_bwd": (ctypes.c_int, [ctypes.c_int, P, P, P, P, P, P] + [ctypes.c_int] * 4 + [P]),
+    "atom_k_attn_bwd_noalloc": (ctypes.c_int, [ctypes.c_int, P, P, P, P, P] + [ctypes.c_int] * 4 + [P]),
     "atom_k_colsum_part_floats": (I64, [I64, ctypes.c_int]),
     "atom_k_colsum": (ctypes.c_int, [ctypes.c_int, P, I64, ctypes.c_int, P, P, P]),
     "atom_k_xent": (ctypes.c_int, [ctypes.c_int, P, I64, P, P, I64, P, I64, ctypes.c_int, ctypes.c_float, P]),
@@ -443,6 +444,13 @@ def atom_k_attn_fwd(dtype, qkv, o, lse, B, T, H, dh, stream=None):
 
 def atom_k_attn_bwd(dtype, qkv, o, dout, lse, delta, dqkv, B, T, H, dh, stream=None):
     _kcall("atom_k_attn_bwd", dtype, qkv, o, dout, lse, delta, dqkv, B, T, H, dh, stream)
+
+
+ATOM_ATTN_NOALLOC_MAX_ROWS = 1 << 20
+
+
+def atom_k_attn_bwd_noalloc(dtype, qkv, o, dout, lse, dqkv, B, T, H, dh, stream=None):
+    _kcall("atom_k_attn_bwd_noalloc", dtype, qkv, o, dout, lse, dqkv, B, T, H, dh, stream)
 
 
 def atom_k_colsum_part_floats(rows, cols):
