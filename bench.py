@@ -212,6 +212,12 @@ def main():
     ap.add_argument("--config", default="6.7b")
     ap.add_argument("--accum", type=int, default=None, help="gradient-accumulation degree C")
     ap.add_argument("--budget-gb", type=float, default=None, help="device budget (default: the config's)")
+    ap.add_argument("--ckpt-host", action="store_true",
+                    help="keep block-input checkpoints beyond a four-entry device ring in host memory (the 13B "
+                         "configuration's policy; needed for large C under 24 GB)")
+    ap.add_argument("--layers", type=int, default=None,
+                    help="override the layer count (kernel profiling at the configuration's shapes in less time; "
+                         "not a benchmark of the named model)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sequential", action="store_true", help="one atom_step call per step (no cross-step overlap)")
     ap.add_argument("--schedule", choices=["atom", "paper"], default="atom",
@@ -252,6 +258,10 @@ def main():
     cfg = synthetic.CONFIGS[args.config]
     if args.accum:
         cfg = cfg.with_(accum=args.accum)
+    if args.ckpt_host:
+        cfg = cfg.with_(ckpt_host=True)
+    if args.layers:
+        cfg = cfg.with_(n_layer=args.layers)
     budget = int(args.budget_gb * 1e9) if args.budget_gb else (cfg.budget_bytes or (1 << 50))
     torch.cuda.set_device(0)
 
@@ -431,7 +441,8 @@ def main():
         "dtype": cfg.dtype,
         "data": "synthetic (seeded N(0,0.02) weights, uniform tokens)",
         "config": {
-            "workload": (f"GPT-3 {args.config} swapped training step: {cfg.n_layer} layers, d_model {cfg.d_model}, "
+            "workload": (("[layer count overridden for profiling] " if args.layers else "")
+                         + f"GPT-3 {args.config} swapped training step: {cfg.n_layer} layers, d_model {cfg.d_model}, "
                          f"{cfg.n_head} heads, MLP {cfg.d_mlp}, vocab {cfg.vocab}; batch {cfg.batch} x seq "
                          f"{cfg.seq_len}, accum {cfg.accum}; "
                          + ("one step per call; " if args.sequential else
@@ -439,7 +450,8 @@ def main():
                          + (f"device budget {budget / 1e9:.0f} GB" if budget < (1 << 49) else "whole model resident")
                          + ("; paper schedule (one node per group, two weight slots)" if args.schedule == "paper"
                             else "")
-                         + ("; weights retained across the steps of the call" if args.retain else "")),
+                         + ("; weights retained across the steps of the call" if args.retain else "")
+                         + ("; block-input checkpoints in host memory" if cfg.ckpt_host else "")),
             "global_batch": args.steps * cfg.accum * cfg.batch,
             "global_batch_unit": "sequences (timed steps x accum x batch)",
             "micro_batch": cfg.batch,

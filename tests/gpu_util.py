@@ -61,6 +61,18 @@ def rel_err(got, ref):
     return float(np.max(np.abs(got - ref)) / (den if den > 0 else 1.0))
 
 
+def elem_err(got, ref, floor=1e-2):
+    """Elementwise relative error with a floor: max_i |g_i - r_i| / max(|r_i|, floor * max|r|).
+
+    Complements the normwise rel_err: an element far below the tensor's scale
+    is measured against floor * max|r| instead of its own magnitude."""
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    top = np.max(np.abs(ref))
+    den = np.maximum(np.abs(ref), floor * (top if top > 0 else 1.0))
+    return float(np.max(np.abs(got - ref) / den))
+
+
 def dt_code(dtype):
     from paper_2403_10504_amd import atom as A
 

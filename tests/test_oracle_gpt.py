@@ -86,12 +86,35 @@ def test_fd_wte_rows_of_used_and_unused_tokens():
         assert abs((lp - lm) / (2 * h) - grads[0]["wte"][v, col]) < 1e-8
 
 
-def torch_reference_step(cfg, w, tok):
-    """The same model from PyTorch library routines, fp64 autograd."""
+def torch_logits(cfg, P, inp):
+    """Logits [B, T, V] of the model from PyTorch library routines (fp64)."""
     torch = pytest.importorskip("torch")
     F = torch.nn.functional
     L, d, H = cfg.n_layer, cfg.d_model, cfg.n_head
     dh = d // H
+    B, T = inp.shape
+    x = P[0]["wte"][inp] + P[0]["wpe"][:T][None]
+    for l in range(L):
+        p = P[1 + l]
+        a = F.layer_norm(x, (d,), p["ln1_g"], p["ln1_b"], eps=1e-5)
+        qkv = F.linear(a, p["w_qkv"], p["b_qkv"])
+        q, k, v = qkv.split(d, dim=-1)
+        q = q.reshape(B, T, H, dh).transpose(1, 2)
+        k = k.reshape(B, T, H, dh).transpose(1, 2)
+        v = v.reshape(B, T, H, dh).transpose(1, 2)
+        o = F.scaled_dot_product_attention(q, k, v, is_causal=True)
+        o = o.transpose(1, 2).reshape(B, T, d)
+        x = x + F.linear(o, p["w_o"], p["b_o"])
+        c = F.layer_norm(x, (d,), p["ln2_g"], p["ln2_b"], eps=1e-5)
+        x = x + F.linear(F.gelu(F.linear(c, p["w_fc"], p["b_fc"]), approximate="tanh"), p["w_pr"], p["b_pr"])
+    p = P[L + 1]
+    return F.linear(F.layer_norm(x, (d,), p["lnf_g"], p["lnf_b"], eps=1e-5), p["w_head"])
+
+
+def torch_reference_step(cfg, w, tok):
+    """The same model from PyTorch library routines, fp64 autograd."""
+    torch = pytest.importorskip("torch")
+    F = torch.nn.functional
     P = [{k: torch.tensor(np.asarray(v, np.float64), requires_grad=True) for k, v in p.items()} for p in w]
     C, B, T1 = tok.shape
     T = T1 - 1
@@ -99,26 +122,24 @@ def torch_reference_step(cfg, w, tok):
     for m in range(C):
         inp = torch.tensor(tok[m, :, :T].astype(np.int64))
         tgt = torch.tensor(tok[m, :, 1:].astype(np.int64))
-        x = P[0]["wte"][inp] + P[0]["wpe"][:T][None]
-        for l in range(L):
-            p = P[1 + l]
-            a = F.layer_norm(x, (d,), p["ln1_g"], p["ln1_b"], eps=1e-5)
-            qkv = F.linear(a, p["w_qkv"], p["b_qkv"])
-            q, k, v = qkv.split(d, dim=-1)
-            q = q.reshape(B, T, H, dh).transpose(1, 2)
-            k = k.reshape(B, T, H, dh).transpose(1, 2)
-            v = v.reshape(B, T, H, dh).transpose(1, 2)
-            o = F.scaled_dot_product_attention(q, k, v, is_causal=True)
-            o = o.transpose(1, 2).reshape(B, T, d)
-            x = x + F.linear(o, p["w_o"], p["b_o"])
-            c = F.layer_norm(x, (d,), p["ln2_g"], p["ln2_b"], eps=1e-5)
-            x = x + F.linear(F.gelu(F.linear(c, p["w_fc"], p["b_fc"]), approximate="tanh"), p["w_pr"], p["b_pr"])
-        p = P[L + 1]
-        z = F.linear(F.layer_norm(x, (d,), p["lnf_g"], p["lnf_b"], eps=1e-5), p["w_head"])
+        z = torch_logits(cfg, P, inp)
         total = total + F.cross_entropy(z.reshape(-1, cfg.vocab), tgt.reshape(-1), reduction="sum")
     loss = total / (C * B * T)
     loss.backward()
     return float(loss.detach()), [{k: t.grad.numpy() for k, t in p.items()} for p in P]
+
+
+def test_forward_logits_matches_torch_fp64():
+    torch = pytest.importorskip("torch")
+    cfg = FD_CFG
+    w = rand_weights(cfg, seed=21)
+    tok = rand_tokens(cfg, seed=22)
+    inp = tok[0, :, :cfg.seq_len]
+    got = gpt.forward_logits(cfg, w, inp)
+    P = [{k: torch.tensor(np.asarray(v, np.float64)) for k, v in p.items()} for p in w]
+    ref = torch_logits(cfg, P, torch.tensor(inp.astype(np.int64))).numpy()
+    assert got.shape == ref.shape == (cfg.batch, cfg.seq_len, cfg.vocab)
+    assert np.max(np.abs(got - ref)) <= 1e-12 * np.max(np.abs(ref))
 
 
 @pytest.mark.parametrize("cfg", [FD_CFG, FD_CFG.with_(batch=1, accum=1, seq_len=9, n_layer=1, n_head=4, d_model=16, d_mlp=64, vocab=31)])
