@@ -1,9 +1,10 @@
 """Build libatom.so in-tree for gfx950 with hipcc.
 
-Usage: python -m paper_2403_10504_amd.build [-v]
+Usage: python -m paper_2403_10504_amd.build [-v] [--changed]
 
 Every source is compiled on each call (the build check compiles from
-scratch).  HIP sources get `-Xclang -target-feature -Xclang -packed-fp32-ops`
+scratch); --changed recompiles only the objects older than their source or
+any header of csrc/ or include/ (a developer's rebuild).  HIP sources get `-Xclang -target-feature -Xclang -packed-fp32-ops`
 so the compiler never emits packed fp32 arithmetic; the host pass warns that
 it does not know the feature, which is harmless.
 """
@@ -46,7 +47,18 @@ def _run(cmd, verbose):
         print(out, flush=True)
 
 
-def build(verbose: bool = False, jobs: int | None = None) -> str:
+def _stale(src, obj):
+    if not os.path.exists(obj):
+        return True
+    t = os.path.getmtime(obj)
+    deps = [os.path.join(CSRC, src)]
+    deps += [os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".h")]
+    inc = os.path.join(os.path.dirname(HERE), "include")
+    deps += [os.path.join(inc, f) for f in os.listdir(inc) if f.endswith(".h")]
+    return any(os.path.getmtime(p) > t for p in deps)
+
+
+def build(verbose: bool = False, jobs: int | None = None, changed_only: bool = False) -> str:
     hipcc = _hipcc()
     os.makedirs(BUILD, exist_ok=True)
     common = ["-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function", "-I", CSRC]
@@ -59,11 +71,15 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
                      "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
                      "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
+        if changed_only and not _stale(src, obj):
+            cmds.pop()
     for src in CXX_SOURCES:
         obj = os.path.join(BUILD, src + ".o")
         cmds.append(["g++", "-O3", *common, "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
-    jobs = jobs or min(8, len(cmds))
+        if changed_only and not _stale(src, obj):
+            cmds.pop()
+    jobs = jobs or max(1, min(8, len(cmds)))
     with ThreadPoolExecutor(jobs) as ex:
         list(ex.map(lambda c: _run(c, verbose), cmds))
     tmp = LIB + ".tmp"
@@ -73,4 +89,4 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, changed_only="--changed" in sys.argv))

@@ -347,23 +347,34 @@ __global__ void __launch_bounds__(256, ATOM_ATTN_FWD_OCC) attn_fwd_kernel(const 
   }
 }
 
-// Work item of a workgroup in a [n_x blocks][B*H heads] grid.  The hardware
-// hands consecutive linear ids to the 8 XCDs in turn, so with the plain ids an
-// XCD would see only blocks x = k and k+8 of every head: under the causal
-// mask the last XCD did 2.4x the work of the first, and every XCD read every
-// head's K and V.  Each XCD instead takes a contiguous range of (head, block)
-// pairs: whole heads, all their blocks (equal work, one head's tiles in one
-// L2).  heavy_last: block x does work growing with x, so x runs from the
-// heaviest down and the light blocks fill in behind.
+// Work item of a workgroup in a [n_x blocks][B*H heads] grid.  Under the
+// causal mask the blocks of a head carry unequal work (block x of the
+// forward visits x+1 key tiles), so the items are handed out heaviest first
+// over all heads: a workgroup that starts late then has little left to do,
+// and the kernel does not wait on a heavy block that started behind a run of
+// light ones (heaviest-first within each head, one head after another, left
+// the 6.7B forward with about 1.1 of its 2 resident waves per SIMD on
+// average).  The hardware hands consecutive linear ids to the 8 XCDs in
+// turn; when the heads split evenly over them, each XCD takes its own eighth
+// of the heads (all their blocks), so one head's K and V stay in one L2.
+// heavy_last: block x does work growing with x (forward, dQ); otherwise
+// shrinking (dK/dV).
 struct BlockId {
   int x, bh;
 };
 __device__ __forceinline__ BlockId attn_block(bool heavy_last) {
-  const int n_x = gridDim.x, total = gridDim.x * gridDim.y;
+  const int n_x = gridDim.x, n_bh = gridDim.y;
   const int lin = blockIdx.y * n_x + blockIdx.x;
-  const int v = (total & 7) == 0 ? (lin & 7) * (total >> 3) + (lin >> 3) : lin;
-  const int x = v % n_x;
-  return BlockId{heavy_last ? n_x - 1 - x : x, v / n_x};
+  int rank, bh;  // rank 0 = the heaviest block
+  if ((n_bh & 7) == 0) {
+    const int per = n_bh >> 3, i = lin >> 3;  // heads per XCD; item index inside the XCD
+    rank = i / per;
+    bh = (lin & 7) * per + i % per;
+  } else {
+    rank = lin / n_bh;
+    bh = lin % n_bh;
+  }
+  return BlockId{heavy_last ? n_x - 1 - rank : rank, bh};
 }
 
 // ------------------------------------------- forward, bf16, direct loads
@@ -528,8 +539,7 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_dl_kernel(const bf16_t* __res
       vfrag(vf[0], vs, 0, 0);
 #pragma unroll
       for (int g = 0; g < G; ++g) {
-        float mx = fmaxf(mloc[g], __shfl_xor(mloc[g], 16, 64));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * sc;
+        const float mx = rows4_max(mloc[g]) * sc;
         if (__builtin_amdgcn_ballot_w64(mx > m_i[g] + RESCALE_LOG2) != 0) {
           const float m_new = fmaxf(m_i[g], mx);
           const float alpha = ex2(m_i[g] - m_new);
@@ -567,8 +577,7 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_dl_kernel(const bf16_t* __res
 #pragma unroll
   for (int g = 0; g < G; ++g) {
     const int qi = qw + g * 16 + lr;
-    float l_tot = l_i[g] + __shfl_xor(l_i[g], 16, 64);
-    l_tot += __shfl_xor(l_tot, 32, 64);
+    const float l_tot = rows4_sum(l_i[g]);
     if (qi < Tn) {
       const float inv = 1.f / l_tot;
       bf16_t* orow = o + (static_cast<int64_t>(b) * Tn + qi) * d + h * DH;

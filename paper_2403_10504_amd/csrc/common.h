@@ -140,6 +140,37 @@ ATOM_DEV float wave_max(float v) {
   return v;
 }
 
+// Reductions over the lane pairs (l, l ^ 16) and (l, l ^ 32) on the VALU:
+// v_permlane16_swap / v_permlane32_swap exchange rows of 16 (32) lanes
+// between two registers, so with both operands = v a lane ends up holding
+// the even-row and the odd-row value of its pair in that order (the same
+// order in both lanes of the pair, so both get the same bits).  A
+// __shfl_xor goes through the LDS crossbar (ds_bpermute) with its latency.
+ATOM_DEV void pair16(float v, float& lo, float& hi) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  lo = __uint_as_float(r[0]);
+  hi = __uint_as_float(r[1]);
+}
+ATOM_DEV void pair32(float v, float& lo, float& hi) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  lo = __uint_as_float(r[0]);
+  hi = __uint_as_float(r[1]);
+}
+// max and sum over the four lanes l, l ^ 16, l ^ 32, l ^ 48, as
+// (v0 op v1) op (v2 op v3) with v_k the value of row k of the wave.
+ATOM_DEV float rows4_max(float v) {
+  float a, b;
+  pair16(v, a, b);
+  pair32(fmaxf(a, b), a, b);
+  return fmaxf(a, b);
+}
+ATOM_DEV float rows4_sum(float v) {
+  float a, b;
+  pair16(v, a, b);
+  pair32(a + b, a, b);
+  return a + b;
+}
+
 // GELU, tanh form, and its derivative.
 // GELU, tanh form, through 0.5 (1 + tanh y) = s = 1 / (1 + exp(-2y)) with
 // y = c (u + a u^3): one hardware exp2 and one reciprocal (each within a few

@@ -268,9 +268,10 @@ def test_layernorm_fwd_bwd(dtype, rows, d):
 
 # ----------------------------------------------------------------- attention
 # ragged T, T = 1, several heads and batches, and long loops (many key and
-# query tiles through the two-stage pipelines) at both head sizes
+# query tiles through the two-stage pipelines) at both head sizes; B*H a
+# multiple of 8 takes the per-XCD split of the heads in the work-item order
 ATTN_CASES = [(2, 100, 2, 64), (1, 128, 3, 128), (1, 1, 1, 64), (2, 200, 1, 128), (1, 64, 2, 64), (1, 257, 1, 64),
-              (1, 1000, 2, 128), (2, 600, 1, 64)]
+              (1, 1000, 2, 128), (2, 600, 1, 64), (2, 300, 4, 64), (1, 520, 16, 128), (4, 130, 6, 64)]
 
 
 def attn_inputs(B, T, H, dh, dtype, seed):
