@@ -264,6 +264,149 @@ __global__ void __launch_bounds__(256) ln_bwd_wave_kernel(const T* __restrict__ 
   }
 }
 
+// Backward for d >= 1024: one workgroup (four waves) per block of LNT_ROWS
+// consecutive rows.  Thread t owns columns 4t + 1024j (j < NCH, 4-vector
+// loads), so each wave reads contiguous 512-byte (bf16) or 1 KB (fp32) runs;
+// every thread keeps gamma and its columns' running sums of dy*xhat and dy
+// in registers over the block's rows and writes them as the block's partial
+// (part[block][2][d]), no LDS pass.  The row sums meet in LDS (one barrier
+// per row, double-buffered), and the next row's dy and x are requested
+// before the current row's reduction (up to d = 4096), so a workgroup keeps
+// two rows of loads in flight.  (One wave per row with 64 columns per lane held 256 registers
+// of column sums and row values: one wave per SIMD, 2.5 TB/s in the step.)
+constexpr int LNT_ROWS = 8;
+
+template <typename T, int NCH>
+__global__ void __launch_bounds__(256) ln_bwd_team_kernel(const T* __restrict__ dy, const float* __restrict__ x,
+                                                          const float* __restrict__ mean,
+                                                          const float* __restrict__ rstd, const T* __restrict__ gamma,
+                                                          float* __restrict__ dres, T* __restrict__ dres_lp,
+                                                          int accumulate, float* __restrict__ part, int64_t rows,
+                                                          int d) {
+  constexpr bool PF = NCH <= 4;
+  __shared__ float red[2][4][2];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * LNT_ROWS;
+  const int nrow = static_cast<int>(min(static_cast<int64_t>(LNT_ROWS), rows - r0));
+  const float inv_d = 1.f / static_cast<float>(d);
+  bool on[NCH];
+  float gam[NCH * 4], ca[NCH * 4], cb[NCH * 4];
+#pragma unroll
+  for (int j = 0; j < NCH; ++j) {
+    const int c = 4 * tid + 1024 * j;
+    on[j] = c < d;
+    Vec4<T> vg;
+    if (on[j]) vg.load(gamma + c);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      gam[4 * j + i] = on[j] ? vg.get(i) : 0.f;
+      ca[4 * j + i] = 0.f;
+      cb[4 * j + i] = 0.f;
+    }
+  }
+  float gv[NCH * 4], xv[NCH * 4];
+  auto load_row = [&](int64_t row, float* g, float* xx) {
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) {
+      if (on[j]) {
+        const int c = 4 * tid + 1024 * j;
+        Vec4<T> vy;
+        vy.load(dy + row * d + c);
+        const float4 v = *reinterpret_cast<const float4*>(x + row * d + c);
+        const float xs[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          g[4 * j + i] = vy.get(i);
+          xx[4 * j + i] = xs[i];
+        }
+      }
+    }
+  };
+  load_row(r0, gv, xv);
+  for (int k = 0; k < nrow; ++k) {
+    const int64_t row = r0 + k;
+    const float mu = mean[row], r = rstd[row];
+    float* h = xv;  // xhat replaces x in place
+    float sa = 0.f, sb = 0.f;
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) {
+      if (on[j]) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int e = 4 * j + i;
+          h[e] = (xv[e] - mu) * r;
+          const float gp = gv[e] * gam[e];
+          sa += gp;
+          sb += gp * h[e];
+          ca[e] += gv[e] * h[e];
+          cb[e] += gv[e];
+        }
+      }
+    }
+    // the next row's loads go out now when the registers allow (PF)
+    float ng[PF ? NCH * 4 : 1], nx[PF ? NCH * 4 : 1];
+    if constexpr (PF) {
+      if (k + 1 < nrow) load_row(row + 1, ng, nx);
+    }
+    float prev[NCH * 4];
+    if (accumulate) {
+#pragma unroll
+      for (int j = 0; j < NCH; ++j) {
+        if (on[j]) {
+          const float4 v = *reinterpret_cast<const float4*>(dres + row * d + 4 * tid + 1024 * j);
+          prev[4 * j] = v.x;
+          prev[4 * j + 1] = v.y;
+          prev[4 * j + 2] = v.z;
+          prev[4 * j + 3] = v.w;
+        }
+      }
+    }
+    sa = wave_sum(sa);
+    sb = wave_sum(sb);
+    const int buf = k & 1;
+    if (lane == 0) {
+      red[buf][w][0] = sa;
+      red[buf][w][1] = sb;
+    }
+    __syncthreads();
+    const float a = (((red[buf][0][0] + red[buf][1][0]) + red[buf][2][0]) + red[buf][3][0]) * inv_d;
+    const float b = (((red[buf][0][1] + red[buf][1][1]) + red[buf][2][1]) + red[buf][3][1]) * inv_d;
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) {
+      if (on[j]) {
+        const int c = 4 * tid + 1024 * j;
+        float o[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int e = 4 * j + i;
+          const float dx = r * (gv[e] * gam[e] - a - h[e] * b);
+          o[i] = accumulate ? prev[e] + dx : dx;
+        }
+        *reinterpret_cast<float4*>(dres + row * d + c) = make_float4(o[0], o[1], o[2], o[3]);
+        if (dres_lp) Vec4<T>::store(dres_lp + row * d + c, o);
+      }
+    }
+    if constexpr (PF) {
+#pragma unroll
+      for (int e = 0; e < NCH * 4; ++e) {
+        gv[e] = ng[e];
+        xv[e] = nx[e];
+      }
+    } else {
+      if (k + 1 < nrow) load_row(row + 1, gv, xv);
+    }
+  }
+  float* p = part + static_cast<int64_t>(blockIdx.x) * 2 * d;
+#pragma unroll
+  for (int j = 0; j < NCH; ++j) {
+    if (on[j]) {
+      const int c = 4 * tid + 1024 * j;
+      *reinterpret_cast<float4*>(p + c) = make_float4(ca[4 * j], ca[4 * j + 1], ca[4 * j + 2], ca[4 * j + 3]);
+      *reinterpret_cast<float4*>(p + d + c) = make_float4(cb[4 * j], cb[4 * j + 1], cb[4 * j + 2], cb[4 * j + 3]);
+    }
+  }
+}
+
 // ------------------------------------------------------------- column sums
 // Rows per partial sum: 16, so that a [4096][4096] input gives 1024
 // workgroups (four per CU) whose loads are all issued before the first add
@@ -556,6 +699,10 @@ hipError_t ln_fwd_t(const float* x, const void* gamma, const void* beta, void* y
 }
 
 bool lnw_usable(int d) { return d % 256 == 0 && d / 256 <= LNW_MAXCH; }
+#ifndef ATOM_LN_TEAM
+#define ATOM_LN_TEAM 1
+#endif
+bool lnt_usable(int d) { return ATOM_LN_TEAM && d >= 1024 && d % 4 == 0 && d <= 8192; }
 
 template <typename T>
 hipError_t ln_bwd_t(const void* dy, const float* x, const float* mean, const float* rstd, const void* gamma,
@@ -565,6 +712,20 @@ hipError_t ln_bwd_t(const void* dy, const float* x, const float* mean, const flo
   auto g = static_cast<const T*>(gamma);
   auto lp = static_cast<T*>(dres_lp);
   const int ac = acc ? 1 : 0;
+  if (lnt_usable(d)) {
+    dim3 grid(static_cast<unsigned>((rows + LNT_ROWS - 1) / LNT_ROWS)), block(256);
+#define ATOM_LNT(CH)                                                                                             \
+  hipLaunchKernelGGL((ln_bwd_team_kernel<T, CH>), grid, block, 0, s, a0, x, mean, rstd, g, dres, lp, ac, part, rows, \
+                     d)
+    if (ne <= 4) ATOM_LNT(1);
+    else if (ne <= 8) ATOM_LNT(2);
+    else if (ne <= 12) ATOM_LNT(3);
+    else if (ne <= 16) ATOM_LNT(4);
+    else if (ne <= 20) ATOM_LNT(5);
+    else ATOM_LNT(8);
+#undef ATOM_LNT
+    return hipGetLastError();
+  }
   if (lnw_usable(d)) {
     const int rpw = lnw_rows_per_wave(rows);
     dim3 wgrid(static_cast<unsigned>((rows + 4 * rpw - 1) / (4 * rpw))), wblock(256);
@@ -605,6 +766,7 @@ hipError_t layernorm_fwd(int dtype, const float* x, const void* gamma, const voi
 }
 
 int64_t layernorm_bwd_blocks(int64_t rows, int d) {
+  if (lnt_usable(d)) return (rows + LNT_ROWS - 1) / LNT_ROWS;
   if (lnw_usable(d)) {
     const int rpw = lnw_rows_per_wave(rows);
     return (rows + 4 * rpw - 1) / (4 * rpw);

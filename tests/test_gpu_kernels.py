@@ -231,7 +231,7 @@ def test_gemm_rejects_unsupported_shapes():
 # ----------------------------------------------------------------- LayerNorm
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("rows,d", [(37, 256), (130, 768), (17, 320), (5, 4096), (3, 5120), (4100, 256),
-                                    (300, 2048), (1031, 5120)])
+                                    (300, 2048), (1031, 5120), (77, 1088), (16, 8192), (41, 1024)])
 def test_layernorm_fwd_bwd(dtype, rows, d):
     r = U.rng(rows + d)
     x = (r.standard_normal((rows, d)) * 2 + 0.5).astype(np.float32)
