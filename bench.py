@@ -226,7 +226,9 @@ def main():
                          "groups stay for the backward, every other group is loaded again in the backward)")
     ap.add_argument("--optimizer", action="store_true",
                     help="after the timed global batch, run the host AdamW step once (timed on its own, "
-                         "not part of the step throughput, as in the paper)")
+                         "not part of the step throughput, as in the paper), then time one more global batch "
+                         "followed by the update, and one with the update armed (applied group by group as the "
+                         "last step's gradients land)")
     ap.add_argument("--measured-plan", action="store_true",
                     help="profile every node on the GPU (atom_profile_nodes) and plan the timed steps with those "
                          "costs instead of the analytic ones")
@@ -319,9 +321,12 @@ def main():
         plan = mplan
     sess.zero_grads()
 
-    def run(n):
-        """n steps (tokens[i] for step i); returns the losses."""
+    def run(n, arm=None):
+        """n steps (tokens[i] for step i); returns the losses.  arm(): called
+        before the call that runs the last step (an armed optimizer update)."""
         if args.sequential:
+            if arm:
+                raise SystemExit("--optimizer times pipelined calls; drop --sequential")
             out = []
             for i in range(n):
                 out.append(sess.step(tokens[i]))
@@ -329,6 +334,8 @@ def main():
             return out
         out = []
         for i0 in range(0, n, A.MAX_STEPS_PER_CALL):
+            if arm and i0 + A.MAX_STEPS_PER_CALL >= n:
+                arm()
             out.extend(sess.steps(tokens[i0:min(n, i0 + A.MAX_STEPS_PER_CALL)]).tolist())
             log(f"steps {i0}..{i0 + len(out) - 1}: {sess.stats().step_s * 1e3:.1f} ms/step")
         return out
@@ -530,6 +537,7 @@ def main():
             "frac": round(max(t_mfma, t_link) / (ms_per_step / 1e3), 4),
         }
     if args.optimizer:
+        A.atom_probe_gemm(sess.ctx, 0, 0, -1)
         t0 = time.perf_counter()
         A.atom_optimizer_init(sess.ctx)
         t_init = time.perf_counter() - t0
@@ -537,10 +545,34 @@ def main():
         A.atom_optimizer_step(sess.ctx, 1e-4, 1.0 / args.steps, 1)
         t_opt = time.perf_counter() - t0
         n_par = synthetic.param_count(cfg)
-        result["optimizer"] = {"kind": "host AdamW (fp32 master, moments), once per global batch",
-                               "init_s": round(t_init, 3), "step_s": round(t_opt, 3),
-                               "params": n_par, "host_gbs": round(n_par * 34 / t_opt / 1e9, 1)}
         log(f"host AdamW over {n_par / 1e9:.2f} B parameters: {t_opt:.2f} s (init {t_init:.2f} s)")
+        # one global batch, then the update (the paper's order) ...
+        t0 = time.perf_counter()
+        run(args.steps)
+        t_mid = time.perf_counter()
+        A.atom_optimizer_step(sess.ctx, 1e-4, 1.0 / args.steps, 2)
+        t_after = time.perf_counter() - t0
+        t_upd = time.perf_counter() - t_mid
+        # ... and one with the update armed: each group is updated as soon as
+        # its last gradients of the global batch are accumulated
+        t0 = time.perf_counter()
+        run(args.steps, arm=lambda: A.atom_optimizer_arm(sess.ctx, 1e-4, 1.0 / args.steps, 3))
+        t_armed = time.perf_counter() - t0
+        st_arm = sess.stats()
+        tok_gb = cfg.tokens_per_step * args.steps
+        result["optimizer"] = {
+            "kind": "host AdamW (fp32 master and moments), once per global batch",
+            "state_memory": "pinned" if st_arm.opt_state_pinned else "pageable (the system refused to pin it)",
+            "init_s": round(t_init, 3), "step_s": round(t_opt, 3), "params": n_par,
+            "host_gbs": round(n_par * 34 / t_opt / 1e9, 1),
+            "global_batch_steps": args.steps,
+            "global_batch_then_update_s": round(t_after, 3), "update_after_s": round(t_upd, 3),
+            "global_batch_armed_update_s": round(t_armed, 3),
+            "armed_update_host_s": round(st_arm.host_update_s, 3), "armed_groups": st_arm.updated_groups,
+            "tokens_per_s_update_after": round(tok_gb / t_after, 1),
+            "tokens_per_s_update_armed": round(tok_gb / t_armed, 1)}
+        log(f"global batch + update: {t_after:.2f} s (update {t_upd:.2f} s); armed: {t_armed:.2f} s "
+            f"(update work {st_arm.host_update_s:.2f} s over {st_arm.updated_groups} groups)")
     sess.close()
     if not args.no_cpu_baseline:
         log("timing the oracle on the host (cpu_baseline)")

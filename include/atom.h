@@ -240,7 +240,9 @@ void atom_ctx_destroy(atom_ctx* ctx);
 
 /* Host buffers of a node: which = 0 weights (working dtype, writable),
  * 1 fp32 gradient accumulators (sum over committed steps), 2 gradients of
- * the last step in the working dtype. */
+ * the last step in the working dtype; with the optimizer state allocated
+ * (atom_optimizer_init, else ATOM_ESTATE): 3 fp32 master weights, 4 and 5
+ * the fp32 first and second AdamW moments. */
 int atom_host_tensor(atom_ctx* ctx, int32_t node, int32_t which, void** ptr, uint64_t* bytes);
 
 /* Zero the fp32 gradient accumulators. */
@@ -321,7 +323,9 @@ int atom_set_retention(atom_ctx* ctx, int32_t on);
  * is complete, learning rate 1e-4 after a linear warm-up, betas 0.9 and
  * 0.999).  atom_optimizer_init allocates fp32 master weights (copied from
  * the host model) and the two moments (zero), 12 bytes per parameter of
- * pageable memory.  atom_optimizer_step waits for all work, then for every
+ * pinned host memory, or pageable memory when the system refuses to pin that
+ * much (atom_stats.opt_state_pinned tells which; the GPU never reads this
+ * state).  atom_optimizer_step waits for all work, then for every
  * parameter: g = grad_scale * accumulator (e.g. 1 / steps of the global
  * batch), m = beta1 m + (1 - beta1) g, v = beta2 v + (1 - beta2) g^2,
  * p = p (1 - lr wd) - lr (m / (1 - beta1^step)) / (sqrt(v / (1 - beta2^step))
@@ -335,6 +339,18 @@ typedef struct atom_adamw {
 } atom_adamw;
 int atom_optimizer_init(atom_ctx* ctx);
 int atom_optimizer_step(atom_ctx* ctx, const atom_adamw* hp, float grad_scale, int32_t step);
+/* The same update, applied during the next atom_step / atom_steps call
+ * instead of after it: in that call's last step, as soon as a group's
+ * gradients have been added to the accumulators (the group's last gradients
+ * of the global batch, Section III-E), the host thread pool updates that
+ * group's parameters, so the update of the groups that finish their backward
+ * first overlaps the backward of the others on the GPU.  The call returns
+ * once every group is updated; the result (host model, master weights,
+ * moments, zeroed accumulators) is bitwise that of the call followed by
+ * atom_optimizer_step with the same arguments.  One-shot: the call consumes
+ * it (also when it fails, in which case the update may cover only some
+ * groups).  ATOM_ESTATE before atom_optimizer_init. */
+int atom_optimizer_arm(atom_ctx* ctx, const atom_adamw* hp, float grad_scale, int32_t step);
 
 /* Measured node costs for the planner (the per-layer profile of Section
  * III-D: loading time t^u, forward time t^f, backward time t^b and working
@@ -365,6 +381,9 @@ typedef struct atom_stats {
   uint64_t h2d_bytes, d2h_bytes;
   double step_s, host_accum_s;
   int32_t swap_ins, swap_outs;
+  double host_update_s;      /* host time of an armed optimizer update (whole call) */
+  int32_t updated_groups;    /* groups that update covered */
+  int32_t opt_state_pinned;  /* optimizer state allocated in pinned memory (else pageable, or absent) */
 } atom_stats;
 int atom_get_stats(atom_ctx* ctx, atom_stats* out);
 

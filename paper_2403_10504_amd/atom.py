@@ -25,7 +25,7 @@ ATOM_F32, ATOM_BF16 = 0, 1
 ATOM_CKPT_DEVICE, ATOM_CKPT_HOST = 0, 1
 (ATOM_EPI_STORE, ATOM_EPI_STORE_F32, ATOM_EPI_ACC_F32, ATOM_EPI_BIAS, ATOM_EPI_BIAS_GELU, ATOM_EPI_BIAS_RESID,
  ATOM_EPI_GELU_BWD) = range(7)
-WEIGHTS, GRAD_ACC, GRAD_LAST = 0, 1, 2
+WEIGHTS, GRAD_ACC, GRAD_LAST, MASTER, MOMENT1, MOMENT2 = 0, 1, 2, 3, 4, 5
 
 
 class atom_config(ctypes.Structure):
@@ -74,7 +74,9 @@ class atom_tensor_desc(ctypes.Structure):
 
 class atom_stats(ctypes.Structure):
     _fields_ = [("h2d_bytes", ctypes.c_uint64), ("d2h_bytes", ctypes.c_uint64), ("step_s", ctypes.c_double),
-                ("host_accum_s", ctypes.c_double), ("swap_ins", ctypes.c_int32), ("swap_outs", ctypes.c_int32)]
+                ("host_accum_s", ctypes.c_double), ("swap_ins", ctypes.c_int32), ("swap_outs", ctypes.c_int32),
+                ("host_update_s", ctypes.c_double), ("updated_groups", ctypes.c_int32),
+                ("opt_state_pinned", ctypes.c_int32)]
 
 
 class AtomError(RuntimeError):
@@ -117,6 +119,7 @@ _SIGS = {
     "atom_profile_nodes": (ctypes.c_int, [P, P, P, I32]),
     "atom_optimizer_init": (ctypes.c_int, [P]),
     "atom_optimizer_step": (ctypes.c_int, [P, P, ctypes.c_float, I32]),
+    "atom_optimizer_arm": (ctypes.c_int, [P, P, ctypes.c_float, I32]),
     "atom_last_error": (ctypes.c_char_p, [P]),
     "atom_k_gemm": (ctypes.c_int, [ctypes.c_int] * 7 + [P, I64, P, I64, P, I64, P, P, P, I64, P, U64, P]),
     "atom_k_layernorm_fwd": (ctypes.c_int, [ctypes.c_int, P, P, P, P, P, P, I64, ctypes.c_int, P]),
@@ -405,6 +408,11 @@ def atom_optimizer_init(ctx):
 def atom_optimizer_step(ctx, lr, grad_scale, step, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0):
     hp = atom_adamw(lr, beta1, beta2, eps, weight_decay)
     _check(lib().atom_optimizer_step(ctx, _ref(hp), grad_scale, step), ctx)
+
+
+def atom_optimizer_arm(ctx, lr, grad_scale, step, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0):
+    hp = atom_adamw(lr, beta1, beta2, eps, weight_decay)
+    _check(lib().atom_optimizer_arm(ctx, _ref(hp), grad_scale, step), ctx)
 
 
 def atom_link_bench(ctx, nbytes: int, iters: int):

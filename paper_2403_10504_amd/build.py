@@ -22,7 +22,8 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libatom.so")
 ARCH = "gfx950"
 
-HIP_SOURCES = ["gemm.hip", "attention.hip", "attention_f32.hip", "rowops.hip", "runtime.cpp", "transfer.cpp", "capi_kernels.cpp"]
+HIP_SOURCES = ["gemm.hip", "attention.hip", "attention_f32.hip", "rowops.hip", "runtime.cpp", "nodes.cpp", "schedule.cpp",
+               "host_accum.cpp", "transfer.cpp", "capi_kernels.cpp"]
 # per-source optimisation level (see attention_f32.hip)
 OPT = {"attention_f32.hip": "-O1"}
 CXX_SOURCES = ["plan.cpp"]

@@ -39,7 +39,7 @@ class Session:
         for tname, rows, cols, off, tbytes in self.layout[node]:
             if tname == name:
                 esz = np.dtype(self.elem).itemsize
-                if which == A.GRAD_ACC:
+                if which in (A.GRAD_ACC, A.MASTER, A.MOMENT1, A.MOMENT2):  # fp32, element-indexed
                     dtype, off, count = np.float32, off // esz * 4, tbytes // esz
                 else:
                     dtype, count = self.elem, tbytes // esz
@@ -79,7 +79,9 @@ class Session:
         return self.grads(A.WEIGHTS)
 
     def grads(self, which: int = A.GRAD_ACC):
-        """Gradients as float32 arrays: accumulators (default) or the last step's."""
+        """Gradients as float32 arrays: accumulators (default) or the last step's;
+        also the weights (WEIGHTS) and the optimizer's fp32 master weights and
+        moments (MASTER, MOMENT1, MOMENT2)."""
         import synthetic
 
         out = []
@@ -87,7 +89,7 @@ class Session:
             p = {}
             for name, rows, cols, _, _ in self.layout[node]:
                 v = np.array(self.host_view(node, name, which))
-                if which != A.GRAD_ACC and self.elem == np.uint16:
+                if which in (A.WEIGHTS, A.GRAD_LAST) and self.elem == np.uint16:
                     v = synthetic.bf16_bits_to_f32(v)
                 if name == "w_head":
                     v = v[: self.cfg.vocab]
