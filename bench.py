@@ -42,8 +42,8 @@ HBM_PEAK_GBS = 8000.0
 # --copy-calibration 2147483648`, each scaled by what the counter reads for
 # the plain copy kernel of known size (profiles/gemm_wgrad_6.7b_hbm_traffic.md).
 # Valid only for the kernel sources it was measured on.
-WGRAD_TRAFFIC = {"sources_sha256": "6b95969b8bedcd64d1c806cac43b3496df7bd74a1c7e50cdf07fa046c845cf33",
-                 "bytes_per_launch": 725704458}
+WGRAD_TRAFFIC = {"sources_sha256": "5b2c7ed08ef49c4e14822aaf57262fccd09a2efe914ec142e5b6281a7b7cd87c",
+                 "bytes_per_launch": 725832891}
 TRAFFIC_SOURCES = ("gemm.hip", "common.h", "launch.h")
 
 
@@ -378,7 +378,8 @@ def main():
     pred_call = ends[-1] / len(ends)
     pred_one = A.atom_plan_predict(c, plan, costs, duplex, 1)[0][0]
     steady = ((ends[-1] - ends[-3]) / 2.0) if len(ends) >= 3 else None
-    log(f"predicted {pred_call * 1e3:.1f} ms per step of the call (steady {steady and steady * 1e3:.1f}), "
+    steady_txt = f"{steady * 1e3:.1f} ms" if steady is not None else "needs 3 steps"
+    log(f"predicted {pred_call * 1e3:.1f} ms per step of the call (steady {steady_txt}), "
         f"{pred_one * 1e3:.1f} ms for one step alone")
 
     # Parity of the timed path: the last timed step's gradients and loss
