@@ -404,8 +404,12 @@ struct FwdDL {
   __device__ static int vswz(int r) { return DH == 128 ? 2 * (r & 7) : 2 * ((r >> 1) & 3); }
 };
 
+// Waves per SIMD the register allocation must allow (the second launch bound):
+// two at d_h 128 (230 registers: two workgroups per CU, as the LDS allows);
+// four at d_h 64, where 128 registers suffice and four workgroups fit the LDS
+// (82 against 88 us at GPT-3 Small's shape; five spill).
 template <int DH, int G>
-__global__ void __launch_bounds__(256, 2) attn_fwd_dl_kernel(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ o,
+__global__ void __launch_bounds__(256, DH == 64 ? 4 : 2) attn_fwd_dl_kernel(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ o,
                                                              float* __restrict__ lse, int B, int Tn, int H) {
   using F = FwdDL<DH>;
   constexpr int NS = DH / 32, NCT = DH / 16, BQ = 4 * 16 * G, RB = DH * 2;
@@ -947,8 +951,12 @@ __global__ void __launch_bounds__(64 * NW, ATOM_ATTN_DQ_OCC) attn_bwd_dq_kernel(
 template <int DH>
 __device__ __forceinline__ int dsw(int r);
 
+// Launch bounds of both backward kernels: at d_h 64 four waves per SIMD (108
+// registers; two eight-wave workgroups per CU: 264 against 291 us for the
+// whole backward at GPT-3 Small's shape), at d_h 128 two (244 and 174
+// registers, one workgroup per CU; 128 registers would spill).
 template <int DH, int W>
-__global__ void __launch_bounds__(64 * W) attn_bwd_dkdv_dl_kernel(const bf16_t* __restrict__ qkv,
+__global__ void __launch_bounds__(64 * W, DH == 64 ? 4 : 2) attn_bwd_dkdv_dl_kernel(const bf16_t* __restrict__ qkv,
                                                                   const bf16_t* __restrict__ dout,
                                                                   const float* __restrict__ lse,
                                                                   const float* __restrict__ delta,
@@ -1134,7 +1142,7 @@ __device__ __forceinline__ int dsw(int r) {
 }
 
 template <int DH, int NW>
-__global__ void __launch_bounds__(64 * NW) attn_bwd_dq_dl_kernel(const bf16_t* __restrict__ qkv,
+__global__ void __launch_bounds__(64 * NW, DH == 64 ? 4 : 2) attn_bwd_dq_dl_kernel(const bf16_t* __restrict__ qkv,
                                                                 const bf16_t* __restrict__ dout,
                                                                 const float* __restrict__ lse,
                                                                 const float* __restrict__ delta,
