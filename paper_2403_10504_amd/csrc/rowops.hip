@@ -597,6 +597,79 @@ __global__ void __launch_bounds__(256) xent_kernel(const float* __restrict__ z, 
   if (tid == 0) loss_rows[row] = (y >= 0 && y < V) ? lse - zr[y] : __builtin_nanf("");
 }
 
+// Cross-entropy with the row in registers: 1024 threads per row, thread t
+// owns the 16-byte chunks t + 1024 i (i < NV) of the fp32 logits, so the row
+// is read from HBM once (the two-pass kernel above reads it twice, with
+// 4-byte loads).  Max, then the sum of 2^((z - max) log2 e) kept in the same
+// registers, then dz = (p - onehot) scale from them: three block reductions,
+// each wave's shuffles then the 16 waves in a fixed order.  Columns V..lddz-1
+// of dz are zeroed; the loss row is lse - z[y] (NaN for y outside [0, V)).
+// Needs ldz and lddz multiples of 4 and 16-byte aligned rows (dispatch).
+template <typename T, int NV>
+__global__ void __launch_bounds__(1024) xent_reg_kernel(const float* __restrict__ z, int64_t ldz,
+                                                        const int32_t* __restrict__ tgt, T* __restrict__ dz,
+                                                        int64_t lddz, float* __restrict__ loss_rows, int V,
+                                                        float scale) {
+  __shared__ float red[3][16];
+  const int64_t row = blockIdx.x;
+  const float* zr = z + row * ldz;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  constexpr float L2E = 1.4426950408889634f;
+  float x[NV][4];
+  float m = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = 4 * (tid + 1024 * i);
+    if (c + 4 <= V) {
+      const float4 v = *reinterpret_cast<const float4*>(zr + c);
+      x[i][0] = v.x;
+      x[i][1] = v.y;
+      x[i][2] = v.z;
+      x[i][3] = v.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[i][e] = c + e < V ? zr[c + e] : -INFINITY;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) m = fmaxf(m, x[i][e]);
+  }
+  m = wave_max(m);
+  if (lane == 0) red[0][w] = m;
+  __syncthreads();
+  m = red[0][0];
+#pragma unroll
+  for (int i = 1; i < 16; ++i) m = fmaxf(m, red[0][i]);
+  const float mb = m * L2E;
+  float sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[i][e] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[i][e], L2E, -mb));  // 0 for the -inf fill
+      sum += x[i][e];
+    }
+  sum = wave_sum(sum);
+  if (lane == 0) red[1][w] = sum;
+  __syncthreads();
+  sum = red[1][0];
+#pragma unroll
+  for (int i = 1; i < 16; ++i) sum += red[1][i];
+  const float inv = 1.f / sum;
+  const int y = tgt[row];
+  T* dr = dz + row * lddz;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = 4 * (tid + 1024 * i);
+    if (c >= lddz) break;
+    float g[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) g[e] = c + e < V ? (x[i][e] * inv - (c + e == y ? 1.f : 0.f)) * scale : 0.f;
+    Vec4<T>::store(dr + c, g);  // lddz is a multiple of 4: the chunk is inside the row
+  }
+  // a target outside [0, V) gives a NaN loss instead of an out-of-range read
+  if (tid == 0) loss_rows[row] = (y >= 0 && y < V) ? m + logf(sum) - zr[y] : __builtin_nanf("");
+}
+
 // ---------------------------------------------------------------- helpers
 __global__ void __launch_bounds__(256) sum_fixed_kernel(const float* __restrict__ x, int64_t n,
                                                         float* __restrict__ out) {
@@ -869,6 +942,29 @@ hipError_t xent_fwd_bwd(int dtype, const float* logits, int64_t ldz, const int32
                         float* loss_rows, int64_t rows, int V, float scale, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   if (V <= 0 || lddz < V || ldz < V) return hipErrorInvalidValue;
+  const int esz = dtype == DT_BF16 ? 2 : 4;
+  const int nv = static_cast<int>((lddz + 4095) / 4096);  // 16-byte chunks per thread
+  if (ldz % 4 == 0 && lddz % 4 == 0 && reinterpret_cast<uintptr_t>(logits) % 16 == 0 &&
+      reinterpret_cast<uintptr_t>(dz) % (4 * esz) == 0 && nv <= 16) {
+    dim3 g1(static_cast<unsigned>(rows)), b1(1024);
+#define ATOM_XR(NV)                                                                                                 \
+  do {                                                                                                              \
+    if (dtype == DT_BF16)                                                                                           \
+      hipLaunchKernelGGL((xent_reg_kernel<bf16_t, NV>), g1, b1, 0, s, logits, ldz, tgt, static_cast<bf16_t*>(dz), \
+                         lddz, loss_rows, V, scale);                                                                \
+    else                                                                                                            \
+      hipLaunchKernelGGL((xent_reg_kernel<float, NV>), g1, b1, 0, s, logits, ldz, tgt, static_cast<float*>(dz),   \
+                         lddz, loss_rows, V, scale);                                                                \
+  } while (0)
+    if (nv <= 1) ATOM_XR(1);
+    else if (nv <= 2) ATOM_XR(2);
+    else if (nv <= 4) ATOM_XR(4);
+    else if (nv <= 8) ATOM_XR(8);
+    else if (nv <= 13) ATOM_XR(13);
+    else ATOM_XR(16);
+#undef ATOM_XR
+    return hipGetLastError();
+  }
   dim3 grid(static_cast<unsigned>(rows)), block(256);
   if (dtype == DT_BF16)
     hipLaunchKernelGGL(xent_kernel<bf16_t>, grid, block, 0, s, logits, ldz, tgt, static_cast<bf16_t*>(dz), lddz,

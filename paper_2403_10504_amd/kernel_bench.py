@@ -4,6 +4,7 @@ python -m paper_2403_10504_amd.kernel_bench attention [fwd|bwd|all] [iters]
 python -m paper_2403_10504_amd.kernel_bench gemm [iters]
 python -m paper_2403_10504_amd.kernel_bench gemm_layouts [iters]
 python -m paper_2403_10504_amd.kernel_bench layernorm [iters]
+python -m paper_2403_10504_amd.kernel_bench xent [iters]
 
 attention: causal attention at the 6.7B shape (B 2, T 2048, 32 heads of 128),
 GPT-3 Small's (B 8, 12 heads of 64) and 13B's (B 1, 40 heads of 128); the
@@ -135,6 +136,20 @@ def layernorm(iters=50):
         print(f"layernorm bwd rows={rows} d={d}: {us:.1f} us, {alg / us / 1e3:.0f} GB/s algorithmic", flush=True)
 
 
+def xent(iters=20):
+    """The LM head's cross-entropy over 2048-row chunks of fp32 logits (GPT-3 vocabulary)."""
+    for rows, V, ld in ((2048, 50257, 50304), (4096, 50257, 50304)):
+        z = torch.randn(rows, ld, device="cuda") * 3
+        tgt = torch.randint(0, V, (rows,), device="cuda", dtype=torch.int32)
+        dz = torch.empty(rows, ld, device="cuda", dtype=torch.bfloat16)
+        loss = torch.empty(rows, device="cuda")
+        us = _time(lambda: A.atom_k_xent(1, z.data_ptr(), ld, tgt.data_ptr(), dz.data_ptr(), ld, loss.data_ptr(), rows,
+                                         V, 1.0 / rows), iters)
+        alg = rows * ld * (4 + 2)
+        print(f"xent rows={rows} V={V}: {us:.1f} us, {alg / us / 1e3:.0f} GB/s algorithmic "
+              f"(fp32 logits read once, bf16 dz written once)", flush=True)
+
+
 def main(argv):
     if not torch.cuda.is_available():
         raise SystemExit("kernel_bench needs a GPU")
@@ -145,6 +160,8 @@ def main(argv):
         gemm(int(argv[2]) if len(argv) > 2 else 20)
     elif what == "gemm_layouts":
         gemm_layouts(int(argv[2]) if len(argv) > 2 else 20)
+    elif what == "xent":
+        xent(int(argv[2]) if len(argv) > 2 else 20)
     elif what == "layernorm":
         layernorm(int(argv[2]) if len(argv) > 2 else 50)
     else:

@@ -314,7 +314,8 @@ def test_attention_fwd_bwd(dtype, B, T, H, dh):
 
 # ------------------------------------------------------- cross-entropy etc.
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-@pytest.mark.parametrize("rows,V,ld", [(33, 1000, 1024), (5, 50257, 50304), (1, 7, 128)])
+@pytest.mark.parametrize("rows,V,ld", [(33, 1000, 1024), (5, 50257, 50304), (1, 7, 128), (3, 4097, 4100), (4, 1003, 1003),
+                                      (2, 65000, 65536)])
 def test_cross_entropy_rows(dtype, rows, V, ld):
     r = U.rng(rows + V)
     z = np.zeros((rows, ld), np.float32)
