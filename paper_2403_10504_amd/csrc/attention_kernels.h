@@ -975,8 +975,13 @@ __global__ void __launch_bounds__(64 * W, DH == 64 ? 4 : 2) attn_bwd_dkdv_dl_ker
   constexpr int NS = DH / 32, NCT = DH / 16, NT = 64 * W, RB = DH * 2, BKEYS = 16 * W;
   constexpr int LPT = F::TILE / (NT * 16);
   static_assert(LPT >= 1 && F::TILE % (NT * 16) == 0, "tile split");
-  constexpr int STAGE = 2 * F::TILE + 2 * BT * 4;  // Q, dO, LSE (log2 units), D
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * STAGE];
+  constexpr int STAGE = 2 * F::TILE + 2 * BT * 4;  // Q, dO, LSE (log2 units), D of one 64-query tile
+  // Two query tiles per pipeline stage, so one barrier per 128 queries: the
+  // wave's work between barriers doubles (373 against 377 us for the whole
+  // backward at the 6.7B shape, 262 against 273 at d_h 64); the loop over
+  // the two stays rolled (unrolled, 40 bytes spill at d_h 128)
+  constexpr int SUB = 2;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * SUB * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 15, lg = lane >> 4;
@@ -1022,18 +1027,19 @@ __global__ void __launch_bounds__(64 * W, DH == 64 ? 4 : 2) attn_bwd_dkdv_dl_ker
   // LSE and D of a tile's rows: read into registers, stored to LDS after the
   // tile's compute (rows past the end get LSE = +inf, so their P is 0)
   float pre_lse = 0.f, pre_del = 0.f;
+  // (thread tid < SUB*BT reads row tid % BT of sub-tile tid / BT)
   auto read_rows = [&](int i0) {
-    if (tid < BT) {
+    if (tid < SUB * BT) {
       const int i = i0 + tid;
       pre_lse = i < Tn ? lse_b[i] * LOG2E : INFINITY;
       pre_del = i < Tn ? del_b[i] : 0.f;
     }
   };
   auto store_rows = [&](int st) {
-    if (tid < BT) {
-      float* rows = reinterpret_cast<float*>(lds + st * STAGE + 2 * F::TILE);
-      rows[tid] = pre_lse;
-      rows[BT + tid] = pre_del;
+    if (tid < SUB * BT) {
+      float* rows = reinterpret_cast<float*>(lds + (st * SUB + tid / BT) * STAGE + 2 * F::TILE);
+      rows[tid % BT] = pre_lse;
+      rows[BT + tid % BT] = pre_del;
     }
   };
   auto rowfrag = [&](Frag<bf16_t>& f, const uint8_t* st, int it, int s) {
@@ -1050,114 +1056,125 @@ __global__ void __launch_bounds__(64 * W, DH == 64 ? 4 : 2) attn_bwd_dkdv_dl_ker
 
   const int qt0 = k0 / BT, n_qt = (Tn + BT - 1) / BT;
   const bool tail_keys = kw + 16 > Tn;  // some of this wave's keys are past the end
+  // the SUB tiles from query tile qt into stage st (tiles past the end are skipped)
+  auto load_stage = [&](int st, int qt) {
+#pragma unroll
+    for (int u = 0; u < SUB; ++u)
+      if (qt + u < n_qt) load_tile(st * SUB + u, (qt + u) * BT);
+  };
   if (qt0 < n_qt) {
-    load_tile(0, qt0 * BT);
+    load_stage(0, qt0);
     read_rows(qt0 * BT);
     store_rows(0);
   }
-  for (int qt = qt0; qt < n_qt; ++qt) {
-    const int i0 = qt * BT, cur = (qt - qt0) & 1;
+  for (int qs0 = qt0; qs0 < n_qt; qs0 += SUB) {
+    const int cur = ((qs0 - qt0) / SUB) & 1;
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
     asm volatile("s_barrier" ::: "memory");
-    const bool more = qt + 1 < n_qt;
+    const bool more = qs0 + SUB < n_qt;
     if (more) {
-      load_tile(cur ^ 1, i0 + BT);
-      read_rows(i0 + BT);
+      load_stage(cur ^ 1, qs0 + SUB);
+      read_rows((qs0 + SUB) * BT);
     }
-    if (i0 + BT - 1 >= kw && kw < Tn) {  // some query of the tile sees some key of this wave
-      const uint8_t* qs = lds + cur * STAGE;
-      const uint8_t* os = qs + F::TILE;
-      const float* lse_s = reinterpret_cast<const float*>(qs + 2 * F::TILE);
-      const float* del_s = lse_s + BT;
-      float p[4][4], ds[4][4];
-      const bool mask = i0 < kw + 15 || tail_keys;  // diagonal tile or keys past the end
-      if constexpr (DH == 128) {
-        // One branch-free block per tile (the mask a template parameter), so
-        // the exponentials of 16 queries overlap the next 16 queries' MFMAs;
-        // LDS reads stay in their 16-query step (sched_barrier lets only VALU
-        // and MFMA cross), else the scheduler hoists every step's fragments
-        // and spills (380 against 393 us for the backward at the 6.7B shape).
-        auto score_tile = [&](auto MASK_) {
-          constexpr bool MASK = decltype(MASK_)::value;
+#pragma unroll 1
+    for (int u = 0; u < SUB; ++u) {
+      const int qt = qs0 + u, i0 = qt * BT, stg = cur * SUB + u;
+      if (qt >= n_qt) break;
+      if (i0 + BT - 1 >= kw && kw < Tn) {  // some query of the tile sees some key of this wave
+        const uint8_t* qs = lds + stg * STAGE;
+        const uint8_t* os = qs + F::TILE;
+        const float* lse_s = reinterpret_cast<const float*>(qs + 2 * F::TILE);
+        const float* del_s = lse_s + BT;
+        float p[4][4], ds[4][4];
+        const bool mask = i0 < kw + 15 || tail_keys;  // diagonal tile or keys past the end
+        if constexpr (DH == 128) {
+          // One branch-free block per tile (the mask a template parameter), so
+          // the exponentials of 16 queries overlap the next 16 queries' MFMAs;
+          // LDS reads stay in their 16-query step (sched_barrier lets only VALU
+          // and MFMA cross), else the scheduler hoists every step's fragments
+          // and spills (380 against 393 us for the backward at the 6.7B shape).
+          auto score_tile = [&](auto MASK_) {
+            constexpr bool MASK = decltype(MASK_)::value;
+#pragma unroll
+            for (int it = 0; it < 4; ++it) {
+              Frag<bf16_t> qf[NS], of[NS];
+#pragma unroll
+              for (int s = 0; s < NS; ++s) {
+                rowfrag(qf[s], qs, it, s);
+                rowfrag(of[s], os, it, s);
+              }
+              f32x4_t sa = f32x4_t{0.f, 0.f, 0.f, 0.f}, dp = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+              for (int s = 0; s < NS; ++s) {
+                mfma16(sa, qf[s], kf[s]);  // S[i][j]: lane holds key kj, queries 4lg + r
+                mfma16(dp, of[s], vf[s]);  // dP[i][j]
+              }
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const int il = it * 16 + 4 * lg + r;
+                float pv = ex2(__builtin_fmaf(sa[r], sc, -lse_s[il]));
+                if constexpr (MASK) pv = ((kj <= i0 + il) & (kj < Tn)) ? pv : 0.f;
+                p[it][r] = pv;
+                ds[it][r] = pv * (dp[r] - del_s[il]);
+              }
+              __builtin_amdgcn_sched_barrier(0x000A);
+            }
+          };
+          if (mask) score_tile(std::true_type{});
+          else score_tile(std::false_type{});
+        } else {
+          // d_h 64: fragments one step ahead and the mask a runtime test (the
+          // branch-free form spills within the 128 registers of four waves per SIMD)
+          Frag<bf16_t> qf[2][NS], of[2][NS];
+#pragma unroll
+          for (int s = 0; s < NS; ++s) {
+            rowfrag(qf[0][s], qs, 0, s);
+            rowfrag(of[0][s], os, 0, s);
+          }
 #pragma unroll
           for (int it = 0; it < 4; ++it) {
-            Frag<bf16_t> qf[NS], of[NS];
+            if (it + 1 < 4) {
 #pragma unroll
-            for (int s = 0; s < NS; ++s) {
-              rowfrag(qf[s], qs, it, s);
-              rowfrag(of[s], os, it, s);
+              for (int s = 0; s < NS; ++s) {
+                rowfrag(qf[(it + 1) & 1][s], qs, it + 1, s);
+                rowfrag(of[(it + 1) & 1][s], os, it + 1, s);
+              }
             }
             f32x4_t sa = f32x4_t{0.f, 0.f, 0.f, 0.f}, dp = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
-              mfma16(sa, qf[s], kf[s]);  // S[i][j]: lane holds key kj, queries 4lg + r
-              mfma16(dp, of[s], vf[s]);  // dP[i][j]
+              mfma16(sa, qf[it & 1][s], kf[s]);
+              mfma16(dp, of[it & 1][s], vf[s]);
             }
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const int il = it * 16 + 4 * lg + r;
               float pv = ex2(__builtin_fmaf(sa[r], sc, -lse_s[il]));
-              if constexpr (MASK) pv = ((kj <= i0 + il) & (kj < Tn)) ? pv : 0.f;
+              if (mask) pv = ((kj <= i0 + il) & (kj < Tn)) ? pv : 0.f;
               p[it][r] = pv;
               ds[it][r] = pv * (dp[r] - del_s[il]);
             }
-            __builtin_amdgcn_sched_barrier(0x000A);
           }
-        };
-        if (mask) score_tile(std::true_type{});
-        else score_tile(std::false_type{});
-      } else {
-        // d_h 64: fragments one step ahead and the mask a runtime test (the
-        // branch-free form spills within the 128 registers of four waves per SIMD)
-        Frag<bf16_t> qf[2][NS], of[2][NS];
-#pragma unroll
-        for (int s = 0; s < NS; ++s) {
-          rowfrag(qf[0][s], qs, 0, s);
-          rowfrag(of[0][s], os, 0, s);
         }
+        Frag<bf16_t> ot2[2], qt2[2];
+        trfrag(ot2[0], os, 0, 0);
+        trfrag(qt2[0], qs, 0, 0);
 #pragma unroll
-        for (int it = 0; it < 4; ++it) {
-          if (it + 1 < 4) {
+        for (int s2 = 0; s2 < 2; ++s2) {
+          Frag<bf16_t> pf, dsf;
+          frag_from_pair(pf, p, s2);
+          frag_from_pair(dsf, ds, s2);
 #pragma unroll
-            for (int s = 0; s < NS; ++s) {
-              rowfrag(qf[(it + 1) & 1][s], qs, it + 1, s);
-              rowfrag(of[(it + 1) & 1][s], os, it + 1, s);
+          for (int c = 0; c < NCT; ++c) {
+            const int n = s2 * NCT + c;
+            if (n + 1 < 2 * NCT) {
+              trfrag(ot2[(n + 1) & 1], os, (n + 1) / NCT, (n + 1) % NCT);
+              trfrag(qt2[(n + 1) & 1], qs, (n + 1) / NCT, (n + 1) % NCT);
             }
+            mfma16(acc_dv[c], ot2[n & 1], pf);   // dV^T[c][j]
+            mfma16(acc_dk[c], qt2[n & 1], dsf);  // dK^T[c][j]
           }
-          f32x4_t sa = f32x4_t{0.f, 0.f, 0.f, 0.f}, dp = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int s = 0; s < NS; ++s) {
-            mfma16(sa, qf[it & 1][s], kf[s]);
-            mfma16(dp, of[it & 1][s], vf[s]);
-          }
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int il = it * 16 + 4 * lg + r;
-            float pv = ex2(__builtin_fmaf(sa[r], sc, -lse_s[il]));
-            if (mask) pv = ((kj <= i0 + il) & (kj < Tn)) ? pv : 0.f;
-            p[it][r] = pv;
-            ds[it][r] = pv * (dp[r] - del_s[il]);
-          }
-        }
-      }
-      Frag<bf16_t> ot2[2], qt2[2];
-      trfrag(ot2[0], os, 0, 0);
-      trfrag(qt2[0], qs, 0, 0);
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
-        Frag<bf16_t> pf, dsf;
-        frag_from_pair(pf, p, s2);
-        frag_from_pair(dsf, ds, s2);
-#pragma unroll
-        for (int c = 0; c < NCT; ++c) {
-          const int n = s2 * NCT + c;
-          if (n + 1 < 2 * NCT) {
-            trfrag(ot2[(n + 1) & 1], os, (n + 1) / NCT, (n + 1) % NCT);
-            trfrag(qt2[(n + 1) & 1], qs, (n + 1) / NCT, (n + 1) % NCT);
-          }
-          mfma16(acc_dv[c], ot2[n & 1], pf);   // dV^T[c][j]
-          mfma16(acc_dk[c], qt2[n & 1], dsf);  // dK^T[c][j]
         }
       }
     }
