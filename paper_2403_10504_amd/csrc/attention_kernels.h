@@ -1217,7 +1217,11 @@ __global__ void __launch_bounds__(64 * NW, DH == 64 ? 4 : 2) attn_bwd_dq_dl_kern
   constexpr int NS = DH / 32, NCT = DH / 16, BQ = NW * 16, NT = 64 * NW, RB = DH * 2;
   constexpr int LPT = F::TILE / (NT * 16);  // direct loads per thread per tile and operand
   static_assert(LPT >= 1 && F::TILE % (NT * 16) == 0, "tile split");
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * F::STAGE];
+  // Two key tiles per pipeline stage, one barrier per 128 keys (at d_h 64
+  // 254-260 against 272 us for the whole backward at GPT-3 Small's shape;
+  // unchanged at d_h 128, where one workgroup per CU leaves the LDS for it)
+  constexpr int SUB = 2;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * SUB * F::STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 15, lg = lane >> 4;
@@ -1270,63 +1274,74 @@ __global__ void __launch_bounds__(64 * NW, DH == 64 ? 4 : 2) attn_bwd_dq_dl_kern
   };
 
   const int n_kt = min((Tn + BT - 1) / BT, (min(q0 + BQ, Tn) - 1) / BT + 1);
-  load_tile(0, 0);
-  for (int kt = 0; kt < n_kt; ++kt) {
-    const int j0 = kt * BT, cur = kt & 1;
+  // the SUB key tiles from tile kt into stage st (tiles past the last are skipped)
+  auto load_stage = [&](int st, int kt) {
+#pragma unroll
+    for (int u = 0; u < SUB; ++u)
+      if (kt + u < n_kt) load_tile(st * SUB + u, (kt + u) * BT);
+  };
+  load_stage(0, 0);
+  for (int ks0 = 0; ks0 < n_kt; ks0 += SUB) {
+    const int cur = (ks0 / SUB) & 1;
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
     asm volatile("s_barrier" ::: "memory");
-    if (kt + 1 < n_kt) load_tile(cur ^ 1, j0 + BT);
-    if (j0 <= qw + 15) {
-      const uint8_t* ks = lds + cur * F::STAGE;
-      const uint8_t* vs = ks + F::TILE;
-      float ds[4][4];
-      // one branch-free block per tile (the mask a template parameter)
-      auto score_tile = [&](auto MASK_) {
-        constexpr bool MASK = decltype(MASK_)::value;
-        Frag<bf16_t> kf[2][NS], vf[2][NS];
-#pragma unroll
-        for (int s = 0; s < NS; ++s) {
-          rowfrag(kf[0][s], ks, 0, s, true);
-          rowfrag(vf[0][s], vs, 0, s, false);
-        }
-#pragma unroll
-        for (int jt = 0; jt < 4; ++jt) {
-          if (jt + 1 < 4) {
-#pragma unroll
-            for (int s = 0; s < NS; ++s) {
-              rowfrag(kf[(jt + 1) & 1][s], ks, jt + 1, s, true);
-              rowfrag(vf[(jt + 1) & 1][s], vs, jt + 1, s, false);
-            }
-          }
-          f32x4_t sa = f32x4_t{0.f, 0.f, 0.f, 0.f}, dp = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    if (ks0 + SUB < n_kt) load_stage(cur ^ 1, ks0 + SUB);
+#pragma unroll 1
+    for (int u = 0; u < SUB; ++u) {
+      const int kt = ks0 + u, j0 = kt * BT, stg = cur * SUB + u;
+      if (kt >= n_kt) break;
+      if (j0 <= qw + 15) {
+        const uint8_t* ks = lds + stg * F::STAGE;
+        const uint8_t* vs = ks + F::TILE;
+        float ds[4][4];
+        // one branch-free block per tile (the mask a template parameter)
+        auto score_tile = [&](auto MASK_) {
+          constexpr bool MASK = decltype(MASK_)::value;
+          Frag<bf16_t> kf[2][NS], vf[2][NS];
 #pragma unroll
           for (int s = 0; s < NS; ++s) {
-            mfma16(sa, kf[jt & 1][s], qf[s]);  // S^T[j][i]: lane holds one query, keys 4lg + r
-            mfma16(dp, vf[jt & 1][s], of[s]);  // dP^T[j][i]
+            rowfrag(kf[0][s], ks, 0, s, true);
+            rowfrag(vf[0][s], vs, 0, s, false);
           }
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int j = j0 + jt * 16 + 4 * lg + r;
-            float pv = ex2(__builtin_fmaf(sa[r], sc, -lse_i));
-            if constexpr (MASK) pv = ((j <= qi) & (j < Tn)) ? pv : 0.f;
-            ds[jt][r] = pv * (dp[r] - del_i);
+          for (int jt = 0; jt < 4; ++jt) {
+            if (jt + 1 < 4) {
+#pragma unroll
+              for (int s = 0; s < NS; ++s) {
+                rowfrag(kf[(jt + 1) & 1][s], ks, jt + 1, s, true);
+                rowfrag(vf[(jt + 1) & 1][s], vs, jt + 1, s, false);
+              }
+            }
+            f32x4_t sa = f32x4_t{0.f, 0.f, 0.f, 0.f}, dp = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+              mfma16(sa, kf[jt & 1][s], qf[s]);  // S^T[j][i]: lane holds one query, keys 4lg + r
+              mfma16(dp, vf[jt & 1][s], of[s]);  // dP^T[j][i]
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int j = j0 + jt * 16 + 4 * lg + r;
+              float pv = ex2(__builtin_fmaf(sa[r], sc, -lse_i));
+              if constexpr (MASK) pv = ((j <= qi) & (j < Tn)) ? pv : 0.f;
+              ds[jt][r] = pv * (dp[r] - del_i);
+            }
           }
-        }
-      };
-      if (j0 + BT > qw || j0 + BT > Tn) score_tile(std::true_type{});
-      else score_tile(std::false_type{});
-      Frag<bf16_t> kt2[2];
-      trfrag(kt2[0], ks, 0, 0);
+        };
+        if (j0 + BT > qw || j0 + BT > Tn) score_tile(std::true_type{});
+        else score_tile(std::false_type{});
+        Frag<bf16_t> kt2[2];
+        trfrag(kt2[0], ks, 0, 0);
 #pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
-        Frag<bf16_t> dsf;
-        frag_from_pair(dsf, ds, s2);
+        for (int s2 = 0; s2 < 2; ++s2) {
+          Frag<bf16_t> dsf;
+          frag_from_pair(dsf, ds, s2);
 #pragma unroll
-        for (int c = 0; c < NCT; ++c) {
-          const int n = s2 * NCT + c;
-          if (n + 1 < 2 * NCT) trfrag(kt2[(n + 1) & 1], ks, (n + 1) / NCT, (n + 1) % NCT);
-          mfma16(acc_dq[c], kt2[n & 1], dsf);  // dQ^T[c][i]
+          for (int c = 0; c < NCT; ++c) {
+            const int n = s2 * NCT + c;
+            if (n + 1 < 2 * NCT) trfrag(kt2[(n + 1) & 1], ks, (n + 1) / NCT, (n + 1) % NCT);
+            mfma16(acc_dq[c], kt2[n & 1], dsf);  // dQ^T[c][i]
+          }
         }
       }
     }
