@@ -601,7 +601,7 @@ __global__ void __launch_bounds__(256) xent_kernel(const float* __restrict__ z, 
 // owns the 16-byte chunks t + 1024 i (i < NV) of the fp32 logits, so the row
 // is read from HBM once (the two-pass kernel above reads it twice, with
 // 4-byte loads).  Max, then the sum of 2^((z - max) log2 e) kept in the same
-// registers, then dz = (p - onehot) scale from them: three block reductions,
+// registers, then dz = (p - onehot) scale from them: two block reductions,
 // each wave's shuffles then the 16 waves in a fixed order.  Columns V..lddz-1
 // of dz are zeroed; the loss row is lse - z[y] (NaN for y outside [0, V)).
 // Needs ldz and lddz multiples of 4 and 16-byte aligned rows (dispatch).
@@ -610,7 +610,7 @@ __global__ void __launch_bounds__(1024) xent_reg_kernel(const float* __restrict_
                                                         const int32_t* __restrict__ tgt, T* __restrict__ dz,
                                                         int64_t lddz, float* __restrict__ loss_rows, int V,
                                                         float scale) {
-  __shared__ float red[3][16];
+  __shared__ float red[2][16];
   const int64_t row = blockIdx.x;
   const float* zr = z + row * ldz;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
