@@ -1198,13 +1198,17 @@ __global__ void __launch_bounds__(64 * W, DH == 64 ? 4 : 2) attn_bwd_dkdv_dl_ker
 // K and V tiles by direct loads, two stages (as in the forward).  K is read
 // both ways, as row fragments for S^T = K Q^T and transposed (pair order)
 // for dQ^T += K^T dS^T, so its slots use one swizzle that serves both access
-// patterns: dsw(r) = 2 (r & 7) + ((r >> 3) & 1) for 16-chunk rows (16
-// consecutive rows at one chunk, and 8 consecutive rows at one chunk pair,
-// all land on distinct banks), 2 ((r >> 1) & 3) + ((r >> 3) & 1) for 8-chunk
-// rows.
+// patterns: dsw(r) = 2 (r & 7) for 16-chunk rows, 2 ((r >> 1) & 3) for
+// 8-chunk rows, the transposed reads' swizzle of the forward's V.  Measured
+// with the bank-conflict counter on both read forms at both widths: these
+// leave ds_read_b128 of 16 rows at one chunk conflict-free (4 LDS cycles per
+// instruction) as well as the transposed reads (2 cycles); flipping the low
+// bit for rows 8-15 too, so that 16 consecutive rows take 16 distinct
+// chunks, makes ds_read_b128 take 8 cycles (dK/dV 171 -> 162 us at the 6.7B
+// shape without it).
 template <int DH>
 __device__ __forceinline__ int dsw(int r) {
-  return DH == 128 ? 2 * (r & 7) + ((r >> 3) & 1) : 2 * ((r >> 1) & 3) + ((r >> 3) & 1);
+  return DH == 128 ? 2 * (r & 7) : 2 * ((r >> 1) & 3);
 }
 
 template <int DH, int NW>
