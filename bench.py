@@ -236,6 +236,10 @@ def main():
                     help="keep every group's weights on the device across the steps of the call when each group "
                          "has a slot of its own (atom_set_retention: loaded once per global batch, gradients "
                          "still copied out every step); not the default, which loads every weight every step")
+    ap.add_argument("--dense-embedding", action="store_true",
+                    help="move the whole token-embedding matrix and its gradient every step (default: only the "
+                         "rows the step's tokens use cross the host link, atom_set_embedding_rows; the same "
+                         "results bit for bit)")
     ap.add_argument("--seq-steps", type=int, default=3,
                     help="after the timed steps, time this many single-step calls (the survey-literal step: no "
                          "cross-step overlap) and report their median beside the headline")
@@ -340,6 +344,11 @@ def main():
             log(f"steps {i0}..{i0 + len(out) - 1}: {sess.stats().step_s * 1e3:.1f} ms/step")
         return out
 
+    # row-sparse embedding transfers (retention keeps group 0 across steps,
+    # which needs the whole matrix on the device)
+    emb_rows = not args.dense_embedding and not args.retain
+    if emb_rows:
+        sess.set_embedding_rows(True)
     if args.retain:
         sess.set_retention(True)
     if args.warmup:
@@ -426,14 +435,25 @@ def main():
         traffic = WGRAD_TRAFFIC["bytes_per_launch"]
     fl = step_flops(cfg)
     t_mfma = fl / (peak * 1e12)
-    # R0 counts the bytes the configuration forces, whatever the schedule loads
+    # R0 counts the bytes the configuration forces, whatever the schedule
+    # loads: the whole model, less the embedding rows no token of the step
+    # uses when only used rows are moved (averaged over the timed steps)
     forced_h2d = (A.atom_plan_partition(A.make_config(cfg), budget).forced_h2d_bytes if args.schedule == "paper"
                   else plan.forced_h2d_bytes)
+    row_bytes = cfg.d_model * (2 if cfg.dtype == "bf16" else 4)
+    rows_used = [len(np.unique(tokens[i][..., :-1])) for i in range(args.steps)]
+    unused_bytes = (cfg.vocab - float(np.mean(rows_used))) * row_bytes if emb_rows else 0.0
+    forced_h2d = int(round(forced_h2d - unused_bytes))
     t_h2d_r0 = forced_h2d / (h2d_gbs * 1e9)
     t_h2d_r1 = plan.h2d_bytes / (h2d_gbs * 1e9)
     r0 = max(t_mfma, t_h2d_r0)
-    t_link_floor = max(plan.h2d_bytes / (h2d_gbs * 1e9), plan.d2h_bytes / (d2h_gbs * 1e9),
-                       (plan.h2d_bytes + plan.d2h_bytes) / (bidir_gbs * 1e9))
+    # the bytes the timed steps moved each way (the plan's, less the embedding
+    # rows they did not need)
+    # (the stats are the last call's: one step per call with --sequential)
+    last_call_steps = 1 if args.sequential else (args.steps - 1) % A.MAX_STEPS_PER_CALL + 1
+    h2d_step, d2h_step = st.h2d_bytes / last_call_steps, st.d2h_bytes / last_call_steps
+    t_link_floor = max(h2d_step / (h2d_gbs * 1e9), d2h_step / (d2h_gbs * 1e9),
+                       (h2d_step + d2h_step) / (bidir_gbs * 1e9))
 
     result = {
         "metric": "training tokens/sec on 1 MI355X (swapped); % of max(MFMA, H2D) roofline",
@@ -459,6 +479,8 @@ def main():
                          + ("; paper schedule (one node per group, two weight slots)" if args.schedule == "paper"
                             else "")
                          + ("; weights retained across the steps of the call" if args.retain else "")
+                         + ("; only the embedding rows a step's tokens use cross the host link" if emb_rows
+                            else "")
                          + ("; block-input checkpoints in host memory" if cfg.ckpt_host else "")),
             "global_batch": args.steps * cfg.accum * cfg.batch,
             "global_batch_unit": "sequences (timed steps x accum x batch)",
@@ -486,6 +508,8 @@ def main():
             "forced_h2d_bytes": forced_h2d,
             "plan_h2d_bytes": plan.h2d_bytes,
             "d2h_bytes": plan.d2h_bytes,
+            "moved_h2d_bytes_per_step": round(h2d_step),
+            "moved_d2h_bytes_per_step": round(d2h_step),
             "h2d_gbs": round(h2d_gbs, 2),
             "d2h_gbs": round(d2h_gbs, 2),
             "bidir_gbs": round(bidir_gbs, 2),
@@ -520,6 +544,8 @@ def main():
             "measured_one_step_ms": None if seq_ms is None else round(seq_ms, 1),
             "err_one_step": None if seq_ms is None else round(pred_one / (seq_ms / 1e3) - 1.0, 4),
         },
+        "embedding_rows": {"row_sparse": emb_rows, "rows_per_step": round(float(np.mean(rows_used)), 1),
+                           "vocab": cfg.vocab, "bytes_not_moved_per_step_each_way": round(unused_bytes)},
         "link_fit": fit,
         "plan": {"groups": plan.n_groups, "slots": plan.n_slots, "slot_mb": round(plan.slot_bytes / 1e6, 1),
                  "arena_gb": round(plan.arena_bytes / 1e9, 3), "pred_step_ms": round(plan.pred_step_s * 1e3, 1),
@@ -528,11 +554,10 @@ def main():
     }
     if args.retain:
         # loads amortised over the call; the gradients still leave every step
-        h2d_step = st.h2d_bytes / args.steps
-        t_link = max(h2d_step / (h2d_gbs * 1e9), plan.d2h_bytes / (d2h_gbs * 1e9))
+        t_link = max(h2d_step / (h2d_gbs * 1e9), d2h_step / (d2h_gbs * 1e9))
         result["retention"] = {
             "h2d_bytes_per_step": round(h2d_step),
-            "d2h_bytes_per_step": round(st.d2h_bytes / args.steps),
+            "d2h_bytes_per_step": round(d2h_step),
             "t_link_s": t_link,
             "bound": "mfma" if t_mfma >= t_link else "link",
             "frac": round(max(t_mfma, t_link) / (ms_per_step / 1e3), 4),

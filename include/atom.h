@@ -319,6 +319,26 @@ int atom_steps(atom_ctx* ctx, const int32_t* tokens, int32_t n_steps, float* los
  * The next call loads every group again.  ATOM_EINVAL for a NULL ctx. */
 int atom_set_retention(atom_ctx* ctx, int32_t on);
 
+/* Row-sparse embedding transfers (default off).  A step reads only the rows
+ * of wte its input tokens name, and only those rows of the wte gradient are
+ * nonzero (the embedding lookup of Section III-B's first layer; its backward
+ * adds each token's output gradient into its own row).  With this on, the
+ * swap-in of group 0 copies only the step's distinct rows of wte (ascending
+ * id, packed at the start of the slot's wte region) and its swap-out only
+ * their gradients, which the host accumulation adds to their rows: at most
+ * min(V, accum * batch * seq_len) rows each way instead of V.  The kernels
+ * address the packed rows through the step's remapped ids.  Losses, the fp32
+ * accumulators and the host gradient buffer (atom_host_tensor which = 2 of
+ * node 0, spread back to full rows when asked for, after waiting for all
+ * work) are bitwise those with it off; atom_stats counts the bytes that
+ * actually moved.  Allocates a pinned staging buffer of min(V, accum * batch
+ * * seq_len) rows on first use (ATOM_ENOMEM_HOST if refused).  Waits for all
+ * work, drops weight residency and requires tokens to be set again (atom_step
+ * and atom_steps set them).  ATOM_ESTATE while retention across steps is on
+ * (a retained group 0 would hold an earlier step's rows; atom_set_retention
+ * refuses the converse in the same way); ATOM_EINVAL for a NULL ctx. */
+int atom_set_embedding_rows(atom_ctx* ctx, int32_t on);
+
 /* Host optimizer (Section V-B: AdamW on the host CPUs once a global batch
  * is complete, learning rate 1e-4 after a linear warm-up, betas 0.9 and
  * 0.999).  atom_optimizer_init allocates fp32 master weights (copied from

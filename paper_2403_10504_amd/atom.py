@@ -111,6 +111,7 @@ _SIGS = {
     "atom_step": (ctypes.c_int, [P, P, P]),
     "atom_steps": (ctypes.c_int, [P, P, ctypes.c_int32, P]),
     "atom_set_retention": (ctypes.c_int, [P, ctypes.c_int32]),
+    "atom_set_embedding_rows": (ctypes.c_int, [P, ctypes.c_int32]),
     "atom_get_stats": (ctypes.c_int, [P, P]),
     "atom_ctx_config": (ctypes.c_int, [P, P, P]),
     "atom_probe_gemm": (ctypes.c_int, [P, I32, I32, I32]),
@@ -358,6 +359,10 @@ def atom_step(ctx, tokens) -> float:
 
 def atom_set_retention(ctx, on: bool):
     _check(lib().atom_set_retention(ctx, int(bool(on))), ctx)
+
+
+def atom_set_embedding_rows(ctx, on: bool):
+    _check(lib().atom_set_embedding_rows(ctx, int(bool(on))), ctx)
 
 
 def atom_steps(ctx, tokens) -> np.ndarray:

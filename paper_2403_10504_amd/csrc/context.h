@@ -159,6 +159,19 @@ struct atom_ctx {
   std::vector<hipEvent_t> ev_ckw, ev_cku;         // per ring entry: after its writer / its last reader
   std::vector<char> cku_recorded;
 
+  // Row-sparse embedding transfers (atom_set_embedding_rows): a step's
+  // token ids are remapped to the positions of the distinct ids it uses
+  // (ascending); group 0's swap-in copies only those rows of wte, packed at
+  // the start of the slot's wte region, and its swap-out only their
+  // gradients, packed the same way in the gradient slot and in h_g; the host
+  // accumulation adds each packed row to its own row.
+  bool emb_rows_on = false;
+  bool emb_packed[2] = {false, false};  // the parity's tokens address packed rows
+  std::vector<int32_t> emb_rows[2];     // the parity's distinct token ids, ascending
+  std::vector<int32_t> acc_rows0;       // rows of group 0's queued accumulation (empty: dense)
+  std::vector<int32_t> g_rows0;         // rows of the packed node-0 gradient in h_g (empty: dense)
+  uint8_t* h_emb_stage = nullptr;       // pinned staging of the packed rows of a swap-in
+
   // per-step validation state, by parity
   bool tokens_ok[2] = {false, false};
   std::vector<char> fwd_done[2], bwd_done[2];  // [node][micro]
@@ -252,6 +265,16 @@ inline int slot_of(atom_ctx* c, int par, int g) {
 inline int ck_entry(atom_ctx* c, int idx, int micro) { return (c->ck_host ? idx % CKPT_RING : idx) * c->C + micro; }
 inline bool ck_evicted(atom_ctx* c, int idx) { return c->ck_host && idx + CKPT_RING <= c->L; }
 inline size_t ck_key(atom_ctx* c, int idx, int micro) { return static_cast<size_t>(idx) * c->C + micro; }
+
+// wte is node 0's first tensor: its byte offset in node 0 (= in group 0),
+// its bytes, and the bytes of one row.
+inline uint64_t wte_off(atom_ctx* c) { return c->tens[0][0].offset; }
+inline uint64_t wte_bytes(atom_ctx* c) { return c->tens[0][0].bytes; }
+inline uint64_t wte_row_bytes(atom_ctx* c) { return static_cast<uint64_t>(c->d) * c->e; }
+// Rows of wte the kernels of a step of parity par address.
+inline int emb_vocab(atom_ctx* c, int par) {
+  return c->emb_packed[par] ? static_cast<int>(c->emb_rows[par].size()) : c->V;
+}
 
 // Gradient target of a tensor: fp32 accumulation slot (bf16 with C > 1) or
 // the group's gradient slot in the working dtype.

@@ -26,7 +26,11 @@ void accum_range<uint16_t>(float* acc, const uint16_t* g, uint64_t n) {
 void accumulate_group(atom_ctx* c, int gi) {
   const int g = gi % c->G;
   const uint8_t* hg = c->h_g;
-  const auto& rs = c->group_ranges[g];
+  const auto& rows = c->acc_rows0;  // group 0 with row-sparse embedding: wte's packed rows
+  const uint64_t wte_el = (c->node_off[0] + wte_off(c)) / c->e;
+  std::vector<Range> rs;
+  for (const Range& r : c->group_ranges[g])
+    if (!(g == 0 && !rows.empty() && r.off == wte_el)) rs.push_back(r);
   uint64_t total = 0;
   for (auto& r : rs) total += r.n;
   const int nt = c->pool->size();
@@ -46,6 +50,21 @@ void accumulate_group(atom_ctx* c, int gi) {
       pos += r.n;
     }
   });
+  if (g == 0 && !rows.empty()) {
+    // packed row i of h_g's wte region goes to row rows[i]; every other row
+    // of the gradient is zero, which adds nothing
+    const uint64_t d = c->d, nr = rows.size();
+    c->pool->run([&](int ti) {
+      const int nt = c->pool->size();
+      for (uint64_t i = nr * ti / nt, e = nr * (ti + 1) / nt; i < e; ++i) {
+        float* acc = c->h_acc + wte_el + static_cast<uint64_t>(rows[i]) * d;
+        if (c->dt == DT_BF16)
+          accum_range<uint16_t>(acc, reinterpret_cast<const uint16_t*>(hg) + wte_el + i * d, d);
+        else
+          accum_range<float>(acc, reinterpret_cast<const float*>(hg) + wte_el + i * d, d);
+      }
+    });
+  }
 }
 
 // fp32 -> bf16 bits, round to nearest even (finite inputs).

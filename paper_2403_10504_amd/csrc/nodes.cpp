@@ -311,8 +311,9 @@ int head_forward_backward(atom_ctx* c, int node, int micro) {
 int embed_forward(atom_ctx* c, int micro) {
   const int32_t* tok = reinterpret_cast<const int32_t*>(A(c, c->lay.tok_in + c->par * c->lay.tok_stride)) +
                        static_cast<int64_t>(micro) * c->N;
-  KCHK(c, embed_fwd(c->dt, tok, wptr(c, 0, T_WTE), wptr(c, 0, T_WPE), ckpt_ptr(c, 0, micro), c->N, c->T, c->V, c->d,
-                    c->cs));
+  // with row-sparse embedding transfers the ids address the step's packed rows
+  KCHK(c, embed_fwd(c->dt, tok, wptr(c, 0, T_WTE), wptr(c, 0, T_WPE), ckpt_ptr(c, 0, micro), c->N, c->T,
+                    emb_vocab(c, c->par), c->d, c->cs));
   return ATOM_OK;
 }
 
@@ -325,8 +326,8 @@ int embed_backward(atom_ctx* c, int micro) {
   const int32_t* seg = reinterpret_cast<const int32_t*>(A(c, L.emb_seg + ts)) + static_cast<int64_t>(micro) * (N + 1);
   const int32_t* uniq = reinterpret_cast<const int32_t*>(A(c, L.emb_uniq + ts)) + static_cast<int64_t>(micro) * N;
   GradTarget te = gptr(c, 0, T_WTE, micro), tp = gptr(c, 0, T_WPE, micro);
-  KCHK(c, embed_bwd(te.dtype, dres, perm, seg, uniq, c->n_uniq[c->par][micro], te.p, tp.p, c->V, c->T, c->B, c->d,
-                    te.accumulate, c->cs));
+  KCHK(c, embed_bwd(te.dtype, dres, perm, seg, uniq, c->n_uniq[c->par][micro], te.p, tp.p, emb_vocab(c, c->par), c->T,
+                    c->B, c->d, te.accumulate, c->cs));
   return ATOM_OK;
 }
 

@@ -1,6 +1,8 @@
 // C ABI of the swapped step: context creation (pinned host model, arena
 // layout, DMA engines and worker threads), the per-group calls, whole steps,
 // measurement hooks (GEMM probe, link benchmark, node profile) and stats.
+#include <sched.h>
+
 #include "context.h"
 
 using namespace atom::rt;
@@ -140,10 +142,16 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
     atom_ctx_destroy(c);
     return ATOM_ENOMEM_HOST;
   }
-  // accumulation threads: the cores minus two for the calling thread and the
-  // transfer workers (at most 16; the sum is bound by host memory bandwidth)
-  unsigned hw = std::thread::hardware_concurrency();
-  int nthreads = static_cast<int>(std::min(16u, std::max(1u, hw > 3 ? hw - 2 : 1u)));
+  // accumulation threads: the CPUs this process may run on, less six for
+  // the calling thread, the two transfer workers and the process's other
+  // threads, at most 16 (the sum is bound by host memory bandwidth).  The
+  // transfer workers must not wait for a CPU: with 14 accumulation threads on
+  // 16 CPUs the 6.7B pipelined step took 302 ms, with 8-10 threads 286-288
+  // ms, with 4 (too slow to keep up) 324 ms.
+  cpu_set_t cpus;
+  const int n_cpu = sched_getaffinity(0, sizeof(cpus), &cpus) == 0 ? CPU_COUNT(&cpus)
+                                                                   : static_cast<int>(std::thread::hardware_concurrency());
+  const int nthreads = std::max(1, std::min(16, n_cpu - 6));
   c->pool = new HostPool(nthreads);
   {
     // zero host buffers in parallel
@@ -252,6 +260,7 @@ void atom_ctx_destroy(atom_ctx* c) {
   for (auto p : c->h_tok)
     if (p) (void)hipHostFree(p);
   if (c->h_ck) (void)hipHostFree(c->h_ck);
+  if (c->h_emb_stage) (void)hipHostFree(c->h_emb_stage);
   free(c->h_acc);
   for (float* p : {c->h_master, c->h_m, c->h_v}) {
     if (p && c->opt_pinned) (void)hipHostFree(p);
@@ -263,6 +272,18 @@ void atom_ctx_destroy(atom_ctx* c) {
 int atom_host_tensor(atom_ctx* c, int32_t node, int32_t which, void** ptr, uint64_t* bytes) {
   if (!c || !ptr || node < 0 || node > c->L + 1 || which < 0 || which > 5) return fail(c, ATOM_EINVAL, "bad argument");
   if (which >= 3 && !c->h_master) return fail(c, ATOM_ESTATE, "atom_optimizer_init was not called");
+  if (which == 2 && node == 0 && !c->g_rows0.empty()) {
+    // the last node-0 gradient arrived as packed rows of wte: spread them to
+    // their rows (the others are zero), once every copy has landed
+    int st = sync_all(c);
+    if (st != ATOM_OK) return st;
+    uint8_t* w = c->h_g + c->node_off[0] + wte_off(c);
+    const uint64_t rb = wte_row_bytes(c), nr = c->g_rows0.size();
+    std::vector<uint8_t> packed(w, w + nr * rb);
+    memset(w, 0, wte_bytes(c));
+    for (uint64_t i = 0; i < nr; ++i) memcpy(w + static_cast<uint64_t>(c->g_rows0[i]) * rb, packed.data() + i * rb, rb);
+    c->g_rows0.clear();
+  }
   const uint64_t off = c->node_off[node], eoff = off / c->e;
   switch (which) {
     case 0: *ptr = c->h_w + off; break;
@@ -350,7 +371,33 @@ int atom_steps(atom_ctx* c, const int32_t* tokens, int32_t n, float* losses) {
 
 int atom_set_retention(atom_ctx* c, int32_t on) {
   if (!c) return ATOM_EINVAL;
+  if (on && c->emb_rows_on)
+    return fail(c, ATOM_ESTATE, "retention across steps needs whole embedding loads (atom_set_embedding_rows off)");
   c->retain = on != 0;
+  return ATOM_OK;
+}
+
+int atom_set_embedding_rows(atom_ctx* c, int32_t on) {
+  if (!c) return ATOM_EINVAL;
+  if (on && c->retain)
+    return fail(c, ATOM_ESTATE, "row-sparse embedding transfers need retention across steps off");
+  int st = sync_all(c);
+  if (st != ATOM_OK) return st;
+  if (on && !c->h_emb_stage) {
+    // a step uses at most min(V, C*B*T) distinct ids
+    const uint64_t rows = std::min<uint64_t>(c->V, static_cast<uint64_t>(c->C) * c->N);
+    const hipError_t e = hipHostMalloc(reinterpret_cast<void**>(&c->h_emb_stage), rows * wte_row_bytes(c),
+                                       hipHostMallocDefault);
+    if (e != hipSuccess) {
+      c->h_emb_stage = nullptr;
+      return fail(c, ATOM_ENOMEM_HOST, std::string("hipHostMalloc of the embedding-row staging failed: ") +
+                                           hipGetErrorString(e));
+    }
+  }
+  c->emb_rows_on = on != 0;
+  // the next step sets its tokens (remapped or not) and loads every group
+  drop_residency(c);
+  c->tokens_ok[0] = c->tokens_ok[1] = false;
   return ATOM_OK;
 }
 

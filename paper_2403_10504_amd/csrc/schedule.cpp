@@ -99,18 +99,33 @@ int upload_tokens(atom_ctx* c, int par, const int32_t* tokens) {
   int32_t* perm = tgt + C * N;
   int32_t* seg = perm + C * N;
   int32_t* uniq = seg + C * (N + 1);
-  std::vector<int32_t> count(c->V), start(c->V);
-  for (int64_t m = 0; m < C; ++m) {
+  for (int64_t m = 0; m < C; ++m)
     for (int64_t b = 0; b < c->B; ++b)
       for (int64_t t = 0; t < T; ++t) {
         inp[m * N + b * T + t] = tokens[(m * c->B + b) * (T + 1) + t];
         tgt[m * N + b * T + t] = tokens[(m * c->B + b) * (T + 1) + t + 1];
       }
-    // stable counting sort of token positions by token id
+  std::vector<int32_t> count(c->V), start(c->V);
+  // row-sparse embedding: the step's distinct ids in ascending order, and
+  // the inputs remapped to their positions (targets keep the ids)
+  c->emb_packed[par] = c->emb_rows_on;
+  c->emb_rows[par].clear();
+  if (c->emb_rows_on) {
+    for (int64_t i = 0; i < C * N; ++i) count[inp[i]] = 1;
+    for (int v = 0; v < c->V; ++v)
+      if (count[v]) {
+        start[v] = static_cast<int32_t>(c->emb_rows[par].size());
+        c->emb_rows[par].push_back(v);
+      }
+    for (int64_t i = 0; i < C * N; ++i) inp[i] = start[inp[i]];
+  }
+  const int Vr = emb_vocab(c, par);
+  for (int64_t m = 0; m < C; ++m) {
+    // stable counting sort of token positions by (remapped) token id
     std::fill(count.begin(), count.end(), 0);
     for (int64_t n = 0; n < N; ++n) ++count[inp[m * N + n]];
     int nu = 0, pos = 0;
-    for (int v = 0; v < c->V; ++v) {
+    for (int v = 0; v < Vr; ++v) {
       start[v] = pos;
       if (count[v]) {
         uniq[m * N + nu] = v;
@@ -164,18 +179,32 @@ int swap_in_impl(atom_ctx* c, int par, int g) {
   uint8_t* dst = A(c, c->lay.wslots + static_cast<uint64_t>(s) * c->plan.slot_bytes);
   const uint8_t* src = c->h_w + c->group_off[g];
   const uint64_t bytes = c->group_bytes[g];
+  // row-sparse embedding: group 0 (node 0 first) takes only the step's rows of wte
+  std::vector<int32_t> rows;
+  if (g == 0 && c->emb_packed[par]) rows = c->emb_rows[par];
+  const uint64_t moved = rows.empty() ? bytes : bytes - wte_bytes(c) + rows.size() * wte_row_bytes(c);
   uint64_t gen;
   {
     std::lock_guard<std::mutex> l(c->xm);
     gen = ++c->load_req[gi];
   }
-  c->h2d_worker->submit([c, gi, wait_ev, dst, src, bytes, gen]() -> std::string {
+  c->h2d_worker->submit([c, gi, wait_ev, dst, src, bytes, gen, rows]() -> std::string {
     std::string err;
     hipError_t e = hipSuccess;
     if (wait_ev)
       while ((e = hipEventQuery(wait_ev)) == hipErrorNotReady) usleep(POLL_US);
     if (e != hipSuccess) err = std::string("waiting for the slot: ") + hipGetErrorString(e);
-    if (err.empty()) err = c->dma_in.copy(dst, src, bytes);
+    if (err.empty() && rows.empty()) err = c->dma_in.copy(dst, src, bytes);
+    if (err.empty() && !rows.empty()) {
+      // the rows packed in pinned staging, copied to the start of the wte
+      // region; then whatever the group holds around wte
+      const uint64_t wo = wte_off(c), rb = wte_row_bytes(c), we = wo + wte_bytes(c);
+      for (size_t i = 0; i < rows.size(); ++i)
+        memcpy(c->h_emb_stage + i * rb, src + wo + static_cast<uint64_t>(rows[i]) * rb, rb);
+      err = c->dma_in.copy(dst + wo, c->h_emb_stage, rows.size() * rb);
+      if (err.empty() && wo > 0) err = c->dma_in.copy(dst, src, wo);
+      if (err.empty()) err = c->dma_in.copy(dst + we, src + we, bytes - we);
+    }
     {
       // published even on failure, so no waiter hangs; the error surfaces at the next sync
       std::lock_guard<std::mutex> l(c->xm);
@@ -188,7 +217,7 @@ int swap_in_impl(atom_ctx* c, int par, int g) {
   c->resident[gi] = 1;
   c->need_wait[gi] = 1;
   c->lastuse_recorded[gi] = 0;
-  c->stats.h2d_bytes += bytes;
+  c->stats.h2d_bytes += moved;
   c->stats.swap_ins += 1;
   return ATOM_OK;
 }
@@ -390,13 +419,18 @@ int swap_out_impl(atom_ctx* c, int par, int g) {
     return fail(c, ATOM_ESTATE, "group " + std::to_string(g) + " backward incomplete");
   const int gs = c->gslot_of[gi];
   uint8_t* gsl = A(c, c->lay.gslots + static_cast<uint64_t>(gs) * c->plan.slot_bytes);
+  // row-sparse embedding: group 0's wte gradient is the step's rows, packed
+  std::vector<int32_t> rows;
+  if (g == 0 && c->emb_packed[par]) rows = c->emb_rows[par];
   if (use_accslot(c)) {
     // fp32 accumulation slot -> working dtype in the gradient slot, per tensor
     for (int n = c->plan.first[g]; n <= c->plan.last[g]; ++n)
-      for (auto& t : c->tens[n]) {
+      for (size_t ti = 0; ti < c->tens[n].size(); ++ti) {
+        const auto& t = c->tens[n][ti];
         const uint64_t in_group = c->node_off[n] - c->group_off[g] + t.offset;
+        const uint64_t tb = n == 0 && ti == 0 && !rows.empty() ? rows.size() * wte_row_bytes(c) : t.bytes;
         KCHK(c, convert_f32(c->dt, reinterpret_cast<const float*>(A(c, c->lay.accslot + 2 * in_group)),
-                            gsl + in_group, static_cast<int64_t>(t.bytes / c->e), c->cs));
+                            gsl + in_group, static_cast<int64_t>(tb / c->e), c->cs));
       }
   }
   {
@@ -409,8 +443,9 @@ int swap_out_impl(atom_ctx* c, int par, int g) {
   HIPCHK(c, hipEventRecord(c->ev_gready[gi], c->cs));
   uint8_t* dst = c->h_g + c->group_off[g];
   const uint64_t bytes = c->group_bytes[g];
+  const uint64_t moved = rows.empty() ? bytes : bytes - wte_bytes(c) + rows.size() * wte_row_bytes(c);
   const int job = gi | (c->upd_capture ? ACC_UPDATE : 0);  // the armed update follows this accumulation
-  c->d2h_worker->submit([c, gi, gs, dst, gsl, bytes, job]() -> std::string {
+  c->d2h_worker->submit([c, gi, gs, dst, gsl, bytes, job, rows]() -> std::string {
     // the group's range of the host buffer has been added to the accumulators
     // (copies run in submission order, so an earlier step's copy of the group
     // has already queued its accumulation)
@@ -419,7 +454,20 @@ int swap_out_impl(atom_ctx* c, int par, int g) {
     hipError_t e;
     while ((e = hipEventQuery(c->ev_gready[gi])) == hipErrorNotReady) usleep(POLL_US);
     if (e != hipSuccess) err = std::string("waiting for gradients: ") + hipGetErrorString(e);
-    if (err.empty()) err = c->dma.copy(dst, gsl, bytes);
+    if (err.empty() && rows.empty()) err = c->dma.copy(dst, gsl, bytes);
+    if (err.empty() && !rows.empty()) {
+      // the packed rows to the start of h_g's wte region, then the rest of the group
+      const uint64_t wo = wte_off(c), we = wo + wte_bytes(c);
+      err = c->dma.copy(dst + wo, gsl + wo, rows.size() * wte_row_bytes(c));
+      if (err.empty() && wo > 0) err = c->dma.copy(dst, gsl, wo);
+      if (err.empty()) err = c->dma.copy(dst + we, gsl + we, bytes - we);
+    }
+    if (err.empty() && gi % c->G == 0) {
+      // no accumulation of group 0 is queued (waited for above): its rows,
+      // and the layout of node 0's gradient in h_g, are this copy's
+      c->acc_rows0 = rows;
+      c->g_rows0 = rows;
+    }
     if (err.empty()) {
       std::lock_guard<std::mutex> l(c->acc_m);
       c->acc_q.push_back(job);
@@ -435,7 +483,7 @@ int swap_out_impl(atom_ctx* c, int par, int g) {
     c->xcv.notify_all();
     return err;
   });
-  c->stats.d2h_bytes += bytes;
+  c->stats.d2h_bytes += moved;
   c->stats.swap_outs += 1;
   return ATOM_OK;
 }

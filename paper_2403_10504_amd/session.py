@@ -109,6 +109,10 @@ class Session:
         """Load each group once per steps() call when every group has a slot."""
         A.atom_set_retention(self.ctx, on)
 
+    def set_embedding_rows(self, on: bool):
+        """Move only the embedding rows a step's tokens use across the host link."""
+        A.atom_set_embedding_rows(self.ctx, on)
+
     def zero_grads(self):
         A.atom_zero_grads(self.ctx)
 
