@@ -288,7 +288,8 @@ def test_ctx_create_rejects_bad_arguments_without_gpu():
 
 
 def test_context_calls_reject_a_null_context_without_gpu():
-    for call in (lambda: A.atom_set_retention(None, True), lambda: A.atom_optimizer_init(None)):
+    for call in (lambda: A.atom_set_retention(None, True), lambda: A.atom_optimizer_init(None),
+                 lambda: A.atom_set_embedding_rows(None, True)):
         with pytest.raises(A.AtomError) as e:
             call()
         assert e.value.status == A.ATOM_EINVAL
