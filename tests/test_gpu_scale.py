@@ -40,12 +40,14 @@ def say(msg):
     print(f"[scale] {msg}", flush=True)
 
 
-def run(cfg, plan, tok, pipelined, label):
+def run(cfg, plan, tok, pipelined, label, rows=False):
     t0 = time.time()
     say(f"{label}: {plan.n_groups} groups, {plan.n_slots} slots, {plan.n_gslots} gradient slots, "
-        f"arena {plan.arena_bytes / 1e9:.2f} GB, {'pipelined' if pipelined else 'sequential'}")
+        f"arena {plan.arena_bytes / 1e9:.2f} GB, {'pipelined' if pipelined else 'sequential'}"
+        f"{', embedding rows only' if rows else ''}")
     with Session(cfg, plan=plan) as s:
         s.load_weights()
+        s.set_embedding_rows(rows)
         if pipelined:
             losses = s.steps(tok)
         else:
@@ -95,6 +97,12 @@ def test_6p7b_width_bench_plan_pipelined():
     assert_same(res, pipe, "swapped vs resident")
     got = run(cfg, planned, tok, True, "6.7B width, planned")
     assert_same(res, got, "planned vs resident")
+    # the bench line's default: only the embedding rows a step uses cross the link
+    rows = run(cfg, bench, tok, True, "6.7B width, bench plan", rows=True)
+    assert_same(pipe, rows, "embedding rows only vs whole rows")
+    unused = sum(cfg.vocab - len(np.unique(t[..., :-1])) for t in tok) * cfg.d_model * 2
+    assert pipe[3].h2d_bytes - rows[3].h2d_bytes == unused
+    assert pipe[3].d2h_bytes - rows[3].d2h_bytes == unused
 
 
 def test_13b_width_host_checkpoint_ring_evicts():
@@ -122,6 +130,12 @@ def test_13b_width_host_checkpoint_ring_evicts():
     rcfg, rplan = resident(cfg)
     res = run(rcfg, rplan, tok, False, "13B width, resident")
     assert_same(res, pipe, "swapped vs resident")
+    # only the embedding rows a step uses, with group 0 reloaded in the backward
+    rows = run(cfg, plan, tok, True, "13B width, host checkpoints", rows=True)
+    assert_same(pipe, rows, "embedding rows only vs whole rows (host checkpoints)")
+    unused = sum(cfg.vocab - len(np.unique(t[..., :-1])) for t in tok) * cfg.d_model * 2
+    assert pipe[3].d2h_bytes - rows[3].d2h_bytes == unused
+    assert pipe[3].h2d_bytes - rows[3].h2d_bytes == 2 * unused  # loaded in the forward and the backward
 
 
 def test_xl_width_planned_with_backward_reloads():
