@@ -445,13 +445,14 @@ def main():
     unused_bytes = (cfg.vocab - float(np.mean(rows_used))) * row_bytes if emb_rows else 0.0
     forced_h2d = int(round(forced_h2d - unused_bytes))
     t_h2d_r0 = forced_h2d / (h2d_gbs * 1e9)
-    t_h2d_r1 = plan.h2d_bytes / (h2d_gbs * 1e9)
     r0 = max(t_mfma, t_h2d_r0)
     # the bytes the timed steps moved each way (the plan's, less the embedding
-    # rows they did not need)
+    # rows they did not need; with retention, the call's loads over its steps)
     # (the stats are the last call's: one step per call with --sequential)
     last_call_steps = 1 if args.sequential else (args.steps - 1) % A.MAX_STEPS_PER_CALL + 1
     h2d_step, d2h_step = st.h2d_bytes / last_call_steps, st.d2h_bytes / last_call_steps
+    # R1: R0 with the bytes the schedule moved in
+    t_h2d_r1 = h2d_step / (h2d_gbs * 1e9)
     t_link_floor = max(h2d_step / (h2d_gbs * 1e9), d2h_step / (d2h_gbs * 1e9),
                        (h2d_step + d2h_step) / (bidir_gbs * 1e9))
 
