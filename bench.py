@@ -382,10 +382,20 @@ def main():
         raise RuntimeError(f"non-finite loss: {losses}")
 
     # the schedule model's prediction of this call and of one step alone
-    # (measured node costs, measured link sharing)
-    ends, _ = A.atom_plan_predict(c, plan, costs, duplex, min(args.steps, A.MAX_STEPS_PER_CALL))
+    # (measured node costs, measured link sharing; with only the used
+    # embedding rows moved, node 0's copy times scaled to the bytes moved)
+    pcosts = costs
+    if emb_rows:
+        src = A.costs_array(costs)
+        pcosts = (A.atom_node_cost * len(src))(*src)  # a copy
+        row_b = cfg.d_model * (2 if cfg.dtype == "bf16" else 4)
+        n0 = pcosts[0].weight_bytes
+        moved0 = n0 - (cfg.vocab - np.mean([len(np.unique(tokens[i][..., :-1])) for i in range(args.steps)])) * row_b
+        pcosts[0].t_load *= moved0 / n0
+        pcosts[0].t_store *= moved0 / n0
+    ends, _ = A.atom_plan_predict(c, plan, pcosts, duplex, min(args.steps, A.MAX_STEPS_PER_CALL))
     pred_call = ends[-1] / len(ends)
-    pred_one = A.atom_plan_predict(c, plan, costs, duplex, 1)[0][0]
+    pred_one = A.atom_plan_predict(c, plan, pcosts, duplex, 1)[0][0]
     steady = ((ends[-1] - ends[-3]) / 2.0) if len(ends) >= 3 else None
     steady_txt = f"{steady * 1e3:.1f} ms" if steady is not None else "needs 3 steps"
     log(f"predicted {pred_call * 1e3:.1f} ms per step of the call (steady {steady_txt}), "
@@ -535,7 +545,8 @@ def main():
         "grad_check": grad_check,
         "prediction": {
             "model": "event model of the schedule (compute stream, two DMA engines sharing the host link)",
-            "costs": "measured node costs (atom_profile_nodes) and the measured link sharing",
+            "costs": "measured node costs (atom_profile_nodes) and the measured link sharing"
+                     + ("; node 0's copies scaled to the embedding rows moved" if emb_rows else ""),
             "duplex": round(duplex, 4),
             "pred_ms_per_step": round(pred_call * 1e3, 1),
             "measured_ms_per_step": round(elapsed / args.steps * 1e3, 1),
