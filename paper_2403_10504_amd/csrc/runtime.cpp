@@ -144,10 +144,11 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
   }
   // accumulation threads: the CPUs this process may run on, less six for
   // the calling thread, the two transfer workers and the process's other
-  // threads, at most 16 (the sum is bound by host memory bandwidth).  The
-  // transfer workers must not wait for a CPU: with 14 accumulation threads on
-  // 16 CPUs the 6.7B pipelined step took 302 ms, with 8-10 threads 286-288
-  // ms, with 4 (too slow to keep up) 324 ms.
+  // threads, at most 16.  The sum is bound by host memory bandwidth: more
+  // threads add no speed, and they take bandwidth from the DMA engines'
+  // copies (6.7B pipelined step with 14 threads on 16 CPUs: 302 ms, also at
+  // nice 10; with 8-10 threads 286-288 ms, the same accumulation time; with
+  // 4, too few to keep up, 324 ms).
   cpu_set_t cpus;
   const int n_cpu = sched_getaffinity(0, sizeof(cpus), &cpus) == 0 ? CPU_COUNT(&cpus)
                                                                    : static_cast<int>(std::thread::hardware_concurrency());
