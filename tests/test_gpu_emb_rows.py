@@ -52,6 +52,8 @@ CASES = {
     "f32_singletons_k2": (TINY.with_(n_layer=3), lambda n: list(range(n)), 2),
     # bf16, two micro-batches (fp32 accumulation slot), three slots
     "bf16_accum2_k3": (TINY.with_(dtype="bf16", accum=2, n_layer=3), lambda n: list(range(n)), 3),
+    # fp32, three micro-batches (the gradient slot accumulates in place)
+    "f32_accum3_k2": (TINY.with_(accum=3, n_layer=2), lambda n: list(range(n)), 2),
     # the whole model in one group: wte is followed by every other tensor
     "f32_resident": (TINY.with_(n_layer=2), lambda n: [n - 1], 1),
     # groups of two nodes: group 0 is the embedding and the first block
