@@ -207,7 +207,9 @@ def cpu_baseline(cfg):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20, help="timed steps (one global batch, one pipelined call)")
+    ap.add_argument("--steps", type=int, default=64,
+                    help="timed steps: one global batch in one pipelined call (64, the most one atom_steps call "
+                         "takes; the paper synchronises once per global batch of 256 mini-batches)")
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="6.7b")
     ap.add_argument("--accum", type=int, default=None, help="gradient-accumulation degree C")
