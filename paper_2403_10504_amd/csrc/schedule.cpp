@@ -41,6 +41,8 @@
 // gradient slots).  Every kernel reduces in a fixed
 // order, so a step gives bitwise the same result for any plan and any
 // pipelining.
+#include <system_error>
+
 #include "context.h"
 
 namespace atom {
@@ -208,8 +210,17 @@ int swap_in_impl(atom_ctx* c, int par, int g) {
           memcpy(c->h_emb_stage + i * rb, src + wo + static_cast<uint64_t>(rows[i]) * rb, rb);
       };
       std::vector<std::thread> helpers;
-      for (int t = 1; t < np; ++t) helpers.emplace_back(pack, t);
+      int t_done = np;  // helpers 1..t_done-1 started; the rest is packed here
+      for (int t = 1; t < np; ++t) {
+        try {
+          helpers.emplace_back(pack, t);
+        } catch (const std::system_error&) {
+          t_done = t;
+          break;
+        }
+      }
       pack(0);
+      for (int t = t_done; t < np; ++t) pack(t);
       for (auto& h : helpers) h.join();
       err = c->dma_in.copy(dst + wo, c->h_emb_stage, rows.size() * rb);
       if (err.empty() && wo > 0) err = c->dma_in.copy(dst, src, wo);
