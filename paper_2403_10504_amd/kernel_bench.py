@@ -14,7 +14,7 @@ the 6.7B layer shapes for k = 2048, 4096, 8192, with the fit t = a + b k.
 gemm_layouts: the 6.7B block's GEMMs in the three operand layouts the step
 uses (forward, data gradient, weight gradient), store epilogue.
 layernorm: the LayerNorm backward (accumulate, bf16 copy, both partial sums)
-at the four GPT-3 widths.  One line per measurement; times from HIP events.
+and forward (bf16 output, row statistics) at the four GPT-3 widths.  One line per measurement; times from HIP events.
 """
 from __future__ import annotations
 
@@ -134,6 +134,11 @@ def layernorm(iters=50):
                                                   dbet.data_ptr(), part.data_ptr(), rows, d, None), iters)
         alg = rows * d * (2 + 4 + 4 + 4 + 2)
         print(f"layernorm bwd rows={rows} d={d}: {us:.1f} us, {alg / us / 1e3:.0f} GB/s algorithmic", flush=True)
+        bt = torch.zeros(d, device="cuda").to(torch.bfloat16)
+        us = _time(lambda: A.atom_k_layernorm_fwd(1, x.data_ptr(), gm.data_ptr(), bt.data_ptr(), lp.data_ptr(),
+                                                  mean.data_ptr(), rs.data_ptr(), rows, d, None), iters)
+        alg = rows * (d * (4 + 2) + 8)
+        print(f"layernorm fwd rows={rows} d={d}: {us:.1f} us, {alg / us / 1e3:.0f} GB/s algorithmic", flush=True)
 
 
 def xent(iters=20):
