@@ -44,15 +44,16 @@ class HostPool {
     for (auto& t : th_) t.join();
   }
   int size() const { return n_; }
-  // Runs fn(i) for i in [0, n) on all threads; returns when all are done.
-  // Not reentrant (one job at a time): during steps only the accumulation
-  // thread calls it; the context's other users (zeroing, optimizer) first
-  // drain every copy and the accumulation queue (sync_all), so no two
-  // callers overlap.
-  void run(const std::function<void(int)>& fn) {
+  // Runs fn(i) for i in [0, active) (active <= size(); the other threads
+  // skip the job); returns when all are done.  Not reentrant (one job at a
+  // time): during steps only the accumulation thread calls it; the context's
+  // other users (zeroing, optimizer) first drain every copy and the
+  // accumulation queue (sync_all), so no two callers overlap.
+  void run(const std::function<void(int)>& fn, int active) {
     {
       std::lock_guard<std::mutex> l(m_);
       fn_ = &fn;
+      active_ = std::max(1, std::min(active, n_));
       pending_ = n_ - 1;
       ++gen_;
     }
@@ -68,14 +69,16 @@ class HostPool {
     uint64_t seen = 0;
     for (;;) {
       const std::function<void(int)>* f;
+      bool run_it;
       {
         std::unique_lock<std::mutex> l(m_);
         cv_.wait(l, [&] { return gen_ != seen; });
         seen = gen_;
         if (stop_) return;
         f = fn_;
+        run_it = i < active_;
       }
-      (*f)(i);
+      if (run_it) (*f)(i);
       {
         std::lock_guard<std::mutex> l(m_);
         if (--pending_ == 0) done_cv_.notify_one();
@@ -87,6 +90,7 @@ class HostPool {
   std::mutex m_;
   std::condition_variable cv_, done_cv_;
   const std::function<void(int)>* fn_ = nullptr;
+  int active_ = 1;
   int pending_ = 0;
   uint64_t gen_ = 0;
   bool stop_ = false;
@@ -180,8 +184,10 @@ struct atom_ctx {
   hipEvent_t ev_tok[2] = {nullptr, nullptr};
   bool tok_recorded[2] = {false, false};
 
-  // host accumulation
+  // host accumulation (acc_threads of the pool's threads while steps run,
+  // all of them for work that runs alone)
   HostPool* pool = nullptr;
+  int acc_threads = 1;
   std::thread acc_thread;
   std::mutex acc_m;
   std::condition_variable acc_cv, acc_done_cv;
@@ -303,7 +309,7 @@ int embed_backward(atom_ctx* c, int micro);
 // host_accum.cpp: host gradient accumulation (and the optimizer's update)
 constexpr int ACC_UPDATE = 1 << 24;  // flag on a queued instance: update the group after adding
 void acc_loop(atom_ctx* c);
-void adamw_nodes(atom_ctx* c, int first, int last, const atom_adamw& hp, float grad_scale, int32_t step);
+void adamw_nodes(atom_ctx* c, int first, int last, const atom_adamw& hp, float grad_scale, int32_t step, int nt);
 int wait_accum(atom_ctx* c);
 void wait_accum_group(atom_ctx* c, int g);
 

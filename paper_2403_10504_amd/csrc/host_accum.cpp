@@ -33,7 +33,7 @@ void accumulate_group(atom_ctx* c, int gi) {
     if (!(g == 0 && !rows.empty() && r.off == wte_el)) rs.push_back(r);
   uint64_t total = 0;
   for (auto& r : rs) total += r.n;
-  const int nt = c->pool->size();
+  const int nt = c->acc_threads;
   c->pool->run([&](int ti) {
     // split the concatenated ranges into nt equal pieces
     const uint64_t lo = total * ti / nt, hi = total * (ti + 1) / nt;
@@ -49,13 +49,12 @@ void accumulate_group(atom_ctx* c, int gi) {
       }
       pos += r.n;
     }
-  });
+  }, nt);
   if (g == 0 && !rows.empty()) {
     // packed row i of h_g's wte region goes to row rows[i]; every other row
     // of the gradient is zero, which adds nothing
     const uint64_t d = c->d, nr = rows.size();
     c->pool->run([&](int ti) {
-      const int nt = c->pool->size();
       for (uint64_t i = nr * ti / nt, e = nr * (ti + 1) / nt; i < e; ++i) {
         float* acc = c->h_acc + wte_el + static_cast<uint64_t>(rows[i]) * d;
         if (c->dt == DT_BF16)
@@ -63,7 +62,7 @@ void accumulate_group(atom_ctx* c, int gi) {
         else
           accum_range<float>(acc, reinterpret_cast<const float*>(hg) + wte_el + i * d, d);
       }
-    });
+    }, nt);
   }
 }
 
@@ -80,7 +79,7 @@ inline uint16_t host_bf16(float f) {
 // working-dtype weights and zeroes the accumulators.  Each element's
 // arithmetic is the same whatever the range and the thread split, so an update
 // group by group equals one over the whole model bit for bit.
-void adamw_nodes(atom_ctx* c, int first, int last, const atom_adamw& hp, float grad_scale, int32_t step) {
+void adamw_nodes(atom_ctx* c, int first, int last, const atom_adamw& hp, float grad_scale, int32_t step, int nt) {
   // per-tensor element ranges with their decay flag
   struct Seg {
     uint64_t off, n;
@@ -104,7 +103,6 @@ void adamw_nodes(atom_ctx* c, int first, int last, const atom_adamw& hp, float g
   const float bc2 = static_cast<float>(1.0 - std::pow(b2d, step));
   const bool bf = c->dt == DT_BF16;
   c->pool->run([&](int ti) {
-    const int nt = c->pool->size();
     const uint64_t lo = total * ti / nt, hi = total * (ti + 1) / nt;
     uint64_t pos = 0;
     for (const Seg& sg : segs) {
@@ -126,7 +124,7 @@ void adamw_nodes(atom_ctx* c, int first, int last, const atom_adamw& hp, float g
       }
       pos += sg.n;
     }
-  });
+  }, nt);
 }
 
 void acc_loop(atom_ctx* c) {
@@ -151,7 +149,8 @@ void acc_loop(atom_ctx* c) {
       // the armed optimizer step to its parameters now, while the GPU runs
       // the backward of the groups before it
       const int g = gi % c->G;
-      adamw_nodes(c, c->plan.first[g], c->plan.last[g], c->upd_hp, c->upd_scale, c->upd_step);
+      adamw_nodes(c, c->plan.first[g], c->plan.last[g], c->upd_hp, c->upd_scale, c->upd_step,
+                  c->acc_threads);
       c->upd_seconds += std::chrono::duration<double>(std::chrono::steady_clock::now() - t1).count();
       ++c->upd_groups;
     }
@@ -226,8 +225,8 @@ int atom_optimizer_init(atom_ctx* c) {
       }
     }
   }
+  const int nt = c->pool->size();
   c->pool->run([&](int ti) {
-    const int nt = c->pool->size();
     const uint64_t lo = n * ti / nt, hi = n * (ti + 1) / nt;
     for (uint64_t i = lo; i < hi; ++i) {
       if (c->dt == DT_BF16) {
@@ -239,7 +238,7 @@ int atom_optimizer_init(atom_ctx* c) {
     }
     memset(c->h_m + lo, 0, (hi - lo) * 4);
     memset(c->h_v + lo, 0, (hi - lo) * 4);
-  });
+  }, nt);
   return ATOM_OK;
 }
 
@@ -248,7 +247,7 @@ int atom_optimizer_step(atom_ctx* c, const atom_adamw* hp, float grad_scale, int
   if (!c->h_master) return fail(c, ATOM_ESTATE, "atom_optimizer_init was not called");
   int st = sync_all(c);
   if (st != ATOM_OK) return st;
-  adamw_nodes(c, 0, c->L + 1, *hp, grad_scale, step);
+  adamw_nodes(c, 0, c->L + 1, *hp, grad_scale, step, c->pool->size());
   drop_residency(c);
   return ATOM_OK;
 }

@@ -142,29 +142,30 @@ int atom_ctx_create(const atom_config* cfg, const atom_plan* plan, void* dev_are
     atom_ctx_destroy(c);
     return ATOM_ENOMEM_HOST;
   }
-  // accumulation threads: the CPUs this process may run on, less six for
-  // the calling thread, the two transfer workers and the process's other
-  // threads, at most 16.  The sum is bound by host memory bandwidth: more
-  // threads add no speed, and they take bandwidth from the DMA engines'
-  // copies (6.7B pipelined step with 14 threads on 16 CPUs: 302 ms, also at
-  // nice 10; with 8-10 threads 286-288 ms, the same accumulation time; with
-  // 4, too few to keep up, 324 ms).
+  // host threads: the CPUs this process may run on, less two for the
+  // calling thread and the transfer workers, at most 16.  Work that runs
+  // alone (zeroing, the optimizer step) uses all of them.  The accumulation
+  // that runs beside the step's copies uses six fewer: the sum is bound by
+  // host memory bandwidth, so more threads add no speed and take bandwidth
+  // from the DMA engines' copies (6.7B pipelined step with 14 threads on 16
+  // CPUs: 302 ms, also at nice 10; with 8-10 threads 286-288 ms, the same
+  // accumulation time; with 4, too few to keep up, 324 ms).
   cpu_set_t cpus;
   const int n_cpu = sched_getaffinity(0, sizeof(cpus), &cpus) == 0 ? CPU_COUNT(&cpus)
                                                                    : static_cast<int>(std::thread::hardware_concurrency());
-  const int nthreads = std::max(1, std::min(16, n_cpu - 6));
-  c->pool = new HostPool(nthreads);
+  c->pool = new HostPool(std::max(1, std::min(16, n_cpu - 2)));
+  c->acc_threads = std::max(1, std::min(16, n_cpu - 6));
   {
     // zero host buffers in parallel
     const uint64_t nb = c->model_bytes;
+    const int nt = c->pool->size();
     c->pool->run([&](int ti) {
-      const int nt = c->pool->size();
       const uint64_t lo = nb * ti / nt, hi = nb * (ti + 1) / nt;
       memset(c->h_w + lo, 0, hi - lo);
       memset(c->h_g + lo, 0, hi - lo);
       const uint64_t elo = n_elem * ti / nt, ehi = n_elem * (ti + 1) / nt;
       memset(c->h_acc + elo, 0, (ehi - elo) * 4);
-    });
+    }, nt);
   }
   const int GI2 = 2 * c->G;
   c->slot_owner.assign(c->K, -1);
