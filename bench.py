@@ -237,7 +237,11 @@ def main():
     ap.add_argument("--retain", action="store_true",
                     help="keep every group's weights on the device across the steps of the call when each group "
                          "has a slot of its own (atom_set_retention: loaded once per global batch, gradients "
-                         "still copied out every step); not the default, which loads every weight every step")
+                         "still copied out every step); the default only for a configuration without a device "
+                         "budget (the whole model resident, GPT-3 Small); under a budget every weight is loaded "
+                         "every step")
+    ap.add_argument("--no-retain", action="store_true",
+                    help="load every weight every step also when the whole model is resident")
     ap.add_argument("--dense-embedding", action="store_true",
                     help="move the whole token-embedding matrix and its gradient every step (default: only the "
                          "rows the step's tokens use cross the host link, atom_set_embedding_rows; the same "
@@ -346,12 +350,17 @@ def main():
             log(f"steps {i0}..{i0 + len(out) - 1}: {sess.stats().step_s * 1e3:.1f} ms/step")
         return out
 
+    # a configuration without a device budget keeps its weights on the device
+    # across the steps of a global batch (the host model changes only at the
+    # update between global batches)
+    resident = budget >= (1 << 49) and args.schedule == "atom"
+    retain = args.retain or (resident and not args.no_retain)
     # row-sparse embedding transfers (retention keeps group 0 across steps,
     # which needs the whole matrix on the device)
-    emb_rows = not args.dense_embedding and not args.retain
+    emb_rows = not args.dense_embedding and not retain
     if emb_rows:
         sess.set_embedding_rows(True)
-    if args.retain:
+    if retain:
         sess.set_retention(True)
     if args.warmup:
         losses = run(args.warmup)
@@ -395,7 +404,7 @@ def main():
         moved0 = n0 - (cfg.vocab - np.mean([len(np.unique(tokens[i][..., :-1])) for i in range(args.steps)])) * row_b
         pcosts[0].t_load *= moved0 / n0
         pcosts[0].t_store *= moved0 / n0
-    ends, _ = A.atom_plan_predict(c, plan, pcosts, duplex, min(args.steps, A.MAX_STEPS_PER_CALL))
+    ends, _ = A.atom_plan_predict(c, plan, pcosts, duplex, min(args.steps, A.MAX_STEPS_PER_CALL), retain=retain)
     pred_call = ends[-1] / len(ends)
     pred_one = A.atom_plan_predict(c, plan, pcosts, duplex, 1)[0][0]
     steady = ((ends[-1] - ends[-3]) / 2.0) if len(ends) >= 3 else None
@@ -449,13 +458,18 @@ def main():
     t_mfma = fl / (peak * 1e12)
     # R0 counts the bytes the configuration forces, whatever the schedule
     # loads: the whole model, less the embedding rows no token of the step
-    # uses when only used rows are moved (averaged over the timed steps)
+    # uses when only used rows are moved (averaged over the timed steps), or
+    # once per call when the weights are retained
     forced_h2d = (A.atom_plan_partition(A.make_config(cfg), budget).forced_h2d_bytes if args.schedule == "paper"
                   else plan.forced_h2d_bytes)
     row_bytes = cfg.d_model * (2 if cfg.dtype == "bf16" else 4)
     rows_used = [len(np.unique(tokens[i][..., :-1])) for i in range(args.steps)]
     unused_bytes = (cfg.vocab - float(np.mean(rows_used))) * row_bytes if emb_rows else 0.0
-    forced_h2d = int(round(forced_h2d - unused_bytes))
+    forced_h2d = forced_h2d - unused_bytes
+    if retain and not args.sequential:
+        # weights retained across the steps of a call: one load per call
+        forced_h2d *= math.ceil(args.steps / A.MAX_STEPS_PER_CALL) / args.steps
+    forced_h2d = int(round(forced_h2d))
     t_h2d_r0 = forced_h2d / (h2d_gbs * 1e9)
     r0 = max(t_mfma, t_h2d_r0)
     # the bytes the timed steps moved each way (the plan's, less the embedding
@@ -491,7 +505,7 @@ def main():
                          + (f"device budget {budget / 1e9:.0f} GB" if budget < (1 << 49) else "whole model resident")
                          + ("; paper schedule (one node per group, two weight slots)" if args.schedule == "paper"
                             else "")
-                         + ("; weights retained across the steps of the call" if args.retain else "")
+                         + ("; weights retained across the steps of the call" if retain else "")
                          + ("; only the embedding rows a step's tokens use cross the host link" if emb_rows
                             else "")
                          + ("; block-input checkpoints in host memory" if cfg.ckpt_host else "")),
@@ -548,7 +562,8 @@ def main():
         "prediction": {
             "model": "event model of the schedule (compute stream, two DMA engines sharing the host link)",
             "costs": "measured node costs (atom_profile_nodes) and the measured link sharing"
-                     + ("; node 0's copies scaled to the embedding rows moved" if emb_rows else ""),
+                     + ("; node 0's copies scaled to the embedding rows moved" if emb_rows else "")
+                     + ("; weights retained: only the call's first step loads" if retain else ""),
             "duplex": round(duplex, 4),
             "pred_ms_per_step": round(pred_call * 1e3, 1),
             "measured_ms_per_step": round(elapsed / args.steps * 1e3, 1),
@@ -566,7 +581,7 @@ def main():
                  **plan_info},
         "loss": losses[-1],
     }
-    if args.retain:
+    if retain:
         # loads amortised over the call; the gradients still leave every step
         t_link = max(h2d_step / (h2d_gbs * 1e9), d2h_step / (d2h_gbs * 1e9))
         result["retention"] = {

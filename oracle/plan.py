@@ -142,8 +142,16 @@ def transfer_bytes(groups, costs, K, ckpt_bytes=0):
     return h2d + ckpt_bytes, sum(W) + ckpt_bytes
 
 
-def build_jobs(groups, costs, accum, K, R, n_steps, n_layer=None, ck_host=False, t_ck_out=0.0, t_ck_in=0.0):
-    """Jobs of a call of n_steps steps: (server, duration, deps, step, kind) in issue order."""
+def build_jobs(groups, costs, accum, K, R, n_steps, n_layer=None, ck_host=False, t_ck_out=0.0, t_ck_in=0.0,
+               retain=False):
+    """Jobs of a call of n_steps steps: (server, duration, deps, step, kind) in issue order.
+
+    retain: each group has its own slot (K = G) and its weights stay on the
+    device for the whole call (the host model changes only between global
+    batches, Section III-C), so the steps after the first load nothing: their
+    loads keep their place in the order with no length."""
+    if retain and K != len(groups):
+        raise ValueError("retention needs a slot per group")
     G = len(groups)
     L = len(costs) - 2 if n_layer is None else n_layer
     head = L + 1
@@ -215,8 +223,8 @@ def build_jobs(groups, costs, accum, K, R, n_steps, n_layer=None, ck_host=False,
             elif s + 1 < n_steps:
                 jn = K - 1 - j
                 jb = groups[jn]
-                load[(s + 1, jn)] = add("I", sum(costs[i]["t_load"] for i in range(jb[0], jb[1] + 1)),
-                                        [last_c[j]], s, "load")
+                t_in = 0.0 if retain else sum(costs[i]["t_load"] for i in range(jb[0], jb[1] + 1))
+                load[(s + 1, jn)] = add("I", t_in, [last_c[j]], s, "load")
     return jobs
 
 
@@ -272,9 +280,9 @@ def step_ends(jobs, end, n_steps):
     return out
 
 
-def simulate(groups, costs, accum, K, R, n_steps=1, duplex=1.0, **ck):
+def simulate(groups, costs, accum, K, R, n_steps=1, duplex=1.0, retain=False, **ck):
     """(forward end of step 0, list of step end times) of a call of n_steps steps."""
-    jobs = build_jobs(groups, costs, accum, K, R, n_steps, **ck)
+    jobs = build_jobs(groups, costs, accum, K, R, n_steps, retain=retain, **ck)
     end = run_jobs(jobs, duplex)
     t_fwd = max(end[i] for i, jb in enumerate(jobs) if jb[3] == 0 and jb[4] == "fwd")
     return t_fwd, step_ends(jobs, end, n_steps)

@@ -96,7 +96,7 @@ _SIGS = {
     "atom_reserve_bytes": (ctypes.c_int, [P, P]),
     "atom_plan_search": (ctypes.c_int, [P, U64, U64, P, I32, P, P]),
     "atom_plan_partition": (ctypes.c_int, [P, U64, P, I32, P, P]),
-    "atom_plan_predict": (ctypes.c_int, [P, P, P, I32, ctypes.c_double, I32, P, P]),
+    "atom_plan_predict": (ctypes.c_int, [P, P, P, I32, ctypes.c_double, I32, I32, P, P]),
     "atom_plan_fixed": (ctypes.c_int, [P, I32, P, I32, I32, P]),
     "atom_ctx_create": (ctypes.c_int, [P, P, P, U64, P, P]),
     "atom_ctx_destroy": (None, [P]),
@@ -260,15 +260,18 @@ def atom_plan_partition(c: atom_config, budget: int, costs=None, strict=False, d
     return p
 
 
-def atom_plan_predict(c: atom_config, plan: atom_plan, costs=None, duplex=0.0, n_steps=1):
-    """(step end times of one call of n_steps steps, forward end of step 0)."""
+def atom_plan_predict(c: atom_config, plan: atom_plan, costs=None, duplex=0.0, n_steps=1, retain=False):
+    """(step end times of one call of n_steps steps, forward end of step 0);
+    retain: weights kept across the steps of the call (atom_set_retention)."""
     ends = (ctypes.c_double * n_steps)()
     fwd = ctypes.c_double()
+    r = 1 if retain else 0
     if costs is None:
-        _check(lib().atom_plan_predict(_ref(c), _ref(plan), None, 0, float(duplex), n_steps, ends, _ref(fwd)))
+        _check(lib().atom_plan_predict(_ref(c), _ref(plan), None, 0, float(duplex), n_steps, r, ends, _ref(fwd)))
     else:
         arr = costs_array(costs)
-        _check(lib().atom_plan_predict(_ref(c), _ref(plan), arr, len(arr), float(duplex), n_steps, ends, _ref(fwd)))
+        _check(lib().atom_plan_predict(_ref(c), _ref(plan), arr, len(arr), float(duplex), n_steps, r, ends,
+                                       _ref(fwd)))
     return list(ends), fwd.value
 
 

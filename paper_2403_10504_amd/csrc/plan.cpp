@@ -210,7 +210,10 @@ double sum_store(const Model& m, int a, int b) {
   return t;
 }
 
-void build_jobs(const Model& m, const Groups& g, int n_steps, JobList* out) {
+// retain: every group has a slot of its own and keeps its weights from one
+// step of the call to the next, so only step 0 loads (the later steps' loads
+// are zero-length jobs at the same place in the issue order).
+void build_jobs(const Model& m, const Groups& g, int n_steps, bool retain, JobList* out) {
   const int G = static_cast<int>(g.size()), K = m.K, R = m.R, L = m.L, head = L + 1;
   auto evicted = [&](int i) { return m.ck_host && i >= 0 && i + CKPT_RING <= L; };
   JobList& J = *out;
@@ -274,7 +277,7 @@ void build_jobs(const Model& m, const Groups& g, int n_steps, JobList* out) {
         reload[j - K] = J.add(SI, sum_load(m, g[j - K].first, g[j - K].second), {last_c[j]}, s, K_LOAD);
       else if (s + 1 < n_steps)
         load[s + 1][K - 1 - j] =
-            J.add(SI, sum_load(m, g[K - 1 - j].first, g[K - 1 - j].second), {last_c[j]}, s, K_LOAD);
+            J.add(SI, retain ? 0.0 : sum_load(m, g[K - 1 - j].first, g[K - 1 - j].second), {last_c[j]}, s, K_LOAD);
     }
   }
 }
@@ -348,10 +351,10 @@ bool run_jobs(const JobList& J, double duplex, std::vector<double>* end_out) {
 
 // Step end times (last compute job or last gradient copy of each step) and
 // the forward end of step 0.
-bool simulate(const Model& m, const Groups& g, int n_steps, double duplex, std::vector<double>* ends,
+bool simulate(const Model& m, const Groups& g, int n_steps, bool retain, double duplex, std::vector<double>* ends,
               double* t_fwd) {
   JobList J;
-  build_jobs(m, g, n_steps, &J);
+  build_jobs(m, g, n_steps, retain, &J);
   std::vector<double> end;
   if (!run_jobs(J, duplex, &end)) return false;
   ends->assign(n_steps, 0.0);
@@ -438,9 +441,9 @@ Eval check(const Search& p, const Groups& g, int k_fixed = 0, int r_fixed = 0) {
 bool predict(const Search& p, const Groups& g, Eval* ev) {
   const Model m{p.c, p.n, p.L, p.C, ev->K, ev->R, p.ck_host, p.t_ck_out, p.t_ck_in};
   std::vector<double> ends;
-  if (!simulate(m, g, 1, p.duplex, &ends, &ev->t_fwd)) return false;
+  if (!simulate(m, g, 1, false, p.duplex, &ends, &ev->t_fwd)) return false;
   ev->t_first = ends[0];
-  if (!simulate(m, g, PIPE_STEPS, p.duplex, &ends, nullptr)) return false;
+  if (!simulate(m, g, PIPE_STEPS, false, p.duplex, &ends, nullptr)) return false;
   ev->t_step = (ends[PIPE_STEPS - 1] - ends[PIPE_STEPS - 3]) / 2.0;
   return true;
 }
@@ -778,9 +781,10 @@ int atom_plan_fixed(const atom_config* cfg, int32_t n_groups, const int32_t* las
 }
 
 int atom_plan_predict(const atom_config* cfg, const atom_plan* plan, const atom_node_cost* costs, int32_t n_costs,
-                      double duplex, int32_t n_steps, double* ends, double* fwd_s) {
+                      double duplex, int32_t n_steps, int32_t retain, double* ends, double* fwd_s) {
   if (!cfg || !plan || !ends || !check_config(*cfg).empty() || n_steps < 1 || n_steps > MAX_STEPS_PER_CALL)
     return ATOM_EINVAL;
+  if (retain && plan->n_slots != plan->n_groups) return ATOM_EINVAL;
   const int n = cfg->n_layer + 2;
   if (plan->n_nodes != n || plan->n_groups < 1 || plan->n_groups > n || plan->n_slots < 1 ||
       plan->n_slots > plan->n_groups || plan->n_gslots < 2 || plan->n_gslots > ATOM_MAX_GSLOTS ||
@@ -802,7 +806,7 @@ int atom_plan_predict(const atom_config* cfg, const atom_plan* plan, const atom_
   const Search p = make_search(*cfg, 0, 0, c.data(), n, duplex);
   const Model m{c.data(), n, n - 2, cfg->accum, plan->n_slots, plan->n_gslots, p.ck_host, p.t_ck_out, p.t_ck_in};
   std::vector<double> e;
-  if (!simulate(m, g, n_steps, p.duplex, &e, fwd_s)) return ATOM_EINVAL;
+  if (!simulate(m, g, n_steps, retain != 0, p.duplex, &e, fwd_s)) return ATOM_EINVAL;
   for (int s = 0; s < n_steps; ++s) ends[s] = e[s];
   return ATOM_OK;
 }

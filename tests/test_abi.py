@@ -262,6 +262,16 @@ def test_plan_predict_matches_the_oracle_schedule():
         ends, fwd = A.atom_plan_predict(c, plan, costs, duplex, n_steps)
         t_fwd, want = OP.simulate(plan.groups(), costs, 1, 6, 3, n_steps, duplex, **ck_times(cfg, costs))
         assert ends == want and fwd == t_fwd
+    # retention (a slot per group): only step 0 loads
+    full = A.atom_plan_fixed(c, list(range(cfg.n_nodes)), cfg.n_nodes, 3)
+    for n_steps, duplex in ((1, 0.85), (4, 0.5), (3, 1.0)):
+        ends, fwd = A.atom_plan_predict(c, full, costs, duplex, n_steps, retain=True)
+        t_fwd, want = OP.simulate(full.groups(), costs, 1, cfg.n_nodes, 3, n_steps, duplex, retain=True,
+                                  **ck_times(cfg, costs))
+        assert ends == want and fwd == t_fwd
+        assert ends[-1] <= A.atom_plan_predict(c, full, costs, duplex, n_steps)[0][-1] * (1 + 1e-12)
+    with pytest.raises(A.AtomError):
+        A.atom_plan_predict(c, plan, costs, 0.5, 2, retain=True)  # 6 slots for 8 groups
     # the plan's own predictions are the default-duplex ones
     ends, _ = A.atom_plan_predict(c, plan, None, 0.0, OP.PIPE_STEPS)
     assert plan.pred_step_s == (ends[-1] - ends[-3]) / 2.0

@@ -72,6 +72,33 @@ def test_shared_link_between_steps(duplex, want):
     assert ends == want
 
 
+def test_retained_weights_load_once_per_call():
+    # one group of three nodes (load 1 s each, forward 2 s, backward 3 s, the
+    # head none, store 1 s each), one slot: T_c = 3 x 2 + 2 x 3 = 12 s of
+    # compute per step.  Retained, only step 0 loads and each later step's
+    # compute follows the previous one's at once: end of step s = load +
+    # (s + 1) T_c + store, whatever the link sharing (the engines never run
+    # together).  Reloaded with the link shared (duplex 1): (s + 1)(load +
+    # T_c) + store; at duplex 0.5 each load runs beside the previous step's
+    # gradient copy at half rate (3 s of each: 6 s), so step 0's copy ends at
+    # 15 + 6 = 21, step 1's (beside step 2's load) at 21 + 12 + 6 = 39 and
+    # step 2's at 39 + 12 + 3 = 54.
+    c = [dict(weight_bytes=1, mem_bytes=0, cut_bytes=1, t_fwd=2.0, t_bwd=b, t_load=1.0, t_store=1.0)
+         for b in (3.0, 3.0, 0.0)]
+    for duplex in (1.0, 0.5):
+        _, ends = P.simulate([(0, 2)], c, accum=1, K=1, R=2, n_steps=3, duplex=duplex, retain=True)
+        assert ends == [3.0 + 12.0 * (s + 1) + 3.0 for s in range(3)]
+    _, ends = P.simulate([(0, 2)], c, accum=1, K=1, R=2, n_steps=3, duplex=1.0)
+    assert ends == [15.0 * (s + 1) + 3.0 for s in range(3)]
+    _, ends = P.simulate([(0, 2)], c, accum=1, K=1, R=2, n_steps=3, duplex=0.5)
+    assert ends == [21.0, 39.0, 54.0]
+    # a call of one step is the same either way; fewer slots than groups
+    # cannot retain
+    assert P.simulate([(0, 2)], c, 1, 1, 2, 1, 0.5, retain=True) == P.simulate([(0, 2)], c, 1, 1, 2, 1, 0.5)
+    with pytest.raises(ValueError):
+        P.simulate([(0, 0), (1, 2)], c, 1, 1, 2, 2, 1.0, retain=True)
+
+
 def test_gradient_slots_throttle_the_backward():
     # five one-node groups, all resident, slow copies out: with R gradient
     # slots, the backward of the group R claims later waits for the copy out
