@@ -395,26 +395,33 @@ __device__ __forceinline__ BlockId attn_block(bool heavy_last) {
 //      aligned chunk pair (vswz is even, so pairs stay pairs).
 // Keys past the end read the last row (finite data; their scores are masked
 // to -inf, so they weigh zero).
-template <int DH>
+template <int DH, int NT = 256>
 struct FwdDL {
   static constexpr int CPR = DH / 8;             // chunks per row
   static constexpr int TILE = BT * DH * 2;       // bytes of a K or V tile
   static constexpr int STAGE = 2 * TILE;
-  static constexpr int LPT = TILE / (256 * 16);  // direct loads per thread per tile and operand
+  static constexpr int LPT = TILE / (NT * 16);   // direct loads per thread per tile and operand
   static_assert(DH == 64 || DH == 128, "head size");
   __device__ static int kswz(int r) { return DH == 128 ? (r & 15) : ((r >> 1) & 7); }
   __device__ static int vswz(int r) { return DH == 128 ? 2 * (r & 7) : 2 * ((r >> 1) & 3); }
 };
 
-// Waves per SIMD the register allocation must allow (the second launch bound):
-// two at d_h 128 (230 registers: two workgroups per CU, as the LDS allows);
-// four at d_h 64, where 128 registers suffice and four workgroups fit the LDS
-// (82 against 88 us at GPT-3 Small's shape; five spill).
-template <int DH, int G>
-__global__ void __launch_bounds__(256, DH == 64 ? 4 : 2) attn_fwd_dl_kernel(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ o,
-                                                             float* __restrict__ lse, int B, int Tn, int H) {
-  using F = FwdDL<DH>;
-  constexpr int NS = DH / 32, NCT = DH / 16, BQ = 4 * 16 * G, RB = DH * 2;
+// NW waves of G groups of 16 queries per workgroup.  Waves per SIMD the
+// register allocation must allow (the second launch bound): four with eight
+// waves of one group (d_h 128: two workgroups per CU, as the LDS allows, in
+// 128 registers with a spill of nine; against four waves of two groups at two
+// waves per SIMD, 230 registers: 90-92 against 92-96 us at the 6.7B shape,
+// 59 against 68-69 at 13B's, whose 40 heads leave the last round of work
+// items less full); four with four waves of two groups at d_h 64, where 128
+// registers suffice and four workgroups fit the LDS (82 against 88 us at
+// GPT-3 Small's shape; five spill).
+template <int DH, int G, int NW>
+__global__ void __launch_bounds__(64 * NW, (DH == 64 || G == 1) ? 4 : 2)
+    attn_fwd_dl_kernel(const bf16_t* __restrict__ qkv, bf16_t* __restrict__ o, float* __restrict__ lse, int B, int Tn,
+                       int H) {
+  constexpr int NT = 64 * NW;
+  using F = FwdDL<DH, NT>;
+  constexpr int NS = DH / 32, NCT = DH / 16, BQ = NW * 16 * G, RB = DH * 2;
   __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * F::STAGE];
 
   // the wave index through readfirstlane, so that everything derived from
@@ -456,7 +463,7 @@ __global__ void __launch_bounds__(256, DH == 64 ? 4 : 2) attn_fwd_dl_kernel(cons
   const bf16_t* vsrc[F::LPT];
 #pragma unroll
   for (int q = 0; q < F::LPT; ++q) {
-    const int id = q * 256 + tid, row = id / F::CPR, slot = id % F::CPR;
+    const int id = q * NT + tid, row = id / F::CPR, slot = id % F::CPR;
     ksrc[q] = kb + static_cast<int64_t>(row) * ld + (slot ^ F::kswz(row)) * 8;
     vsrc[q] = vb + static_cast<int64_t>(row) * ld + (slot ^ F::vswz(row)) * 8;
   }
@@ -465,13 +472,13 @@ __global__ void __launch_bounds__(256, DH == 64 ? 4 : 2) attn_fwd_dl_kernel(cons
     const bool whole = j0 + BT <= Tn;
 #pragma unroll
     for (int q = 0; q < F::LPT; ++q) {
-      const uint32_t lo = __builtin_amdgcn_readfirstlane((q * 256 + w * 64) * 16);
+      const uint32_t lo = __builtin_amdgcn_readfirstlane((q * NT + w * 64) * 16);
       if (whole) {
         const int64_t off = static_cast<int64_t>(j0) * ld;
         lds_dma16(ksrc[q] + off, kl + lo);
         lds_dma16(vsrc[q] + off, vl + lo);
       } else {
-        const int id = q * 256 + tid, row = id / F::CPR, slot = id % F::CPR;
+        const int id = q * NT + tid, row = id / F::CPR, slot = id % F::CPR;
         const int64_t gr = static_cast<int64_t>(min(j0 + row, Tn - 1)) * ld;
         lds_dma16(kb + gr + (slot ^ F::kswz(row)) * 8, kl + lo);
         lds_dma16(vb + gr + (slot ^ F::vswz(row)) * 8, vl + lo);
@@ -1366,7 +1373,15 @@ __global__ void __launch_bounds__(64 * NW, DH == 64 ? 4 : 2) attn_bwd_dq_dl_kern
 // and query groups (GQ) and waves (WQ) of the dQ kernel; bf16 takes the
 // direct-load kernels, fp32 the register-staged ones.  dQ: eight waves of 16
 // queries (two waves per SIMD within the register file) beat four waves of 32
-// queries (one wave per SIMD): 1.14x.
+// queries (one wave per SIMD): 1.14x.  The bf16 forward at d_h 128 takes
+// ATOM_FWD_G128 groups per wave in workgroups of ATOM_FWD_NW128 waves (one
+// group, eight waves: see attn_fwd_dl_kernel), at d_h 64 two groups in four.
+#ifndef ATOM_FWD_G128
+#define ATOM_FWD_G128 1
+#endif
+#ifndef ATOM_FWD_NW128
+#define ATOM_FWD_NW128 8
+#endif
 template <typename T, int DH>
 struct ACfg {
   static constexpr int G = sizeof(T) == 2 ? 2 : 1;
@@ -1378,13 +1393,16 @@ struct ACfg {
 template <typename T, int DH>
 hipError_t fwd_t(const void* qkv, void* o, float* lse, int B, int Tn, int H, hipStream_t s) {
   constexpr int G = ACfg<T, DH>::G;
-  dim3 grid((Tn + 64 * G - 1) / (64 * G), B * H), block(256);
-  if constexpr (sizeof(T) == 2)
-    hipLaunchKernelGGL((attn_fwd_dl_kernel<DH, G>), grid, block, 0, s, static_cast<const bf16_t*>(qkv),
+  if constexpr (sizeof(T) == 2) {
+    constexpr int FG = DH == 128 ? ATOM_FWD_G128 : 2, FNW = DH == 128 ? ATOM_FWD_NW128 : 4;
+    dim3 grid((Tn + 16 * FG * FNW - 1) / (16 * FG * FNW), B * H), block(64 * FNW);
+    hipLaunchKernelGGL((attn_fwd_dl_kernel<DH, FG, FNW>), grid, block, 0, s, static_cast<const bf16_t*>(qkv),
                        static_cast<bf16_t*>(o), lse, B, Tn, H);
-  else
+  } else {
+    dim3 grid((Tn + 64 * G - 1) / (64 * G), B * H), block(256);
     hipLaunchKernelGGL((attn_fwd_kernel<T, DH, G>), grid, block, 0, s, static_cast<const T*>(qkv), static_cast<T*>(o),
                        lse, B, Tn, H);
+  }
   return hipGetLastError();
 }
 
