@@ -40,14 +40,15 @@ def say(msg):
     print(f"[scale] {msg}", flush=True)
 
 
-def run(cfg, plan, tok, pipelined, label, rows=False):
+def run(cfg, plan, tok, pipelined, label, rows=False, retain=False):
     t0 = time.time()
     say(f"{label}: {plan.n_groups} groups, {plan.n_slots} slots, {plan.n_gslots} gradient slots, "
         f"arena {plan.arena_bytes / 1e9:.2f} GB, {'pipelined' if pipelined else 'sequential'}"
-        f"{', embedding rows only' if rows else ''}")
+        f"{', embedding rows only' if rows else ''}{', weights retained' if retain else ''}")
     with Session(cfg, plan=plan) as s:
         s.load_weights()
         s.set_embedding_rows(rows)
+        s.set_retention(retain)
         if pipelined:
             losses = s.steps(tok)
         else:
@@ -157,3 +158,23 @@ def test_xl_width_planned_with_backward_reloads():
     rcfg, rplan = resident(cfg)
     res = run(rcfg, rplan, tok, False, "XL width, resident")
     assert_same(res, pipe, "swapped vs resident")
+
+
+def test_small_width_resident_retained():
+    # GPT-3 Small's bench default: no device budget, so the planner makes the
+    # whole model one group in one slot, and the weights stay on the device
+    # across the steps of the call (loaded once instead of once per step);
+    # d_h = 64 kernels at the full width
+    cfg = synthetic.CONFIGS["small"].with_(n_layer=3)
+    c = A.make_config(cfg)
+    plan = A.atom_plan_partition(c, 1 << 50)
+    assert plan.n_groups == 1 and plan.n_slots == 1, plan.groups()
+    tok = tokens_for(cfg, N_STEPS)
+    ret = run(cfg, plan, tok, True, "Small width, resident", retain=True)
+    pipe = run(cfg, plan, tok, True, "Small width, resident")
+    seq = run(cfg, plan, tok, False, "Small width, resident")
+    assert_same(seq, pipe, "pipelined vs sequential")
+    assert_same(pipe, ret, "retained vs loaded every step")
+    weights = sum(A.atom_node_layout(c, n)[1] for n in range(cfg.n_nodes))
+    assert pipe[3].h2d_bytes == N_STEPS * weights and ret[3].h2d_bytes == weights
+    assert ret[3].d2h_bytes == pipe[3].d2h_bytes == N_STEPS * weights
