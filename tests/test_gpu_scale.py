@@ -2,8 +2,9 @@
 
 The step the benchmark times runs many groups in many weight slots, lets
 gradient copies lag the backward through up to 16 gradient slots, keeps the
-13B block inputs in a host ring, reloads XL groups in the backward, and
-pipelines the steps of a global batch.  None of that changes arithmetic: the
+13B block inputs in a host ring, reloads XL groups in the backward, keeps
+GPT-3 Small's one resident group on the device across the steps of a call,
+and pipelines the steps of a global batch.  None of that changes arithmetic: the
 same kernels run in the same order on the same weights, so every loss, the
 fp32 host accumulators and the last step's gradients must be bitwise those of
 
