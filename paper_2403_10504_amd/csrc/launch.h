@@ -55,6 +55,10 @@ hipError_t colsum_partial(int in_dtype, const void* x, int64_t rows, int cols, i
 // type: DT_F32 with accumulate flag, or the element type (overwrite).
 hipError_t sum_parts(const float* part, int64_t nparts, int cols, int64_t part_stride, int out_dtype, void* out,
                      bool accumulate, hipStream_t s);
+// The same with two targets of one dtype and mode in one launch: columns
+// c < split go to out[c], the rest to out2[c - split].
+hipError_t sum_parts2(const float* part, int64_t nparts, int cols, int64_t part_stride, int out_dtype, void* out,
+                      void* out2, int split, bool accumulate, hipStream_t s);
 
 // Embedding: x[n] = wte[tok[n]] + wpe[n % T] (x fp32); ids outside [0, V)
 // give NaN rows.

@@ -193,8 +193,13 @@ int ln_grad(atom_ctx* c, const void* dy, const float* x, const float* mu, const 
   const int d = c->d;
   KCHK(c, layernorm_bwd(c->dt, dy, x, mu, rs, gamma, dres, dres_lp, acc, part, c->N, d, c->cs));
   const int64_t np = layernorm_bwd_blocks(c->N, d);
-  KCHK(c, sum_parts(part, np, d, 2 * static_cast<int64_t>(d), tg.dtype, tg.p, tg.accumulate, c->cs));
-  KCHK(c, sum_parts(part + d, np, d, 2 * static_cast<int64_t>(d), tb.dtype, tb.p, tb.accumulate, c->cs));
+  // the partials are [np][2d], gamma's columns then beta's
+  if (tg.dtype == tb.dtype && tg.accumulate == tb.accumulate) {
+    KCHK(c, sum_parts2(part, np, 2 * d, 2 * static_cast<int64_t>(d), tg.dtype, tg.p, tb.p, d, tg.accumulate, c->cs));
+  } else {
+    KCHK(c, sum_parts(part, np, d, 2 * static_cast<int64_t>(d), tg.dtype, tg.p, tg.accumulate, c->cs));
+    KCHK(c, sum_parts(part + d, np, d, 2 * static_cast<int64_t>(d), tb.dtype, tb.p, tb.accumulate, c->cs));
+  }
   return ATOM_OK;
 }
 

@@ -466,9 +466,12 @@ __global__ void __launch_bounds__(256) colsum_partial_kernel(const T* __restrict
 // scheduling.
 constexpr int SP_COLS = 16, SP_SLICES = 16;
 
+// Column c of the partials goes to out[c] below split and to out2[c - split]
+// from there on (two targets in one launch: a LayerNorm's gamma and beta).
 template <typename TO>
 __global__ void __launch_bounds__(256) sum_parts_kernel(const float* __restrict__ part, int64_t nparts, int cols,
-                                                        int64_t stride, TO* __restrict__ out, int accumulate) {
+                                                        int64_t stride, TO* __restrict__ out, TO* __restrict__ out2,
+                                                        int split, int accumulate) {
   __shared__ float sh[SP_SLICES][SP_COLS];
   const int cl = threadIdx.x % SP_COLS, sl = threadIdx.x / SP_COLS;
   const int c = blockIdx.x * SP_COLS + cl;
@@ -491,8 +494,9 @@ __global__ void __launch_bounds__(256) sum_parts_kernel(const float* __restrict_
     float t = sh[0][cl];
 #pragma unroll
     for (int i = 1; i < SP_SLICES; ++i) t += sh[i][cl];
-    if (accumulate) t += to_f<TO>(out[c]);
-    out[c] = from_f<TO>(t);
+    TO* dst = c < split ? out + c : out2 + (c - split);
+    if (accumulate) t += to_f<TO>(*dst);
+    *dst = from_f<TO>(t);
   }
 }
 
@@ -883,17 +887,22 @@ hipError_t colsum_partial(int in_dtype, const void* x, int64_t rows, int cols, i
   return hipGetLastError();
 }
 
-hipError_t sum_parts(const float* part, int64_t nparts, int cols, int64_t part_stride, int out_dtype, void* out,
-                     bool accumulate, hipStream_t s) {
-  if (cols <= 0) return hipErrorInvalidValue;
+hipError_t sum_parts2(const float* part, int64_t nparts, int cols, int64_t part_stride, int out_dtype, void* out,
+                      void* out2, int split, bool accumulate, hipStream_t s) {
+  if (cols <= 0 || split < 0 || split > cols) return hipErrorInvalidValue;
   dim3 grid(static_cast<unsigned>((cols + SP_COLS - 1) / SP_COLS)), block(256);
   if (out_dtype == DT_BF16)
     hipLaunchKernelGGL(sum_parts_kernel<bf16_t>, grid, block, 0, s, part, nparts, cols, part_stride,
-                       static_cast<bf16_t*>(out), accumulate ? 1 : 0);
+                       static_cast<bf16_t*>(out), static_cast<bf16_t*>(out2), split, accumulate ? 1 : 0);
   else
     hipLaunchKernelGGL(sum_parts_kernel<float>, grid, block, 0, s, part, nparts, cols, part_stride,
-                       static_cast<float*>(out), accumulate ? 1 : 0);
+                       static_cast<float*>(out), static_cast<float*>(out2), split, accumulate ? 1 : 0);
   return hipGetLastError();
+}
+
+hipError_t sum_parts(const float* part, int64_t nparts, int cols, int64_t part_stride, int out_dtype, void* out,
+                     bool accumulate, hipStream_t s) {
+  return sum_parts2(part, nparts, cols, part_stride, out_dtype, out, out, cols, accumulate, s);
 }
 
 hipError_t embed_fwd(int dtype, const int32_t* tok, const void* wte, const void* wpe, float* x, int64_t n_tok,
