@@ -223,8 +223,8 @@ int atom_plan_fixed(const atom_config* cfg, int32_t n_groups, const int32_t* las
  * model atom_plan documents: ends[s] for s < n_steps; *fwd_s (may be NULL)
  * the end of step 0's forward.  retain != 0 models atom_set_retention (every
  * group in a slot of its own keeps its weights across the steps of the call,
- * so only step 0 loads; ATOM_EINVAL if the plan has fewer slots than groups).
- * ATOM_EINVAL for a bad plan or count. */
+ * so only step 0 loads; like retention itself, no effect when the plan has
+ * fewer slots than groups).  ATOM_EINVAL for a bad plan or count. */
 int atom_plan_predict(const atom_config* cfg, const atom_plan* plan, const atom_node_cost* costs, int32_t n_costs,
                       double duplex, int32_t n_steps, int32_t retain, double* ends, double* fwd_s);
 

@@ -146,12 +146,13 @@ def build_jobs(groups, costs, accum, K, R, n_steps, n_layer=None, ck_host=False,
                retain=False):
     """Jobs of a call of n_steps steps: (server, duration, deps, step, kind) in issue order.
 
-    retain: each group has its own slot (K = G) and its weights stay on the
+    retain: when each group has its own slot (K = G) its weights stay on the
     device for the whole call (the host model changes only between global
     batches, Section III-C), so the steps after the first load nothing: their
-    loads keep their place in the order with no length."""
-    if retain and K != len(groups):
-        raise ValueError("retention needs a slot per group")
+    loads keep their place in the order with no length.  With fewer slots
+    than groups every group is loaded again each step and retain changes
+    nothing."""
+    retain = retain and K >= len(groups)
     G = len(groups)
     L = len(costs) - 2 if n_layer is None else n_layer
     head = L + 1

@@ -784,7 +784,6 @@ int atom_plan_predict(const atom_config* cfg, const atom_plan* plan, const atom_
                       double duplex, int32_t n_steps, int32_t retain, double* ends, double* fwd_s) {
   if (!cfg || !plan || !ends || !check_config(*cfg).empty() || n_steps < 1 || n_steps > MAX_STEPS_PER_CALL)
     return ATOM_EINVAL;
-  if (retain && plan->n_slots != plan->n_groups) return ATOM_EINVAL;
   const int n = cfg->n_layer + 2;
   if (plan->n_nodes != n || plan->n_groups < 1 || plan->n_groups > n || plan->n_slots < 1 ||
       plan->n_slots > plan->n_groups || plan->n_gslots < 2 || plan->n_gslots > ATOM_MAX_GSLOTS ||
@@ -806,7 +805,9 @@ int atom_plan_predict(const atom_config* cfg, const atom_plan* plan, const atom_
   const Search p = make_search(*cfg, 0, 0, c.data(), n, duplex);
   const Model m{c.data(), n, n - 2, cfg->accum, plan->n_slots, plan->n_gslots, p.ck_host, p.t_ck_out, p.t_ck_in};
   std::vector<double> e;
-  if (!simulate(m, g, n_steps, retain != 0, p.duplex, &e, fwd_s)) return ATOM_EINVAL;
+  // as atom_set_retention: no effect unless every group has a slot of its own
+  const bool ret = retain != 0 && plan->n_slots == plan->n_groups;
+  if (!simulate(m, g, n_steps, ret, p.duplex, &e, fwd_s)) return ATOM_EINVAL;
   for (int s = 0; s < n_steps; ++s) ends[s] = e[s];
   return ATOM_OK;
 }

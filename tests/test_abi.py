@@ -270,8 +270,8 @@ def test_plan_predict_matches_the_oracle_schedule():
                                   **ck_times(cfg, costs))
         assert ends == want and fwd == t_fwd
         assert ends[-1] <= A.atom_plan_predict(c, full, costs, duplex, n_steps)[0][-1] * (1 + 1e-12)
-    with pytest.raises(A.AtomError):
-        A.atom_plan_predict(c, plan, costs, 0.5, 2, retain=True)  # 6 slots for 8 groups
+    # 6 slots for 8 groups: every group is loaded again each step, as without retention
+    assert A.atom_plan_predict(c, plan, costs, 0.5, 3, retain=True) == A.atom_plan_predict(c, plan, costs, 0.5, 3)
     # the plan's own predictions are the default-duplex ones
     ends, _ = A.atom_plan_predict(c, plan, None, 0.0, OP.PIPE_STEPS)
     assert plan.pred_step_s == (ends[-1] - ends[-3]) / 2.0
