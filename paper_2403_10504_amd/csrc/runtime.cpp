@@ -306,7 +306,13 @@ int atom_zero_grads(atom_ctx* c) {
   // in an accumulation: wait for all of them, not only the queued ones
   int s = sync_all(c);
   if (s != ATOM_OK) return s;
-  memset(c->h_acc, 0, c->model_bytes / c->e * 4);
+  // on every pool thread (nothing else runs on the pool after sync_all)
+  const uint64_t n = c->model_bytes / c->e;
+  const int nt = c->pool->size();
+  c->pool->run([&](int ti) {
+    const uint64_t lo = n * ti / nt, hi = n * (ti + 1) / nt;
+    memset(c->h_acc + lo, 0, (hi - lo) * 4);
+  }, nt);
   return ATOM_OK;
 }
 
