@@ -256,7 +256,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               f"(the data-parallel path across GPUs is a design, not an implementation).", file=sys.stderr)
         sys.exit(2)
 
